@@ -1,0 +1,588 @@
+/*
+ * ilw_oracle.c -- CPU oracle for the integer-only I-LW-DETR operators.
+ *
+ * TEST INFRASTRUCTURE ONLY: the plain, slow, obviously correct reference the
+ * GPU library is checked against.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg load it; the GPU library never does, and the
+ * two share no code.
+ *
+ * Each function follows one statement of the paper, named at its definition:
+ *   Sec. 3.2.1 / eq. (linear_quant)  integer linear layer, dyadic rescale
+ *   Sec. 3.2.2                       dyadic multiply-and-shift rescale
+ *   Sec. 3.3 (opening paragraph)     I-ViT integer LayerNorm, Newton sqrt
+ *   Sec. 3.3.1, Alg. 1               ShiftExp, SD-ShiftGELU
+ *   Sec. 3.3.2, Alg. 2               Constrained Shiftmax, CalibrateShift
+ *   Sec. 3.1.1                       nearest-neighbour deformable sampling
+ * Readings of points the paper leaves open are stated where they are used.
+ *
+ * Intermediates that could leave 64 bits are computed in __int128; all
+ * divisions are written as explicit floor divisions, so nothing here relies
+ * on implementation-defined shifts of negative numbers.
+ */
+#include "ilw_oracle.h"
+
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Symmetric int8 activations without zero point (Sec. 4.4, "8/8/16"):
+ * reading: the saturation range is the symmetric [-127, 127]. */
+#define ORC_QMAX 127
+#define ORC_QMIN (-127)
+
+static void orc_require(int cond, const char* what) {
+  if (!cond) {
+    fprintf(stderr, "ilw oracle: precondition violated: %s\n", what);
+    abort();
+  }
+}
+
+/* floor(a / b) for b != 0, written out from the definition. */
+static __int128 floor_div(__int128 a, __int128 b) {
+  __int128 q = a / b; /* C truncates toward zero */
+  if ((a % b) != 0 && ((a < 0) != (b < 0))) q -= 1;
+  return q;
+}
+
+static __int128 pow2(int32_t s) { return (__int128)1 << s; }
+
+int64_t orc_floor_div_pow2(int64_t v, int32_t s) {
+  orc_require(s >= 0 && s <= 62, "shift in [0, 62]");
+  return (int64_t)floor_div(v, pow2(s));
+}
+
+static int32_t sat8(__int128 v) {
+  if (v > ORC_QMAX) return ORC_QMAX;
+  if (v < ORC_QMIN) return ORC_QMIN;
+  return (int32_t)v;
+}
+
+/* Dyadic requantization (Sec. 3.2.1, eq. linear_quant: scales applied after
+ * the integer accumulation; Sec. 3.2.2: the rescale is an integer dyadic
+ * multiply-and-shift).  Reading: round half up, i.e.
+ *   y = sat8( floor( (acc * mult + 2^(shift-1)) / 2^shift ) ).            */
+int32_t orc_requant(int64_t acc, int32_t mult, int32_t shift) {
+  orc_require(shift >= 1 && shift <= 62, "requant shift in [1, 62]");
+  __int128 v = (__int128)acc * mult + pow2(shift - 1);
+  return sat8(floor_div(v, pow2(shift)));
+}
+
+/* Two-input dyadic add onto a common output scale (Sec. 3.2.2: branches are
+ * rescaled to one output scale by dyadic multiply-and-shift and summed in
+ * integers).  Used for the residual connections of the encoder block. */
+int32_t orc_residual(int32_t a, int32_t b, int32_t mult_a, int32_t mult_b,
+                     int32_t shift) {
+  orc_require(shift >= 1 && shift <= 62, "residual shift in [1, 62]");
+  __int128 v = (__int128)a * mult_a + (__int128)b * mult_b + pow2(shift - 1);
+  return sat8(floor_div(v, pow2(shift)));
+}
+
+/* ShiftExp (Alg. 1, function ShiftExp), for a non-positive input I with
+ * I0 = round(1/S) passed in as an integer.  Returns I_exp; the matching scale
+ * is S / 2^k_inter. */
+int64_t orc_shiftexp(int64_t I, int32_t I0, int32_t k_inter) {
+  orc_require(I <= 0, "ShiftExp input must be <= 0");
+  orc_require(I0 >= 1, "I0 >= 1");
+  orc_require(k_inter >= 1 && k_inter <= 30, "k_inter in [1, 30]");
+  /* I * log2(e) approximated as I + I/2 - I/16 with floor shifts */
+  int64_t Ie = I + (int64_t)floor_div(I, 2) - (int64_t)floor_div(I, 16);
+  /* lower-bound clipping at k_inter * (-I0) */
+  int64_t lo = -(int64_t)k_inter * I0;
+  if (Ie < lo) Ie = lo;
+  /* integer part q = floor(Ie / (-I0)) and decimal part r */
+  int64_t q = (int64_t)floor_div(Ie, -(int64_t)I0);
+  int64_t r = -(Ie - q * (-(int64_t)I0));
+  orc_require(q >= 0 && q <= k_inter, "ShiftExp integer part in [0, k_inter]");
+  orc_require(r >= 0 && r < I0, "ShiftExp decimal part in [0, I0)");
+  /* 2^(-r/I0) approximated linearly: I_b = (-r >> 1) + I0 */
+  int64_t Ib = (int64_t)floor_div(-r, 2) + I0;
+  return (int64_t)((__int128)Ib * pow2(k_inter - (int32_t)q));
+}
+
+/* CalibrateShift (Alg. 2; Sec. 3.3.2 equations for M_req, M_target, s_d). */
+int32_t orc_calibrate_shift(int64_t s_sum, int32_t m_p, int32_t M_hw) {
+  orc_require(s_sum >= 1, "S_sum >= 1");
+  /* M_req = ceil(log2(S_sum)): the smallest M with 2^M >= S_sum */
+  int32_t M_req = 0;
+  while (pow2(M_req) < s_sum) M_req++;
+  int32_t M_target = M_req + m_p;
+  int32_t s_d = M_target - M_hw;
+  return s_d > 0 ? s_d : 0;
+}
+
+/* Constrained Shiftmax over one row (Alg. 2, ConstrainedShiftmax; Sec. 3.3.2).
+ * s_d_static >= 0 uses that calibrated denominator shift (the text calibrates
+ * one s_d per Shiftmax block); s_d_static == -1 recomputes it from the row's
+ * own S_sum as the algorithm listing does.  The final output formula is the
+ * one the section ends with (I_exp times F, then one shift that includes
+ * s_d).  Reading: the result is stored as a signed k_out-bit integer, so it is
+ * limited to 2^(k_out-1) - 1. */
+void orc_shiftmax_row(const int32_t* x, int32_t d, int32_t I0, int32_t k_inter,
+                      int32_t k_out, int32_t m_p, int32_t s_d_static,
+                      int32_t* out, int64_t* diag) {
+  orc_require(d >= 1, "row length >= 1");
+  orc_require(k_out >= 2 && k_out <= 16, "k_out in [2, 16]");
+  const int32_t M_hw = 31;
+  int64_t* e = (int64_t*)malloc(sizeof(int64_t) * (size_t)d);
+  orc_require(e != NULL, "allocation");
+
+  int32_t I_max = x[0];
+  for (int32_t i = 1; i < d; i++)
+    if (x[i] > I_max) I_max = x[i];
+
+  int64_t S_sum = 0;
+  for (int32_t i = 0; i < d; i++) {
+    int64_t I_delta = (int64_t)x[i] - I_max; /* <= 0 */
+    e[i] = orc_shiftexp(I_delta, I0, k_inter);
+    S_sum += e[i];
+  }
+
+  int32_t s_d = s_d_static >= 0 ? s_d_static
+                                : orc_calibrate_shift(S_sum, m_p, M_hw);
+  orc_require(s_d >= 0 && s_d <= 40, "s_d in [0, 40]");
+
+  /* quotient-remainder accumulation of the shifted denominator */
+  int64_t sum_Q = 0, sum_r = 0;
+  for (int32_t i = 0; i < d; i++) {
+    int64_t Q = (int64_t)floor_div(e[i], pow2(s_d));
+    int64_t r = e[i] - (int64_t)(Q * pow2(s_d));
+    sum_Q += Q;
+    sum_r += r;
+  }
+  int64_t S_R = sum_Q + (int64_t)floor_div(sum_r, pow2(s_d));
+  /* the decomposition recovers the exact shifted sum */
+  orc_require(S_R == (int64_t)floor_div(S_sum, pow2(s_d)),
+              "quotient-remainder sum equals floor(S_sum / 2^s_d)");
+
+  const int64_t lim = 2147483647; /* 2^31 - 1 */
+  if (S_R < 1) S_R = 1;
+  if (S_R > lim) S_R = lim;
+  int64_t F = lim / S_R; /* both positive: C division is the floor */
+
+  int32_t out_shift = 31 - k_out + 1 + s_d;
+  int64_t out_max = (int64_t)pow2(k_out - 1) - 1;
+  for (int32_t i = 0; i < d; i++) {
+    __int128 v = floor_div((__int128)e[i] * F, pow2(out_shift));
+    if (v > out_max) v = out_max;
+    out[i] = (int32_t)v;
+  }
+  if (diag) {
+    diag[0] = S_sum;
+    diag[1] = s_d;
+    diag[2] = S_R;
+    diag[3] = F;
+  }
+  free(e);
+}
+
+/* I-ViT Shiftmax with a fixed division precision M (Sec. 3.3.2, eq.
+ * shiftmax_original): out_i = (floor((2^M - 1) / S_sum) * I_exp_i) >>
+ * (M - (k_out - 1)).  Kept as the baseline the constrained form extends. */
+void orc_shiftmax_ivit_row(const int32_t* x, int32_t d, int32_t I0,
+                           int32_t k_inter, int32_t k_out, int32_t M,
+                           int32_t* out) {
+  orc_require(d >= 1, "row length >= 1");
+  int32_t I_max = x[0];
+  for (int32_t i = 1; i < d; i++)
+    if (x[i] > I_max) I_max = x[i];
+  __int128 S_sum = 0;
+  for (int32_t i = 0; i < d; i++)
+    S_sum += orc_shiftexp((int64_t)x[i] - I_max, I0, k_inter);
+  __int128 factor = floor_div(pow2(M) - 1, S_sum);
+  for (int32_t i = 0; i < d; i++) {
+    __int128 e = orc_shiftexp((int64_t)x[i] - I_max, I0, k_inter);
+    out[i] = (int32_t)floor_div(factor * e, pow2(M - (k_out - 1)));
+  }
+}
+
+/* IntDiv, which Alg. 1 uses without defining.  Reading: the I-ViT integer
+ * division of eq. shiftmax_original with M = M_hw = 31 applied to one
+ * numerator, giving a k_out-bit ratio with scale 2^-(k_out-1):
+ *   IntDiv(a, b) = (floor((2^31 - 1) / b) * a) >> (31 - (k_out - 1)).      */
+int64_t orc_intdiv(int64_t a, int64_t b, int32_t k_out) {
+  orc_require(b >= 1, "IntDiv denominator >= 1");
+  orc_require(a >= 0, "IntDiv numerator >= 0");
+  __int128 factor = floor_div(pow2(31) - 1, b);
+  return (int64_t)floor_div(factor * a, pow2(31 - (k_out - 1)));
+}
+
+/* SD-ShiftGELU (Alg. 1; Sec. 3.3.1): GELU(x) ~ x * sigmoid(1.702 x) with a
+ * sign-dependent sigmoid, so that each element is processed on its own.
+ * Returns I_out = I_x * I_div, whose scale is S_x * 2^-(k_out-1). */
+int64_t orc_sdshiftgelu(int32_t x, int32_t I0, int32_t k_inter,
+                        int32_t k_out) {
+  int64_t I = x;
+  /* 1.702 * I as I + I/2 + I/8 + I/16 with floor shifts */
+  int64_t Ip = I + (int64_t)floor_div(I, 2) + (int64_t)floor_div(I, 8) +
+               (int64_t)floor_div(I, 16);
+  int64_t Ishift = Ip > 0 ? Ip : 0; /* ReLU(I_p) */
+  int64_t Idelta = Ip - Ishift;     /* <= 0 */
+  int64_t a = orc_shiftexp(Idelta, I0, k_inter);
+  int64_t a2 = orc_shiftexp(-Ishift, I0, k_inter);
+  int64_t Idiv = orc_intdiv(a, a + a2, k_out);
+  return I * Idiv;
+}
+
+/* The I-ViT ShiftGELU that SD-ShiftGELU replaces (Sec. 3.3.1): the sigmoid
+ * argument is shifted by the vector maximum max_ip (>= 0) of I_p instead of
+ * by ReLU(I_p) element by element. */
+int64_t orc_ivit_shiftgelu(int32_t x, int32_t max_ip, int32_t I0,
+                           int32_t k_inter, int32_t k_out) {
+  orc_require(max_ip >= 0, "vector maximum of I_p must be >= 0");
+  int64_t I = x;
+  int64_t Ip = I + (int64_t)floor_div(I, 2) + (int64_t)floor_div(I, 8) +
+               (int64_t)floor_div(I, 16);
+  orc_require(Ip <= max_ip, "max_ip is the vector maximum");
+  int64_t a = orc_shiftexp(Ip - max_ip, I0, k_inter);
+  int64_t a2 = orc_shiftexp(-(int64_t)max_ip, I0, k_inter);
+  int64_t Idiv = orc_intdiv(a, a + a2, k_out);
+  return I * Idiv;
+}
+
+/* Integer square root by Newton's method with a fixed iteration count
+ * (Sec. 3.3: I-ViT's LayerNorm, 10 iterations, raised to 20 for the decoder).
+ * Reading: the I-BERT/I-ViT form, started from the fixed estimate 2^16 and
+ * iterated k <- floor((k + floor(V / k)) / 2) exactly `iters` times.  A fixed
+ * start is what makes the iteration count matter.  V == 0 returns 0. */
+int64_t orc_isqrt_newton(int64_t V, int32_t iters) {
+  orc_require(V >= 0, "V >= 0");
+  orc_require(iters >= 1 && iters <= 64, "iterations in [1, 64]");
+  if (V == 0) return 0;
+  int64_t k = 65536;
+  for (int32_t t = 0; t < iters; t++) {
+    orc_require(k >= 1, "Newton iterate stays positive for V >= 1");
+    k = (int64_t)floor_div((__int128)k + floor_div(V, k), 2);
+  }
+  return k;
+}
+
+/* Integer LayerNorm of one row of C int8 channels (Sec. 3.3: the I-ViT
+ * formulation is adopted).  The paper does not restate the formula; reading:
+ *   mu  = floor((2*sum(x) + C) / (2*C))            mean, rounded half up
+ *   y_i = x_i - mu;  V = sum(y_i^2)
+ *   sigma = Newton isqrt of V (iters steps)
+ *   F   = floor((2^31 - 1) / sigma);  n_i = floor(y_i * F / 2)
+ *         (n_i has scale sqrt(C) / 2^30: it is y_i / std * 2^30 / sqrt(C))
+ *   o_i = sat8(requant(n_i + beta_i; mult_i, shift_i))
+ * gamma is folded into the (possibly negative) per-channel multiplier and
+ * beta is an integer at the scale of n.  A constant row (V == 0) has n = 0. */
+void orc_int_layernorm_row(const int8_t* x, int32_t C, const int32_t* beta,
+                           const int32_t* mult, const int32_t* shift,
+                           int32_t n_q, int32_t iters, int8_t* y,
+                           int64_t* diag) {
+  orc_require(C >= 1, "C >= 1");
+  orc_require(n_q == 1 || n_q == C, "dyadic is per-tensor or per-channel");
+  int64_t S = 0;
+  for (int32_t i = 0; i < C; i++) S += x[i];
+  int64_t mu = (int64_t)floor_div((__int128)2 * S + C, (__int128)2 * C);
+  int64_t V = 0;
+  for (int32_t i = 0; i < C; i++) {
+    int64_t yi = x[i] - mu;
+    V += yi * yi;
+  }
+  int64_t sigma = orc_isqrt_newton(V, iters);
+  int64_t F = sigma > 0 ? (int64_t)2147483647 / sigma : 0;
+  for (int32_t i = 0; i < C; i++) {
+    int64_t yi = x[i] - mu;
+    int64_t n = sigma > 0 ? (int64_t)floor_div((__int128)yi * F, 2) : 0;
+    int32_t q = n_q == 1 ? 0 : i;
+    y[i] = (int8_t)orc_requant(n + beta[i], mult[q], shift[q]);
+  }
+  if (diag) {
+    diag[0] = mu;
+    diag[1] = V;
+    diag[2] = sigma;
+    diag[3] = F;
+  }
+}
+
+void orc_int_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
+                       const int32_t* beta, const int32_t* mult,
+                       const int32_t* shift, int32_t n_q, int32_t iters) {
+  for (int64_t r = 0; r < rows; r++)
+    orc_int_layernorm_row(x + r * C, C, beta, mult, shift, n_q, iters,
+                          y + r * C, NULL);
+}
+
+/* Integer linear layer (Sec. 3.2.1, eq. linear_quant): the multiply-
+ * accumulate runs in integers; acc[m][n] = b[n] + sum_k x[m][k] * w[n][k].
+ * x is [M, K] and w is [N, K], both row-major. */
+void orc_linear_acc(const int8_t* x, const int8_t* w, const int32_t* b,
+                    int64_t M, int32_t N, int32_t K, int32_t* acc) {
+  for (int64_t m = 0; m < M; m++)
+    for (int32_t n = 0; n < N; n++) {
+      int64_t s = b ? b[n] : 0;
+      for (int32_t k = 0; k < K; k++)
+        s += (int32_t)x[m * K + k] * (int32_t)w[(int64_t)n * K + k];
+      orc_require(s >= INT32_MIN && s <= INT32_MAX, "accumulator fits int32");
+      acc[m * N + n] = (int32_t)s;
+    }
+}
+
+/* Linear layer followed by the per-channel (weights) dyadic requantization to
+ * a per-tensor int8 activation (Sec. 3.2.1). */
+void orc_linear(const int8_t* x, const int8_t* w, const int32_t* b, int64_t M,
+                int32_t N, int32_t K, const int32_t* mult, const int32_t* shift,
+                int32_t n_q, int8_t* y) {
+  orc_require(n_q == 1 || n_q == N, "dyadic is per-tensor or per-channel");
+  int32_t* acc = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+  orc_require(acc != NULL, "allocation");
+  for (int64_t m = 0; m < M; m++) {
+    orc_linear_acc(x + m * K, w, b, 1, N, K, acc);
+    for (int32_t n = 0; n < N; n++) {
+      int32_t q = n_q == 1 ? 0 : n;
+      y[m * N + n] = (int8_t)orc_requant(acc[n], mult[q], shift[q]);
+    }
+  }
+  free(acc);
+}
+
+void orc_residual_tensor(const int8_t* a, const int8_t* b, int8_t* y,
+                         int64_t n, int32_t mult_a, int32_t mult_b,
+                         int32_t shift) {
+  for (int64_t i = 0; i < n; i++)
+    y[i] = (int8_t)orc_residual(a[i], b[i], mult_a, mult_b, shift);
+}
+
+void orc_shiftmax_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                       int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                       int32_t s_d_static) {
+  int32_t* in = (int32_t*)malloc(sizeof(int32_t) * (size_t)cols);
+  int32_t* out = (int32_t*)malloc(sizeof(int32_t) * (size_t)cols);
+  orc_require(in && out, "allocation");
+  for (int64_t r = 0; r < rows; r++) {
+    for (int32_t i = 0; i < cols; i++) in[i] = x[r * cols + i];
+    orc_shiftmax_row(in, cols, I0, k_inter, k_out, m_p, s_d_static, out, NULL);
+    for (int32_t i = 0; i < cols; i++) y[r * cols + i] = (int8_t)out[i];
+  }
+  free(in);
+  free(out);
+}
+
+/* SD-ShiftGELU over a tensor, then the dyadic requantization of I_out to the
+ * int8 input of the next linear layer (activations are per-tensor int8,
+ * Sec. 3.2.1; the paper's operator itself stops at (I_out, S_out)). */
+void orc_sdshiftgelu_tensor(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
+                            int32_t k_inter, int32_t k_out, int32_t out_mult,
+                            int32_t out_shift) {
+  for (int64_t i = 0; i < n; i++)
+    y[i] = (int8_t)orc_requant(orc_sdshiftgelu(x[i], I0, k_inter, k_out),
+                               out_mult, out_shift);
+}
+
+/* Integer multi-head attention of one image (the encoder's MatMul and
+ * Softmax operators, Table ablation_study; Sec. 3.2.1 for the matmuls,
+ * Sec. 3.3.2 for Shiftmax).  Window attention (LW-DETR mixes window and
+ * global attention) partitions the grid_h x grid_w token grid into
+ * win_h x win_w windows that attend only inside themselves; global attention
+ * is the single window covering the grid.  Per window and head:
+ *   S = Q K^T (int32) -> per-tensor dyadic requant -> int8 scores
+ *   P = ConstrainedShiftmax(row of S)        (scale 2^-(k_out-1))
+ *   O = P V (int32)  -> per-tensor dyadic requant -> int8, heads concatenated */
+void orc_attention(const int8_t* qkv, int32_t grid_h, int32_t grid_w,
+                   int32_t win_h, int32_t win_w, int32_t D, int32_t heads,
+                   int32_t head_dim, int32_t score_mult, int32_t score_shift,
+                   int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                   int32_t s_d_static, int32_t pv_mult, int32_t pv_shift,
+                   int8_t* out) {
+  if (win_h == 0) {
+    win_h = grid_h;
+    win_w = grid_w;
+  }
+  orc_require(heads * head_dim == D, "heads * head_dim == dim");
+  orc_require(grid_h % win_h == 0 && grid_w % win_w == 0,
+              "windows tile the grid");
+  int32_t Tw = win_h * win_w;
+  int32_t D3 = 3 * D;
+  int64_t* tok = (int64_t*)malloc(sizeof(int64_t) * (size_t)Tw);
+  int32_t* srow = (int32_t*)malloc(sizeof(int32_t) * (size_t)Tw);
+  int32_t* P = (int32_t*)malloc(sizeof(int32_t) * (size_t)Tw * Tw);
+  orc_require(tok && srow && P, "allocation");
+  for (int32_t wy = 0; wy < grid_h / win_h; wy++)
+    for (int32_t wx = 0; wx < grid_w / win_w; wx++) {
+      /* token index of each window-local position */
+      for (int32_t iy = 0; iy < win_h; iy++)
+        for (int32_t ix = 0; ix < win_w; ix++)
+          tok[iy * win_w + ix] =
+              (int64_t)(wy * win_h + iy) * grid_w + (wx * win_w + ix);
+      for (int32_t h = 0; h < heads; h++) {
+        int32_t qo = h * head_dim, ko = D + h * head_dim,
+                vo = 2 * D + h * head_dim;
+        for (int32_t i = 0; i < Tw; i++) {
+          for (int32_t j = 0; j < Tw; j++) {
+            int64_t s = 0;
+            for (int32_t c = 0; c < head_dim; c++)
+              s += (int32_t)qkv[tok[i] * D3 + qo + c] *
+                   (int32_t)qkv[tok[j] * D3 + ko + c];
+            srow[j] = orc_requant(s, score_mult, score_shift);
+          }
+          orc_shiftmax_row(srow, Tw, I0, k_inter, k_out, m_p, s_d_static,
+                           P + (int64_t)i * Tw, NULL);
+        }
+        for (int32_t i = 0; i < Tw; i++)
+          for (int32_t c = 0; c < head_dim; c++) {
+            int64_t o = 0;
+            for (int32_t j = 0; j < Tw; j++)
+              o += (int64_t)P[(int64_t)i * Tw + j] *
+                   qkv[tok[j] * D3 + vo + c];
+            out[tok[i] * D + qo + c] = (int8_t)orc_requant(o, pv_mult, pv_shift);
+          }
+      }
+    }
+  free(tok);
+  free(srow);
+  free(P);
+}
+
+/* One integer encoder block.  The paper lists the encoder's operators
+ * (Linear, MatMul, Softmax, GELU, LayerNorm; Table ablation_study) and calls
+ * the encoder a plain ViT; reading: the pre-LayerNorm ViT order
+ *   h  = LN1(x);  a = Attn(QKV(h));  x1 = Res(proj(a), x)
+ *   h2 = LN2(x1); g = rq(SD-ShiftGELU(fc1(h2)));  y = Res(fc2(g), x1)
+ * with every tensor between operators an int8 per-tensor activation. */
+void orc_block_forward(const orc_block* p, const int8_t* x, int8_t* y,
+                       int32_t B, int32_t grid_h, int32_t grid_w,
+                       int32_t win_h, int32_t win_w) {
+  const int32_t D = p->dim, Hm = p->mlp_dim;
+  const int64_t T = (int64_t)grid_h * grid_w;
+  int8_t* h = (int8_t*)malloc((size_t)(T * D));
+  int8_t* qkv = (int8_t*)malloc((size_t)(T * 3 * D));
+  int8_t* att = (int8_t*)malloc((size_t)(T * D));
+  int8_t* pr = (int8_t*)malloc((size_t)(T * D));
+  int8_t* x1 = (int8_t*)malloc((size_t)(T * D));
+  int8_t* f1 = (int8_t*)malloc((size_t)(T * Hm));
+  int8_t* g = (int8_t*)malloc((size_t)(T * Hm));
+  int8_t* f2 = (int8_t*)malloc((size_t)(T * D));
+  orc_require(h && qkv && att && pr && x1 && f1 && g && f2, "allocation");
+  for (int32_t b = 0; b < B; b++) {
+    const int8_t* xb = x + (int64_t)b * T * D;
+    int8_t* yb = y + (int64_t)b * T * D;
+    orc_int_layernorm(xb, h, T, D, p->ln1_beta, p->ln1_mult, p->ln1_shift,
+                      p->ln1_nq, p->ln_iters);
+    orc_linear(h, p->w_qkv, p->b_qkv, T, 3 * D, D, p->qkv_mult, p->qkv_shift,
+               p->qkv_nq, qkv);
+    orc_attention(qkv, grid_h, grid_w, win_h, win_w, D, p->heads, p->head_dim,
+                  p->score_mult, p->score_shift, p->smax_I0, p->smax_k_inter,
+                  p->smax_k_out, p->smax_m_p, p->smax_s_d, p->pv_mult,
+                  p->pv_shift, att);
+    orc_linear(att, p->w_proj, p->b_proj, T, D, D, p->proj_mult,
+               p->proj_shift, p->proj_nq, pr);
+    orc_residual_tensor(pr, xb, x1, T * D, p->res1_mult_a, p->res1_mult_b,
+                        p->res1_shift);
+    orc_int_layernorm(x1, h, T, D, p->ln2_beta, p->ln2_mult, p->ln2_shift,
+                      p->ln2_nq, p->ln_iters);
+    orc_linear(h, p->w_fc1, p->b_fc1, T, Hm, D, p->fc1_mult, p->fc1_shift,
+               p->fc1_nq, f1);
+    orc_sdshiftgelu_tensor(f1, g, T * Hm, p->gelu_I0, p->gelu_k_inter,
+                           p->gelu_k_out, p->gelu_mult, p->gelu_shift);
+    orc_linear(g, p->w_fc2, p->b_fc2, T, D, Hm, p->fc2_mult, p->fc2_shift,
+               p->fc2_nq, f2);
+    orc_residual_tensor(f2, x1, yb, T * D, p->res2_mult_a, p->res2_mult_b,
+                        p->res2_shift);
+  }
+  free(h);
+  free(qkv);
+  free(att);
+  free(pr);
+  free(x1);
+  free(f1);
+  free(g);
+  free(f2);
+}
+
+/* Nearest-neighbour deformable sampling location (Sec. 3.1.1: bilinear
+ * interpolation is replaced by taking the nearest grid point).  Reading of
+ * the fixed-point arithmetic, which the paper does not give: the reference
+ * point is Q16 in [0, 1) of the map, offsets are Q8 pixels of this level;
+ *   X = floor(ref_x * W / 2^8) + off_x       (Q8 pixel coordinate)
+ *   ix = floor(X / 2^8)                      (pixel whose cell holds X)
+ * which is the nearest pixel centre under the half-pixel convention.  A
+ * sample outside the map contributes nothing (zero padding). */
+int64_t orc_deform_nearest_index(int32_t ref_x, int32_t ref_y, int32_t off_x,
+                                 int32_t off_y, int32_t H, int32_t W) {
+  int64_t X = (int64_t)floor_div((__int128)ref_x * W, 256) + off_x;
+  int64_t Y = (int64_t)floor_div((__int128)ref_y * H, 256) + off_y;
+  int64_t ix = (int64_t)floor_div(X, 256);
+  int64_t iy = (int64_t)floor_div(Y, 256);
+  if (ix < 0 || ix >= W || iy < 0 || iy >= H) return -1;
+  return iy * W + ix;
+}
+
+/* Multi-scale deformable attention core (Sec. 3.1.1 with the decoder's
+ * Softmax as Constrained Shiftmax, Sec. 3.3.2):
+ *   value  int8  [B, S_total, heads, head_dim]  (levels stacked, level_start)
+ *   ref    int32 [B, Q, 2]                      Q16 (x, y) in [0, 1)
+ *   offsets int16 [B, Q, heads, L, P, 2]         Q8 pixels (x, y)
+ *   logits int8  [B, Q, heads, L*P]  -> P = ConstrainedShiftmax per (b,q,h)
+ *   out    int8  [B, Q, heads*head_dim] = sat8(rq(sum P * sampled value))
+ * mode 0: nearest sampling (the paper's).  mode 1: a fixed-point bilinear
+ * variant (Q8 weights on the half-pixel grid, corners outside contribute 0,
+ * the 2^16 weight scale removed by 16 extra bits of the output shift). */
+void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
+                     const int32_t* level_start, int32_t L, int32_t P,
+                     const int32_t* ref, const int16_t* offsets,
+                     const int8_t* logits, int8_t* out, int32_t B, int32_t Q,
+                     int32_t heads, int32_t head_dim, int32_t S_total,
+                     int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                     int32_t s_d_static, int32_t out_mult, int32_t out_shift,
+                     int32_t mode) {
+  orc_require(mode == 0 || mode == 1, "mode is 0 (nearest) or 1 (bilinear)");
+  const int32_t LP = L * P;
+  int32_t* lg = (int32_t*)malloc(sizeof(int32_t) * (size_t)LP);
+  int32_t* pw = (int32_t*)malloc(sizeof(int32_t) * (size_t)LP);
+  __int128* acc = (__int128*)malloc(sizeof(__int128) * (size_t)head_dim);
+  orc_require(lg && pw && acc, "allocation");
+  for (int32_t b = 0; b < B; b++)
+    for (int32_t q = 0; q < Q; q++)
+      for (int32_t h = 0; h < heads; h++) {
+        int64_t bqh = ((int64_t)b * Q + q) * heads + h;
+        for (int32_t i = 0; i < LP; i++) lg[i] = logits[bqh * LP + i];
+        orc_shiftmax_row(lg, LP, I0, k_inter, k_out, m_p, s_d_static, pw,
+                         NULL);
+        for (int32_t c = 0; c < head_dim; c++) acc[c] = 0;
+        int32_t rx = ref[((int64_t)b * Q + q) * 2 + 0];
+        int32_t ry = ref[((int64_t)b * Q + q) * 2 + 1];
+        for (int32_t l = 0; l < L; l++) {
+          int32_t Hl = level_hw[2 * l + 0], Wl = level_hw[2 * l + 1];
+          for (int32_t pt = 0; pt < P; pt++) {
+            int64_t oidx = ((bqh * L + l) * P + pt) * 2;
+            int32_t ox = offsets[oidx + 0], oy = offsets[oidx + 1];
+            int32_t wgt = pw[l * P + pt];
+            if (mode == 0) {
+              int64_t idx = orc_deform_nearest_index(rx, ry, ox, oy, Hl, Wl);
+              if (idx < 0) continue;
+              int64_t row = ((int64_t)b * S_total + level_start[l] + idx) *
+                                heads + h;
+              for (int32_t c = 0; c < head_dim; c++)
+                acc[c] += (__int128)wgt * value[row * head_dim + c];
+            } else {
+              /* half-pixel grid: pixel centres sit at X = 256*i + 128 */
+              int64_t X = (int64_t)floor_div((__int128)rx * Wl, 256) + ox - 128;
+              int64_t Y = (int64_t)floor_div((__int128)ry * Hl, 256) + oy - 128;
+              int64_t x0 = (int64_t)floor_div(X, 256), fx = X - 256 * x0;
+              int64_t y0 = (int64_t)floor_div(Y, 256), fy = Y - 256 * y0;
+              for (int32_t dy = 0; dy < 2; dy++)
+                for (int32_t dx = 0; dx < 2; dx++) {
+                  int64_t xi = x0 + dx, yi = y0 + dy;
+                  if (xi < 0 || xi >= Wl || yi < 0 || yi >= Hl) continue;
+                  int64_t w = (dx ? fx : 256 - fx) * (dy ? fy : 256 - fy);
+                  int64_t row = ((int64_t)b * S_total + level_start[l] +
+                                 yi * Wl + xi) * heads + h;
+                  for (int32_t c = 0; c < head_dim; c++)
+                    acc[c] += (__int128)wgt * w * value[row * head_dim + c];
+                }
+            }
+          }
+        }
+        int32_t sh = mode == 0 ? out_shift : out_shift + 16;
+        for (int32_t c = 0; c < head_dim; c++) {
+          orc_require(acc[c] >= INT64_MIN && acc[c] <= INT64_MAX,
+                      "sampling accumulator fits int64");
+          out[bqh * head_dim + c] = (int8_t)orc_requant((int64_t)acc[c],
+                                                        out_mult, sh);
+        }
+      }
+  free(lg);
+  free(pw);
+  free(acc);
+}

@@ -1,0 +1,126 @@
+/*
+ * ilw_oracle.h -- CPU oracle for the integer-only I-LW-DETR operators.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is the plain, slow, obviously correct
+ * reference that the GPU path is checked against.  Only the test-suite, the
+ * smoke check and the benchmark's CPU-baseline leg may load it.  It shares no
+ * code, header, table or constant with the GPU library, and the GPU library
+ * never calls it.
+ *
+ * Every function follows one statement of the paper ("Enabling Fully
+ * Integer-Only Inference for Lightweight Detection Transformers"): the
+ * section, equation or algorithm is named at each definition.  Where the paper
+ * leaves a detail open (rounding mode, saturation range, IntDiv, the integer
+ * LayerNorm formula, block order, sampling arithmetic), the reading taken is
+ * stated at the definition.
+ *
+ * All arithmetic is integer.  Intermediates that may exceed 64 bits are done
+ * in __int128 so that no overflow reasoning is needed to trust the oracle.
+ */
+#ifndef ILW_ORACLE_H
+#define ILW_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- scalar building blocks -------------------------------------------- */
+int64_t orc_floor_div_pow2(int64_t v, int32_t s);
+int32_t orc_requant(int64_t acc, int32_t mult, int32_t shift);
+int32_t orc_residual(int32_t a, int32_t b, int32_t mult_a, int32_t mult_b,
+                     int32_t shift);
+int64_t orc_shiftexp(int64_t I, int32_t I0, int32_t k_inter);
+int32_t orc_calibrate_shift(int64_t s_sum, int32_t m_p, int32_t M_hw);
+int64_t orc_intdiv(int64_t a, int64_t b, int32_t k_out);
+int64_t orc_sdshiftgelu(int32_t x, int32_t I0, int32_t k_inter, int32_t k_out);
+int64_t orc_ivit_shiftgelu(int32_t x, int32_t max_ip, int32_t I0,
+                           int32_t k_inter, int32_t k_out);
+int64_t orc_isqrt_newton(int64_t V, int32_t iters);
+
+/* ---- row / tensor operators -------------------------------------------- */
+/* diag (may be NULL) receives {S_sum, s_d, S_R, F}. */
+void orc_shiftmax_row(const int32_t* x, int32_t d, int32_t I0, int32_t k_inter,
+                      int32_t k_out, int32_t m_p, int32_t s_d_static,
+                      int32_t* out, int64_t* diag);
+void orc_shiftmax_ivit_row(const int32_t* x, int32_t d, int32_t I0,
+                           int32_t k_inter, int32_t k_out, int32_t M,
+                           int32_t* out);
+void orc_shiftmax_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                       int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                       int32_t s_d_static);
+void orc_sdshiftgelu_tensor(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
+                            int32_t k_inter, int32_t k_out, int32_t out_mult,
+                            int32_t out_shift);
+/* diag (may be NULL) receives {mean, V, sigma, F} for the row. */
+void orc_int_layernorm_row(const int8_t* x, int32_t C, const int32_t* beta,
+                           const int32_t* mult, const int32_t* shift,
+                           int32_t n_q, int32_t iters, int8_t* y,
+                           int64_t* diag);
+void orc_int_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
+                       const int32_t* beta, const int32_t* mult,
+                       const int32_t* shift, int32_t n_q, int32_t iters);
+void orc_linear_acc(const int8_t* x, const int8_t* w, const int32_t* b,
+                    int64_t M, int32_t N, int32_t K, int32_t* acc);
+void orc_linear(const int8_t* x, const int8_t* w, const int32_t* b, int64_t M,
+                int32_t N, int32_t K, const int32_t* mult, const int32_t* shift,
+                int32_t n_q, int8_t* y);
+void orc_residual_tensor(const int8_t* a, const int8_t* b, int8_t* y,
+                         int64_t n, int32_t mult_a, int32_t mult_b,
+                         int32_t shift);
+
+/* Integer attention of one image: qkv is the int8 [T, 3*D] QKV output
+ * (q | k | v, head-major inside each part), out is int8 [T, D]. */
+void orc_attention(const int8_t* qkv, int32_t grid_h, int32_t grid_w,
+                   int32_t win_h, int32_t win_w, int32_t D, int32_t heads,
+                   int32_t head_dim, int32_t score_mult, int32_t score_shift,
+                   int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                   int32_t s_d_static, int32_t pv_mult, int32_t pv_shift,
+                   int8_t* out);
+
+/* Parameters of one integer encoder block, host arrays. */
+typedef struct {
+  int32_t dim, heads, head_dim, mlp_dim, ln_iters;
+  const int32_t* ln1_beta; const int32_t* ln1_mult; const int32_t* ln1_shift;
+  int32_t ln1_nq;
+  const int8_t* w_qkv; const int32_t* b_qkv;
+  const int32_t* qkv_mult; const int32_t* qkv_shift; int32_t qkv_nq;
+  int32_t score_mult, score_shift;
+  int32_t smax_I0, smax_k_inter, smax_k_out, smax_m_p, smax_s_d;
+  int32_t pv_mult, pv_shift;
+  const int8_t* w_proj; const int32_t* b_proj;
+  const int32_t* proj_mult; const int32_t* proj_shift; int32_t proj_nq;
+  int32_t res1_mult_a, res1_mult_b, res1_shift;
+  const int32_t* ln2_beta; const int32_t* ln2_mult; const int32_t* ln2_shift;
+  int32_t ln2_nq;
+  const int8_t* w_fc1; const int32_t* b_fc1;
+  const int32_t* fc1_mult; const int32_t* fc1_shift; int32_t fc1_nq;
+  int32_t gelu_I0, gelu_k_inter, gelu_k_out, gelu_mult, gelu_shift;
+  const int8_t* w_fc2; const int32_t* b_fc2;
+  const int32_t* fc2_mult; const int32_t* fc2_shift; int32_t fc2_nq;
+  int32_t res2_mult_a, res2_mult_b, res2_shift;
+} orc_block;
+
+/* x, y int8 [B, grid_h*grid_w, dim]; win_h == 0 means global attention. */
+void orc_block_forward(const orc_block* p, const int8_t* x, int8_t* y,
+                       int32_t B, int32_t grid_h, int32_t grid_w,
+                       int32_t win_h, int32_t win_w);
+
+/* Deformable sampling location of one sample: returns the flat pixel index
+ * y*W + x inside the level, or -1 when the sample falls outside the map. */
+int64_t orc_deform_nearest_index(int32_t ref_x, int32_t ref_y, int32_t off_x,
+                                 int32_t off_y, int32_t H, int32_t W);
+void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
+                     const int32_t* level_start, int32_t L, int32_t P,
+                     const int32_t* ref, const int16_t* offsets,
+                     const int8_t* logits, int8_t* out, int32_t B, int32_t Q,
+                     int32_t heads, int32_t head_dim, int32_t S_total,
+                     int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                     int32_t s_d_static, int32_t out_mult, int32_t out_shift,
+                     int32_t mode);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,208 @@
+"""Seeded synthetic inputs for the integer encoder block and the deformable
+sampling layer.
+
+This module only draws integers.  It holds none of the method's arithmetic, so
+the tests can feed the same arrays to the CPU oracle and to the GPU library.
+Shapes follow the detector the paper quantizes: a ViT encoder on a 640x640
+image with patch size 16 (40x40 = 1600 tokens), window and global attention,
+and a multi-scale deformable decoder layer.  No dataset is used.
+
+Distributions (all integer-uniform, inclusive):
+  int8 activations and weights   [-127, 127]
+  int32 GEMM biases              [-2^15, 2^15]
+  GEMM dyadic multipliers        [2^29, 2^30]; shifts see ``SHIFTS``
+  Shiftmax / GELU I0             [8, 64]
+  LayerNorm beta                 [-2^26, 2^26] (scale of the normalized value)
+  LayerNorm multipliers          +-[2^29, 2^30] (about 1 in 8 negative: the
+                                 multiplier carries gamma, which may be < 0)
+  residual multipliers           [2^29, 2^30], shift 31
+Draw order: block parameters in struct order, then the block input.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+# Shift ranges per requantization point.  "baseline" is the distribution the
+# headline workload is specified with (GEMM shifts 30..38, which saturates many
+# outputs); "wide" keeps most values inside int8 so that the rounding paths are
+# exercised by the parity tests.
+SHIFTS = {
+    "baseline": {"gemm": (30, 38), "gemm_k4": (30, 38), "score": (30, 38),
+                 "pv": (30, 38), "gelu": (35, 38), "ln": (49, 51)},
+    "wide": {"gemm": (39, 42), "gemm_k4": (40, 43), "score": (38, 41),
+             "pv": (34, 37), "gelu": (34, 37), "ln": (49, 51)},
+}
+
+
+@dataclass(frozen=True)
+class EncoderWorkload:
+    name: str
+    batch: int
+    grid_h: int
+    grid_w: int
+    dim: int
+    heads: int
+    head_dim: int
+    mlp_dim: int
+    # per block: (win_h, win_w); (0, 0) is global attention
+    windows: tuple = field(default_factory=tuple)
+
+    @property
+    def tokens(self) -> int:
+        return self.grid_h * self.grid_w
+
+    def gemm_ops(self) -> int:
+        """Algorithmic int8 ops (2*M*N*K) of one forward over all blocks: the
+        QKV, projection and MLP linears, plus Q K^T and P V per window."""
+        T, D, Hm, B = self.tokens, self.dim, self.mlp_dim, self.batch
+        linear = 2 * T * D * (3 * D + D + Hm + Hm)
+        ops = 0
+        for wh, ww in self.windows:
+            tw = T if wh == 0 else wh * ww
+            n_win = T // tw
+            attn = 2 * 2 * n_win * tw * tw * D  # QK^T and PV over all heads
+            ops += linear + attn
+        return ops * B
+
+
+@dataclass(frozen=True)
+class DeformWorkload:
+    name: str
+    batch: int
+    queries: int
+    dim: int
+    heads: int
+    head_dim: int
+    levels: tuple  # ((H, W), ...)
+    points: int
+
+
+def _alt(n, win):
+    """n blocks alternating window / global, window first."""
+    return tuple(win if i % 2 == 0 else (0, 0) for i in range(n))
+
+
+WORKLOADS = {
+    # one integer ViT block, 16x16 tokens, global attention
+    "block_t256_d192": EncoderWorkload("block_t256_d192", 1, 16, 16, 192, 3, 64,
+                                       768, ((0, 0),)),
+    # ViT-tiny-shaped encoder on 640x640 / patch 16, 6 blocks, 2x2 windows of
+    # 20x20 tokens alternating with global attention
+    "encoder_t1600_d192_b1": EncoderWorkload("encoder_t1600_d192_b1", 1, 40, 40,
+                                             192, 3, 64, 768, _alt(6, (20, 20))),
+    # medium-shaped encoder, 10 blocks, batch 8
+    "encoder_t1600_d384_b8": EncoderWorkload("encoder_t1600_d384_b8", 8, 40, 40,
+                                             384, 6, 64, 1536, _alt(10, (20, 20))),
+    # the tiny encoder at batch 32 (51200 tokens per layer)
+    "encoder_t1600_d192_b32": EncoderWorkload("encoder_t1600_d192_b32", 32, 40, 40,
+                                              192, 3, 64, 768, _alt(6, (20, 20))),
+}
+
+DEFORM_WORKLOADS = {
+    "deform_q300_d256_b8": DeformWorkload("deform_q300_d256_b8", 8, 300, 256, 8, 32,
+                                          ((80, 80), (40, 40), (20, 20)), 4),
+}
+
+# Config order of the five workloads (encoder block, tiny encoder, medium
+# encoder, tiny encoder at batch 32, deformable layer).
+CONFIG_ORDER = ["block_t256_d192", "encoder_t1600_d192_b1", "encoder_t1600_d384_b8",
+                "encoder_t1600_d192_b32", "deform_q300_d256_b8"]
+
+
+def _u(rng, lo, hi, shape=None, dtype=np.int32):
+    return rng.integers(lo, hi, size=shape, endpoint=True).astype(dtype)
+
+
+def _dy(rng, n, shift_range):
+    mult = _u(rng, 1 << 29, 1 << 30, n)
+    shift = _u(rng, shift_range[0], shift_range[1], n)
+    return mult, shift
+
+
+def block_params(rng: np.random.Generator, dim: int, heads: int, head_dim: int,
+                 mlp_dim: int, variant: str = "baseline", ln_iters: int = 10,
+                 smax_s_d: int = -1) -> dict:
+    """Parameters of one integer encoder block, drawn in struct order."""
+    sh = SHIFTS[variant]
+    D, Hm = dim, mlp_dim
+    p = {"dim": D, "heads": heads, "head_dim": head_dim, "mlp_dim": Hm,
+         "ln_iters": ln_iters}
+
+    def ln(prefix):
+        p[prefix + "_beta"] = _u(rng, -(1 << 26), 1 << 26, D)
+        mag = _u(rng, 1 << 29, 1 << 30, D)
+        sign = np.where(rng.integers(0, 8, size=D) == 0, -1, 1).astype(np.int32)
+        p[prefix + "_mult"] = (mag * sign).astype(np.int32)
+        p[prefix + "_shift"] = _u(rng, sh["ln"][0], sh["ln"][1], D)
+
+    def lin(prefix, n, k, rng_key):
+        p["w_" + prefix] = _u(rng, -127, 127, (n, k), np.int8)
+        p["b_" + prefix] = _u(rng, -(1 << 15), 1 << 15, n)
+        p[prefix + "_mult"], p[prefix + "_shift"] = _dy(rng, n, sh[rng_key])
+
+    ln("ln1")
+    lin("qkv", 3 * D, D, "gemm")
+    p["score_mult"], p["score_shift"] = (int(v[0]) for v in _dy(rng, 1, sh["score"]))
+    p["smax_I0"] = int(_u(rng, 8, 64))
+    p["smax_k_inter"], p["smax_k_out"], p["smax_m_p"] = 16, 8, 4
+    p["smax_s_d"] = smax_s_d
+    p["pv_mult"], p["pv_shift"] = (int(v[0]) for v in _dy(rng, 1, sh["pv"]))
+    lin("proj", D, D, "gemm")
+    p["res1_mult_a"] = int(_u(rng, 1 << 29, 1 << 30))
+    p["res1_mult_b"] = int(_u(rng, 1 << 29, 1 << 30))
+    p["res1_shift"] = 31
+    ln("ln2")
+    lin("fc1", Hm, D, "gemm")
+    p["gelu_I0"] = int(_u(rng, 8, 64))
+    p["gelu_k_inter"], p["gelu_k_out"] = 16, 8
+    p["gelu_mult"], p["gelu_shift"] = (int(v[0]) for v in _dy(rng, 1, sh["gelu"]))
+    lin("fc2", D, Hm, "gemm_k4")
+    p["res2_mult_a"] = int(_u(rng, 1 << 29, 1 << 30))
+    p["res2_mult_b"] = int(_u(rng, 1 << 29, 1 << 30))
+    p["res2_shift"] = 31
+    return p
+
+
+def encoder_inputs(wl: EncoderWorkload, seed: int, variant: str = "baseline",
+                   batch: int | None = None):
+    """Returns (list of block parameter dicts, int8 input [B, T, D])."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    blocks = [block_params(rng, wl.dim, wl.heads, wl.head_dim, wl.mlp_dim, variant)
+              for _ in wl.windows]
+    B = wl.batch if batch is None else batch
+    x = _u(rng, -127, 127, (B, wl.tokens, wl.dim), np.int8)
+    return blocks, x
+
+
+def deform_inputs(wl: DeformWorkload, seed: int, batch: int | None = None,
+                  queries: int | None = None) -> dict:
+    """Inputs of the deformable sampling core: value maps, Q16 reference
+    points, Q8 pixel offsets (+-8 px, so some samples leave the map), logits
+    over the L*P samples, and the output requantization."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    B = wl.batch if batch is None else batch
+    Q = wl.queries if queries is None else queries
+    L, P, H, Dh = len(wl.levels), wl.points, wl.heads, wl.head_dim
+    level_hw = np.array(wl.levels, np.int32).reshape(L, 2)
+    sizes = level_hw[:, 0] * level_hw[:, 1]
+    level_start = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int32)
+    S = int(sizes.sum())
+    d = {
+        "level_hw": level_hw,
+        "level_start": level_start,
+        "value": _u(rng, -127, 127, (B, S, H, Dh), np.int8),
+        "ref": _u(rng, 0, 65535, (B, Q, 2)),
+        "offsets": _u(rng, -2048, 2048, (B, Q, H, L, P, 2), np.int16),
+        "logits": _u(rng, -127, 127, (B, Q, H, L * P), np.int8),
+        "I0": 16,
+    }
+    d["out_mult"] = int(_u(rng, 1 << 29, 1 << 30))
+    d["out_shift"] = int(_u(rng, 33, 36))
+    return d
+
+
+def int8_tensor(seed: int, shape, lo: int = -127, hi: int = 127) -> np.ndarray:
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return _u(rng, lo, hi, shape, np.int8)

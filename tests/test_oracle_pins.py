@@ -1,0 +1,419 @@
+"""Pins of the CPU oracle to what the paper and mathematics fix.
+
+None of these re-run the oracle's own formula.  Each compares the oracle with
+something independent of it: hand-derived worked examples of the paper's
+algorithms (tests/golden), exact rational arithmetic, numpy / math / torch
+library routines, closed forms, error bounds derived from the algorithms, and
+invariants (budget, zero mean, translation and permutation invariance).
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+
+
+@pytest.fixture(scope="module")
+def golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def frac_requant(acc, m, s):
+    """Round-half-up of acc*m/2^s from exact rationals, saturated to int8."""
+    v = math.floor(Fraction(acc * m, 2 ** s) + Fraction(1, 2))
+    return max(-127, min(127, v))
+
+
+# ------------------------------------------------------------------ worked examples
+def test_worked_shiftexp(orc, golden):
+    for case in golden["shiftexp"]:
+        assert orc.shiftexp(case["I"], case["I0"], case["k_inter"]) == case["I_exp"], case
+
+
+def test_worked_shiftmax(orc, golden):
+    for case in golden["shiftmax"]:
+        out, (S_sum, s_d, S_R, F) = orc.shiftmax_row(case["x"], case["I0"], case["k_inter"],
+                                                     case["k_out"], case["m_p"], -1)
+        assert list(out) == case["out"], case
+        assert (S_sum, s_d, S_R, F) == (case["S_sum"], case["s_d"], case["S_R"], case["F"])
+
+
+def test_worked_sdshiftgelu(orc, golden):
+    for case in golden["sdshiftgelu"]:
+        assert orc.sdshiftgelu(case["x"], case["I0"], case["k_inter"],
+                               case["k_out"]) == case["I_out"], case
+
+
+def test_worked_newton_and_layernorm(orc, golden):
+    for case in golden["isqrt_newton"]:
+        assert orc.isqrt_newton(case["V"], case["iters"]) == case["sigma"], case
+    for case in golden["layernorm"]:
+        C = len(case["x"])
+        one = np.ones(C, np.int32)
+        for iters, key in ((10, "sigma_10"), (20, "sigma_20")):
+            _, (mean, V, sigma, F) = orc.int_layernorm_row(
+                case["x"], np.zeros(C), one * (1 << 30), one * 40, iters)
+            assert (mean, V, sigma) == (case["mean"], case["V"], case[key])
+            assert F == (2 ** 31 - 1) // sigma
+
+
+# ------------------------------------------------------------------ linear (O1, O2)
+def test_linear_acc_brute_force_python_ints(orc):
+    rng = np.random.default_rng(11)
+    for _ in range(40):
+        M, N, K = rng.integers(1, 9, size=3)
+        x = rng.integers(-127, 128, (M, K)).astype(np.int8)
+        w = rng.integers(-127, 128, (N, K)).astype(np.int8)
+        b = rng.integers(-2 ** 15, 2 ** 15 + 1, N).astype(np.int32)
+        acc = orc.linear_acc(x, w, b)
+        for m in range(M):
+            for n in range(N):
+                ref = int(b[n]) + sum(int(x[m, k]) * int(w[n, k]) for k in range(K))
+                assert acc[m, n] == ref
+
+
+def test_linear_acc_matches_numpy_matmul(orc):
+    rng = np.random.default_rng(12)
+    x = rng.integers(-127, 128, (37, 200)).astype(np.int8)
+    w = rng.integers(-127, 128, (50, 200)).astype(np.int8)
+    b = rng.integers(-2 ** 15, 2 ** 15 + 1, 50).astype(np.int32)
+    ref = x.astype(np.int64) @ w.astype(np.int64).T + b
+    assert np.array_equal(orc.linear_acc(x, w, b), ref)
+
+
+def test_requant_exact_rationals_random_and_ties(orc):
+    rng = np.random.default_rng(13)
+    for _ in range(3000):
+        s = int(rng.integers(1, 63))
+        m = int(rng.integers(-(2 ** 31) + 1, 2 ** 31))
+        acc = int(rng.integers(-(2 ** 25), 2 ** 25))
+        assert orc.requant(acc, m, s) == frac_requant(acc, m, s)
+    # exact ties acc*m == (2j+1) * 2^(s-1): both signs round toward +inf
+    for s in (1, 5, 30, 33, 38, 50):
+        e = min(s - 1, 30)
+        for j in range(-70, 70):
+            acc, m = (2 * j + 1) * 2 ** (s - 1 - e), 2 ** e
+            assert orc.requant(acc, m, s) == max(-127, min(127, j + 1)), (s, j)
+
+
+def test_linear_requant_matches_numpy_and_fractions(orc):
+    rng = np.random.default_rng(14)
+    M, N, K = 9, 24, 64
+    x = rng.integers(-127, 128, (M, K)).astype(np.int8)
+    w = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    b = rng.integers(-2 ** 15, 2 ** 15 + 1, N).astype(np.int32)
+    mult = rng.integers(2 ** 29, 2 ** 30 + 1, N).astype(np.int32)
+    shift = rng.integers(33, 41, N).astype(np.int32)
+    y = orc.linear(x, w, b, mult, shift)
+    acc = x.astype(np.int64) @ w.astype(np.int64).T + b
+    for m in range(M):
+        for n in range(N):
+            assert y[m, n] == frac_requant(int(acc[m, n]), int(mult[n]), int(shift[n]))
+    # per-tensor dyadic equals per-channel with repeated values
+    y1 = orc.linear(x, w, b, mult[:1], shift[:1])
+    yN = orc.linear(x, w, b, np.repeat(mult[:1], N), np.repeat(shift[:1], N))
+    assert np.array_equal(y1, yN)
+
+
+def test_residual_exact_rationals(orc):
+    rng = np.random.default_rng(15)
+    for _ in range(2000):
+        a, b = (int(v) for v in rng.integers(-127, 128, 2))
+        ma, mb = (int(v) for v in rng.integers(-(2 ** 31) + 1, 2 ** 31, 2))
+        s = int(rng.integers(1, 63))
+        ref = math.floor(Fraction(a * ma + b * mb, 2 ** s) + Fraction(1, 2))
+        assert orc.residual(a, b, ma, mb, s) == max(-127, min(127, ref))
+        assert orc.residual(a, b, ma, 0, s) == orc.requant(a, ma, s)
+
+
+# ------------------------------------------------------------------ ShiftExp (O4)
+def shiftexp_bounds(x_abs, I0):
+    """Relative error window of ShiftExp against exp, derived from Alg. 1:
+    I*log2(e) is taken as 1.4375*I with floor shifts (exponent off by
+    -0.0052|x| - 0.94/I0 .. +0.5/I0 in base 2), and 2^-f is replaced by
+    1 - f/2 with a floor of at most 1/(2 I0) (factor in [1 - 1/I0, 1.0616])."""
+    lo = (1 - 1 / I0) * 2 ** (0.005195 * x_abs - 0.5 / I0)
+    hi = 1.0616 * 2 ** (0.005195 * x_abs + 0.9375 / I0)
+    return lo, hi
+
+
+@pytest.mark.parametrize("I0", [8, 16, 64, 256, 1024])
+def test_shiftexp_error_bound_against_exp(orc, I0):
+    k = 16
+    for I in range(0, -10 * I0 - 1, -max(1, I0 // 64)):
+        x = I / I0
+        approx = orc.shiftexp(I, I0, k) / (I0 * 2 ** k)
+        ratio = approx / math.exp(x)
+        lo, hi = shiftexp_bounds(abs(x), I0)
+        assert lo - 1e-12 <= ratio <= hi + 1e-12, (I, I0, ratio, lo, hi)
+
+
+def test_shiftexp_closed_forms_and_monotone(orc):
+    for I0 in (1, 3, 16, 100, 8191):
+        assert orc.shiftexp(0, I0, 16) == I0 * 2 ** 16          # exp(0) = 1
+        assert orc.shiftexp(-(10 ** 6), I0, 16) == I0           # clip: 2^-16
+        prev = 0
+        for I in range(-40 * I0 - 5, 1, max(1, I0 // 50)):
+            e = orc.shiftexp(I, I0, 16)
+            assert e >= prev
+            prev = e
+    for k in (8, 12, 16, 20):
+        assert orc.shiftexp(0, 16, k) == 16 * 2 ** k
+
+
+# ------------------------------------------------------------------ Shiftmax (O5)
+def test_calibrate_shift_closed_form(orc):
+    # M_req = ceil(log2(S)): powers of two and their successors
+    for M in range(1, 45):
+        s_pow = 2 ** M
+        assert orc.calibrate_shift(s_pow, 4, 31) == max(M + 4 - 31, 0)
+        assert orc.calibrate_shift(s_pow + 1, 4, 31) == max(M + 1 + 4 - 31, 0)
+    assert orc.calibrate_shift(1, 4, 31) == 0
+    for S in (3, 1000, 10 ** 9, 5 * 10 ** 10):
+        assert orc.calibrate_shift(S, 4, 31) == max(math.ceil(math.log2(S)) + 4 - 31, 0)
+
+
+def float_softmax(x):
+    z = np.exp(x - x.max())
+    return z / z.sum()
+
+
+@pytest.mark.parametrize("d", [1, 2, 12, 64, 256, 400, 1600])
+def test_shiftmax_budget_and_identity(orc, d):
+    rng = np.random.default_rng(100 + d)
+    for _ in range(40 if d < 1000 else 8):
+        I0 = int(rng.integers(4, 8193))
+        x = rng.integers(-127, 128, d)
+        out, (S_sum, s_d, S_R, F) = orc.shiftmax_row(x, I0)
+        # quotient-remainder accumulation equals the exact shifted sum
+        assert S_R == max(1, min(2 ** 31 - 1, S_sum >> s_d))
+        tot = int(out.sum())
+        assert 0 <= out.min() and out.max() <= 127
+        assert tot <= 128 and (s_d > 0 or tot <= 127)
+        # dynamic s_d keeps S_R below 2^(31-m_p): the sum stays near 2^7
+        assert S_R <= 2 ** 27
+        assert tot >= (2 ** 31 - 1 - 2 ** 27) / 2 ** 24 - d - 1
+
+
+@pytest.mark.parametrize("I0", [16, 64, 256])
+def test_shiftmax_against_float_softmax(orc, I0):
+    rng = np.random.default_rng(7 + I0)
+    for d in (4, 12, 64, 400):
+        for _ in range(10):
+            # logits within |x| <= 10 in real units so ShiftExp is unclipped
+            span = min(127, 5 * I0)
+            x = rng.integers(-span, span + 1, d)
+            out, _ = orc.shiftmax_row(x, I0)
+            p = float_softmax(x / I0)
+            lo, hi = shiftexp_bounds(span * 2 / I0, I0)
+            rel = hi / shiftexp_bounds(0, I0)[0] - 1
+            assert np.all(np.abs(out / 128 - p) <= rel * p + 2 / 128), (d, I0)
+
+
+def test_shiftmax_invariances(orc):
+    rng = np.random.default_rng(21)
+    for _ in range(50):
+        d = int(rng.integers(1, 300))
+        I0 = int(rng.integers(4, 200))
+        x = rng.integers(-100, 101, d)
+        out, _ = orc.shiftmax_row(x, I0)
+        c = int(rng.integers(-27, 27))
+        assert np.array_equal(orc.shiftmax_row(x + c, I0)[0], out)        # shift
+        perm = rng.permutation(d)
+        assert np.array_equal(orc.shiftmax_row(x[perm], I0)[0], out[perm])  # permute
+        order = np.argsort(x, kind="stable")
+        assert np.all(np.diff(out[order]) >= 0)                            # monotone
+
+
+def test_shiftmax_uniform_rows_closed_form(orc):
+    for d in (1, 2, 3, 12, 100, 1600):
+        for I0 in (8, 16, 64):
+            out, _ = orc.shiftmax_row(np.full(d, 5), I0)
+            assert len(set(out.tolist())) == 1
+            assert math.floor(128 / d) - 1 <= out[0] <= math.floor(128 / d)
+
+
+def test_shiftmax_reduces_to_ivit_when_sd_zero(orc):
+    """With s_d = 0 and S_sum within 31 bits the constrained form is the fixed
+    M = 31 Shiftmax of I-ViT (eq. shiftmax_original), written here with exact
+    Python integers from that equation."""
+    rng = np.random.default_rng(22)
+    seen = 0
+    for _ in range(200):
+        d = int(rng.integers(1, 64))
+        I0 = int(rng.integers(2, 64))
+        x = rng.integers(-127, 128, d)
+        out, (S_sum, s_d, _, _) = orc.shiftmax_row(x, I0)
+        if s_d != 0:
+            continue
+        seen += 1
+        e = [orc.shiftexp(int(v) - int(x.max()), I0, 16) for v in x]
+        factor = (2 ** 31 - 1) // sum(e)
+        ref = [(factor * ei) >> (31 - 7) for ei in e]
+        assert list(out) == ref
+    assert seen > 50
+
+
+def test_ivit_shiftmax_collapses_where_constrained_does_not(orc):
+    """The failure the paper describes: once S_sum exceeds 2^31 - 1 the fixed
+    M = 31 factor floor((2^31-1)/S_sum) is 0 and every output collapses, while
+    the shifted denominator keeps the row on its 2^7 budget.  Eight equal
+    maxima (each 2^29 at I0 = 8192) and 1592 clipped entries: the exact
+    softmax puts 1/8 on each maximum, i.e. 16 at scale 2^-7."""
+    d, I0 = 1600, 8192
+    x = np.full(d, -10 ** 6, np.int32)
+    x[:8] = 0
+    assert orc.shiftmax_ivit_row(x, I0).max() == 0
+    out, (S_sum, s_d, _, _) = orc.shiftmax_row(x, I0)
+    assert S_sum > 2 ** 31 and s_d > 0
+    assert list(out[:8]) == [15] * 8 or list(out[:8]) == [16] * 8
+    assert out[8:].max() == 0
+
+
+def test_shiftmax_static_sd_equals_dynamic_when_equal(orc):
+    rng = np.random.default_rng(23)
+    for _ in range(40):
+        x = rng.integers(-127, 128, 400)
+        I0 = int(rng.integers(64, 4096))
+        out, (_, s_d, _, _) = orc.shiftmax_row(x, I0)
+        out2, _ = orc.shiftmax_row(x, I0, s_d=s_d)
+        assert np.array_equal(out, out2)
+
+
+# ------------------------------------------------------------------ IntDiv, GELU (O6, O7)
+def test_intdiv_against_exact_ratio(orc):
+    rng = np.random.default_rng(31)
+    for _ in range(3000):
+        b = int(rng.integers(1, 2 ** 23))
+        a = int(rng.integers(0, b + 1))
+        v = orc.intdiv(a, b, 8)
+        exact = math.floor(Fraction(128 * a, b))
+        assert exact - 1 <= v <= exact
+    for I0 in (8, 16, 32, 64):
+        b = 2 * I0 * 2 ** 16
+        assert orc.intdiv(b // 2, b, 8) == 63
+
+
+def gelu_ref(x):
+    return x / (1 + math.exp(-1.702 * x))
+
+
+@pytest.mark.parametrize("I0", [8, 16, 32, 64])
+def test_sdshiftgelu_against_float_gelu_exhaustive(orc, I0):
+    """All 255 int8 inputs.  Error budget of the integer sigmoid: 1.702 taken
+    as 1.6875 (|dz| <= 0.0145|x|), ShiftExp's relative window, the IntDiv floor
+    (1/128), and floor shifts of I_p (<= 3/I0 in the argument)."""
+    S = 1 / I0
+    for x in range(-127, 128):
+        v = orc.sdshiftgelu(x, I0) * S / 128
+        xr = x * S
+        lo, hi = shiftexp_bounds(1.6875 * abs(xr), I0)
+        eta = max(hi - 1, 1 - lo)
+        tol_sigma = 0.25 * (0.0145 * abs(xr) + 3 * S) + 0.275 * eta + 2 / 128
+        assert abs(v - gelu_ref(xr)) <= abs(xr) * tol_sigma + 1e-12, (x, I0)
+
+
+def test_sdshiftgelu_sign_and_monotone(orc):
+    for I0 in range(4, 132):
+        outs = [orc.sdshiftgelu(x, I0) for x in range(-127, 128)]
+        assert outs[127] == 0
+        for x, o in zip(range(-127, 128), outs):
+            assert o == 0 or (o > 0) == (x > 0)
+        pos = outs[127:]
+        assert all(b >= a for a, b in zip(pos, pos[1:]))
+
+
+def test_sdshiftgelu_equals_ivit_when_vector_max_is_zero(orc):
+    """On a vector whose maximum 1.702-scaled input is 0, subtracting the
+    vector maximum (I-ViT) and subtracting ReLU(I_p) (SD-ShiftGELU) coincide."""
+    for I0 in (8, 16, 64):
+        for x in range(-127, 1):
+            assert orc.sdshiftgelu(x, I0) == orc.ivit_shiftgelu(x, 0, I0)
+
+
+# ------------------------------------------------------------------ LayerNorm (O8)
+def test_newton_against_math_isqrt(orc):
+    # converged: floor(sqrt(V)), or floor+1 exactly when V+1 is a perfect square
+    for V in list(range(1, 5000)) + list(range(2 ** 20, 2 ** 20 + 3000)):
+        r = math.isqrt(V)
+        s = orc.isqrt_newton(V, 20)
+        if math.isqrt(V + 1) ** 2 == V + 1:
+            assert s in (r, r + 1), V
+        else:
+            assert s == r, V
+    rng = np.random.default_rng(41)
+    for V in rng.integers(2 ** 18, 2 ** 30, 2000):
+        r = math.isqrt(int(V))
+        assert orc.isqrt_newton(int(V), 10) in (r, r + 1)
+    # Newton from above never undershoots floor(sqrt(V))
+    for V in rng.integers(1, 2 ** 26, 2000):
+        for it in (1, 5, 10):
+            assert orc.isqrt_newton(int(V), it) >= math.isqrt(int(V))
+
+
+def ln_float(x, beta, mult, shift):
+    C = x.shape[0]
+    z = (x - x.mean()) / x.std()
+    n = z * 2 ** 30 / math.sqrt(C)
+    return np.clip((n + beta) * mult / 2.0 ** shift, -127, 127)
+
+
+def test_layernorm_properties(orc):
+    rng = np.random.default_rng(42)
+    for C in (8, 64, 192, 384):
+        for _ in range(20):
+            x = rng.integers(-100, 101, C).astype(np.int8)
+            beta = rng.integers(-(2 ** 26), 2 ** 26, C).astype(np.int32)
+            mult = (rng.integers(2 ** 29, 2 ** 30, C) *
+                    rng.choice([-1, 1], C)).astype(np.int32)
+            shift = rng.integers(52, 55, C).astype(np.int32)
+            y, (mean, V, sigma, F) = orc.int_layernorm_row(x, beta, mult, shift, 10)
+            s = int(x.astype(np.int64).sum())
+            assert abs(s - C * mean) * 2 <= C                          # zero mean
+            assert V == int(((x.astype(np.int64) - mean) ** 2).sum())
+            # translation invariance (the mean absorbs the shift)
+            c = int(rng.integers(-20, 21))
+            y2, _ = orc.int_layernorm_row((x + c).astype(np.int8), beta, mult, shift, 10)
+            assert np.array_equal(y, y2)
+            # Newton's estimate never undershoots floor(sqrt(V)); converged
+            # when V is large enough for ten steps from 2^16
+            assert sigma >= math.isqrt(V)
+            # normalization against float arithmetic with the same sigma:
+            # n = (x - mean) * 2^30 / sigma up to the rounded mean (0.5 in y)
+            # and two floors, then the dyadic output scale and one rounding
+            xf = x.astype(np.float64)
+            n_ref = (xf - xf.mean()) * 2.0 ** 30 / sigma
+            ref = np.clip((n_ref + beta) * mult / 2.0 ** shift, -127, 127)
+            amp = np.abs(mult) / 2.0 ** shift
+            tol = 1.0 + amp * (0.5 * 2.0 ** 30 / sigma + 2)
+            assert np.all(np.abs(y - ref) <= tol), (C, np.abs(y - ref).max())
+            # and the float LayerNorm itself once Newton has converged
+            if V >= 2 ** 18:
+                assert sigma in (math.isqrt(V), math.isqrt(V) + 1)
+                lnf = ln_float(xf, beta, mult, shift)
+                z = np.abs(xf - xf.mean()) / xf.std()
+                amp2 = amp * 2.0 ** 30 / math.sqrt(C)
+                tol2 = 1.0 + amp2 * (0.5 / xf.std() + z * 2.0 / sigma)
+                assert np.all(np.abs(y - lnf) <= tol2)
+
+
+def test_layernorm_constant_row_and_per_tensor(orc):
+    rng = np.random.default_rng(43)
+    C = 192
+    beta = rng.integers(-(2 ** 26), 2 ** 26, C).astype(np.int32)
+    mult = rng.integers(2 ** 29, 2 ** 30, C).astype(np.int32)
+    shift = rng.integers(30, 40, C).astype(np.int32)
+    for val in (-127, 0, 5, 127):
+        y, (_, V, sigma, _) = orc.int_layernorm_row(np.full(C, val), beta, mult, shift)
+        assert V == 0 and sigma == 0
+        ref = [frac_requant(int(beta[i]), int(mult[i]), int(shift[i])) for i in range(C)]
+        assert list(y) == ref
+    x = rng.integers(-127, 128, C).astype(np.int8)
+    y1, _ = orc.int_layernorm_row(x, beta, mult[:1], shift[:1])
+    yC, _ = orc.int_layernorm_row(x, beta, np.repeat(mult[:1], C), np.repeat(shift[:1], C))
+    assert np.array_equal(y1, yC)
