@@ -1,0 +1,228 @@
+/*
+ * ilw.h -- C ABI of libilw.so: the integer-only I-LW-DETR encoder block and
+ * deformable sampling on AMD Instinct MI355X (gfx950).
+ *
+ * Operators follow "Enabling Fully Integer-Only Inference for Lightweight
+ * Detection Transformers" (I-LW-DETR).  Every tensor is an integer tensor;
+ * float scales exist only offline, folded into the integer constants passed
+ * here (I0 = round(1/S) for ShiftExp, dyadic multiplier/shift pairs for every
+ * rescale).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     never allocates, frees or retains them.  Small descriptor arrays that
+ *     are documented as HOST arrays are read before the call returns.
+ *   - Layouts are row-major with the channel dimension contiguous.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL is the default
+ *     stream) and perform no implicit synchronization.
+ *   - Return ILW_OK (0) or a negative ilw_status.  Argument errors are found
+ *     on the host BEFORE anything is launched, and the output is then left
+ *     untouched; ilw_last_error() gives the reason.  Kernel faults surface at
+ *     the caller's next synchronization.  Launch failures return ILW_E_HIP.
+ *   - Rescaling is dyadic: y = sat8(floor((acc * mult + 2^(shift-1)) / 2^shift))
+ *     (round half up), sat8 clamps to the symmetric int8 range [-127, 127].
+ *   - int8 tensors and weights must be 16-byte aligned and their row lengths
+ *     multiples of 16 where stated.
+ *   - Thread-safe: the only global state is a thread-local error string.
+ */
+#ifndef ILW_H
+#define ILW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ILW_ABI_VERSION 1
+
+typedef enum {
+  ILW_OK = 0,
+  ILW_E_NULL = -1,        /* a required pointer is NULL                    */
+  ILW_E_SHAPE = -2,       /* sizes inconsistent or not positive             */
+  ILW_E_PARAM = -3,       /* a scalar parameter is out of its range         */
+  ILW_E_UNSUPPORTED = -4, /* valid but outside what the kernels implement   */
+  ILW_E_WORKSPACE = -5,   /* workspace missing or smaller than required     */
+  ILW_E_HIP = -6          /* the HIP runtime reported an error              */
+} ilw_status;
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char* ilw_last_error(void);
+/* ILW_ABI_VERSION of the loaded library. */
+int ilw_abi_version(void);
+
+/* Dyadic rescale factors as DEVICE arrays of n entries: n == 1 applies one
+ * factor to every channel (per-tensor), n == channels one per channel
+ * (per-channel weights, Sec. 3.2.1).  mult is any int32 except INT32_MIN
+ * (negative values are allowed where gamma folds in), shift in [1, 62];
+ * device-side values are the caller's responsibility. */
+typedef struct {
+  const int32_t* mult;
+  const int32_t* shift;
+  int32_t n;
+} ilw_dyadic;
+
+/* ------------------------------------------------------------------------
+ * Integer linear layer with dyadic requantization (Sec. 3.2.1, eq.
+ * linear_quant: integer multiply-accumulate, scales applied after it; Sec.
+ * 3.2.2: rescale by dyadic multiply-and-shift).
+ *   y[m][n] = sat8(rq(b[n] + sum_k x[m][k] * w[n][k]; rq.mult[n], rq.shift[n]))
+ * x int8 [M, K], w int8 [N, K], b int32 [N] (may be NULL: zero bias),
+ * y int8 [M, N].  K and N multiples of 16; M >= 0 (M == 0 is a no-op).
+ * The accumulator must fit int32 (K * 127^2 + |b| < 2^31).  y must not alias x.
+ */
+int ilw_linear(const int8_t* x, const int8_t* w, const int32_t* b, ilw_dyadic rq,
+               int8_t* y, int64_t M, int32_t N, int32_t K, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Constrained Shiftmax (Sec. 3.3.2, Alg. 2) over `rows` contiguous rows of
+ * `cols` int8 scores each.  I0 = round(1/S_x) in [1, 2^14 - 1]; k_inter in
+ * [1, 16] (16 in the paper's 8/8/16 setting); k_out in [2, 8]; m_p in [0, 31]
+ * (the paper uses 4); the hardware division precision is fixed to 31.
+ * s_d >= 0 uses that calibrated denominator shift for every row (the text
+ * calibrates one s_d per Shiftmax block); s_d == -1 derives it per row from
+ * the row's exponential sum (CalibrateShift as in the algorithm listing).
+ * Output in [0, 2^(k_out-1) - 1] with scale 2^-(k_out-1); a value that would
+ * reach 2^(k_out-1) (possible only with an oversized static s_d) is limited
+ * to 2^(k_out-1) - 1 because the output is a signed k_out-bit integer.
+ * y may alias x.  cols in [1, 65536].
+ */
+int ilw_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
+                 int32_t k_inter, int32_t k_out, int32_t m_p, int32_t s_d,
+                 void* stream);
+
+/* ------------------------------------------------------------------------
+ * SD-ShiftGELU (Sec. 3.3.1, Alg. 1) element-wise over n int8 values, then the
+ * dyadic requantization of I_out = I_x * I_div (scale S_x * 2^-(k_out-1)) to
+ * the int8 activation of the next layer:  y = sat8(rq(I_out; out_mult,
+ * out_shift)).  IntDiv, which the algorithm uses without a definition, is the
+ * fixed-precision integer division of eq. shiftmax_original with M = 31.
+ * I0 in [1, 2^14 - 1], k_inter in [1, 16], k_out in [2, 8], out_shift in
+ * [1, 62].  y may alias x.
+ */
+int ilw_sdshiftgelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
+                    int32_t k_inter, int32_t k_out, int32_t out_mult,
+                    int32_t out_shift, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Integer LayerNorm (Sec. 3.3: I-ViT's formulation with an integer square
+ * root by Newton's method; 10 iterations, 20 for the decoder) over `rows`
+ * rows of C int8 channels:
+ *   mu = floor((2*sum x + C) / (2C));  y_i = x_i - mu;  V = sum y_i^2
+ *   sigma: k <- floor((k + floor(V/k)) / 2), newton_iters times from k = 2^16
+ *   n_i = floor(y_i * floor((2^31 - 1) / sigma) / 2)     (0 when V == 0)
+ *   out_i = sat8(rq(n_i + beta_i; out.mult_i, out.shift_i))
+ * gamma is folded into the (signed) output multiplier; beta int32 [C] is at
+ * the scale of n (DEVICE array).  C in [4, 16384], a multiple of 4;
+ * newton_iters in [1, 64].  y may alias x.
+ */
+int ilw_int_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
+                      const int32_t* beta, ilw_dyadic out, int32_t newton_iters,
+                      void* stream);
+
+/* ------------------------------------------------------------------------
+ * Two-input dyadic add onto one output scale (Sec. 3.2.2: branches rescaled
+ * to a common scale by dyadic multiply-and-shift and summed in integers); the
+ * residual connection of the encoder block:
+ *   y = sat8(floor((a * mult_a + b * mult_b + 2^(shift-1)) / 2^shift))
+ * a, b, y int8 [n]; shift in [1, 62].  y may alias a or b.
+ */
+int ilw_residual_add(const int8_t* a, const int8_t* b, int8_t* y, int64_t n,
+                     int32_t mult_a, int32_t mult_b, int32_t shift, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Integer multi-head attention over window or global token groups: per
+ * window and head, S = Q K^T (int32) -> per-tensor dyadic -> int8 scores;
+ * P = Constrained Shiftmax of each score row; O = P V (int32) -> per-tensor
+ * dyadic -> int8, heads concatenated (the encoder's MatMul and Softmax
+ * operators, Table ablation_study; Sec. 3.2.1 and Sec. 3.3.2).
+ *   qkv int8 [batch, grid_h*grid_w, 3*dim]: q | k | v, head h at columns
+ *       h*head_dim .. of each part.
+ *   out int8 [batch, grid_h*grid_w, dim].
+ * win_h == win_w == 0 selects global attention; otherwise win_h x win_w
+ * windows tile the grid (LW-DETR's window attention).  head_dim == 64;
+ * dim == heads * 64; tokens per window in [1, 2048].  The workspace
+ * (ilw_attention_workspace_bytes) holds the window-major Q, K and V^T copies.
+ */
+typedef struct {
+  int32_t score_mult, score_shift;  /* S -> int8 scores (folds 1/sqrt(d_h)) */
+  int32_t I0, k_inter, k_out, m_p, s_d; /* Constrained Shiftmax, as above   */
+  int32_t pv_mult, pv_shift;        /* P V -> int8                          */
+} ilw_attn_params;
+
+size_t ilw_attention_workspace_bytes(int32_t batch, int32_t grid_h, int32_t grid_w,
+                                     int32_t win_h, int32_t win_w, int32_t dim);
+int ilw_attention(const int8_t* qkv, int8_t* out, int32_t batch, int32_t grid_h,
+                  int32_t grid_w, int32_t win_h, int32_t win_w, int32_t dim,
+                  int32_t heads, int32_t head_dim, const ilw_attn_params* ap,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * One integer pre-LayerNorm ViT encoder block (the encoder operators of
+ * Table ablation_study in the plain-ViT order):
+ *   h = LN1(x);  a = Attn(QKV(h));  x1 = Res(proj(a), x)
+ *   h2 = LN2(x1); g = rq(SD-ShiftGELU(fc1(h2)));  y = Res(fc2(g), x1)
+ * Weights are int8 [out, in] with int32 biases and per-channel dyadic
+ * requantization (Sec. 3.2.1); every activation between operators is int8.
+ * All pointers in the struct are DEVICE pointers; the struct itself is read
+ * on the host during the call.  Residuals: y = sat8(rq2(branch * mult_a +
+ * skip * mult_b; shift)).  dim and mlp_dim multiples of 16, head_dim == 64.
+ */
+typedef struct {
+  int32_t dim, heads, head_dim, mlp_dim, ln_iters;
+  const int32_t* ln1_beta; ilw_dyadic ln1_out;
+  const int8_t* w_qkv; const int32_t* b_qkv; ilw_dyadic qkv;   /* [3*dim, dim] */
+  ilw_attn_params attn;
+  const int8_t* w_proj; const int32_t* b_proj; ilw_dyadic proj; /* [dim, dim]  */
+  int32_t res1_mult_a, res1_mult_b, res1_shift;
+  const int32_t* ln2_beta; ilw_dyadic ln2_out;
+  const int8_t* w_fc1; const int32_t* b_fc1; ilw_dyadic fc1;   /* [mlp, dim]   */
+  int32_t gelu_I0, gelu_k_inter, gelu_k_out, gelu_mult, gelu_shift;
+  const int8_t* w_fc2; const int32_t* b_fc2; ilw_dyadic fc2;   /* [dim, mlp]   */
+  int32_t res2_mult_a, res2_mult_b, res2_shift;
+} ilw_block_params;
+
+/* Bytes of caller-owned device workspace ilw_block_forward needs (0 on
+ * invalid arguments, with ilw_last_error set). */
+size_t ilw_block_workspace_bytes(const ilw_block_params* p, int32_t batch,
+                                 int32_t grid_h, int32_t grid_w, int32_t win_h,
+                                 int32_t win_w);
+/* x, y int8 [batch, grid_h*grid_w, dim]; y may alias x (x is last read
+ * before y is first written, in stream order).  The workspace must not
+ * alias x or y. */
+int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y,
+                      int32_t batch, int32_t grid_h, int32_t grid_w, int32_t win_h,
+                      int32_t win_w, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
+/* ------------------------------------------------------------------------
+ * Multi-scale deformable sampling core of the decoder's cross-attention
+ * (Sec. 3.1.1: bilinear interpolation replaced by nearest-neighbour
+ * sampling; the attention weights come from Constrained Shiftmax, Sec. 3.3.2):
+ *   value   int8  [B, S, heads, head_dim], the L levels stacked, level l at
+ *           rows level_start[l] .. + H_l*W_l (row-major y, x)
+ *   level_hw    HOST int32 [L][2] = (H_l, W_l), each in [1, 32767]
+ *   level_start HOST int32 [L];  S = sum H_l*W_l
+ *   ref     int32 [B, Q, 2]  reference point (x, y), Q16 fraction of the map
+ *   offsets int16 [B, Q, heads, L, P, 2]  (x, y) in Q8 pixels of level l
+ *   logits  int8  [B, Q, heads, L*P] -> Constrained Shiftmax per (b, q, h)
+ *           with I0, k_inter = 16, k_out = 8, m_p = 4, s_d (as ilw_shiftmax)
+ *   out     int8  [B, Q, heads*head_dim] = sat8(rq(sum_{l,p} P * sample))
+ * Location: X = floor(ref_x * W_l / 2^8) + off_x (Q8), pixel ix = floor(X/2^8);
+ * samples outside the map contribute 0.  mode 0 = nearest (the paper);
+ * mode 1 = a fixed-point bilinear variant on the half-pixel grid with Q8
+ * weights whose 2^16 scale is removed by 16 extra bits of out_shift.
+ * head_dim a multiple of 4 in [4, 256]; L in [1, 8]; L*P in [1, 64].
+ */
+int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
+                    const int32_t* level_start, int32_t L, int32_t P,
+                    const int32_t* ref, const int16_t* offsets, const int8_t* logits,
+                    int8_t* out, int32_t B, int32_t Q, int32_t heads, int32_t head_dim,
+                    int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
+                    int32_t mode, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ILW_H */

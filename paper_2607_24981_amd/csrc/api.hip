@@ -1,0 +1,515 @@
+// api.hip -- the C ABI of libilw.so (declared in include/ilw.h): argument
+// validation on the host before anything is launched, workspace layout, and
+// kernel launches on the caller's stream.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "ilw_internal.h"
+
+using namespace ilw;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return ILW_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(ILW_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#define REQUIRE(cond, code, ...)            \
+  do {                                      \
+    if (!(cond)) return fail(code, __VA_ARGS__); \
+  } while (0)
+
+int check_dyadic(const ilw_dyadic& d, int32_t channels, const char* name) {
+  REQUIRE(d.mult && d.shift, ILW_E_NULL, "%s: mult/shift must not be NULL", name);
+  REQUIRE(d.n == 1 || d.n == channels, ILW_E_SHAPE,
+          "%s: n = %d must be 1 (per-tensor) or %d (per-channel)", name, d.n, channels);
+  return ILW_OK;
+}
+
+int check_shift(int32_t s, const char* name) {
+  REQUIRE(s >= 1 && s <= 62, ILW_E_PARAM, "%s = %d must be in [1, 62]", name, s);
+  return ILW_OK;
+}
+
+int check_mult(int32_t m, const char* name) {
+  REQUIRE(m != INT32_MIN, ILW_E_PARAM, "%s must not be INT32_MIN", name);
+  return ILW_OK;
+}
+
+int check_shiftmax(int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p, int32_t s_d) {
+  REQUIRE(I0 >= 1 && I0 < (1 << 14), ILW_E_PARAM, "I0 = %d must be in [1, 2^14 - 1]", I0);
+  REQUIRE(k_inter >= 1 && k_inter <= 16, ILW_E_PARAM, "k_inter = %d must be in [1, 16]",
+          k_inter);
+  REQUIRE(k_out >= 2 && k_out <= 8, ILW_E_PARAM, "k_out = %d must be in [2, 8]", k_out);
+  REQUIRE(m_p >= 0 && m_p <= 31, ILW_E_PARAM, "m_p = %d must be in [0, 31]", m_p);
+  REQUIRE(s_d >= -1 && s_d <= 31, ILW_E_PARAM, "s_d = %d must be -1 or in [0, 31]", s_d);
+  return ILW_OK;
+}
+
+int check_gelu(int32_t I0, int32_t k_inter, int32_t k_out, int32_t mult, int32_t shift) {
+  REQUIRE(I0 >= 1 && I0 < (1 << 14), ILW_E_PARAM, "GELU I0 = %d must be in [1, 2^14 - 1]",
+          I0);
+  REQUIRE(k_inter >= 1 && k_inter <= 16, ILW_E_PARAM, "GELU k_inter = %d must be in [1, 16]",
+          k_inter);
+  REQUIRE(k_out >= 2 && k_out <= 8, ILW_E_PARAM, "GELU k_out = %d must be in [2, 8]", k_out);
+  int e;
+  if ((e = check_mult(mult, "GELU out_mult"))) return e;
+  return check_shift(shift, "GELU out_shift");
+}
+
+// Geometry of window or global attention over a grid.
+struct Geometry {
+  int32_t T, nwx, nW, wh, ww, Tw, Twp;
+};
+
+int check_geometry(int32_t batch, int32_t gh, int32_t gw, int32_t wh, int32_t ww,
+                   Geometry* g) {
+  REQUIRE(batch >= 0, ILW_E_SHAPE, "batch = %d must be >= 0", batch);
+  REQUIRE(gh >= 1 && gw >= 1, ILW_E_SHAPE, "grid %dx%d must be positive", gh, gw);
+  REQUIRE((int64_t)gh * gw <= (1 << 24), ILW_E_SHAPE, "grid %dx%d too large", gh, gw);
+  if (wh == 0 && ww == 0) {
+    wh = gh;
+    ww = gw;
+  }
+  REQUIRE(wh >= 1 && ww >= 1 && gh % wh == 0 && gw % ww == 0, ILW_E_SHAPE,
+          "window %dx%d must tile the %dx%d grid", wh, ww, gh, gw);
+  g->T = gh * gw;
+  g->wh = wh;
+  g->ww = ww;
+  g->nwx = gw / ww;
+  g->nW = (gh / wh) * g->nwx;
+  g->Tw = wh * ww;
+  REQUIRE(g->Tw <= 2048, ILW_E_UNSUPPORTED, "%d tokens per window exceed the 2048 limit",
+          g->Tw);
+  REQUIRE((int64_t)batch * g->nW <= 65535, ILW_E_UNSUPPORTED,
+          "batch * windows = %lld exceeds 65535", (long long)batch * g->nW);
+  g->Twp = (g->Tw + 63) & ~63;
+  return ILW_OK;
+}
+
+int check_attn(const ilw_attn_params* ap) {
+  REQUIRE(ap, ILW_E_NULL, "attention parameters must not be NULL");
+  int e;
+  if ((e = check_mult(ap->score_mult, "score_mult"))) return e;
+  if ((e = check_shift(ap->score_shift, "score_shift"))) return e;
+  if ((e = check_mult(ap->pv_mult, "pv_mult"))) return e;
+  if ((e = check_shift(ap->pv_shift, "pv_shift"))) return e;
+  return check_shiftmax(ap->I0, ap->k_inter, ap->k_out, ap->m_p, ap->s_d);
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Window-major Q/K/V^T buffers carved from a workspace.
+size_t qkv_bytes(int32_t batch, const Geometry& g, int32_t D, QkvLayout* L, int8_t* base) {
+  const int32_t H = D / 64;
+  const size_t qk = (size_t)batch * g.nW * H * g.Tw * 64;
+  const size_t vt = (size_t)batch * g.nW * H * 64 * g.Twp;
+  if (L) {
+    L->q = base;
+    L->k = base + align256(qk);
+    L->vt = base + 2 * align256(qk);
+    L->T = g.T;
+    L->D = D;
+    L->H = H;
+    L->grid_w = g.nwx * g.ww;
+    L->win_h = g.wh;
+    L->win_w = g.ww;
+    L->nwx = g.nwx;
+    L->nW = g.nW;
+    L->Tw = g.Tw;
+    L->Twp = g.Twp;
+  }
+  return 2 * align256(qk) + align256(vt);
+}
+
+AttnArgs attn_args(const QkvLayout& L, int8_t* out, int32_t batch,
+                   const ilw_attn_params& ap) {
+  AttnArgs a;
+  a.q = L.q;
+  a.k = L.k;
+  a.vt = L.vt;
+  a.out = out;
+  a.B = batch;
+  a.T = L.T;
+  a.D = L.D;
+  a.H = L.H;
+  a.grid_w = L.grid_w;
+  a.win_h = L.win_h;
+  a.win_w = L.win_w;
+  a.nwx = L.nwx;
+  a.nW = L.nW;
+  a.Tw = L.Tw;
+  a.Twp = L.Twp;
+  a.score_mult = ap.score_mult;
+  a.score_shift = ap.score_shift;
+  a.I0 = ap.I0;
+  a.k_inter = ap.k_inter;
+  a.k_out = ap.k_out;
+  a.m_p = ap.m_p;
+  a.s_d = ap.s_d;
+  a.pv_mult = ap.pv_mult;
+  a.pv_shift = ap.pv_shift;
+  return a;
+}
+
+GemmArgs gemm_args(const int8_t* x, const int8_t* w, const int32_t* b, const ilw_dyadic& d,
+                   int8_t* y, int64_t M, int32_t N, int32_t K) {
+  GemmArgs a = {};
+  a.x = x;
+  a.w = w;
+  a.bias = b;
+  a.mult = d.mult;
+  a.shift = d.shift;
+  a.nq = d.n;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.y = y;
+  return a;
+}
+
+struct BlockLayout {
+  QkvLayout qkv;
+  int8_t *h, *att, *x1, *g;
+  size_t total;
+};
+
+size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
+                    int8_t* base, BlockLayout* out) {
+  const size_t M = (size_t)batch * g.T;
+  size_t off = 0;
+  BlockLayout L;
+  L.h = base + off;
+  off += align256(M * p->dim);
+  size_t q = qkv_bytes(batch, g, p->dim, &L.qkv, base + off);
+  off += q;
+  L.att = base + off;
+  off += align256(M * p->dim);
+  L.x1 = base + off;
+  off += align256(M * p->dim);
+  L.g = base + off;
+  off += align256(M * p->mlp_dim);
+  L.total = off;
+  if (out) *out = L;
+  return off;
+}
+
+int check_block(const ilw_block_params* p, int32_t batch, int32_t gh, int32_t gw,
+                int32_t wh, int32_t ww, Geometry* g) {
+  REQUIRE(p, ILW_E_NULL, "block parameters must not be NULL");
+  REQUIRE(p->head_dim == 64, ILW_E_UNSUPPORTED, "head_dim = %d: only 64 is implemented",
+          p->head_dim);
+  REQUIRE(p->heads >= 1 && p->dim == p->heads * p->head_dim, ILW_E_SHAPE,
+          "dim = %d must equal heads (%d) * head_dim", p->dim, p->heads);
+  REQUIRE(p->dim % 16 == 0 && p->mlp_dim >= 16 && p->mlp_dim % 16 == 0, ILW_E_SHAPE,
+          "dim = %d and mlp_dim = %d must be multiples of 16", p->dim, p->mlp_dim);
+  REQUIRE(p->mlp_dim <= 65536 && p->dim <= 16384, ILW_E_UNSUPPORTED,
+          "dim/mlp_dim too large");
+  REQUIRE(p->ln_iters >= 1 && p->ln_iters <= 64, ILW_E_PARAM,
+          "ln_iters = %d must be in [1, 64]", p->ln_iters);
+  REQUIRE(p->ln1_beta && p->ln2_beta, ILW_E_NULL, "LayerNorm beta must not be NULL");
+  REQUIRE(p->w_qkv && p->w_proj && p->w_fc1 && p->w_fc2, ILW_E_NULL,
+          "weights must not be NULL");
+  REQUIRE(aligned16(p->w_qkv) && aligned16(p->w_proj) && aligned16(p->w_fc1) &&
+              aligned16(p->w_fc2),
+          ILW_E_PARAM, "weights must be 16-byte aligned");
+  int e;
+  if ((e = check_dyadic(p->ln1_out, p->dim, "ln1_out"))) return e;
+  if ((e = check_dyadic(p->ln2_out, p->dim, "ln2_out"))) return e;
+  if ((e = check_dyadic(p->qkv, 3 * p->dim, "qkv"))) return e;
+  if ((e = check_dyadic(p->proj, p->dim, "proj"))) return e;
+  if ((e = check_dyadic(p->fc1, p->mlp_dim, "fc1"))) return e;
+  if ((e = check_dyadic(p->fc2, p->dim, "fc2"))) return e;
+  if ((e = check_attn(&p->attn))) return e;
+  if ((e = check_gelu(p->gelu_I0, p->gelu_k_inter, p->gelu_k_out, p->gelu_mult,
+                      p->gelu_shift)))
+    return e;
+  if ((e = check_mult(p->res1_mult_a, "res1_mult_a")) || (e = check_mult(p->res1_mult_b, "res1_mult_b")) ||
+      (e = check_shift(p->res1_shift, "res1_shift")) ||
+      (e = check_mult(p->res2_mult_a, "res2_mult_a")) || (e = check_mult(p->res2_mult_b, "res2_mult_b")) ||
+      (e = check_shift(p->res2_shift, "res2_shift")))
+    return e;
+  return check_geometry(batch, gh, gw, wh, ww, g);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ilw_last_error(void) { return g_err.c_str(); }
+
+int ilw_abi_version(void) { return ILW_ABI_VERSION; }
+
+int ilw_linear(const int8_t* x, const int8_t* w, const int32_t* b, ilw_dyadic rq, int8_t* y,
+               int64_t M, int32_t N, int32_t K, void* stream) {
+  REQUIRE(M >= 0 && N >= 16 && K >= 16, ILW_E_SHAPE, "M=%lld N=%d K=%d invalid",
+          (long long)M, N, K);
+  REQUIRE(N % 16 == 0 && K % 16 == 0, ILW_E_SHAPE, "N=%d and K=%d must be multiples of 16",
+          N, K);
+  REQUIRE(K <= 131072, ILW_E_UNSUPPORTED, "K=%d: the int32 accumulator needs K <= 131072",
+          K);
+  REQUIRE((M + 127) / 128 * ((N + 127) / 128) < (int64_t)1 << 31, ILW_E_UNSUPPORTED,
+          "too many tiles");
+  if (M == 0) return ok();
+  REQUIRE(x && w && y, ILW_E_NULL, "x, w and y must not be NULL");
+  REQUIRE(aligned16(x) && aligned16(w) && ((uintptr_t)y & 3) == 0, ILW_E_PARAM,
+          "x and w must be 16-byte aligned, y 4-byte aligned");
+  int e;
+  if ((e = check_dyadic(rq, N, "rq"))) return e;
+  GemmArgs a = gemm_args(x, w, b, rq, y, M, N, K);
+  return hip_status(launch_gemm(EPI_STORE, a, (hipStream_t)stream), "ilw_linear");
+}
+
+int ilw_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
+                 int32_t k_inter, int32_t k_out, int32_t m_p, int32_t s_d, void* stream) {
+  REQUIRE(rows >= 0 && cols >= 1 && cols <= 65536, ILW_E_SHAPE,
+          "rows=%lld cols=%d invalid (cols in [1, 65536])", (long long)rows, cols);
+  REQUIRE((rows + 3) / 4 < (int64_t)1 << 31, ILW_E_UNSUPPORTED, "too many rows");
+  int e;
+  if ((e = check_shiftmax(I0, k_inter, k_out, m_p, s_d))) return e;
+  if (rows == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  return hip_status(launch_shiftmax(x, y, rows, cols, I0, k_inter, k_out, m_p, s_d,
+                                    (hipStream_t)stream),
+                    "ilw_shiftmax");
+}
+
+int ilw_sdshiftgelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0, int32_t k_inter,
+                    int32_t k_out, int32_t out_mult, int32_t out_shift, void* stream) {
+  REQUIRE(n >= 0, ILW_E_SHAPE, "n=%lld must be >= 0", (long long)n);
+  int e;
+  if ((e = check_gelu(I0, k_inter, k_out, out_mult, out_shift))) return e;
+  if (n == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  REQUIRE(aligned16(x) && aligned16(y), ILW_E_PARAM, "x and y must be 16-byte aligned");
+  return hip_status(launch_gelu(x, y, n, I0, k_inter, k_out, out_mult, out_shift,
+                                (hipStream_t)stream),
+                    "ilw_sdshiftgelu");
+}
+
+int ilw_int_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
+                      const int32_t* beta, ilw_dyadic out, int32_t newton_iters,
+                      void* stream) {
+  REQUIRE(rows >= 0 && C >= 4 && C <= 16384 && C % 4 == 0, ILW_E_SHAPE,
+          "rows=%lld C=%d invalid (C a multiple of 4 in [4, 16384])", (long long)rows, C);
+  REQUIRE(newton_iters >= 1 && newton_iters <= 64, ILW_E_PARAM,
+          "newton_iters = %d must be in [1, 64]", newton_iters);
+  REQUIRE((rows + 3) / 4 < (int64_t)1 << 31, ILW_E_UNSUPPORTED, "too many rows");
+  int e;
+  if ((e = check_dyadic(out, C, "out"))) return e;
+  if (rows == 0) return ok();
+  REQUIRE(x && y && beta, ILW_E_NULL, "x, y and beta must not be NULL");
+  REQUIRE(((uintptr_t)x & 3) == 0 && ((uintptr_t)y & 3) == 0, ILW_E_PARAM,
+          "x and y must be 4-byte aligned");
+  return hip_status(launch_layernorm(x, y, rows, C, beta, out.mult, out.shift, out.n,
+                                     newton_iters, (hipStream_t)stream),
+                    "ilw_int_layernorm");
+}
+
+int ilw_residual_add(const int8_t* a, const int8_t* b, int8_t* y, int64_t n, int32_t mult_a,
+                     int32_t mult_b, int32_t shift, void* stream) {
+  REQUIRE(n >= 0, ILW_E_SHAPE, "n=%lld must be >= 0", (long long)n);
+  int e;
+  if ((e = check_mult(mult_a, "mult_a")) || (e = check_mult(mult_b, "mult_b")) ||
+      (e = check_shift(shift, "shift")))
+    return e;
+  if (n == 0) return ok();
+  REQUIRE(a && b && y, ILW_E_NULL, "a, b and y must not be NULL");
+  REQUIRE(aligned16(a) && aligned16(b) && aligned16(y), ILW_E_PARAM,
+          "a, b and y must be 16-byte aligned");
+  return hip_status(launch_residual(a, b, y, n, mult_a, mult_b, shift, (hipStream_t)stream),
+                    "ilw_residual_add");
+}
+
+size_t ilw_attention_workspace_bytes(int32_t batch, int32_t grid_h, int32_t grid_w,
+                                     int32_t win_h, int32_t win_w, int32_t dim) {
+  Geometry g;
+  if (check_geometry(batch, grid_h, grid_w, win_h, win_w, &g)) return 0;
+  if (dim < 64 || dim % 64) {
+    fail(ILW_E_SHAPE, "dim = %d must be a positive multiple of 64", dim);
+    return 0;
+  }
+  ok();
+  return qkv_bytes(batch, g, dim, nullptr, nullptr);
+}
+
+int ilw_attention(const int8_t* qkv, int8_t* out, int32_t batch, int32_t grid_h,
+                  int32_t grid_w, int32_t win_h, int32_t win_w, int32_t dim, int32_t heads,
+                  int32_t head_dim, const ilw_attn_params* ap, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  REQUIRE(head_dim == 64, ILW_E_UNSUPPORTED, "head_dim = %d: only 64 is implemented",
+          head_dim);
+  REQUIRE(heads >= 1 && dim == heads * head_dim, ILW_E_SHAPE,
+          "dim = %d must equal heads (%d) * head_dim", dim, heads);
+  Geometry g;
+  int e;
+  if ((e = check_geometry(batch, grid_h, grid_w, win_h, win_w, &g))) return e;
+  if ((e = check_attn(ap))) return e;
+  if (batch == 0) return ok();
+  REQUIRE(qkv && out, ILW_E_NULL, "qkv and out must not be NULL");
+  REQUIRE(aligned16(qkv) && aligned16(out), ILW_E_PARAM,
+          "qkv and out must be 16-byte aligned");
+  const size_t need = qkv_bytes(batch, g, dim, nullptr, nullptr);
+  REQUIRE(workspace && workspace_bytes >= need, ILW_E_WORKSPACE,
+          "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
+  QkvLayout L;
+  qkv_bytes(batch, g, dim, &L, (int8_t*)workspace);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t he = launch_qkv_relayout(qkv, batch, L, s);
+  if (he == hipSuccess) he = launch_attention(attn_args(L, out, batch, *ap), s);
+  return hip_status(he, "ilw_attention");
+}
+
+size_t ilw_block_workspace_bytes(const ilw_block_params* p, int32_t batch, int32_t grid_h,
+                                 int32_t grid_w, int32_t win_h, int32_t win_w) {
+  Geometry g;
+  if (check_block(p, batch, grid_h, grid_w, win_h, win_w, &g)) return 0;
+  ok();
+  return block_layout(p, batch, g, nullptr, nullptr);
+}
+
+int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int32_t batch,
+                      int32_t grid_h, int32_t grid_w, int32_t win_h, int32_t win_w,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  Geometry g;
+  int e;
+  if ((e = check_block(p, batch, grid_h, grid_w, win_h, win_w, &g))) return e;
+  if (batch == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  REQUIRE(aligned16(x) && aligned16(y), ILW_E_PARAM, "x and y must be 16-byte aligned");
+  const size_t need = block_layout(p, batch, g, nullptr, nullptr);
+  REQUIRE(workspace && workspace_bytes >= need, ILW_E_WORKSPACE,
+          "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
+  BlockLayout L;
+  block_layout(p, batch, g, (int8_t*)workspace, &L);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t M = (int64_t)batch * g.T;
+  const int32_t D = p->dim, Hm = p->mlp_dim;
+  hipError_t he;
+
+  // h = LN1(x)
+  he = launch_layernorm(x, L.h, M, D, p->ln1_beta, p->ln1_out.mult, p->ln1_out.shift,
+                        p->ln1_out.n, p->ln_iters, s);
+  if (he != hipSuccess) return hip_status(he, "block LN1");
+  // q, k, v^T = QKV(h), scattered window-major
+  GemmArgs a = gemm_args(L.h, p->w_qkv, p->b_qkv, p->qkv, nullptr, M, 3 * D, D);
+  a.qkv = L.qkv;
+  if ((he = launch_gemm(EPI_QKV, a, s)) != hipSuccess) return hip_status(he, "block QKV");
+  // att = Attn(q, k, v)
+  if ((he = launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s)) != hipSuccess)
+    return hip_status(he, "block attention");
+  // x1 = Res(proj(att), x)
+  a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
+  a.resid = x;
+  a.res_ma = p->res1_mult_a;
+  a.res_mb = p->res1_mult_b;
+  a.res_shift = p->res1_shift;
+  if ((he = launch_gemm(EPI_RESID, a, s)) != hipSuccess) return hip_status(he, "block proj");
+  // h = LN2(x1)
+  he = launch_layernorm(L.x1, L.h, M, D, p->ln2_beta, p->ln2_out.mult, p->ln2_out.shift,
+                        p->ln2_out.n, p->ln_iters, s);
+  if (he != hipSuccess) return hip_status(he, "block LN2");
+  // g = rq(SD-ShiftGELU(fc1(h)))
+  a = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
+  a.g_I0 = p->gelu_I0;
+  a.g_kinter = p->gelu_k_inter;
+  a.g_kout = p->gelu_k_out;
+  a.g_mult = p->gelu_mult;
+  a.g_shift = p->gelu_shift;
+  if ((he = launch_gemm(EPI_GELU, a, s)) != hipSuccess) return hip_status(he, "block fc1");
+  // y = Res(fc2(g), x1)
+  a = gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
+  a.resid = L.x1;
+  a.res_ma = p->res2_mult_a;
+  a.res_mb = p->res2_mult_b;
+  a.res_shift = p->res2_shift;
+  if ((he = launch_gemm(EPI_RESID, a, s)) != hipSuccess) return hip_status(he, "block fc2");
+  return ok();
+}
+
+int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
+                    int32_t L, int32_t P, const int32_t* ref, const int16_t* offsets,
+                    const int8_t* logits, int8_t* out, int32_t B, int32_t Q, int32_t heads,
+                    int32_t head_dim, int32_t I0, int32_t s_d, int32_t out_mult,
+                    int32_t out_shift, int32_t mode, void* stream) {
+  REQUIRE(level_hw && level_start, ILW_E_NULL, "level_hw and level_start (host) required");
+  REQUIRE(L >= 1 && L <= kMaxLevels && P >= 1 && L * P <= 64, ILW_E_SHAPE,
+          "L=%d P=%d invalid (L in [1, 8], L*P in [1, 64])", L, P);
+  REQUIRE(B >= 0 && Q >= 0 && heads >= 1, ILW_E_SHAPE, "B=%d Q=%d heads=%d invalid", B, Q,
+          heads);
+  REQUIRE(head_dim >= 4 && head_dim <= 256 && head_dim % 4 == 0, ILW_E_SHAPE,
+          "head_dim = %d must be a multiple of 4 in [4, 256]", head_dim);
+  REQUIRE(mode == 0 || mode == 1, ILW_E_PARAM, "mode = %d must be 0 or 1", mode);
+  REQUIRE(I0 >= 1 && I0 < (1 << 14), ILW_E_PARAM, "I0 = %d must be in [1, 2^14 - 1]", I0);
+  REQUIRE(s_d >= -1 && s_d <= 31, ILW_E_PARAM, "s_d = %d must be -1 or in [0, 31]", s_d);
+  int e;
+  if ((e = check_mult(out_mult, "out_mult"))) return e;
+  REQUIRE(out_shift >= 1 && out_shift <= (mode == 0 ? 62 : 46), ILW_E_PARAM,
+          "out_shift = %d out of range for mode %d", out_shift, mode);
+  DeformArgs a = {};
+  int64_t S = 0;
+  for (int32_t l = 0; l < L; ++l) {
+    const int32_t hl = level_hw[2 * l], wl = level_hw[2 * l + 1];
+    REQUIRE(hl >= 1 && hl <= 32767 && wl >= 1 && wl <= 32767, ILW_E_SHAPE,
+            "level %d size %dx%d invalid", l, hl, wl);
+    REQUIRE(level_start[l] >= 0, ILW_E_SHAPE, "level_start[%d] < 0", l);
+    a.hw[l][0] = hl;
+    a.hw[l][1] = wl;
+    a.start[l] = level_start[l];
+    const int64_t end = (int64_t)level_start[l] + (int64_t)hl * wl;
+    S = end > S ? end : S;
+  }
+  REQUIRE(S <= INT32_MAX, ILW_E_SHAPE, "value rows exceed int32");
+  const int64_t groups = (int64_t)B * Q * heads;
+  REQUIRE((groups * (head_dim / 4) + 255) / 256 < (int64_t)1 << 31, ILW_E_UNSUPPORTED,
+          "too many queries");
+  if (groups == 0) return ok();
+  REQUIRE(value && ref && offsets && logits && out, ILW_E_NULL,
+          "value, ref, offsets, logits and out must not be NULL");
+  REQUIRE(((uintptr_t)value & 3) == 0 && ((uintptr_t)out & 3) == 0, ILW_E_PARAM,
+          "value and out must be 4-byte aligned");
+  a.value = value;
+  a.ref = ref;
+  a.offs = offsets;
+  a.logits = logits;
+  a.out = out;
+  a.B = B;
+  a.Q = Q;
+  a.H = heads;
+  a.Dh = head_dim;
+  a.L = L;
+  a.P = P;
+  a.S = (int32_t)S;
+  a.I0 = I0;
+  a.s_d = s_d;
+  a.out_mult = out_mult;
+  a.out_shift = out_shift;
+  a.mode = mode;
+  return hip_status(launch_deform(a, (hipStream_t)stream), "ilw_deform_attn");
+}
+
+}  // extern "C"

@@ -1,0 +1,184 @@
+// ilw_internal.h -- device helpers and launcher declarations shared by the
+// HIP sources of libilw.so.  Not part of the public ABI (include/ilw.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/ilw.h"
+
+namespace ilw {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+constexpr int kQmax = 127;   // symmetric int8 range, no zero point
+constexpr int kQmin = -127;
+
+// ---------------------------------------------------------------- rescaling
+__device__ __forceinline__ int32_t sat8(int64_t v) {
+  return v > kQmax ? kQmax : (v < kQmin ? kQmin : (int32_t)v);
+}
+
+// Dyadic requantization of a 32-bit accumulator, round half up.  The 64-bit
+// product cannot overflow: |acc * mult| < 2^62 and the rounding term <= 2^61.
+__device__ __forceinline__ int32_t rq(int32_t acc, int32_t mult, int32_t shift) {
+  int64_t v = (int64_t)acc * (int64_t)mult + ((int64_t)1 << (shift - 1));
+  return sat8(v >> shift);  // arithmetic shift: floor division by 2^shift
+}
+
+// Same for a 64-bit value, through an exact 128-bit product.
+__device__ __forceinline__ int32_t rq_wide(int64_t acc, int32_t mult, int32_t shift) {
+  __int128 v = (__int128)acc * mult + ((__int128)1 << (shift - 1));
+  v >>= shift;
+  return v > kQmax ? kQmax : (v < kQmin ? kQmin : (int32_t)v);
+}
+
+// Two-input dyadic add onto one scale (|a*ma| + |b*mb| < 2^39).
+__device__ __forceinline__ int32_t rq2(int32_t a, int32_t b, int32_t ma, int32_t mb,
+                                       int32_t shift) {
+  int64_t v = (int64_t)a * ma + (int64_t)b * mb + ((int64_t)1 << (shift - 1));
+  return sat8(v >> shift);
+}
+
+// ---------------------------------------------------------------- ShiftExp
+// ShiftExp of a non-positive input (Alg. 1): the exponent I*log2(e) is
+// I + I/2 - I/16 (floor shifts), clipped at -k_inter*I0, split into an integer
+// part q and a remainder r of I0, and 2^(-r/I0) is taken as 1 - r/(2 I0):
+//   I_exp = (I0 - ceil(r/2)) << (k_inter - q)
+// Result < 2^30 for I0 < 2^14 and k_inter <= 16.
+__device__ __forceinline__ int32_t shift_exp(int32_t I, int32_t I0, int32_t k_inter) {
+  int32_t e = I + (I >> 1) - (I >> 4);
+  e = max(e, -k_inter * I0);
+  uint32_t a = (uint32_t)(-e);
+  uint32_t q = a / (uint32_t)I0;
+  uint32_t r = a - q * (uint32_t)I0;
+  int32_t base = I0 - (int32_t)((r + 1) >> 1);
+  return base << (k_inter - (int32_t)q);
+}
+
+// SD-ShiftGELU of one int8 value (Alg. 1): sign-dependent sigmoid of
+// 1.702*x ~ x + x/2 + x/8 + x/16, ratio taken with the M = 31 integer
+// division, times x.  Returns I_out (|I_out| <= 127 * 2^(k_out-1)).
+__device__ __forceinline__ int32_t sd_gelu(int32_t x, int32_t I0, int32_t k_inter,
+                                           int32_t k_out) {
+  int32_t ip = x + (x >> 1) + (x >> 3) + (x >> 4);
+  int32_t pos = max(ip, 0);
+  uint32_t a = (uint32_t)shift_exp(ip - pos, I0, k_inter);
+  uint32_t a2 = (uint32_t)shift_exp(-pos, I0, k_inter);
+  uint32_t f = 0x7fffffffu / (a + a2);
+  int32_t d = (int32_t)(((uint64_t)f * a) >> (32 - k_out));
+  return x * d;
+}
+
+// Wave-wide reductions (wave64).
+__device__ __forceinline__ int32_t wave_sum_i32(int32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t lo = __shfl_xor((uint32_t)v, o, 64);
+    uint32_t hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
+    v += ((uint64_t)hi << 32) | lo;
+  }
+  return v;
+}
+__device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Denominator shift of Constrained Shiftmax (Alg. 2, CalibrateShift):
+// M_req = ceil(log2(S_sum)) = bit length of S_sum - 1, s_d = max(M_req +
+// m_p - 31, 0).
+__device__ __forceinline__ int32_t calibrate_shift(uint64_t s_sum, int32_t m_p) {
+  int32_t m_req = s_sum <= 1 ? 0 : 64 - __clzll((long long)(s_sum - 1));
+  return max(m_req + m_p - 31, 0);
+}
+
+// Normalization factor F = floor((2^31 - 1) / clamp(S_sum >> s_d, 1, 2^31-1)).
+// S_sum >> s_d is exactly the quotient-remainder sum of Alg. 2.
+__device__ __forceinline__ uint32_t shiftmax_factor(uint64_t s_sum, int32_t s_d) {
+  uint64_t sr = s_sum >> s_d;
+  sr = sr < 1 ? 1 : (sr > 0x7fffffffull ? 0x7fffffffull : sr);
+  return 0x7fffffffu / (uint32_t)sr;
+}
+
+// ---------------------------------------------------------------- launchers
+enum GemmEpilogue { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3 };
+
+// Window-major Q, K, V^T buffers used by the attention kernel:
+//   Q, K [B, nW, H, Tw, 64],  V^T [B, nW, H, 64, Twp]  (Twp = Tw rounded to 64)
+struct QkvLayout {
+  int8_t* q;
+  int8_t* k;
+  int8_t* vt;
+  int32_t T, D, H, grid_w, win_h, win_w, nwx, nW, Tw, Twp;
+};
+
+struct GemmArgs {
+  const int8_t* x;   // [M, K] activations
+  const int8_t* w;   // [N, K] weights
+  const int32_t* bias;
+  const int32_t* mult;
+  const int32_t* shift;
+  int32_t nq;        // 1 per-tensor, N per-channel
+  int64_t M;
+  int32_t N, K;
+  int8_t* y;         // [M, N] output (STORE, GELU, RESID)
+  const int8_t* resid;  // [M, N] skip input (RESID)
+  int32_t res_ma, res_mb, res_shift;
+  int32_t g_I0, g_kinter, g_kout, g_mult, g_shift;  // GELU
+  QkvLayout qkv;     // QKV
+};
+
+hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+
+struct AttnArgs {
+  const int8_t* q;
+  const int8_t* k;
+  const int8_t* vt;
+  int8_t* out;       // [B, T, D] token-major
+  int32_t B, T, D, H, grid_w, win_h, win_w, nwx, nW, Tw, Twp;
+  int32_t score_mult, score_shift, I0, k_inter, k_out, m_p, s_d, pv_mult, pv_shift;
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,
+                               hipStream_t s);
+
+hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
+                            const int32_t* beta, const int32_t* mult,
+                            const int32_t* shift, int32_t nq, int32_t iters,
+                            hipStream_t s);
+hipError_t launch_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                           int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                           int32_t s_d, hipStream_t s);
+hipError_t launch_gelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
+                       int32_t k_inter, int32_t k_out, int32_t mult, int32_t shift,
+                       hipStream_t s);
+hipError_t launch_residual(const int8_t* a, const int8_t* b, int8_t* y, int64_t n,
+                           int32_t ma, int32_t mb, int32_t shift, hipStream_t s);
+
+constexpr int kMaxLevels = 8;
+struct DeformArgs {
+  const int8_t* value;
+  const int32_t* ref;
+  const int16_t* offs;
+  const int8_t* logits;
+  int8_t* out;
+  int32_t B, Q, H, Dh, L, P, S;
+  int32_t hw[kMaxLevels][2];
+  int32_t start[kMaxLevels];
+  int32_t I0, s_d, out_mult, out_shift, mode;
+};
+hipError_t launch_deform(const DeformArgs& a, hipStream_t s);
+
+}  // namespace ilw
