@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of the integer-only I-LW-DETR encoder on one MI355X.
+
+One step is one forward pass of the whole encoder (every block: LayerNorm,
+QKV, attention with Constrained Shiftmax, projection + residual, LayerNorm,
+fc1 + SD-ShiftGELU, fc2 + residual) over one batch of seeded synthetic int8
+tokens that are already resident in HBM.  The default workload is the
+ViT-tiny-shaped encoder on a 640x640 image (1600 tokens, dim 192, 6 blocks
+alternating 2x2 windows of 400 tokens and global attention, batch 1).
+
+Prints ONE JSON line on stdout:
+  value        int8 TOPS: algorithmic GEMM ops (2*M*N*K over QKV, Q K^T, P V,
+               projection, fc1, fc2; attention counted per window) / time
+  images_per_s batch / time per step
+  roofline     the dominant kernel's achieved rate against its peak, timed
+               with HIP events on its launch stream
+  cpu_baseline the CPU oracle on one image of the same workload, single thread
+  parity       the benchmarked output of that image against the oracle
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "int8 TOPS + images/sec, integer-only encoder block, bit-exact vs oracle"
+PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POPS
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def stage_work(wl, B):
+    """Algorithmic work of one forward, per profiling stage:
+    (kind, amount) with kind 'ops' (int8 ops) or 'bytes' (HBM bytes)."""
+    T, D, Hm = wl.tokens, wl.dim, wl.mlp_dim
+    M = B * T
+    nb = len(wl.windows)
+    attn = 0
+    for wh, ww in wl.windows:
+        tw = T if wh == 0 else wh * ww
+        attn += 4 * (T // tw) * tw * tw * D * B
+    return {
+        "gemm_qkv": ("ops", nb * 2 * M * 3 * D * D),
+        "attention": ("ops", attn),
+        "gemm_proj": ("ops", nb * 2 * M * D * D),
+        "gemm_fc1": ("ops", nb * 2 * M * Hm * D),
+        "gemm_fc2": ("ops", nb * 2 * M * D * Hm),
+        # int8 row in and out, plus beta / multiplier / shift per channel
+        "layernorm": ("bytes", nb * 2 * (2 * M * D + 12 * D)),
+    }
+
+
+KERNEL_OF_STAGE = {
+    "attention": ("attention_kernel", "paper_2607_24981_amd/csrc/attention.hip"),
+    "gemm_qkv": ("gemm_i8_kernel<3>", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "gemm_proj": ("gemm_i8_kernel<2>", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "gemm_fc1": ("gemm_i8_kernel<1>", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "gemm_fc2": ("gemm_i8_kernel<2>", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "layernorm": ("layernorm_kernel", "paper_2607_24981_amd/csrc/rowops.hip"),
+}
+
+
+def source_digest(rel):
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(stage, workload):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, only
+    while the kernel source is unchanged since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    kernel, src = KERNEL_OF_STAGE[stage]
+    rec = table.get(workload, {}).get(kernel)
+    if not rec or rec.get("source_sha256_16") != source_digest(src):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="encoder_t1600_d192_b1")
+    ap.add_argument("--batch", type=int, default=None, help="override the batch size")
+    ap.add_argument("--seed", type=int, default=2)
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly")
+    ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE={world}); multi-GPU runs are not part of this build",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_24981_amd import ilw, synth
+
+    if not os.path.exists(ilw.LIB_PATH):
+        from paper_2607_24981_amd import build as hip_build
+        hip_build.build()
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+
+    wl = synth.WORKLOADS[args.workload]
+    B = wl.batch if args.batch is None else args.batch
+    log(f"workload {wl.name}: batch {B}, {wl.tokens} tokens, dim {wl.dim}, "
+        f"{len(wl.windows)} blocks")
+    blocks, x = synth.encoder_inputs(wl, args.seed, "baseline", batch=B)
+    enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
+    xd = ilw.to_device(x)
+    out = torch.empty_like(xd)
+    tmp = torch.empty_like(xd)
+    enc.workspace(B)
+
+    def eager():
+        enc.forward(xd, out, tmp)
+
+    step = eager
+    if not args.no_graph:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                eager()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            eager()
+        step = graph.replay
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall_ms = (t1 - t0) * 1e3 / args.steps
+    ev_ms = ev0.elapsed_time(ev1) / args.steps
+    ops = wl.gemm_ops() * B // wl.batch
+    tops = ops / (wall_ms * 1e-3) / 1e12
+    log(f"timed {args.steps} steps: {wall_ms:.4f} ms/step wall, {ev_ms:.4f} ms/step events, "
+        f"{tops:.2f} TOPS, {B / (wall_ms * 1e-3):.1f} images/s")
+    result = out.cpu().numpy()
+
+    # per-stage kernel time, HIP events around each launch (eager pass)
+    ilw.profile_enable(True)
+    for _ in range(args.profile_steps):
+        eager()
+    torch.cuda.synchronize()
+    prof = ilw.profile_read()
+    ilw.profile_enable(False)
+    work = stage_work(wl, B)
+    stages = {}
+    for name, (kind, amount) in work.items():
+        ms, n = prof[name]
+        if n == 0:
+            continue
+        per_step_ms = ms / args.profile_steps
+        rate = amount / (per_step_ms * 1e-3)
+        stages[name] = {"ms_per_step": round(per_step_ms, 5),
+                        "launches_per_step": n // args.profile_steps,
+                        "ms_per_launch": round(ms / n, 5),
+                        ("TOPS" if kind == "ops" else "GBps"):
+                            round(rate / (1e12 if kind == "ops" else 1e9), 2)}
+    dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
+    kind, amount = work[dom]
+    launches = stages[dom]["launches_per_step"]
+    achieved = amount / (stages[dom]["ms_per_step"] * 1e-3)
+    if kind == "ops":
+        roof = {"bound": "mfma", "achieved": round(achieved / 1e12, 3),
+                "peak": PEAK_INT8_TOPS, "unit": "TOPS"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(achieved / 1e9, 2), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 5)
+    roof["kernel"] = KERNEL_OF_STAGE[dom][0]
+    roof["stage"] = dom
+    roof["ms_per_launch"] = stages[dom]["ms_per_launch"]
+    roof["algorithmic_per_launch"] = amount // (launches * 1)
+    roof["traffic"] = measured_traffic(dom, wl.name)
+    log(f"dominant stage {dom}: {json.dumps(roof)}")
+    log("stages: " + json.dumps(stages))
+
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        if not os.path.exists(oracle._SO):
+            oracle.build()
+        log("cpu baseline: oracle on image 0, single thread ...")
+        c0 = time.perf_counter()
+        y = x[:1]
+        for p, (wh, ww) in zip(blocks, wl.windows):
+            y = oracle.block_forward(p, y, wl.grid_h, wl.grid_w, wh, ww)
+        c1 = time.perf_counter()
+        ops1 = wl.gemm_ops() // wl.batch
+        cpu = {"value": round(ops1 / (c1 - c0) / 1e12, 6), "unit": "TOPS",
+               "images_per_s": round(1 / (c1 - c0), 4), "cores": 1, "kind": "oracle",
+               "sample": f"one image (1 of {B}) of {wl.name}: the full {len(wl.windows)}-block "
+                         f"forward, {ops1 / 1e9:.2f} G int8 ops, {c1 - c0:.1f} s"}
+        bad = int(np.count_nonzero(result[:1] != y))
+        parity = "bit-exact" if bad == 0 else f"{bad} of {y.size} outputs differ"
+        log(f"cpu baseline {cpu['value']} TOPS; parity of image 0: {parity}")
+
+    line = {
+        "metric": METRIC,
+        "value": round(tops, 3),
+        "unit": "TOPS",
+        "images_per_s": round(B / (wall_ms * 1e-3), 2),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "tokens": wl.tokens, "dim": wl.dim,
+                   "heads": wl.heads, "mlp_dim": wl.mlp_dim, "blocks": len(wl.windows),
+                   "attention": "window 20x20 / global alternating",
+                   "launch": "eager" if args.no_graph else "hip graph",
+                   "gemm_ops_per_step": ops},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "parity": parity,
+        "stages": stages,
+    }
+    print(json.dumps(line), flush=True)
+    if parity not in (None, "bit-exact"):
+        sys.exit(1)
+
+
+if __name__ == "__main__":
+    main()

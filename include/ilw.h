@@ -222,6 +222,32 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
                     int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
                     int32_t mode, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Per-stage kernel timing (tracing; off by default).  While enabled, every
+ * kernel that ilw_block_forward, ilw_attention and ilw_deform_attn launch is
+ * bracketed by a pair of HIP events recorded on the caller's stream, and the
+ * launch is attributed to one of the stages below.  Enabling (or disabling)
+ * clears the records.  ilw_profile_read waits for the last recorded event and
+ * returns, per stage, the summed kernel time in milliseconds and the number of
+ * launches (arrays of n_stages entries, HOST memory).  Do not enable it while
+ * a stream is being captured into a graph.  Not thread-safe with respect to
+ * concurrent launches from several threads while enabled.
+ */
+typedef enum {
+  ILW_STAGE_LAYERNORM = 0,   /* both LayerNorms of a block                 */
+  ILW_STAGE_GEMM_QKV = 1,    /* QKV linear, window-major scatter epilogue  */
+  ILW_STAGE_ATTENTION = 2,   /* fused attention (window and global)        */
+  ILW_STAGE_GEMM_PROJ = 3,   /* projection linear + residual epilogue      */
+  ILW_STAGE_GEMM_FC1 = 4,    /* fc1 linear + SD-ShiftGELU epilogue         */
+  ILW_STAGE_GEMM_FC2 = 5,    /* fc2 linear + residual epilogue             */
+  ILW_STAGE_RELAYOUT = 6,    /* token-major QKV -> window-major copy       */
+  ILW_STAGE_DEFORM = 7,      /* deformable sampling                        */
+  ILW_NUM_STAGES = 8
+} ilw_stage;
+
+int ilw_profile_enable(int enable);
+int ilw_profile_read(double* total_ms, int32_t* launches, int32_t n_stages);
+
 #ifdef __cplusplus
 }
 #endif

@@ -4,7 +4,9 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "ilw_internal.h"
 
@@ -33,6 +35,46 @@ int hip_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(ILW_E_HIP, "%s: %s", what, hipGetErrorString(e));
   return ok();
 }
+
+// ---- per-stage timing (tracing) ------------------------------------------
+struct ProfRecord {
+  int stage;
+  hipEvent_t start, stop;
+};
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<ProfRecord> recs;
+} g_prof;
+
+hipEvent_t prof_event() {
+  if (g_prof.used == g_prof.pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_prof.pool.push_back(e);
+  }
+  return g_prof.pool[g_prof.used++];
+}
+
+// Brackets one kernel launch with events when profiling is enabled.
+struct StageTimer {
+  int stage;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  StageTimer(int st, hipStream_t str) : stage(st), s(str) {
+    if (!g_prof.on) return;
+    a = prof_event();
+    b = prof_event();
+    if (a && b) (void)hipEventRecord(a, s);
+  }
+  void done() {
+    if (!g_prof.on || !a || !b) return;
+    (void)hipEventRecord(b, s);
+    g_prof.recs.push_back({stage, a, b});
+  }
+};
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -378,8 +420,17 @@ int ilw_attention(const int8_t* qkv, int8_t* out, int32_t batch, int32_t grid_h,
   QkvLayout L;
   qkv_bytes(batch, g, dim, &L, (int8_t*)workspace);
   hipStream_t s = (hipStream_t)stream;
-  hipError_t he = launch_qkv_relayout(qkv, batch, L, s);
-  if (he == hipSuccess) he = launch_attention(attn_args(L, out, batch, *ap), s);
+  hipError_t he;
+  {
+    StageTimer t(ILW_STAGE_RELAYOUT, s);
+    he = launch_qkv_relayout(qkv, batch, L, s);
+    t.done();
+  }
+  if (he == hipSuccess) {
+    StageTimer t(ILW_STAGE_ATTENTION, s);
+    he = launch_attention(attn_args(L, out, batch, *ap), s);
+    t.done();
+  }
   return hip_status(he, "ilw_attention");
 }
 
@@ -412,26 +463,48 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int
   hipError_t he;
 
   // h = LN1(x)
-  he = launch_layernorm(x, L.h, M, D, p->ln1_beta, p->ln1_out.mult, p->ln1_out.shift,
-                        p->ln1_out.n, p->ln_iters, s);
+  {
+    StageTimer t(ILW_STAGE_LAYERNORM, s);
+    he = launch_layernorm(x, L.h, M, D, p->ln1_beta, p->ln1_out.mult, p->ln1_out.shift,
+                          p->ln1_out.n, p->ln_iters, s);
+    t.done();
+  }
   if (he != hipSuccess) return hip_status(he, "block LN1");
   // q, k, v^T = QKV(h), scattered window-major
   GemmArgs a = gemm_args(L.h, p->w_qkv, p->b_qkv, p->qkv, nullptr, M, 3 * D, D);
   a.qkv = L.qkv;
-  if ((he = launch_gemm(EPI_QKV, a, s)) != hipSuccess) return hip_status(he, "block QKV");
+  {
+    StageTimer t(ILW_STAGE_GEMM_QKV, s);
+    he = launch_gemm(EPI_QKV, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block QKV");
   // att = Attn(q, k, v)
-  if ((he = launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s)) != hipSuccess)
-    return hip_status(he, "block attention");
+  {
+    StageTimer t(ILW_STAGE_ATTENTION, s);
+    he = launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block attention");
   // x1 = Res(proj(att), x)
   a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
   a.resid = x;
   a.res_ma = p->res1_mult_a;
   a.res_mb = p->res1_mult_b;
   a.res_shift = p->res1_shift;
-  if ((he = launch_gemm(EPI_RESID, a, s)) != hipSuccess) return hip_status(he, "block proj");
+  {
+    StageTimer t(ILW_STAGE_GEMM_PROJ, s);
+    he = launch_gemm(EPI_RESID, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block proj");
   // h = LN2(x1)
-  he = launch_layernorm(L.x1, L.h, M, D, p->ln2_beta, p->ln2_out.mult, p->ln2_out.shift,
-                        p->ln2_out.n, p->ln_iters, s);
+  {
+    StageTimer t(ILW_STAGE_LAYERNORM, s);
+    he = launch_layernorm(L.x1, L.h, M, D, p->ln2_beta, p->ln2_out.mult, p->ln2_out.shift,
+                          p->ln2_out.n, p->ln_iters, s);
+    t.done();
+  }
   if (he != hipSuccess) return hip_status(he, "block LN2");
   // g = rq(SD-ShiftGELU(fc1(h)))
   a = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
@@ -440,14 +513,24 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int
   a.g_kout = p->gelu_k_out;
   a.g_mult = p->gelu_mult;
   a.g_shift = p->gelu_shift;
-  if ((he = launch_gemm(EPI_GELU, a, s)) != hipSuccess) return hip_status(he, "block fc1");
+  {
+    StageTimer t(ILW_STAGE_GEMM_FC1, s);
+    he = launch_gemm(EPI_GELU, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block fc1");
   // y = Res(fc2(g), x1)
   a = gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
   a.resid = L.x1;
   a.res_ma = p->res2_mult_a;
   a.res_mb = p->res2_mult_b;
   a.res_shift = p->res2_shift;
-  if ((he = launch_gemm(EPI_RESID, a, s)) != hipSuccess) return hip_status(he, "block fc2");
+  {
+    StageTimer t(ILW_STAGE_GEMM_FC2, s);
+    he = launch_gemm(EPI_RESID, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block fc2");
   return ok();
 }
 
@@ -509,7 +592,41 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t*
   a.out_mult = out_mult;
   a.out_shift = out_shift;
   a.mode = mode;
-  return hip_status(launch_deform(a, (hipStream_t)stream), "ilw_deform_attn");
+  StageTimer t(ILW_STAGE_DEFORM, (hipStream_t)stream);
+  hipError_t he = launch_deform(a, (hipStream_t)stream);
+  t.done();
+  return hip_status(he, "ilw_deform_attn");
+}
+
+int ilw_profile_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = enable != 0;
+  g_prof.recs.clear();
+  g_prof.used = 0;
+  return ok();
+}
+
+int ilw_profile_read(double* total_ms, int32_t* launches, int32_t n_stages) {
+  REQUIRE(total_ms && launches, ILW_E_NULL, "output arrays must not be NULL");
+  REQUIRE(n_stages >= 0, ILW_E_SHAPE, "n_stages < 0");
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  for (int32_t i = 0; i < n_stages; ++i) {
+    total_ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  if (!g_prof.recs.empty()) {
+    hipError_t e = hipEventSynchronize(g_prof.recs.back().stop);
+    if (e != hipSuccess) return hip_status(e, "ilw_profile_read");
+  }
+  for (const ProfRecord& r : g_prof.recs) {
+    if (r.stage >= n_stages) continue;
+    float ms = 0.f;
+    hipError_t e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) return hip_status(e, "ilw_profile_read");
+    total_ms[r.stage] += ms;
+    launches[r.stage] += 1;
+  }
+  return ok();
 }
 
 }  // extern "C"

@@ -70,6 +70,9 @@ _SIGS = {
     "ilw_block_workspace_bytes": (c_size, [ctypes.POINTER(BlockParams)] + [c_i32] * 5),
     "ilw_block_forward": (ctypes.c_int, [ctypes.POINTER(BlockParams), c_vp, c_vp] +
                           [c_i32] * 5 + [c_vp, c_size, c_vp]),
+    "ilw_profile_enable": (ctypes.c_int, [ctypes.c_int]),
+    "ilw_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(c_i32), c_i32]),
     "ilw_deform_attn": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp,
                                        c_vp] + [c_i32] * 9 + [c_vp]),
 }
@@ -326,3 +329,20 @@ def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_
                                B, Q, H, Dh, I0, s_d, out_mult, out_shift, mode, _stream())
     _check(rc, "ilw_deform_attn")
     return out
+
+
+STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
+          "relayout", "deform"]
+
+
+def profile_enable(on: bool = True):
+    _check(lib().ilw_profile_enable(1 if on else 0), "ilw_profile_enable")
+
+
+def profile_read() -> dict:
+    """{stage: (total kernel ms, launches)} of the launches since enabling."""
+    n = len(STAGES)
+    ms = (ctypes.c_double * n)()
+    cnt = (c_i32 * n)()
+    _check(lib().ilw_profile_read(ms, cnt, n), "ilw_profile_read")
+    return {STAGES[i]: (ms[i], cnt[i]) for i in range(n)}

@@ -339,3 +339,34 @@ def test_deform_shapes(mode, s_d):
                                    dev(d["ref"]), dev(offs), dev(d["logits"]), 77, 1 << 30,
                                    30, mode, s_d=s_d))
     assert_same(got, ref, "deform small")
+
+
+def test_encoder_graph_replay():
+    """The benchmark captures the encoder forward into a HIP graph: every
+    replay, interleaved with eager work and synchronizations, must reproduce
+    the eager result."""
+    wl = synth.WORKLOADS["encoder_t1600_d192_b1"]
+    say("encoder graph capture and replay")
+    blocks, x = synth.encoder_inputs(wl, 6, "wide", batch=2)
+    enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
+    xd = dev(x)
+    out, tmp = torch.empty_like(xd), torch.empty_like(xd)
+    ref = host(enc.forward(xd, out, tmp)).copy()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        enc.forward(xd, out, tmp)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        enc.forward(xd, out, tmp)
+    for i in range(4):
+        out.fill_(0)
+        tmp.fill_(0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert_same(host(out), ref, f"replay {i}")
+        other = enc.forward(dev(x[::-1].copy()))  # eager work between replays
+        torch.cuda.synchronize()
+        del other
