@@ -145,6 +145,8 @@ int check_geometry(int32_t batch, int32_t gh, int32_t gw, int32_t wh, int32_t ww
   g->Tw = wh * ww;
   REQUIRE(g->Tw <= 2048, ILW_E_UNSUPPORTED, "%d tokens per window exceed the 2048 limit",
           g->Tw);
+  REQUIRE((int64_t)batch * g->T < ((int64_t)1 << 23), ILW_E_UNSUPPORTED,
+          "batch * tokens = %lld must be below 2^23", (long long)batch * g->T);
   REQUIRE((int64_t)batch * g->nW <= 65535, ILW_E_UNSUPPORTED,
           "batch * windows = %lld exceeds 65535", (long long)batch * g->nW);
   g->Twp = (g->Tw + 63) & ~63;

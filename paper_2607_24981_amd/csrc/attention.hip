@@ -1,5 +1,5 @@
 // attention.hip -- fused integer attention for one (image, window, head,
-// 32-query block) per workgroup:
+// block of query rows) per workgroup:
 //
 //   S = Q K^T (MFMA int8) -> per-tensor dyadic -> int8 scores held in LDS
 //   P = Constrained Shiftmax of every score row (Alg. 2)      (int8 in LDS)
@@ -7,27 +7,45 @@
 //
 // Constrained Shiftmax needs the exact row maximum before any exponential
 // (ShiftExp of x - max cannot be rescaled bit-exactly when the maximum
-// changes), so a whole score row block is kept in LDS instead of the online
-// rescaling used by float attention: 32 rows x Tw int8 scores (51 KB at
-// Tw = 1600).  Because the scores are int8, x - max only takes the values
-// 0 .. -255, so ShiftExp is one table of 256 entries per workgroup, and
-// S_sum >> s_d is exactly the quotient-remainder denominator of Alg. 2.
+// changes), so a whole block of score rows is kept in LDS instead of the
+// online rescaling used by float attention: R rows x Tw int8 scores (51 KB
+// for 32 rows at Tw = 1600).  Because the scores are int8, max - score only
+// takes the values 0..254: ShiftExp is one 256-entry table per workgroup,
+// looked up once per score; the looked-up values stay in registers for the
+// normalization, and S_sum >> s_d is exactly the quotient-remainder
+// denominator of Alg. 2.
+//
+// Per score, the exact integer work is a handful of VALU operations while the
+// two matmuls are 256 int8 MFMA ops (about two VALU lane-ops at the chip's
+// MFMA:VALU ratio), so this kernel is bound by the VALU work of the exact
+// Shiftmax, not by the matrix cores.
 #include "ilw_internal.h"
 
 namespace ilw {
 namespace {
 
-constexpr int AR = 32;  // query rows per workgroup
+// Score requantization with a pre-clamped accumulator: clamping to [-L, L]
+// keeps every saturated result saturated and keeps the shifted value inside
+// int32, so the exact result is one 64-bit multiply-add, one 64-bit shift
+// and a clamp.
+__device__ __forceinline__ int32_t rq_clamped(int32_t acc, int32_t L, int32_t mult,
+                                              int64_t rnd, int32_t shift) {
+  acc = min(max(acc, -L), L);
+  const int64_t v = ((int64_t)acc * mult + rnd) >> shift;
+  return min(max((int32_t)v, kQmin), kQmax);
+}
 
-__global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_row) {
-  extern __shared__ __attribute__((aligned(16))) int8_t sS[];  // [AR][lds_row]
-  __shared__ int32_t elut[256];
-  __shared__ int32_t pmax[4][AR];
-  __shared__ int32_t rmax[AR];
+template <int R, int LPR, bool NARROW, bool RAGGED>
+__global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_row,
+                                                        int32_t clampL) {
+  extern __shared__ __attribute__((aligned(16))) int8_t sS[];  // [R][lds_row]
+  __shared__ uint32_t elut[256];
+  __shared__ int32_t pmax[4][R];
 
+  constexpr int NF = R / 16;  // query fragments of 16 rows
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t Tw = a.Tw, Twp = a.Twp;
-  const int32_t i0 = blockIdx.x * AR;
+  const int32_t i0 = blockIdx.x * R;
   const int32_t h = blockIdx.y;
   const int32_t bw = blockIdx.z;  // image * nW + window
   const int64_t slice = (int64_t)bw * a.H + h;
@@ -35,13 +53,14 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   const int8_t* __restrict__ K = a.k + slice * Tw * 64;
   const int8_t* __restrict__ Vt = a.vt + slice * 64 * Twp;
 
-  elut[tid] = shift_exp(-tid, a.I0, a.k_inter);  // ShiftExp(-d), d = 0..255
+  // ShiftExp(-d) for d = 0..254 (entry 255 is never a valid max - score)
+  elut[tid] = tid < 255 ? (uint32_t)shift_exp(-tid, a.I0, a.k_inter) : 0u;
 
   // Query fragments (MFMA B operand: columns = query rows).  Rows past the
   // window are clamped to a valid row; their results are never stored.
-  v4i qf[2];
+  v4i qf[NF];
 #pragma unroll
-  for (int f = 0; f < 2; ++f) {
+  for (int f = 0; f < NF; ++f) {
     const int32_t r = min(i0 + f * 16 + (lane & 15), Tw - 1);
     qf[f] = *(const v4i*)(Q + (int64_t)r * 64 + (lane >> 4) * 16);
   }
@@ -49,69 +68,100 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   // ---- phase 1: scores.  Waves split the keys in blocks of 16; the key
   // fragment is the A operand, so a lane holds 4 consecutive keys of one row.
   const v4i zero = {0, 0, 0, 0};
-  int32_t mx[2] = {-128, -128};
+  const int32_t sm = a.score_mult, ss = a.score_shift;
+  const int64_t srnd = (int64_t)1 << (ss - 1);
+  int32_t mx[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) mx[f] = -128;
   const int32_t nkb = (Tw + 15) >> 4;
-  for (int32_t kb = wave; kb < nkb; kb += 4) {
+  const int32_t kc = (lane >> 4) * 4;  // first of this lane's 4 keys in a block
+  auto kload = [&](int32_t kb) {
     const int32_t key = min(kb * 16 + (lane & 15), Tw - 1);
-    const v4i kf = *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
-    const int32_t kcol = kb * 16 + (lane >> 4) * 4;
+    return *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
+  };
+  int32_t kb = wave;
+  v4i kf = kb < nkb ? kload(kb) : zero;
+  for (; kb < nkb; kb += 4) {
+    const v4i kn = kb + 4 < nkb ? kload(kb + 4) : zero;  // prefetch
+    const int32_t col = kb * 16 + kc;
 #pragma unroll
-    for (int f = 0; f < 2; ++f) {
+    for (int f = 0; f < NF; ++f) {
       const v4i s = __builtin_amdgcn_mfma_i32_16x16x64_i8(kf, qf[f], zero, 0, 0, 0);
-      uint32_t packed = 0;
+      int32_t v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int32_t v = rq(s[r], a.score_mult, a.score_shift);
-        if (kcol + r < Tw) mx[f] = max(mx[f], v);
-        packed |= (uint32_t)(v & 0xff) << (8 * r);
-      }
-      *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + kcol) = packed;
+      for (int r = 0; r < 4; ++r) v[r] = rq_clamped(s[r], clampL, sm, srnd, ss);
+      // keys past the window repeat the last key (clamped rows), so they
+      // never raise the maximum
+      mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
+      const uint32_t packed = (uint32_t)(v[0] & 0xff) | ((uint32_t)(v[1] & 0xff) << 8) |
+                              ((uint32_t)(v[2] & 0xff) << 16) | ((uint32_t)v[3] << 24);
+      *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + col) = packed;
     }
+    kf = kn;
   }
   // row maxima: combine the 4 lanes sharing a row, then the 4 waves
 #pragma unroll
-  for (int f = 0; f < 2; ++f) {
+  for (int f = 0; f < NF; ++f) {
     mx[f] = max(mx[f], __shfl_xor(mx[f], 16, 64));
     mx[f] = max(mx[f], __shfl_xor(mx[f], 32, 64));
     if (lane < 16) pmax[wave][f * 16 + lane] = mx[f];
   }
   __syncthreads();
-  if (tid < AR)
-    rmax[tid] = max(max(pmax[0][tid], pmax[1][tid]), max(pmax[2][tid], pmax[3][tid]));
-  __syncthreads();
 
-  // ---- phase 2: Constrained Shiftmax of each row, in place.  8 rows per wave.
-  const int32_t nword = (Tw + 3) >> 2;
-  const int32_t pword = Twp >> 2;
-  const int32_t pcap = (1 << (a.k_out - 1)) - 1;
-  for (int rr = wave * 8; rr < wave * 8 + 8; ++rr) {
-    if (i0 + rr >= Tw) break;
-    uint32_t* row = (uint32_t*)(sS + rr * lds_row);
-    const int32_t m = rmax[rr];
-    uint64_t sum = 0;
-    for (int32_t wd = lane; wd < nword; wd += 64) {
-      const uint32_t word = row[wd];
+  // ---- phase 2: Constrained Shiftmax of each row, in place.  LPR lanes
+  // share one row; a lane keeps the ShiftExp values of its elements in
+  // registers between the sum and the normalization.
+  {
+    constexpr int RG = 64 / LPR;   // rows processed together by one wave
+    constexpr int JW = 8;          // words per lane (Twp / 4 <= 8 * LPR)
+    const int sub = lane / LPR, k = lane % LPR;
+    const int32_t nword = Twp >> 2;
+    const int32_t pcap = (1 << (a.k_out - 1)) - 1;
+    for (int rr0 = wave * (R / 4); rr0 < (wave + 1) * (R / 4); rr0 += RG) {
+      const int rr = rr0 + sub;
+      uint32_t* row = (uint32_t*)(sS + rr * lds_row);
+      const int32_t m = max(max(pmax[0][rr], pmax[1][rr]), max(pmax[2][rr], pmax[3][rr]));
+      const uint32_t m4 = (uint32_t)(m + 128) * 0x01010101u;
+      uint32_t e[JW][4];
+      uint64_t sum = 0;
+      uint32_t sum32 = 0;
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
-        if (wd * 4 + b < Tw) sum += (uint32_t)elut[m - (int8_t)(word >> (8 * b))];
-    }
-    sum = wave_sum_u64(sum);
-    const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, a.m_p);
-    const uint32_t F = shiftmax_factor(sum, sd);
-    const int32_t sh = 32 - a.k_out + sd;
-    for (int32_t wd = lane; wd < pword; wd += 64) {
-      const uint32_t word = row[wd];
-      uint32_t outw = 0;
+      for (int j = 0; j < JW; ++j) {
+        const int32_t wd = k + j * LPR;
+        const uint32_t word = wd < nword ? row[wd] : 0x80808080u;
+        // max - score per byte: every valid byte is >= 0, and a borrow from
+        // an invalid (higher) byte never reaches a valid one
+        const uint32_t d4 = m4 - (word ^ 0x80808080u);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        if (wd * 4 + b < Tw) {
-          const uint32_t e = (uint32_t)elut[m - (int8_t)(word >> (8 * b))];
-          uint64_t p = ((uint64_t)e * F) >> sh;
-          p = p > (uint64_t)pcap ? (uint64_t)pcap : p;
-          outw |= (uint32_t)p << (8 * b);
+        for (int b = 0; b < 4; ++b) {
+          uint32_t ev = elut[(d4 >> (8 * b)) & 255];
+          const bool ok = RAGGED ? (wd * 4 + b < Tw) : (wd * 4 < Tw);
+          ev = ok ? ev : 0u;
+          e[j][b] = ev;
+          if (NARROW) sum32 += ev; else sum += ev;
         }
       }
-      row[wd] = outw;  // padding columns become 0
+      if (NARROW) sum = sum32;
+#pragma unroll
+      for (int o = LPR / 2; o > 0; o >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)sum, o, 64);
+        const uint32_t hi = __shfl_xor((uint32_t)(sum >> 32), o, 64);
+        sum += ((uint64_t)hi << 32) | lo;
+      }
+      const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, a.m_p);
+      const uint32_t F = shiftmax_factor(sum, sd);
+      const int32_t sh = 32 - a.k_out + sd;
+#pragma unroll
+      for (int j = 0; j < JW; ++j) {
+        const int32_t wd = k + j * LPR;
+        uint32_t outw = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const uint32_t p = (uint32_t)(((uint64_t)e[j][b] * F) >> sh);
+          outw |= min(p, (uint32_t)pcap) << (8 * b);
+        }
+        if (wd < nword) row[wd] = outw;  // padding columns become 0
+      }
     }
   }
   __syncthreads();
@@ -119,23 +169,27 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   // ---- phase 3: O = P V.  Wave w owns channels 16w..16w+15; V^T is the A
   // operand (rows = channels), P^T the B operand (columns = query rows), so a
   // lane holds 4 consecutive channels of one query row.
-  v4i o[2] = {zero, zero};
+  v4i o[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) o[f] = zero;
   const int32_t c0 = wave * 16;
   const int8_t* vrow = Vt + (int64_t)(c0 + (lane & 15)) * Twp + (lane >> 4) * 16;
   const int8_t* prow = sS + (lane & 15) * lds_row + (lane >> 4) * 16;
+  v4i vf = *(const v4i*)vrow;
   for (int32_t j0 = 0; j0 < Twp; j0 += 64) {
-    const v4i vf = *(const v4i*)(vrow + j0);
+    const v4i vn = j0 + 64 < Twp ? *(const v4i*)(vrow + j0 + 64) : zero;  // prefetch
 #pragma unroll
-    for (int f = 0; f < 2; ++f) {
+    for (int f = 0; f < NF; ++f) {
       const v4i pf = *(const v4i*)(prow + f * 16 * lds_row + j0);
       o[f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(vf, pf, o[f], 0, 0, 0);
     }
+    vf = vn;
   }
   const int32_t b_img = bw / a.nW, w = bw % a.nW;
   const int32_t wy = w / a.nwx, wx = w % a.nwx;
   const int32_t c = c0 + (lane >> 4) * 4;
 #pragma unroll
-  for (int f = 0; f < 2; ++f) {
+  for (int f = 0; f < NF; ++f) {
     const int32_t i = i0 + f * 16 + (lane & 15);
     if (i >= Tw) continue;
     const int32_t t = (wy * a.win_h + i / a.win_w) * a.grid_w + wx * a.win_w + i % a.win_w;
@@ -174,23 +228,60 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(const int8_t* qkv, in
   }
 }
 
+template <int R, int LPR, bool NARROW, bool RAGGED>
+hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
+  const int32_t lds_row = a.Twp + 16;
+  const size_t smem = (size_t)R * lds_row;
+  auto kern = attention_kernel<R, LPR, NARROW, RAGGED>;
+  static size_t configured = 0;
+  if (smem > 65536 && smem > configured) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    configured = smem;
+  }
+  dim3 grid((a.Tw + R - 1) / R, a.H, a.B * a.nW), block(256);
+  hipLaunchKernelGGL(kern, grid, block, smem, s, a, lds_row, clampL);
+  return hipGetLastError();
+}
+
+template <int R, int LPR>
+hipError_t launch_rows(const AttnArgs& a, int32_t clampL, bool narrow, hipStream_t s) {
+  const bool ragged = (a.Tw & 3) != 0;
+  if (narrow) {
+    return ragged ? launch_variant<R, LPR, true, true>(a, clampL, s)
+                  : launch_variant<R, LPR, true, false>(a, clampL, s);
+  }
+  return ragged ? launch_variant<R, LPR, false, true>(a, clampL, s)
+                : launch_variant<R, LPR, false, false>(a, clampL, s);
+}
+
+template <int R>
+hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, hipStream_t s) {
+  // a lane holds at most 8 words (32 scores) of its row
+  if (a.Twp <= 512) return launch_rows<R, 16>(a, clampL, narrow, s);
+  if (a.Twp <= 1024) return launch_rows<R, 32>(a, clampL, narrow, s);
+  return launch_rows<R, 64>(a, clampL, narrow, s);
+}
+
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.B == 0) return hipSuccess;
-  const int32_t lds_row = a.Twp + 16;
-  const size_t smem = (size_t)AR * lds_row;
-  static size_t configured = 0;
-  if (smem > 65536 && smem > configured) {
-    hipError_t e = hipFuncSetAttribute((const void*)attention_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)smem);
-    if (e != hipSuccess) return e;
-    configured = smem;
-  }
-  dim3 grid((a.Tw + AR - 1) / AR, a.H, a.B * a.nW), block(256);
-  hipLaunchKernelGGL(attention_kernel, grid, block, smem, s, a, lds_row);
-  return hipGetLastError();
+  // Accumulator clamp for the score requantization: beyond |acc| = L the
+  // result saturates (|acc * mult| >= 129 * 2^shift) and the product of the
+  // clamped value stays far inside 64 bits.
+  const int64_t am = a.score_mult < 0 ? -(int64_t)a.score_mult : (int64_t)a.score_mult;
+  int64_t L = am == 0 ? 1 : (129 * ((int64_t)1 << a.score_shift)) / am + 1;
+  if (L > ((int64_t)1 << 30)) L = (int64_t)1 << 30;
+  // A lane sums at most 32 ShiftExp values: 32-bit partial sums are exact
+  // while I0 * 2^k_inter < 2^27.
+  const bool narrow = ((int64_t)a.I0 << a.k_inter) < ((int64_t)1 << 27);
+  // Fill the chip: fall back to 16-row blocks when 32-row blocks would give
+  // fewer than two workgroups per CU.
+  const int64_t wg32 = (int64_t)((a.Tw + 31) / 32) * a.H * a.B * a.nW;
+  if (wg32 < 512) return launch_lpr<16>(a, (int32_t)L, narrow, s);
+  return launch_lpr<32>(a, (int32_t)L, narrow, s);
 }
 
 hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,

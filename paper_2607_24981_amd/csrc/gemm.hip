@@ -4,35 +4,72 @@
 //
 //   y[m][n] = epilogue( rq(bias[n] + sum_k x[m][k] * w[n][k]; mult[n], shift[n]) )
 //
-// Tiling: a workgroup of 4 waves computes 128 channels x 128 tokens; each wave
-// a 64 x 64 quadrant as 4 x 4 tiles of v_mfma_i32_16x16x64_i8.  The weight
-// tile is the MFMA A operand (rows = channels) and the activation tile the B
-// operand (columns = tokens), so each lane ends up holding four consecutive
-// channels of one token and stores them as one 32-bit word.  K advances 64
-// bytes per step through double-buffered LDS tiles whose rows are padded to
-// 80 bytes, which keeps the 16-byte fragment reads of a wave free of bank
-// conflicts.  Workgroups are remapped so that each XCD works on a contiguous
-// run of tiles (tokens-major), keeping an activation tile and the weights in
-// that XCD's L2.
+// Tiling: each wave computes 64 channels x 64 tokens as 4 x 4 tiles of
+// v_mfma_i32_16x16x64_i8; a workgroup holds (TN/64) x (TM/64) waves.  The
+// weight tile is the MFMA A operand (rows = channels) and the activation tile
+// the B operand (columns = tokens), so each lane ends up holding four
+// consecutive channels of one token and stores them as one 32-bit word.  K
+// advances 64 bytes per step through double-buffered LDS tiles whose rows are
+// padded to 80 bytes, which keeps the 16-byte fragment reads of a wave free of
+// bank conflicts.  Workgroups are remapped so that each XCD works on a
+// contiguous run of tiles (tokens-major), keeping an activation tile and the
+// weights in that XCD's L2.
+//
+// At K = 192 the exact requantization costs more VALU time than the MFMA work
+// of the tile, so the epilogue is kept to a few instructions per output: the
+// accumulator is clamped to a per-channel bound beyond which the result is
+// saturated anyway, after which one 64-bit multiply-add and one shift give the
+// exact rounded value inside int32.
 #include "ilw_internal.h"
 
 namespace ilw {
 namespace {
 
-constexpr int TN = 128;       // channels per workgroup tile
-constexpr int TM = 128;       // tokens per workgroup tile
 constexpr int TK = 64;        // K bytes per step
 constexpr int LDS_ROW = 80;   // padded LDS row stride (bytes)
 constexpr int NXCD = 8;
 
 __device__ __forceinline__ uint32_t pack4(int32_t a, int32_t b, int32_t c, int32_t d) {
   return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) |
-         ((uint32_t)(c & 0xff) << 16) | ((uint32_t)(d & 0xff) << 24);
+         ((uint32_t)(c & 0xff) << 16) | ((uint32_t)d << 24);
 }
 
-template <int EPI>
-__global__ __launch_bounds__(256) void gemm_i8_kernel(GemmArgs a, int32_t tiles_n,
-                                                      int64_t tiles_total) {
+// Requantization of one channel with its accumulator bound L:
+// |acc| >= L saturates (|acc * mult| > 129 * 2^shift) and L * |mult| / 2^shift
+// stays far inside int32.  Any L in [129 * 2^s / |m| + 1, 2^30 * 2^s / |m|]
+// works, so an fp32 estimate with margin is exact enough.
+struct ChanRq {
+  int32_t L, mult, shift, bias;
+  int64_t rnd;
+  __device__ __forceinline__ void init(int32_t m, int32_t s, int32_t b) {
+    mult = m;
+    shift = s;
+    bias = b;
+    rnd = (int64_t)1 << (s - 1);
+    const float am = fabsf((float)m);
+    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) / am;
+    L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
+  }
+  __device__ __forceinline__ int32_t apply(int32_t acc) const {
+    int32_t a = acc + bias;
+    a = min(max(a, -L), L);
+    const int32_t v = (int32_t)(((int64_t)a * mult + rnd) >> shift);
+    return min(max(v, kQmin), kQmax);
+  }
+};
+
+// n / d for 0 <= n < 2^24 with an fp32 reciprocal and one correction step.
+__device__ __forceinline__ int32_t fdiv(int32_t n, int32_t d, float inv) {
+  int32_t q = (int32_t)((float)n * inv);
+  const int32_t r = n - q * d;
+  q += r < 0 ? -1 : (r >= d ? 1 : 0);
+  return q;
+}
+
+template <int TN, int TM, int EPI>
+__global__ __launch_bounds__(TN * TM / 64) void gemm_i8_kernel(GemmArgs a, int32_t tiles_n,
+                                                               int64_t tiles_total) {
+  constexpr int WN = TN / 64, WM = TM / 64, NT = 64 * WN * WM;
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
   __shared__ int8_t glut[256];
@@ -40,8 +77,8 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmArgs a, int32_t tiles_
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wn = wave & 1;   // channel half of the tile
-  const int wm = wave >> 1;  // token half of the tile
+  const int wn = wave % WN;  // channel block of the tile
+  const int wm = wave / WN;  // token block of the tile
 
   // XCD-aware tile order: dispatch places workgroup i on XCD i % 8; give each
   // XCD a contiguous block of tiles.
@@ -60,8 +97,8 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmArgs a, int32_t tiles_
   if (EPI == EPI_GELU) {
     // SD-ShiftGELU of the requantized fc1 output is a function of one int8
     // value: tabulate it (with its output requantization) once per workgroup.
-    int32_t v = tid - 128;
-    glut[tid] = (int8_t)rq(sd_gelu(v, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
+    for (int t = tid; t < 256; t += NT)
+      glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
   }
 
   const v4i zero = {0, 0, 0, 0};
@@ -71,27 +108,37 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmArgs a, int32_t tiles_
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = zero;
 
-  // Each thread moves two 16-byte chunks of each operand tile per K step.
-  v4i rw[2], rx[2];
+  // Global -> LDS staging: (TN + TM) rows of 64 bytes per K step, 16 bytes
+  // per thread-chunk.
+  constexpr int CW = TN * 4, CX = TM * 4;  // chunks per operand tile
+  constexpr int PW = (CW + NT - 1) / NT, PX = (CX + NT - 1) / NT;
+  v4i rw[PW], rx[PX];
   auto gload = [&](int kt) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * 256;
-      const int row = c >> 2;
+    for (int i = 0; i < PW; ++i) {
+      const int c = tid + i * NT;
       const int k = kt * TK + (c & 3) * 16;
-      const int32_t n = n0 + row;
-      const int64_t m = m0 + row;
-      rw[i] = (n < N && k < K) ? *(const v4i*)(W + (int64_t)n * K + k) : zero;
-      rx[i] = (m < M && k < K) ? *(const v4i*)(X + m * K + k) : zero;
+      const int32_t n = n0 + (c >> 2);
+      rw[i] = (c < CW && n < N && k < K) ? *(const v4i*)(W + (int64_t)n * K + k) : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < PX; ++i) {
+      const int c = tid + i * NT;
+      const int k = kt * TK + (c & 3) * 16;
+      const int64_t m = m0 + (c >> 2);
+      rx[i] = (c < CX && m < M && k < K) ? *(const v4i*)(X + m * K + k) : zero;
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * 256;
-      const int off = (c >> 2) * LDS_ROW + (c & 3) * 16;
-      *(v4i*)(&sW[buf][off]) = rw[i];
-      *(v4i*)(&sX[buf][off]) = rx[i];
+    for (int i = 0; i < PW; ++i) {
+      const int c = tid + i * NT;
+      if (c < CW) *(v4i*)(&sW[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rw[i];
+    }
+#pragma unroll
+    for (int i = 0; i < PX; ++i) {
+      const int c = tid + i * NT;
+      if (c < CX) *(v4i*)(&sX[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rx[i];
     }
   };
 
@@ -121,74 +168,114 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmArgs a, int32_t tiles_
 
   // Epilogue.  Lane holds channels n..n+3 (n = 4*(lane/16) within a 16-tile)
   // of token lane%16 of each of the 4 x 4 tiles.
+  int64_t tok[4];      // per token: output row (STORE/GELU/RESID) or Q/K offset (QKV)
+  int64_t tokv[4];     // QKV: V^T offset of the token
+  bool tok_ok[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t m = m0 + wm * 64 + j * 16 + (lane & 15);
+    tok_ok[j] = m < M;
+    tok[j] = m * N;
+    tokv[j] = 0;
+    if (EPI == EPI_QKV && tok_ok[j]) {
+      const QkvLayout& Lq = a.qkv;
+      const int32_t b = fdiv((int32_t)m, Lq.T, a.inv_T);
+      const int32_t t = (int32_t)m - b * Lq.T;
+      const int32_t ty = fdiv(t, Lq.grid_w, a.inv_gw), tx = t - ty * Lq.grid_w;
+      const int32_t wy = fdiv(ty, Lq.win_h, a.inv_wh), iy = ty - wy * Lq.win_h;
+      const int32_t wx = fdiv(tx, Lq.win_w, a.inv_ww), ix = tx - wx * Lq.win_w;
+      const int64_t bw = (int64_t)b * Lq.nW + wy * Lq.nwx + wx;
+      const int32_t li = iy * Lq.win_w + ix;
+      tok[j] = (bw * Lq.H * Lq.Tw + li) * 64;
+      tokv[j] = bw * Lq.H * 64 * Lq.Twp + li;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int32_t n = n0 + wn * 64 + i * 16 + (lane >> 4) * 4;
     if (n >= N) continue;  // N is a multiple of 16: the 4 channels are all valid
-    int32_t bs[4], ml[4], sh[4];
+    ChanRq cr[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      bs[r] = a.bias ? a.bias[n + r] : 0;
       const int qi = a.nq == 1 ? 0 : n + r;
-      ml[r] = a.mult[qi];
-      sh[r] = a.shift[qi];
+      cr[r].init(a.mult[qi], a.shift[qi], a.bias ? a.bias[n + r] : 0);
+    }
+    int8_t* qk_base = nullptr;
+    int64_t ch_qk = 0, ch_v = 0;
+    bool is_v = false;
+    if (EPI == EPI_QKV) {
+      const QkvLayout& Lq = a.qkv;
+      const int32_t part = n / Lq.D, rem_n = n - part * Lq.D;
+      const int32_t h = rem_n >> 6, c = rem_n & 63;
+      is_v = part == 2;
+      qk_base = part == 0 ? Lq.q : Lq.k;
+      ch_qk = (int64_t)h * Lq.Tw * 64 + c;
+      ch_v = ((int64_t)h * 64 + c) * Lq.Twp;
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int64_t m = m0 + wm * 64 + j * 16 + (lane & 15);
-      if (m >= M) continue;
+      if (!tok_ok[j]) continue;
       int32_t v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = rq(acc[i][j][r] + bs[r], ml[r], sh[r]);
+      for (int r = 0; r < 4; ++r) v[r] = cr[r].apply(acc[i][j][r]);
       if (EPI == EPI_STORE) {
-        *(uint32_t*)(a.y + m * N + n) = pack4(v[0], v[1], v[2], v[3]);
+        *(uint32_t*)(a.y + tok[j] + n) = pack4(v[0], v[1], v[2], v[3]);
       } else if (EPI == EPI_GELU) {
-        *(uint32_t*)(a.y + m * N + n) = pack4(glut[v[0] + 128], glut[v[1] + 128],
-                                              glut[v[2] + 128], glut[v[3] + 128]);
+        *(uint32_t*)(a.y + tok[j] + n) = pack4(glut[v[0] + 128], glut[v[1] + 128],
+                                               glut[v[2] + 128], glut[v[3] + 128]);
       } else if (EPI == EPI_RESID) {
-        const uint32_t s = *(const uint32_t*)(a.resid + m * N + n);
+        const uint32_t s = *(const uint32_t*)(a.resid + tok[j] + n);
         int32_t o[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           o[r] = rq2(v[r], (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
-        *(uint32_t*)(a.y + m * N + n) = pack4(o[0], o[1], o[2], o[3]);
+        *(uint32_t*)(a.y + tok[j] + n) = pack4(o[0], o[1], o[2], o[3]);
       } else {  // EPI_QKV: scatter into window-major Q, K and V^T
-        const QkvLayout& L = a.qkv;
-        const int32_t b = (int32_t)(m / L.T), t = (int32_t)(m % L.T);
-        const int32_t ty = t / L.grid_w, tx = t % L.grid_w;
-        const int32_t w = (ty / L.win_h) * L.nwx + tx / L.win_w;
-        const int32_t li = (ty % L.win_h) * L.win_w + tx % L.win_w;
-        const int32_t part = n / L.D, rem_n = n % L.D;
-        const int32_t h = rem_n >> 6, c = rem_n & 63;
-        const int64_t slice = ((int64_t)b * L.nW + w) * L.H + h;
-        if (part < 2) {
-          int8_t* dst = (part == 0 ? L.q : L.k) + (slice * L.Tw + li) * 64 + c;
-          *(uint32_t*)dst = pack4(v[0], v[1], v[2], v[3]);
+        if (!is_v) {
+          *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(v[0], v[1], v[2], v[3]);
         } else {
-          int8_t* dst = L.vt + (slice * 64 + c) * L.Twp + li;
+          int8_t* dst = a.qkv.vt + tokv[j] + ch_v;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(int64_t)r * L.Twp] = (int8_t)v[r];
+          for (int r = 0; r < 4; ++r) dst[(int64_t)r * a.qkv.Twp] = (int8_t)v[r];
         }
       }
     }
   }
 }
 
-}  // namespace
-
-hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
-  if (a.M == 0) return hipSuccess;
+template <int TN, int TM>
+hipError_t launch_tile(int epi, const GemmArgs& a, hipStream_t s) {
   const int32_t tiles_n = (a.N + TN - 1) / TN;
   const int64_t tiles_m = (a.M + TM - 1) / TM;
   const int64_t total = tiles_m * tiles_n;
-  dim3 grid((unsigned)total), block(256);
+  dim3 grid((unsigned)total), block(TN * TM / 64);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL(gemm_i8_kernel<EPI_STORE>, grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_GELU: hipLaunchKernelGGL(gemm_i8_kernel<EPI_GELU>, grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_RESID: hipLaunchKernelGGL(gemm_i8_kernel<EPI_RESID>, grid, block, 0, s, a, tiles_n, total); break;
-    default: hipLaunchKernelGGL(gemm_i8_kernel<EPI_QKV>, grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_STORE>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_GELU: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_GELU>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_RESID>), grid, block, 0, s, a, tiles_n, total); break;
+    default: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_QKV>), grid, block, 0, s, a, tiles_n, total); break;
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
+  if (a_in.M == 0) return hipSuccess;
+  GemmArgs a = a_in;
+  if (epi == EPI_QKV) {
+    a.inv_T = 1.0f / (float)a.qkv.T;
+    a.inv_gw = 1.0f / (float)a.qkv.grid_w;
+    a.inv_wh = 1.0f / (float)a.qkv.win_h;
+    a.inv_ww = 1.0f / (float)a.qkv.win_w;
+  }
+  // Channel tile: 128 when it divides N, else 64 (N = 192, 576 waste nothing).
+  // Token tile: as large as keeps at least two workgroups per CU busy.
+  const bool n128 = a.N % 128 == 0;
+  const int64_t tiles64 = ((a.M + 63) / 64) * ((a.N + 63) / 64);
+  if (tiles64 < 1024) return launch_tile<64, 64>(epi, a, s);
+  if (n128) return launch_tile<128, 128>(epi, a, s);
+  return launch_tile<64, 256>(epi, a, s);
 }
 
 }  // namespace ilw

@@ -138,6 +138,7 @@ struct GemmArgs {
   int32_t res_ma, res_mb, res_shift;
   int32_t g_I0, g_kinter, g_kout, g_mult, g_shift;  // GELU
   QkvLayout qkv;     // QKV
+  float inv_T, inv_gw, inv_wh, inv_ww;  // QKV: reciprocals for token -> window
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);

@@ -11,20 +11,133 @@ namespace ilw {
 namespace {
 
 // ---------------------------------------------------------------- LayerNorm
-// One wave per row of C (multiple of 4) int8 channels.
+// floor(V / k) for the Newton step.  Newton started at 2^16 >= sqrt(V) never
+// drops below floor(sqrt(V)), so the quotient is below 2^17: an fp32
+// reciprocal estimate is within one of it and one integer correction makes
+// it exact.
+__device__ __forceinline__ uint32_t newton_div(uint32_t V, uint32_t k) {
+  const float qf = (float)V * __builtin_amdgcn_rcpf((float)k);
+  int64_t q = (int64_t)qf;
+  const int64_t r = (int64_t)V - q * (int64_t)k;
+  q += r < 0 ? -1 : (r >= (int64_t)k ? 1 : 0);
+  return (uint32_t)q;
+}
+
+// Integer square root by a fixed number of Newton steps from 2^16.
+__device__ __forceinline__ uint32_t newton_isqrt(uint32_t V, int32_t iters) {
+  if (V == 0) return 0;
+  uint32_t k = 65536;
+  for (int32_t t = 0; t < iters; ++t) k = (k + newton_div(V, k)) >> 1;
+  return k;
+}
+
+// floor((2*sum + C) / (2*C)): the row mean rounded half up.
+__device__ __forceinline__ int32_t mean_half_up(int32_t s, int32_t C) {
+  const int32_t num = 2 * s + C, den = 2 * C;
+  int32_t mu = num / den;
+  if (num % den != 0 && num < 0) mu -= 1;
+  return mu;
+}
+
+// n + beta requantized exactly.  |n| <= 2^30 and |beta| < 2^31 give
+// |t| < 2^32, so u = t * mult fits int64, and
+//   floor((u + 2^(shift-1)) / 2^shift) = ((u >> (shift-1)) + 1) >> 1
+// avoids the rounding add that could overflow.
+__device__ __forceinline__ int32_t ln_out(int64_t t, int32_t mult, int32_t shift) {
+  const int64_t u = t * (int64_t)mult;
+  const int64_t r = ((u >> (shift - 1)) + 1) >> 1;
+  return sat8(r);
+}
+
+// LPR lanes per row, JW words (4 channels each) per lane kept in registers:
+// C <= 4 * LPR * JW.  The per-channel beta / multiplier / shift of a lane's
+// channels are loaded once and reused for every row the wave processes.
+template <int LPR, int JW>
 __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t* y,
                                                         int64_t rows, int32_t C,
                                                         const int32_t* beta,
                                                         const int32_t* mult,
                                                         const int32_t* shift, int32_t nq,
                                                         int32_t iters) {
+  constexpr int RG = 64 / LPR;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane / LPR, k = lane % LPR;
+  const int32_t nw = C >> 2;
+  int32_t pb[JW][4], pm[JW][4], ps[JW][4];
+#pragma unroll
+  for (int j = 0; j < JW; ++j) {
+    const int32_t wd = k + j * LPR;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int32_t c = wd < nw ? wd * 4 + b : 0;
+      const int32_t q = nq == 1 ? 0 : c;
+      pb[j][b] = beta[c];
+      pm[j][b] = mult[q];
+      ps[j][b] = shift[q];
+    }
+  }
+  const int64_t ngroups = (rows + RG - 1) / RG;
+  for (int64_t g = (int64_t)blockIdx.x * 4 + wave; g < ngroups; g += (int64_t)gridDim.x * 4) {
+    const int64_t row = g * RG + sub;
+    const bool live = row < rows;
+    const uint32_t* xr = (const uint32_t*)(x + (live ? row : 0) * C);
+    uint32_t xw[JW];
+    int32_t s = 0;
+#pragma unroll
+    for (int j = 0; j < JW; ++j) {
+      const int32_t wd = k + j * LPR;
+      xw[j] = wd < nw ? xr[wd] : 0u;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) s += (int8_t)(xw[j] >> (8 * b));
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    const int32_t mu = mean_half_up(s, C);
+    uint32_t V = 0;
+#pragma unroll
+    for (int j = 0; j < JW; ++j) {
+      if (k + j * LPR >= nw) continue;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int32_t d = (int8_t)(xw[j] >> (8 * b)) - mu;
+        V += (uint32_t)(d * d);
+      }
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) V += __shfl_xor(V, o, 64);
+    const uint32_t sigma = newton_isqrt(V, iters);
+    const uint32_t F = sigma ? 0x7fffffffu / sigma : 0u;
+    uint32_t* yr = (uint32_t*)(y + (live ? row : 0) * C);
+#pragma unroll
+    for (int j = 0; j < JW; ++j) {
+      const int32_t wd = k + j * LPR;
+      uint32_t o = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int32_t d = (int8_t)(xw[j] >> (8 * b)) - mu;
+        // |d| <= sigma, so |d * F| < 2^31
+        const int64_t n = ((int64_t)d * (int64_t)F) >> 1;
+        o |= (uint32_t)(ln_out(n + pb[j][b], pm[j][b], ps[j][b]) & 0xff) << (8 * b);
+      }
+      if (live && wd < nw) yr[wd] = o;
+    }
+  }
+}
+
+// Rows longer than 2048 channels: one wave per row, values re-read from
+// memory (L1/L2) for each pass.
+__global__ __launch_bounds__(256) void layernorm_long_kernel(const int8_t* x, int8_t* y,
+                                                             int64_t rows, int32_t C,
+                                                             const int32_t* beta,
+                                                             const int32_t* mult,
+                                                             const int32_t* shift,
+                                                             int32_t nq, int32_t iters) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const uint32_t* xr = (const uint32_t*)(x + row * C);
   uint32_t* yr = (uint32_t*)(y + row * C);
   const int32_t nw = C >> 2;
-
   int32_t s = 0;
   for (int32_t w = lane; w < nw; w += 64) {
     const uint32_t v = xr[w];
@@ -32,11 +145,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
     for (int b = 0; b < 4; ++b) s += (int8_t)(v >> (8 * b));
   }
   s = wave_sum_i32(s);
-  // mean rounded half up: floor((2*sum + C) / (2*C)), numerator may be < 0
-  const int32_t num = 2 * s + C, den = 2 * C;
-  int32_t mu = num / den;
-  if (num % den != 0 && num < 0) mu -= 1;
-
+  const int32_t mu = mean_half_up(s, C);
   uint32_t V = 0;
   for (int32_t w = lane; w < nw; w += 64) {
     const uint32_t v = xr[w];
@@ -47,16 +156,8 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
     }
   }
   V = wave_sum_u32(V);
-  // Newton's integer square root from 2^16, a fixed number of steps; the
-  // iterate never drops below floor(sqrt(V)) >= 1 when V > 0.
-  uint32_t sigma = 0;
-  if (V != 0) {
-    uint32_t k = 65536;
-    for (int32_t t = 0; t < iters; ++t) k = (k + V / k) >> 1;
-    sigma = k;
-  }
+  const uint32_t sigma = newton_isqrt(V, iters);
   const uint32_t F = sigma ? 0x7fffffffu / sigma : 0u;
-
   for (int32_t w = lane; w < nw; w += 64) {
     const uint32_t v = xr[w];
     uint32_t o = 0;
@@ -64,11 +165,9 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
     for (int b = 0; b < 4; ++b) {
       const int32_t c = w * 4 + b;
       const int32_t d = (int8_t)(v >> (8 * b)) - mu;
-      // |d| <= sigma, so |d * F| < 2^31 and n fits 31 bits
       const int64_t n = ((int64_t)d * (int64_t)F) >> 1;
       const int32_t q = nq == 1 ? 0 : c;
-      const int32_t r = rq_wide(n + beta[c], mult[q], shift[q]);
-      o |= (uint32_t)(r & 0xff) << (8 * b);
+      o |= (uint32_t)(ln_out(n + beta[c], mult[q], shift[q]) & 0xff) << (8 * b);
     }
     yr[w] = o;
   }
@@ -158,13 +257,29 @@ unsigned stream_grid(int64_t n) {
 
 }  // namespace
 
+template <int LPR, int JW>
+hipError_t launch_ln(const int8_t* x, int8_t* y, int64_t rows, int32_t C, const int32_t* beta,
+                     const int32_t* mult, const int32_t* shift, int32_t nq, int32_t iters,
+                     hipStream_t s) {
+  const int64_t groups = (rows + (64 / LPR) - 1) / (64 / LPR);
+  int64_t wgs = (groups + 3) / 4;
+  if (wgs > 4096) wgs = 4096;
+  hipLaunchKernelGGL((layernorm_kernel<LPR, JW>), dim3((unsigned)wgs), dim3(256), 0, s, x, y,
+                     rows, C, beta, mult, shift, nq, iters);
+  return hipGetLastError();
+}
+
 hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                             const int32_t* beta, const int32_t* mult, const int32_t* shift,
                             int32_t nq, int32_t iters, hipStream_t s) {
   if (rows == 0) return hipSuccess;
+  const int32_t nw = C / 4;
+  if (nw <= 16 * 4) return launch_ln<16, 4>(x, y, rows, C, beta, mult, shift, nq, iters, s);
+  if (nw <= 32 * 4) return launch_ln<32, 4>(x, y, rows, C, beta, mult, shift, nq, iters, s);
+  if (nw <= 64 * 8) return launch_ln<64, 8>(x, y, rows, C, beta, mult, shift, nq, iters, s);
   dim3 grid((unsigned)((rows + 3) / 4)), block(256);
-  hipLaunchKernelGGL(layernorm_kernel, grid, block, 0, s, x, y, rows, C, beta, mult, shift,
-                     nq, iters);
+  hipLaunchKernelGGL(layernorm_long_kernel, grid, block, 0, s, x, y, rows, C, beta, mult,
+                     shift, nq, iters);
   return hipGetLastError();
 }
 
