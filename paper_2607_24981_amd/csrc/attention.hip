@@ -35,6 +35,24 @@ __device__ __forceinline__ int32_t rq_clamped(int32_t acc, int32_t L, int32_t mu
   return min(max((int32_t)v, kQmin), kQmax);
 }
 
+// Bytes 0 of a, b, c, d packed into one word (a in the low byte).
+__device__ __forceinline__ uint32_t pack_bytes(int32_t a, int32_t b, int32_t c, int32_t d) {
+  const uint32_t lo = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0400u);
+  const uint32_t hi = __builtin_amdgcn_perm((uint32_t)d, (uint32_t)c, 0x0c0c0400u);
+  return lo | (hi << 16);
+}
+
+// floor((2^31 - 1) / S_R) for S_R in [1, 2^31 - 1]: an FP64 reciprocal
+// estimate is within one of the quotient; one integer correction makes it
+// exact.
+__device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
+  const double est = 2147483647.0 * __builtin_amdgcn_rcp((double)sr);
+  int64_t q = (int64_t)est;
+  const int64_t r = 2147483647LL - q * (int64_t)sr;
+  q += r < 0 ? -1 : (r >= (int64_t)sr ? 1 : 0);
+  return (uint32_t)q;
+}
+
 template <int R, int LPR, bool NARROW, bool RAGGED>
 __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_row,
                                                         int32_t clampL) {
@@ -43,7 +61,8 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   __shared__ int32_t pmax[4][R];
 
   constexpr int NF = R / 16;  // query fragments of 16 rows
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int32_t Tw = a.Tw, Twp = a.Twp;
   const int32_t i0 = blockIdx.x * R;
   const int32_t h = blockIdx.y;
@@ -79,10 +98,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
     const int32_t key = min(kb * 16 + (lane & 15), Tw - 1);
     return *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
   };
-  int32_t kb = wave;
-  v4i kf = kb < nkb ? kload(kb) : zero;
-  for (; kb < nkb; kb += 4) {
-    const v4i kn = kb + 4 < nkb ? kload(kb + 4) : zero;  // prefetch
+  auto scores = [&](int32_t kb, const v4i& kf) {
     const int32_t col = kb * 16 + kc;
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
@@ -93,11 +109,26 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
       // keys past the window repeat the last key (clamped rows), so they
       // never raise the maximum
       mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
-      const uint32_t packed = (uint32_t)(v[0] & 0xff) | ((uint32_t)(v[1] & 0xff) << 8) |
-                              ((uint32_t)(v[2] & 0xff) << 16) | ((uint32_t)v[3] << 24);
-      *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + col) = packed;
+      *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + col) =
+          pack_bytes(v[0], v[1], v[2], v[3]);
     }
-    kf = kn;
+  };
+  // A ring of four key fragments in flight: the load of block kb + 16 is
+  // issued right after block kb has been consumed.  Loads past the last
+  // block re-read the clamped last key and are never used.
+  v4i k0 = kload(wave), k1 = kload(wave + 4), k2 = kload(wave + 8), k3 = kload(wave + 12);
+  for (int32_t kb = wave; kb < nkb; kb += 16) {
+    scores(kb, k0);
+    k0 = kload(kb + 16);
+    if (kb + 4 >= nkb) break;
+    scores(kb + 4, k1);
+    k1 = kload(kb + 20);
+    if (kb + 8 >= nkb) break;
+    scores(kb + 8, k2);
+    k2 = kload(kb + 24);
+    if (kb + 12 >= nkb) break;
+    scores(kb + 12, k3);
+    k3 = kload(kb + 28);
   }
   // row maxima: combine the 4 lanes sharing a row, then the 4 waves
 #pragma unroll
@@ -128,15 +159,16 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
 #pragma unroll
       for (int j = 0; j < JW; ++j) {
         const int32_t wd = k + j * LPR;
-        const uint32_t word = wd < nword ? row[wd] : 0x80808080u;
+        const uint32_t word = row[min(wd, nword - 1)];  // always inside the row
         // max - score per byte: every valid byte is >= 0, and a borrow from
-        // an invalid (higher) byte never reaches a valid one
-        const uint32_t d4 = m4 - (word ^ 0x80808080u);
+        // an invalid (higher) byte never reaches a valid one.  Words past the
+        // window index table entry 255, which is 0.
+        uint32_t d4 = m4 - (word ^ 0x80808080u);
+        if (!RAGGED) d4 = wd * 4 < Tw ? d4 : 0xffffffffu;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           uint32_t ev = elut[(d4 >> (8 * b)) & 255];
-          const bool ok = RAGGED ? (wd * 4 + b < Tw) : (wd * 4 < Tw);
-          ev = ok ? ev : 0u;
+          if (RAGGED) ev = wd * 4 + b < Tw ? ev : 0u;
           e[j][b] = ev;
           if (NARROW) sum32 += ev; else sum += ev;
         }
@@ -149,18 +181,18 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
         sum += ((uint64_t)hi << 32) | lo;
       }
       const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, a.m_p);
-      const uint32_t F = shiftmax_factor(sum, sd);
+      uint64_t sr = sum >> sd;
+      sr = sr < 1 ? 1 : (sr > 0x7fffffffull ? 0x7fffffffull : sr);
+      const uint32_t F = div_2p31m1((uint32_t)sr);
       const int32_t sh = 32 - a.k_out + sd;
 #pragma unroll
       for (int j = 0; j < JW; ++j) {
         const int32_t wd = k + j * LPR;
-        uint32_t outw = 0;
+        uint32_t p[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const uint32_t p = (uint32_t)(((uint64_t)e[j][b] * F) >> sh);
-          outw |= min(p, (uint32_t)pcap) << (8 * b);
-        }
-        if (wd < nword) row[wd] = outw;  // padding columns become 0
+        for (int b = 0; b < 4; ++b)
+          p[b] = min((uint32_t)(((uint64_t)e[j][b] * F) >> sh), (uint32_t)pcap);
+        if (wd < nword) row[wd] = pack_bytes(p[0], p[1], p[2], p[3]);  // padding -> 0
       }
     }
   }
@@ -175,15 +207,29 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   const int32_t c0 = wave * 16;
   const int8_t* vrow = Vt + (int64_t)(c0 + (lane & 15)) * Twp + (lane >> 4) * 16;
   const int8_t* prow = sS + (lane & 15) * lds_row + (lane >> 4) * 16;
-  v4i vf = *(const v4i*)vrow;
-  for (int32_t j0 = 0; j0 < Twp; j0 += 64) {
-    const v4i vn = j0 + 64 < Twp ? *(const v4i*)(vrow + j0 + 64) : zero;  // prefetch
+  const int32_t last = Twp - 64;  // loads past the end re-read the last block
+  auto vload = [&](int32_t j0) { return *(const v4i*)(vrow + min(j0, last)); };
+  auto pv = [&](int32_t j0, const v4i& vf) {
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       const v4i pf = *(const v4i*)(prow + f * 16 * lds_row + j0);
       o[f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(vf, pf, o[f], 0, 0, 0);
     }
-    vf = vn;
+  };
+  // four V^T fragments in flight, as for the keys
+  v4i v0 = vload(0), v1 = vload(64), v2 = vload(128), v3 = vload(192);
+  for (int32_t j0 = 0; j0 < Twp; j0 += 256) {
+    pv(j0, v0);
+    v0 = vload(j0 + 256);
+    if (j0 + 64 >= Twp) break;
+    pv(j0 + 64, v1);
+    v1 = vload(j0 + 320);
+    if (j0 + 128 >= Twp) break;
+    pv(j0 + 128, v2);
+    v2 = vload(j0 + 384);
+    if (j0 + 192 >= Twp) break;
+    pv(j0 + 192, v3);
+    v3 = vload(j0 + 448);
   }
   const int32_t b_img = bw / a.nW, w = bw % a.nW;
   const int32_t wy = w / a.nwx, wx = w % a.nwx;

@@ -5,7 +5,11 @@
 //   y[m][n] = epilogue( rq(bias[n] + sum_k x[m][k] * w[n][k]; mult[n], shift[n]) )
 //
 // Tiling: each wave computes 64 channels x 64 tokens as 4 x 4 tiles of
-// v_mfma_i32_16x16x64_i8; a workgroup holds (TN/64) x (TM/64) waves.  The
+// v_mfma_i32_16x16x64_i8; a workgroup holds WN x WM waves.  Global loads of
+// the next K step are issued before the MFMAs of the current one; they are
+// unconditional (out-of-range rows are clamped onto valid ones and only feed
+// outputs that are never stored), which keeps the memory counters exact and
+// the loads in flight across the MFMAs.  The
 // weight tile is the MFMA A operand (rows = channels) and the activation tile
 // the B operand (columns = tokens), so each lane ends up holding four
 // consecutive channels of one token and stores them as one 32-bit word.  K
@@ -20,6 +24,9 @@
 // accumulator is clamped to a per-channel bound beyond which the result is
 // saturated anyway, after which one 64-bit multiply-add and one shift give the
 // exact rounded value inside int32.
+#include <stdio.h>
+#include <stdlib.h>
+
 #include "ilw_internal.h"
 
 namespace ilw {
@@ -47,7 +54,7 @@ struct ChanRq {
     bias = b;
     rnd = (int64_t)1 << (s - 1);
     const float am = fabsf((float)m);
-    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) / am;
+    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) * __builtin_amdgcn_rcpf(am);
     L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
   }
   __device__ __forceinline__ int32_t apply(int32_t acc) const {
@@ -66,10 +73,10 @@ __device__ __forceinline__ int32_t fdiv(int32_t n, int32_t d, float inv) {
   return q;
 }
 
-template <int TN, int TM, int EPI>
-__global__ __launch_bounds__(TN * TM / 64) void gemm_i8_kernel(GemmArgs a, int32_t tiles_n,
-                                                               int64_t tiles_total) {
-  constexpr int WN = TN / 64, WM = TM / 64, NT = 64 * WN * WM;
+template <int WN, int WM, int EPI, bool KTAIL>
+__global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32_t tiles_n,
+                                                              int64_t tiles_total) {
+  constexpr int TN = 64 * WN, TM = 64 * WM, NT = 64 * WN * WM;
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
   __shared__ int8_t glut[256];
@@ -109,47 +116,63 @@ __global__ __launch_bounds__(TN * TM / 64) void gemm_i8_kernel(GemmArgs a, int32
     for (int j = 0; j < 4; ++j) acc[i][j] = zero;
 
   // Global -> LDS staging: (TN + TM) rows of 64 bytes per K step, 16 bytes
-  // per thread-chunk.
+  // per thread-chunk.  Rows past N or M are clamped onto the last valid row;
+  // with a K tail (K % 64 != 0) chunks past K are zeroed.
   constexpr int CW = TN * 4, CX = TM * 4;  // chunks per operand tile
   constexpr int PW = (CW + NT - 1) / NT, PX = (CX + NT - 1) / NT;
+  const int8_t* wsrc[PW];
+  const int8_t* xsrc[PX];
+  int kofs[PW > PX ? PW : PX];
+#pragma unroll
+  for (int i = 0; i < PW; ++i) {
+    const int c = min(tid + i * NT, CW - 1);
+    wsrc[i] = W + (int64_t)min(n0 + (c >> 2), N - 1) * K + (c & 3) * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < PX; ++i) {
+    const int c = min(tid + i * NT, CX - 1);
+    xsrc[i] = X + min(m0 + (c >> 2), M - 1) * K + (c & 3) * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < (PW > PX ? PW : PX); ++i) kofs[i] = ((tid + i * NT) & 3) * 16;
   v4i rw[PW], rx[PX];
   auto gload = [&](int kt) {
+    const int kb = kt * TK;
 #pragma unroll
     for (int i = 0; i < PW; ++i) {
-      const int c = tid + i * NT;
-      const int k = kt * TK + (c & 3) * 16;
-      const int32_t n = n0 + (c >> 2);
-      rw[i] = (c < CW && n < N && k < K) ? *(const v4i*)(W + (int64_t)n * K + k) : zero;
+      if (KTAIL) {
+        const bool ok = kb + kofs[i] < K;
+        rw[i] = *(const v4i*)(wsrc[i] + (ok ? kb : 0));
+        if (!ok) rw[i] = zero;
+      } else {
+        rw[i] = *(const v4i*)(wsrc[i] + kb);
+      }
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      const int c = tid + i * NT;
-      const int k = kt * TK + (c & 3) * 16;
-      const int64_t m = m0 + (c >> 2);
-      rx[i] = (c < CX && m < M && k < K) ? *(const v4i*)(X + m * K + k) : zero;
+      if (KTAIL) {
+        const bool ok = kb + kofs[i] < K;
+        rx[i] = *(const v4i*)(xsrc[i] + (ok ? kb : 0));
+        if (!ok) rx[i] = zero;
+      } else {
+        rx[i] = *(const v4i*)(xsrc[i] + kb);
+      }
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < PW; ++i) {
       const int c = tid + i * NT;
-      if (c < CW) *(v4i*)(&sW[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rw[i];
+      if (CW % NT == 0 || c < CW) *(v4i*)(&sW[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rw[i];
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
       const int c = tid + i * NT;
-      if (c < CX) *(v4i*)(&sX[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rx[i];
+      if (CX % NT == 0 || c < CX) *(v4i*)(&sX[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rx[i];
     }
   };
-
-  const int nk = (K + TK - 1) / TK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
   const int frag_off = (lane & 15) * LDS_ROW + (lane >> 4) * 16;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
+  auto compute = [&](int buf) {
     v4i fa[4], fb[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -162,7 +185,16 @@ __global__ __launch_bounds__(TN * TM / 64) void gemm_i8_kernel(GemmArgs a, int32
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    if (kt + 1 < nk) sstore(buf ^ 1);
+  };
+
+  const int nk = (K + TK - 1) / TK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload(kt + 1);
+    compute(kt & 1);
+    if (kt + 1 < nk) sstore((kt + 1) & 1);
     __syncthreads();
   }
 
@@ -243,19 +275,26 @@ __global__ __launch_bounds__(TN * TM / 64) void gemm_i8_kernel(GemmArgs a, int32
   }
 }
 
-template <int TN, int TM>
-hipError_t launch_tile(int epi, const GemmArgs& a, hipStream_t s) {
+template <int WN, int WM, bool KT>
+hipError_t launch_tile_k(int epi, const GemmArgs& a, hipStream_t s) {
+  constexpr int TN = 64 * WN, TM = 64 * WM;
   const int32_t tiles_n = (a.N + TN - 1) / TN;
   const int64_t tiles_m = (a.M + TM - 1) / TM;
   const int64_t total = tiles_m * tiles_n;
-  dim3 grid((unsigned)total), block(TN * TM / 64);
+  dim3 grid((unsigned)total), block(64 * WN * WM);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_STORE>), grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_GELU>), grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_RESID>), grid, block, 0, s, a, tiles_n, total); break;
-    default: hipLaunchKernelGGL((gemm_i8_kernel<TN, TM, EPI_QKV>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_STORE, KT>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_GELU: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_GELU, KT>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID, KT>), grid, block, 0, s, a, tiles_n, total); break;
+    default: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_QKV, KT>), grid, block, 0, s, a, tiles_n, total); break;
   }
   return hipGetLastError();
+}
+
+template <int WN, int WM>
+hipError_t launch_tile(int epi, const GemmArgs& a, hipStream_t s) {
+  return a.K % TK == 0 ? launch_tile_k<WN, WM, false>(epi, a, s)
+                       : launch_tile_k<WN, WM, true>(epi, a, s);
 }
 
 }  // namespace
@@ -269,13 +308,32 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     a.inv_wh = 1.0f / (float)a.qkv.win_h;
     a.inv_ww = 1.0f / (float)a.qkv.win_w;
   }
-  // Channel tile: 128 when it divides N, else 64 (N = 192, 576 waste nothing).
-  // Token tile: as large as keeps at least two workgroups per CU busy.
-  const bool n128 = a.N % 128 == 0;
-  const int64_t tiles64 = ((a.M + 63) / 64) * ((a.N + 63) / 64);
-  if (tiles64 < 1024) return launch_tile<64, 64>(epi, a, s);
-  if (n128) return launch_tile<128, 128>(epi, a, s);
-  return launch_tile<64, 256>(epi, a, s);
+  // Tile override for tuning: ILW_GEMM_TILE=<WN>x<WM> (waves along channels
+  // x waves along tokens), read once.
+  static int ov_wn = -1, ov_wm = -1;
+  if (ov_wn < 0) {
+    const char* e = getenv("ILW_GEMM_TILE");
+    ov_wn = ov_wm = 0;
+    if (e && sscanf(e, "%dx%d", &ov_wn, &ov_wm) != 2) ov_wn = ov_wm = 0;
+  }
+  if (ov_wn > 0) {
+    if (ov_wn == 1 && ov_wm == 1) return launch_tile<1, 1>(epi, a, s);
+    if (ov_wn == 1 && ov_wm == 4) return launch_tile<1, 4>(epi, a, s);
+    if (ov_wn == 2 && ov_wm == 2) return launch_tile<2, 2>(epi, a, s);
+    if (ov_wn == 2 && ov_wm == 4) return launch_tile<2, 4>(epi, a, s);
+    if (ov_wn == 3 && ov_wm == 1) return launch_tile<3, 1>(epi, a, s);
+    if (ov_wn == 3 && ov_wm == 2) return launch_tile<3, 2>(epi, a, s);
+  }
+  // Default tiles, from a sweep over the encoder shapes on MI355X: a single
+  // 64 x 64 wave per workgroup when the grid is small (batch 1); otherwise
+  // 192-channel tiles for the deep-K linears and N = 192, and 128 x 256
+  // tiles for the rest.
+  const int64_t big_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  if (big_tiles < 512) return launch_tile<1, 1>(epi, a, s);
+  if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2>(epi, a, s);
+  if (a.N == 192) return launch_tile<3, 1>(epi, a, s);
+  if (a.N % 128 == 0 && a.N >= 1536) return launch_tile<2, 2>(epi, a, s);
+  return launch_tile<2, 4>(epi, a, s);
 }
 
 }  // namespace ilw

@@ -124,6 +124,134 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
   }
 }
 
+// Newton square root with FP64 steps.  k stays >= floor(sqrt(V)) (Newton
+// from above), so floor(V / k) < 2^17 and a refined FP64 reciprocal is
+// within 2^-33 of V / k; with the 2^-20 bias the floor is exact because a
+// non-integer V / k has a fractional part in [2^-16, 1 - 2^-16].
+__device__ __forceinline__ uint32_t newton_isqrt_f64(uint32_t V, int32_t iters) {
+  if (V == 0) return 0;
+  const double Vd = (double)V;
+  double k = 65536.0;
+  for (int32_t t = 0; t < iters; ++t) {
+    double r = __builtin_amdgcn_rcp(k);
+    r = fma(r, fma(-k, r, 1.0), r);
+    const double q = floor(fma(Vd, r, 0x1p-20));
+    k = floor((k + q) * 0.5);
+  }
+  return (uint32_t)k;
+}
+
+// floor((2^31 - 1) / s) for s in [1, 2^31 - 1] from a refined FP64
+// reciprocal and one integer correction.
+__device__ __forceinline__ uint32_t div_2p31m1_ln(uint32_t s) {
+  double r = __builtin_amdgcn_rcp((double)s);
+  r = fma(r, fma(-(double)s, r, 1.0), r);
+  int64_t q = (int64_t)(2147483647.0 * r);
+  const int64_t rem = 2147483647LL - q * (int64_t)s;
+  q += rem < 0 ? -1 : (rem >= (int64_t)s ? 1 : 0);
+  return (uint32_t)q;
+}
+
+// Per-channel output constants: beta, multiplier, shift and the saturation
+// bound L (|t| >= L saturates; any L in [129 * 2^s / |m| + 1, 2^30 * 2^s / |m|]
+// is exact, so an fp32 estimate with margin is used).
+struct LnChan {
+  int32_t beta, mult, shift, L;
+};
+
+// LPR lanes per row for C a multiple of 16 with C / 16 <= 8 * LPR: the row
+// stays in registers (16-byte chunks), sum and sum of squares come from byte
+// dot products, and the per-channel constants are staged in LDS once per
+// workgroup.  V = sum (x - mu)^2 = sum x^2 - 2 mu sum x + C mu^2 (exact).
+// When every |beta| <= 2^30 the output path stays in 32 bits:
+// |n| <= 2^30 so |n + beta| < 2^31, which is clamped to [-L, L] and then
+// requantized with one 64-bit multiply-add.
+template <int LPR>
+__global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, int8_t* y,
+                                                             int64_t rows, int32_t C,
+                                                             const int32_t* beta,
+                                                             const int32_t* mult,
+                                                             const int32_t* shift, int32_t nq,
+                                                             int32_t iters) {
+  extern __shared__ LnChan prm[];
+  constexpr int RG = 64 / LPR, JC = 8;  // rows per wave, max chunks per lane
+  int wide = 0;
+  for (int32_t c = threadIdx.x; c < C; c += 256) {
+    const int32_t q = nq == 1 ? 0 : c;
+    LnChan p;
+    p.beta = beta[c];
+    p.mult = mult[q];
+    p.shift = shift[q];
+    const float am = fabsf((float)p.mult);
+    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
+    p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
+    prm[c] = p;
+    wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
+  }
+  wide = __syncthreads_or(wide);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane / LPR, k = lane % LPR;
+  const int32_t n16 = C >> 4;
+  const int64_t ngroups = (rows + RG - 1) / RG;
+  for (int64_t g = (int64_t)blockIdx.x * 4 + wave; g < ngroups; g += (int64_t)gridDim.x * 4) {
+    const int64_t row = g * RG + sub;
+    const bool live = row < rows;
+    const v4i* xr = (const v4i*)(x + (live ? row : rows - 1) * C);
+    v4i xv[JC];
+    int32_t S = 0, SS = 0;
+#pragma unroll
+    for (int j = 0; j < JC; ++j) {
+      const int32_t ch = k + j * LPR;
+      xv[j] = xr[min(ch, n16 - 1)];
+      if (ch < n16) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          S = __builtin_amdgcn_sdot4(xv[j][w], 0x01010101, S, false);
+          SS = __builtin_amdgcn_sdot4(xv[j][w], xv[j][w], SS, false);
+        }
+      }
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) {
+      S += __shfl_xor(S, o, 64);
+      SS += __shfl_xor(SS, o, 64);
+    }
+    const int32_t mu = mean_half_up(S, C);
+    const uint32_t V = (uint32_t)(SS - 2 * mu * S + C * mu * mu);
+    const uint32_t sigma = newton_isqrt_f64(V, iters);
+    const int32_t F = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+    v4i* yr = (v4i*)(y + (live ? row : rows - 1) * C);
+#pragma unroll
+    for (int j = 0; j < JC; ++j) {
+      const int32_t ch = k + j * LPR;
+      if (ch >= n16) break;
+      v4i o;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        uint32_t ow = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const LnChan p = prm[ch * 16 + w * 4 + b];
+          const int32_t d = (int8_t)(xv[j][w] >> (8 * b)) - mu;
+          const int32_t n = (d * F) >> 1;  // |d| <= sigma: |d * F| < 2^31
+          int32_t r;
+          if (!wide) {
+            const int32_t t = min(max(n + p.beta, -p.L), p.L);
+            r = (int32_t)(((int64_t)t * p.mult + ((int64_t)1 << (p.shift - 1))) >> p.shift);
+            r = min(max(r, kQmin), kQmax);
+          } else {
+            r = ln_out((int64_t)n + p.beta, p.mult, p.shift);
+          }
+          ow |= (uint32_t)(r & 0xff) << (8 * b);
+        }
+        o[w] = (int32_t)ow;
+      }
+      if (live) yr[ch] = o;
+    }
+  }
+}
+
 // Rows longer than 2048 channels: one wave per row, values re-read from
 // memory (L1/L2) for each pass.
 __global__ __launch_bounds__(256) void layernorm_long_kernel(const int8_t* x, int8_t* y,
@@ -273,6 +401,28 @@ hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                             const int32_t* beta, const int32_t* mult, const int32_t* shift,
                             int32_t nq, int32_t iters, hipStream_t s) {
   if (rows == 0) return hipSuccess;
+  // Many rows of the encoder widths: one row per lane.  The 16-byte row
+  // loads need 16-byte aligned rows.
+  if (C % 16 == 0 && C <= 2048 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 15) == 0) {
+    const int32_t n16 = C / 16;
+    // few rows: more lanes per row so that more waves share the work
+    const int lpr = (n16 <= 32 && rows >= 16384) ? 4 : (n16 <= 64 && rows >= 16384 ? 8 : 16);
+    const int64_t groups = (rows + (64 / lpr) - 1) / (64 / lpr);
+    int64_t wgs = (groups + 3) / 4;
+    if (wgs > 1024) wgs = 1024;
+    const size_t smem = (size_t)C * sizeof(LnChan);
+    dim3 grid((unsigned)wgs), block(256);
+    if (lpr == 4)
+      hipLaunchKernelGGL(layernorm_rows_kernel<4>, grid, block, smem, s, x, y, rows, C, beta,
+                         mult, shift, nq, iters);
+    else if (lpr == 8)
+      hipLaunchKernelGGL(layernorm_rows_kernel<8>, grid, block, smem, s, x, y, rows, C, beta,
+                         mult, shift, nq, iters);
+    else
+      hipLaunchKernelGGL(layernorm_rows_kernel<16>, grid, block, smem, s, x, y, rows, C, beta,
+                         mult, shift, nq, iters);
+    return hipGetLastError();
+  }
   const int32_t nw = C / 4;
   if (nw <= 16 * 4) return launch_ln<16, 4>(x, y, rows, C, beta, mult, shift, nq, iters, s);
   if (nw <= 32 * 4) return launch_ln<32, 4>(x, y, rows, C, beta, mult, shift, nq, iters, s);

@@ -161,6 +161,26 @@ def test_layernorm(rows, C, iters, per_tensor):
     assert_same(got, ref, "layernorm")
 
 
+@pytest.mark.parametrize("rows,C", [(8192, 192), (12345, 384), (9001, 48)])
+@pytest.mark.parametrize("iters,per_tensor", [(10, False), (20, True)])
+def test_layernorm_many_rows(rows, C, iters, per_tensor):
+    """Many rows take the one-row-per-lane kernel (sum / sum of squares)."""
+    say(f"layernorm many rows rows={rows} C={C} iters={iters} per_tensor={per_tensor}")
+    g = rng(rows + C)
+    x = g.integers(-128, 128, (rows, C)).astype(np.int8)
+    x[::97] = 3                          # constant rows
+    x[1::89] = g.integers(-1, 2, C)      # tiny variance
+    nq = 1 if per_tensor else C
+    beta = g.integers(-2 ** 31, 2 ** 31, C).astype(np.int32)
+    beta[::2] >>= 6
+    mult = (g.integers(2 ** 29, 2 ** 31, nq) * g.choice([-1, 1], nq)).astype(np.int32)
+    shift = g.integers(44, 63, nq).astype(np.int32)
+    ref = oracle.int_layernorm(x, beta, mult, shift, iters)
+    t = dev(x)
+    got = host(ilw.ilw_int_layernorm(t, dev(beta), dev(mult), dev(shift), iters, y=t))
+    assert_same(got, ref, "layernorm many rows")
+
+
 def test_layernorm_in_place():
     say("layernorm in place")
     g = rng(12)
