@@ -130,11 +130,10 @@ def main():
     enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
     xd = ilw.to_device(x)
     out = torch.empty_like(xd)
-    tmp = torch.empty_like(xd)
     enc.workspace(B)
 
     def eager():
-        enc.forward(xd, out, tmp)
+        enc.forward(xd, out)
 
     step = eager
     if not args.no_graph:

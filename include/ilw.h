@@ -197,6 +197,29 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y,
                       void* stream);
 
 /* ------------------------------------------------------------------------
+ * A stack of n_blocks encoder blocks (the ViT encoder of LW-DETR, Sec. 3.1;
+ * each block as ilw_block_forward), run in one call so that the LayerNorm
+ * after each residual linear can be computed in that linear's epilogue
+ * (dim 192 or 384; other widths run it as a separate kernel, same result).
+ *   blocks  HOST array of n_blocks parameter structs (device pointers inside),
+ *           all with the same dim; n_blocks in [1, 4096].
+ *   windows HOST int32 [n_blocks][2] = (win_h, win_w) of each block's
+ *           attention; (0, 0) = global attention.
+ *   x, y    int8 [batch, grid_h*grid_w, dim]; y may alias x.  Intermediate
+ *           block outputs are written to y.
+ * The workspace (ilw_encoder_workspace_bytes) is the largest block
+ * workspace; it must not alias x or y.  Results are bit-identical to calling
+ * ilw_block_forward block by block.
+ */
+size_t ilw_encoder_workspace_bytes(const ilw_block_params* blocks, int32_t n_blocks,
+                                   const int32_t* windows, int32_t batch, int32_t grid_h,
+                                   int32_t grid_w);
+int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
+                        const int32_t* windows, const int8_t* x, int8_t* y, int32_t batch,
+                        int32_t grid_h, int32_t grid_w, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Multi-scale deformable sampling core of the decoder's cross-attention
  * (Sec. 3.1.1: bilinear interpolation replaced by nearest-neighbour
  * sampling; the attention weights come from Constrained Shiftmax, Sec. 3.3.2):
@@ -224,9 +247,10 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
 
 /* ------------------------------------------------------------------------
  * Per-stage kernel timing (tracing; off by default).  While enabled, every
- * kernel that ilw_block_forward, ilw_attention and ilw_deform_attn launch is
- * bracketed by a pair of HIP events recorded on the caller's stream, and the
- * launch is attributed to one of the stages below.  Enabling (or disabling)
+ * kernel that ilw_block_forward, ilw_encoder_forward, ilw_attention and
+ * ilw_deform_attn launch is bracketed by a pair of HIP events recorded on the
+ * caller's stream, and the launch is attributed to one of the stages below.
+ * Enabling (or disabling)
  * clears the records.  ilw_profile_read waits for the last recorded event and
  * returns, per stage, the summed kernel time in milliseconds and the number of
  * launches (arrays of n_stages entries, HOST memory).  Do not enable it while
@@ -234,12 +258,12 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
  * concurrent launches from several threads while enabled.
  */
 typedef enum {
-  ILW_STAGE_LAYERNORM = 0,   /* both LayerNorms of a block                 */
+  ILW_STAGE_LAYERNORM = 0,   /* stand-alone LayerNorm kernels              */
   ILW_STAGE_GEMM_QKV = 1,    /* QKV linear, window-major scatter epilogue  */
   ILW_STAGE_ATTENTION = 2,   /* fused attention (window and global)        */
-  ILW_STAGE_GEMM_PROJ = 3,   /* projection linear + residual epilogue      */
+  ILW_STAGE_GEMM_PROJ = 3,   /* projection + residual (+ LN2) epilogue     */
   ILW_STAGE_GEMM_FC1 = 4,    /* fc1 linear + SD-ShiftGELU epilogue         */
-  ILW_STAGE_GEMM_FC2 = 5,    /* fc2 linear + residual epilogue             */
+  ILW_STAGE_GEMM_FC2 = 5,    /* fc2 + residual (+ next LN1) epilogue       */
   ILW_STAGE_RELAYOUT = 6,    /* token-major QKV -> window-major copy       */
   ILW_STAGE_DEFORM = 7,      /* deformable sampling                        */
   ILW_NUM_STAGES = 8

@@ -298,6 +298,138 @@ int check_block(const ilw_block_params* p, int32_t batch, int32_t gh, int32_t gw
   return check_geometry(batch, gh, gw, wh, ww, g);
 }
 
+// LayerNorm can be fused into the epilogue of the residual GEMM that
+// produces its input when one workgroup holds whole rows: 3 or 6 waves of 64
+// channels.
+bool ln_fusable(int32_t D) { return D == 192 || D == 384; }
+
+GemmArgs with_ln(GemmArgs a, const int32_t* beta, const ilw_dyadic& out, int32_t iters,
+                 int8_t* y2) {
+  a.y2 = y2;
+  a.ln_beta = beta;
+  a.ln_mult = out.mult;
+  a.ln_shift = out.shift;
+  a.ln_nq = out.n;
+  a.ln_iters = iters;
+  return a;
+}
+
+// One encoder block: h = LN1(x) (unless h already holds it), attention,
+// x1 = Res(proj(att), x) with LN2 fused when possible, fc1 + GELU, and
+// y = Res(fc2(g), x1), which also leaves LN1 of `next` in h when fusable.
+int run_block(const ilw_block_params* p, const ilw_block_params* next, const int8_t* x,
+              int8_t* y, int32_t batch, const Geometry& g, const BlockLayout& L,
+              bool h_ready, hipStream_t s) {
+  const int64_t M = (int64_t)batch * g.T;
+  const int32_t D = p->dim, Hm = p->mlp_dim;
+  const bool fuse = ln_fusable(D);
+  hipError_t he = hipSuccess;
+
+  // h = LN1(x)
+  if (!h_ready) {
+    StageTimer t(ILW_STAGE_LAYERNORM, s);
+    he = launch_layernorm(x, L.h, M, D, p->ln1_beta, p->ln1_out.mult, p->ln1_out.shift,
+                          p->ln1_out.n, p->ln_iters, s);
+    t.done();
+    if (he != hipSuccess) return hip_status(he, "block LN1");
+  }
+  // q, k, v^T = QKV(h), scattered window-major
+  GemmArgs a = gemm_args(L.h, p->w_qkv, p->b_qkv, p->qkv, nullptr, M, 3 * D, D);
+  a.qkv = L.qkv;
+  {
+    StageTimer t(ILW_STAGE_GEMM_QKV, s);
+    he = launch_gemm(EPI_QKV, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block QKV");
+  // att = Attn(q, k, v)
+  {
+    StageTimer t(ILW_STAGE_ATTENTION, s);
+    he = launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block attention");
+  // x1 = Res(proj(att), x);  h = LN2(x1)
+  a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
+  a.resid = x;
+  a.res_ma = p->res1_mult_a;
+  a.res_mb = p->res1_mult_b;
+  a.res_shift = p->res1_shift;
+  {
+    StageTimer t(ILW_STAGE_GEMM_PROJ, s);
+    he = fuse ? launch_gemm(EPI_RESID_LN, with_ln(a, p->ln2_beta, p->ln2_out, p->ln_iters, L.h), s)
+              : launch_gemm(EPI_RESID, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block proj");
+  if (!fuse) {
+    StageTimer t(ILW_STAGE_LAYERNORM, s);
+    he = launch_layernorm(L.x1, L.h, M, D, p->ln2_beta, p->ln2_out.mult, p->ln2_out.shift,
+                          p->ln2_out.n, p->ln_iters, s);
+    t.done();
+    if (he != hipSuccess) return hip_status(he, "block LN2");
+  }
+  // g = rq(SD-ShiftGELU(fc1(h)))
+  a = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
+  a.g_I0 = p->gelu_I0;
+  a.g_kinter = p->gelu_k_inter;
+  a.g_kout = p->gelu_k_out;
+  a.g_mult = p->gelu_mult;
+  a.g_shift = p->gelu_shift;
+  {
+    StageTimer t(ILW_STAGE_GEMM_FC1, s);
+    he = launch_gemm(EPI_GELU, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block fc1");
+  // y = Res(fc2(g), x1);  h = LN1'(y) of the next block
+  a = gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
+  a.resid = L.x1;
+  a.res_ma = p->res2_mult_a;
+  a.res_mb = p->res2_mult_b;
+  a.res_shift = p->res2_shift;
+  {
+    StageTimer t(ILW_STAGE_GEMM_FC2, s);
+    he = next && fuse
+             ? launch_gemm(EPI_RESID_LN,
+                           with_ln(a, next->ln1_beta, next->ln1_out, next->ln_iters, L.h), s)
+             : launch_gemm(EPI_RESID, a, s);
+    t.done();
+  }
+  if (he != hipSuccess) return hip_status(he, "block fc2");
+  return ok();
+}
+
+int check_encoder(const ilw_block_params* blocks, int32_t n_blocks, const int32_t* windows,
+                  int32_t batch, int32_t grid_h, int32_t grid_w) {
+  REQUIRE(blocks && windows, ILW_E_NULL, "blocks and windows (host) must not be NULL");
+  REQUIRE(n_blocks >= 1 && n_blocks <= 4096, ILW_E_SHAPE, "n_blocks = %d must be in [1, 4096]",
+          n_blocks);
+  for (int32_t b = 0; b < n_blocks; ++b) {
+    Geometry g;
+    int e;
+    if ((e = check_block(&blocks[b], batch, grid_h, grid_w, windows[2 * b],
+                         windows[2 * b + 1], &g)))
+      return e;
+    REQUIRE(blocks[b].dim == blocks[0].dim, ILW_E_SHAPE,
+            "block %d has dim %d, block 0 has %d: the residual stream width must not change",
+            b, blocks[b].dim, blocks[0].dim);
+  }
+  return ILW_OK;
+}
+
+size_t encoder_workspace(const ilw_block_params* blocks, int32_t n_blocks,
+                         const int32_t* windows, int32_t batch, int32_t grid_h, int32_t grid_w) {
+  size_t need = 0;
+  for (int32_t b = 0; b < n_blocks; ++b) {
+    Geometry g;
+    check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
+    const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr);
+    need = n > need ? n : need;
+  }
+  return need;
+}
+
 }  // namespace
 
 extern "C" {
@@ -459,80 +591,46 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int
   REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
   BlockLayout L;
   block_layout(p, batch, g, (int8_t*)workspace, &L);
-  hipStream_t s = (hipStream_t)stream;
-  const int64_t M = (int64_t)batch * g.T;
-  const int32_t D = p->dim, Hm = p->mlp_dim;
-  hipError_t he;
+  return run_block(p, nullptr, x, y, batch, g, L, false, (hipStream_t)stream);
+}
 
-  // h = LN1(x)
-  {
-    StageTimer t(ILW_STAGE_LAYERNORM, s);
-    he = launch_layernorm(x, L.h, M, D, p->ln1_beta, p->ln1_out.mult, p->ln1_out.shift,
-                          p->ln1_out.n, p->ln_iters, s);
-    t.done();
+size_t ilw_encoder_workspace_bytes(const ilw_block_params* blocks, int32_t n_blocks,
+                                   const int32_t* windows, int32_t batch, int32_t grid_h,
+                                   int32_t grid_w) {
+  if (check_encoder(blocks, n_blocks, windows, batch, grid_h, grid_w)) return 0;
+  ok();
+  return encoder_workspace(blocks, n_blocks, windows, batch, grid_h, grid_w);
+}
+
+int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
+                        const int32_t* windows, const int8_t* x, int8_t* y, int32_t batch,
+                        int32_t grid_h, int32_t grid_w, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  int e;
+  if ((e = check_encoder(blocks, n_blocks, windows, batch, grid_h, grid_w))) return e;
+  if (batch == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  REQUIRE(aligned16(x) && aligned16(y), ILW_E_PARAM, "x and y must be 16-byte aligned");
+  const size_t need = encoder_workspace(blocks, n_blocks, windows, batch, grid_h, grid_w);
+  REQUIRE(workspace && workspace_bytes >= need, ILW_E_WORKSPACE,
+          "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  // Block b reads its input from x (b = 0) or y and writes y; LN1 of block
+  // b + 1 is produced by the fc2 epilogue of block b when it can be fused,
+  // into the workspace's h buffer, which sits at the same offset in every
+  // block's layout.
+  bool h_ready = false;
+  for (int32_t b = 0; b < n_blocks; ++b) {
+    Geometry g;
+    check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
+    BlockLayout L;
+    block_layout(&blocks[b], batch, g, (int8_t*)workspace, &L);
+    const ilw_block_params* next = b + 1 < n_blocks ? &blocks[b + 1] : nullptr;
+    if ((e = run_block(&blocks[b], next, b == 0 ? x : y, y, batch, g, L, h_ready, s)))
+      return e;
+    h_ready = next && ln_fusable(blocks[b].dim);
   }
-  if (he != hipSuccess) return hip_status(he, "block LN1");
-  // q, k, v^T = QKV(h), scattered window-major
-  GemmArgs a = gemm_args(L.h, p->w_qkv, p->b_qkv, p->qkv, nullptr, M, 3 * D, D);
-  a.qkv = L.qkv;
-  {
-    StageTimer t(ILW_STAGE_GEMM_QKV, s);
-    he = launch_gemm(EPI_QKV, a, s);
-    t.done();
-  }
-  if (he != hipSuccess) return hip_status(he, "block QKV");
-  // att = Attn(q, k, v)
-  {
-    StageTimer t(ILW_STAGE_ATTENTION, s);
-    he = launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s);
-    t.done();
-  }
-  if (he != hipSuccess) return hip_status(he, "block attention");
-  // x1 = Res(proj(att), x)
-  a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
-  a.resid = x;
-  a.res_ma = p->res1_mult_a;
-  a.res_mb = p->res1_mult_b;
-  a.res_shift = p->res1_shift;
-  {
-    StageTimer t(ILW_STAGE_GEMM_PROJ, s);
-    he = launch_gemm(EPI_RESID, a, s);
-    t.done();
-  }
-  if (he != hipSuccess) return hip_status(he, "block proj");
-  // h = LN2(x1)
-  {
-    StageTimer t(ILW_STAGE_LAYERNORM, s);
-    he = launch_layernorm(L.x1, L.h, M, D, p->ln2_beta, p->ln2_out.mult, p->ln2_out.shift,
-                          p->ln2_out.n, p->ln_iters, s);
-    t.done();
-  }
-  if (he != hipSuccess) return hip_status(he, "block LN2");
-  // g = rq(SD-ShiftGELU(fc1(h)))
-  a = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
-  a.g_I0 = p->gelu_I0;
-  a.g_kinter = p->gelu_k_inter;
-  a.g_kout = p->gelu_k_out;
-  a.g_mult = p->gelu_mult;
-  a.g_shift = p->gelu_shift;
-  {
-    StageTimer t(ILW_STAGE_GEMM_FC1, s);
-    he = launch_gemm(EPI_GELU, a, s);
-    t.done();
-  }
-  if (he != hipSuccess) return hip_status(he, "block fc1");
-  // y = Res(fc2(g), x1)
-  a = gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
-  a.resid = L.x1;
-  a.res_ma = p->res2_mult_a;
-  a.res_mb = p->res2_mult_b;
-  a.res_shift = p->res2_shift;
-  {
-    StageTimer t(ILW_STAGE_GEMM_FC2, s);
-    he = launch_gemm(EPI_RESID, a, s);
-    t.done();
-  }
-  if (he != hipSuccess) return hip_status(he, "block fc2");
   return ok();
 }
 

@@ -80,6 +80,9 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
   __shared__ int8_t glut[256];
+  constexpr bool LN = EPI == EPI_RESID_LN;
+  __shared__ LnChan lnp[LN ? TN : 1];        // LayerNorm constants per channel
+  __shared__ int32_t lnred[LN ? 2 * WN * TM : 1];  // per-wave row sums
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -106,6 +109,25 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     // value: tabulate it (with its output requantization) once per workgroup.
     for (int t = tid; t < 256; t += NT)
       glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
+  }
+
+  int ln_wide = 0;
+  if (LN) {
+    // Stage the LayerNorm constants of the N (= TN) channels of the row.
+    for (int c = tid; c < TN; c += NT) {
+      const int q = a.ln_nq == 1 ? 0 : c;
+      LnChan p;
+      p.beta = a.ln_beta[c];
+      p.mult = a.ln_mult[q];
+      p.shift = a.ln_shift[q];
+      const float am = fabsf((float)p.mult);
+      const float bound =
+          am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
+      p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
+      lnp[c] = p;
+      ln_wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
+    }
+    ln_wide = __syncthreads_or(ln_wide);
   }
 
   const v4i zero = {0, 0, 0, 0};
@@ -222,6 +244,11 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       tokv[j] = bw * Lq.H * 64 * Lq.Twp + li;
     }
   }
+  uint32_t xw[4][4];  // RESID_LN: the residual outputs, 4 channels per word
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) xw[i][j] = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int32_t n = n0 + wn * 64 + i * 16 + (lane >> 4) * 4;
@@ -255,13 +282,15 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       } else if (EPI == EPI_GELU) {
         *(uint32_t*)(a.y + tok[j] + n) = pack4(glut[v[0] + 128], glut[v[1] + 128],
                                                glut[v[2] + 128], glut[v[3] + 128]);
-      } else if (EPI == EPI_RESID) {
+      } else if (EPI == EPI_RESID || EPI == EPI_RESID_LN) {
         const uint32_t s = *(const uint32_t*)(a.resid + tok[j] + n);
         int32_t o[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           o[r] = rq2(v[r], (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
-        *(uint32_t*)(a.y + tok[j] + n) = pack4(o[0], o[1], o[2], o[3]);
+        const uint32_t word = pack4(o[0], o[1], o[2], o[3]);
+        *(uint32_t*)(a.y + tok[j] + n) = word;
+        if (LN) xw[i][j] = word;
       } else {  // EPI_QKV: scatter into window-major Q, K and V^T
         if (!is_v) {
           *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(v[0], v[1], v[2], v[3]);
@@ -270,6 +299,72 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 #pragma unroll
           for (int r = 0; r < 4; ++r) dst[(int64_t)r * a.qkv.Twp] = (int8_t)v[r];
         }
+      }
+    }
+  }
+  if (LN) {
+    // LayerNorm of the residual output rows (same reading as the standalone
+    // operator).  A token's N channels sit in 4 lanes of each of the WN waves
+    // along the channels: reduce in the lane (byte dot products), across the
+    // 4 lanes (shuffles), then across the waves (LDS).
+    int32_t S[4], SS[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      S[j] = 0;
+      SS[j] = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        S[j] = __builtin_amdgcn_sdot4((int32_t)xw[i][j], 0x01010101, S[j], false);
+        SS[j] = __builtin_amdgcn_sdot4((int32_t)xw[i][j], (int32_t)xw[i][j], SS[j], false);
+      }
+      S[j] += __shfl_xor(S[j], 16, 64);
+      S[j] += __shfl_xor(S[j], 32, 64);
+      SS[j] += __shfl_xor(SS[j], 16, 64);
+      SS[j] += __shfl_xor(SS[j], 32, 64);
+      const int t = wm * 64 + j * 16 + (lane & 15);
+      if (lane < 16) {
+        lnred[(wn * TM + t) * 2 + 0] = S[j];
+        lnred[(wn * TM + t) * 2 + 1] = SS[j];
+      }
+    }
+    __syncthreads();
+    int32_t mu[4], F[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = wm * 64 + j * 16 + (lane & 15);
+      int32_t s = 0, ss = 0;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) {
+        s += lnred[(w * TM + t) * 2 + 0];
+        ss += lnred[(w * TM + t) * 2 + 1];
+      }
+      mu[j] = mean_half_up(s, N);
+      const uint32_t V = (uint32_t)(ss - 2 * mu[j] * s + N * mu[j] * mu[j]);
+      const uint32_t sigma = newton_isqrt_f64(V, a.ln_iters);
+      F[j] = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int32_t n = wn * 64 + i * 16 + (lane >> 4) * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (!tok_ok[j]) continue;
+        int32_t o[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const LnChan p = lnp[n + r];
+          const int32_t d = (int8_t)(xw[i][j] >> (8 * r)) - mu[j];
+          const int32_t nn = (d * F[j]) >> 1;  // |d| <= sigma: |d * F| < 2^31
+          if (!ln_wide) {
+            const int32_t t = min(max(nn + p.beta, -p.L), p.L);
+            const int32_t v =
+                (int32_t)(((int64_t)t * p.mult + ((int64_t)1 << (p.shift - 1))) >> p.shift);
+            o[r] = min(max(v, kQmin), kQmax);
+          } else {
+            o[r] = ln_out((int64_t)nn + p.beta, p.mult, p.shift);
+          }
+        }
+        *(uint32_t*)(a.y2 + tok[j] + n) = pack4(o[0], o[1], o[2], o[3]);
       }
     }
   }
@@ -282,10 +377,23 @@ hipError_t launch_tile_k(int epi, const GemmArgs& a, hipStream_t s) {
   const int64_t tiles_m = (a.M + TM - 1) / TM;
   const int64_t total = tiles_m * tiles_n;
   dim3 grid((unsigned)total), block(64 * WN * WM);
+  if constexpr (WN == 6) {
+    // Only the fused LayerNorm epilogue of 384-channel rows uses 6 waves.
+    if (epi != EPI_RESID_LN) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID_LN, KT>), grid, block, 0, s, a, tiles_n, total);
+    return hipGetLastError();
+  }
+  if constexpr (WN != 3) {
+    if (epi == EPI_RESID_LN) return hipErrorInvalidValue;  // needs N = 64 * WN
+  }
   switch (epi) {
     case EPI_STORE: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_STORE, KT>), grid, block, 0, s, a, tiles_n, total); break;
     case EPI_GELU: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_GELU, KT>), grid, block, 0, s, a, tiles_n, total); break;
     case EPI_RESID: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID, KT>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_RESID_LN:
+      if constexpr (WN == 3)
+        hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID_LN, KT>), grid, block, 0, s, a, tiles_n, total);
+      break;
     default: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_QKV, KT>), grid, block, 0, s, a, tiles_n, total); break;
   }
   return hipGetLastError();
@@ -307,6 +415,15 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     a.inv_gw = 1.0f / (float)a.qkv.grid_w;
     a.inv_wh = 1.0f / (float)a.qkv.win_h;
     a.inv_ww = 1.0f / (float)a.qkv.win_w;
+  }
+  if (epi == EPI_RESID_LN) {
+    // The workgroup holds whole rows (N channels) so the LayerNorm statistics
+    // stay on chip: 64 tokens per wave row, two wave rows for big deep-K grids.
+    if (a.N == 192)
+      return (a.K >= 768 && (a.M + 127) / 128 * 2 >= 512) ? launch_tile<3, 2>(epi, a, s)
+                                                          : launch_tile<3, 1>(epi, a, s);
+    if (a.N == 384) return launch_tile<6, 1>(epi, a, s);
+    return hipErrorInvalidValue;
   }
   // Tile override for tuning: ILW_GEMM_TILE=<WN>x<WM> (waves along channels
   // x waves along tokens), read once.

@@ -11,44 +11,6 @@ namespace ilw {
 namespace {
 
 // ---------------------------------------------------------------- LayerNorm
-// floor(V / k) for the Newton step.  Newton started at 2^16 >= sqrt(V) never
-// drops below floor(sqrt(V)), so the quotient is below 2^17: an fp32
-// reciprocal estimate is within one of it and one integer correction makes
-// it exact.
-__device__ __forceinline__ uint32_t newton_div(uint32_t V, uint32_t k) {
-  const float qf = (float)V * __builtin_amdgcn_rcpf((float)k);
-  int64_t q = (int64_t)qf;
-  const int64_t r = (int64_t)V - q * (int64_t)k;
-  q += r < 0 ? -1 : (r >= (int64_t)k ? 1 : 0);
-  return (uint32_t)q;
-}
-
-// Integer square root by a fixed number of Newton steps from 2^16.
-__device__ __forceinline__ uint32_t newton_isqrt(uint32_t V, int32_t iters) {
-  if (V == 0) return 0;
-  uint32_t k = 65536;
-  for (int32_t t = 0; t < iters; ++t) k = (k + newton_div(V, k)) >> 1;
-  return k;
-}
-
-// floor((2*sum + C) / (2*C)): the row mean rounded half up.
-__device__ __forceinline__ int32_t mean_half_up(int32_t s, int32_t C) {
-  const int32_t num = 2 * s + C, den = 2 * C;
-  int32_t mu = num / den;
-  if (num % den != 0 && num < 0) mu -= 1;
-  return mu;
-}
-
-// n + beta requantized exactly.  |n| <= 2^30 and |beta| < 2^31 give
-// |t| < 2^32, so u = t * mult fits int64, and
-//   floor((u + 2^(shift-1)) / 2^shift) = ((u >> (shift-1)) + 1) >> 1
-// avoids the rounding add that could overflow.
-__device__ __forceinline__ int32_t ln_out(int64_t t, int32_t mult, int32_t shift) {
-  const int64_t u = t * (int64_t)mult;
-  const int64_t r = ((u >> (shift - 1)) + 1) >> 1;
-  return sat8(r);
-}
-
 // LPR lanes per row, JW words (4 channels each) per lane kept in registers:
 // C <= 4 * LPR * JW.  The per-channel beta / multiplier / shift of a lane's
 // channels are loaded once and reused for every row the wave processes.
@@ -123,41 +85,6 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
     }
   }
 }
-
-// Newton square root with FP64 steps.  k stays >= floor(sqrt(V)) (Newton
-// from above), so floor(V / k) < 2^17 and a refined FP64 reciprocal is
-// within 2^-33 of V / k; with the 2^-20 bias the floor is exact because a
-// non-integer V / k has a fractional part in [2^-16, 1 - 2^-16].
-__device__ __forceinline__ uint32_t newton_isqrt_f64(uint32_t V, int32_t iters) {
-  if (V == 0) return 0;
-  const double Vd = (double)V;
-  double k = 65536.0;
-  for (int32_t t = 0; t < iters; ++t) {
-    double r = __builtin_amdgcn_rcp(k);
-    r = fma(r, fma(-k, r, 1.0), r);
-    const double q = floor(fma(Vd, r, 0x1p-20));
-    k = floor((k + q) * 0.5);
-  }
-  return (uint32_t)k;
-}
-
-// floor((2^31 - 1) / s) for s in [1, 2^31 - 1] from a refined FP64
-// reciprocal and one integer correction.
-__device__ __forceinline__ uint32_t div_2p31m1_ln(uint32_t s) {
-  double r = __builtin_amdgcn_rcp((double)s);
-  r = fma(r, fma(-(double)s, r, 1.0), r);
-  int64_t q = (int64_t)(2147483647.0 * r);
-  const int64_t rem = 2147483647LL - q * (int64_t)s;
-  q += rem < 0 ? -1 : (rem >= (int64_t)s ? 1 : 0);
-  return (uint32_t)q;
-}
-
-// Per-channel output constants: beta, multiplier, shift and the saturation
-// bound L (|t| >= L saturates; any L in [129 * 2^s / |m| + 1, 2^30 * 2^s / |m|]
-// is exact, so an fp32 estimate with margin is used).
-struct LnChan {
-  int32_t beta, mult, shift, L;
-};
 
 // LPR lanes per row for C a multiple of 16 with C / 16 <= 8 * LPR: the row
 // stays in registers (16-byte chunks), sum and sum of squares come from byte

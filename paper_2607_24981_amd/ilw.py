@@ -70,6 +70,9 @@ _SIGS = {
     "ilw_block_workspace_bytes": (c_size, [ctypes.POINTER(BlockParams)] + [c_i32] * 5),
     "ilw_block_forward": (ctypes.c_int, [ctypes.POINTER(BlockParams), c_vp, c_vp] +
                           [c_i32] * 5 + [c_vp, c_size, c_vp]),
+    "ilw_encoder_workspace_bytes": (c_size, [c_vp, c_i32, c_vp, c_i32, c_i32, c_i32]),
+    "ilw_encoder_forward": (ctypes.c_int, [c_vp, c_i32, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32,
+                                           c_vp, c_size, c_vp]),
     "ilw_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "ilw_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(c_i32), c_i32]),
@@ -280,35 +283,48 @@ def ilw_block_forward(block: DeviceBlock, x, grid_h, grid_w, win_h, win_w, y=Non
 
 
 class Encoder:
-    """A stack of integer encoder blocks sharing one workspace."""
+    """A stack of integer encoder blocks run by ilw_encoder_forward."""
 
     def __init__(self, blocks: list, windows: list, grid_h: int, grid_w: int,
                  device="cuda"):
-        self.blocks = [DeviceBlock(p, device) for p in blocks]
-        self.windows = list(windows)
+        self.blocks = [b if isinstance(b, DeviceBlock) else DeviceBlock(b, device)
+                       for b in blocks]
+        self.windows = [tuple(int(v) for v in w) for w in windows]
+        assert len(self.windows) == len(self.blocks)
         self.grid_h, self.grid_w = grid_h, grid_w
         self.device = device
+        n = len(self.blocks)
+        self._structs = (BlockParams * n)(*[b.struct for b in self.blocks])
+        self._win = np.ascontiguousarray(np.asarray(self.windows, np.int32).reshape(n, 2))
         self._ws = None
 
+    def workspace_bytes(self, B) -> int:
+        n = lib().ilw_encoder_workspace_bytes(ctypes.addressof(self._structs), len(self.blocks),
+                                              self._win.ctypes.data_as(c_vp), B, self.grid_h,
+                                              self.grid_w)
+        if n == 0 and B > 0:
+            raise IlwError(f"ilw_encoder_workspace_bytes: {last_error()}")
+        return n
+
     def workspace(self, B):
-        need = max(b.workspace_bytes(B, self.grid_h, self.grid_w, *w)
-                   for b, w in zip(self.blocks, self.windows))
+        need = self.workspace_bytes(B)
         if self._ws is None or self._ws.numel() < need:
             self._ws = torch.empty(max(need, 16), dtype=torch.int8, device=self.device)
         return self._ws
 
-    def forward(self, x, out=None, tmp=None):
-        """Runs every block; ping-pongs between `out` and `tmp` buffers."""
+    def forward(self, x, out=None):
+        """x int8 [B, T, D] -> int8 [B, T, D] (out may be x)."""
         ws = self.workspace(x.shape[0])
-        bufs = [out if out is not None else torch.empty_like(x),
-                tmp if tmp is not None else torch.empty_like(x)]
-        cur = x
-        n = len(self.blocks)
-        for i, (blk, w) in enumerate(zip(self.blocks, self.windows)):
-            dst = bufs[(n - 1 - i) % 2]  # the last block writes bufs[0]
-            ilw_block_forward(blk, cur, self.grid_h, self.grid_w, *w, y=dst, workspace=ws)
-            cur = dst
-        return cur
+        if out is None:
+            out = torch.empty_like(x)
+        rc = lib().ilw_encoder_forward(ctypes.addressof(self._structs), len(self.blocks),
+                                       self._win.ctypes.data_as(c_vp),
+                                       _dev(x, torch.int8, "x"), _dev(out, torch.int8, "out"),
+                                       x.shape[0], self.grid_h, self.grid_w,
+                                       _dev(ws, torch.int8, "workspace"), ws.numel(),
+                                       _stream())
+        _check(rc, "ilw_encoder_forward")
+        return out
 
 
 def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,

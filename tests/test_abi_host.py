@@ -150,6 +150,38 @@ def test_block_workspace_and_validation():
                                None) == OK
 
 
+def test_encoder_workspace_and_validation():
+    L = ilw.lib()
+    blocks = (ilw.BlockParams * 3)(_block_struct(), _block_struct(), _block_struct())
+    win = (ctypes.c_int32 * 6)(20, 20, 0, 0, 20, 20)
+    n = L.ilw_encoder_workspace_bytes(blocks, 3, win, 2, 40, 40)
+    one = max(L.ilw_block_workspace_bytes(ctypes.byref(_block_struct()), 2, 40, 40, w, w)
+              for w in (0, 20))
+    assert n == one
+    assert L.ilw_encoder_forward(blocks, 3, win, FAKE, FAKE, 2, 40, 40, FAKE, n - 1,
+                                 None) == E_WS
+    assert L.ilw_encoder_forward(blocks, 3, None, FAKE, FAKE, 2, 40, 40, FAKE, n,
+                                 None) == E_NULL
+    assert L.ilw_encoder_forward(blocks, 0, win, FAKE, FAKE, 2, 40, 40, FAKE, n,
+                                 None) == E_SHAPE
+    assert L.ilw_encoder_forward(blocks, 3, win, FAKE, FAKE, 0, 40, 40, None, 0, None) == OK
+    # every block is validated; the residual width must not change
+    mixed = (ilw.BlockParams * 2)(_block_struct(),
+                                  _block_struct(dim=384, heads=6,
+                                                ln1_out=ilw.Dyadic(FAKE, FAKE, 384),
+                                                ln2_out=ilw.Dyadic(FAKE, FAKE, 384),
+                                                qkv=ilw.Dyadic(FAKE, FAKE, 1152)))
+    assert L.ilw_encoder_forward(mixed, 2, win, FAKE, FAKE, 2, 40, 40, FAKE, 1 << 30,
+                                 None) == E_SHAPE
+    assert "residual stream" in ilw.last_error()
+    bad = (ilw.BlockParams * 2)(_block_struct(), _block_struct(gelu_I0=0))
+    assert L.ilw_encoder_forward(bad, 2, win, FAKE, FAKE, 2, 40, 40, FAKE, 1 << 30,
+                                 None) == E_PARAM
+    badwin = (ctypes.c_int32 * 4)(20, 20, 30, 30)
+    assert L.ilw_encoder_forward(blocks, 2, badwin, FAKE, FAKE, 2, 40, 40, FAKE, 1 << 30,
+                                 None) == E_SHAPE
+
+
 def test_attention_and_deform_validation():
     L = ilw.lib()
     ap = ilw.AttnParams(1 << 30, 36, 16, 16, 8, 4, -1, 1 << 30, 36)

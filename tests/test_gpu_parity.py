@@ -318,6 +318,83 @@ def test_encoder_c3_sampled():
         assert_same(full[b:b + 1], one, f"batch independence image {b}")
 
 
+def _encoder_case(D, H, Hm, depth, seed, variant="wide"):
+    g = rng(seed)
+    return [synth.block_params(g, D, H, 64, Hm, variant, ln_iters=12 + 4 * (i % 2),
+                               smax_s_d=(-1 if i % 2 == 0 else 3)) for i in range(depth)]
+
+
+@pytest.mark.parametrize("D,H,Hm,grid,windows,B", [
+    # 192 and 384 channels: LayerNorm fused into the residual linears
+    (192, 3, 768, (9, 12), [(3, 4), (0, 0), (9, 6)], 2),
+    (384, 6, 1536, (7, 10), [(0, 0), (7, 5), (0, 0)], 3),
+    # 256 channels: stand-alone LayerNorm kernels
+    (256, 4, 512, (6, 6), [(3, 3), (0, 0)], 2),
+    # one block: no next block to fuse LN1 into
+    (192, 3, 384, (8, 8), [(4, 4)], 1),
+])
+def test_encoder_shapes(D, H, Hm, grid, windows, B):
+    """ilw_encoder_forward on ragged token counts against the oracle block
+    chain, once into a fresh output and once in place."""
+    say(f"encoder D={D} mlp={Hm} grid={grid} windows={windows} B={B}")
+    blocks = _encoder_case(D, H, Hm, len(windows), D + Hm + B)
+    x = rng(D + 1).integers(-127, 128, (B, grid[0] * grid[1], D)).astype(np.int8)
+    ref = encoder_ref(blocks, windows, x, *grid)
+    enc = ilw.Encoder(blocks, windows, *grid)
+    assert_same(host(enc.forward(dev(x))), ref, "encoder")
+    t = dev(x)
+    assert_same(host(enc.forward(t, out=t)), ref, "encoder in place")
+
+
+@pytest.mark.parametrize("D,H", [(192, 3), (384, 6)])
+def test_encoder_fused_layernorm_edge_params(D, H):
+    """The fused LayerNorm epilogue with per-tensor output constants, |beta|
+    beyond 2^30 (the 64-bit output path) and one constant input row (zero
+    variance)."""
+    say(f"encoder fused LN edge parameters D={D}")
+    blocks = _encoder_case(D, H, 2 * D, 3, 40 + D)
+    g = rng(D)
+    blocks[1]["ln1_mult"] = blocks[1]["ln1_mult"][:1].copy()
+    blocks[1]["ln1_shift"] = blocks[1]["ln1_shift"][:1].copy()
+    blocks[1]["ln2_beta"] = g.integers(-2 ** 31 + 1, 2 ** 31 - 1, D).astype(np.int32)
+    blocks[2]["ln1_beta"][:4] = [2 ** 31 - 1, -(2 ** 31) + 1, 2 ** 30 + 1, -(2 ** 30) - 1]
+    grid, windows = (6, 9), [(3, 3), (0, 0), (2, 3)]
+    x = g.integers(-127, 128, (2, 54, D)).astype(np.int8)
+    x[1, 7] = 5
+    ref = encoder_ref(blocks, windows, x, *grid)
+    enc = ilw.Encoder(blocks, windows, *grid)
+    assert_same(host(enc.forward(dev(x))), ref, "encoder LN edge parameters")
+
+
+def test_encoder_big_grid_sampled():
+    """A grid large enough for the two-wave-row fused fc2 tile (192 channels,
+    deep K), with a ragged token count: sampled images against the oracle."""
+    grid, windows = (20, 20), [(10, 10), (0, 0)]
+    B = 83  # 33200 tokens: not a multiple of 128
+    say(f"encoder big grid B={B}")
+    blocks = _encoder_case(192, 3, 768, 2, 77)
+    x = rng(78).integers(-127, 128, (B, 400, 192)).astype(np.int8)
+    enc = ilw.Encoder(blocks, windows, *grid)
+    full = host(enc.forward(dev(x)))
+    for b in (0, 41, 82):
+        ref = encoder_ref(blocks, windows, x[b:b + 1], *grid)
+        assert_same(full[b:b + 1], ref, f"image {b}")
+
+
+def test_encoder_matches_block_by_block():
+    """The encoder entry point (fused LayerNorms) and the block entry point
+    give the same bytes."""
+    wl = synth.WORKLOADS["encoder_t1600_d192_b1"]
+    say("encoder vs block-by-block")
+    blocks, x = synth.encoder_inputs(wl, 9, "baseline", batch=3)
+    enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
+    a = host(enc.forward(dev(x)))
+    t = dev(x)
+    for blk, w in zip(enc.blocks, wl.windows):
+        ilw.ilw_block_forward(blk, t, wl.grid_h, wl.grid_w, *w, y=t)
+    assert_same(host(t), a, "encoder vs blocks")
+
+
 def test_encoder_deterministic():
     wl = synth.WORKLOADS["encoder_t1600_d192_b1"]
     say("encoder determinism")
@@ -370,20 +447,20 @@ def test_encoder_graph_replay():
     blocks, x = synth.encoder_inputs(wl, 6, "wide", batch=2)
     enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
     xd = dev(x)
-    out, tmp = torch.empty_like(xd), torch.empty_like(xd)
-    ref = host(enc.forward(xd, out, tmp)).copy()
+    out = torch.empty_like(xd)
+    ref = host(enc.forward(xd, out)).copy()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
-        enc.forward(xd, out, tmp)
+        enc.forward(xd, out)
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        enc.forward(xd, out, tmp)
+        enc.forward(xd, out)
     for i in range(4):
         out.fill_(0)
-        tmp.fill_(0)
+        enc.workspace(2).fill_(0)
         g.replay()
         torch.cuda.synchronize()
         assert_same(host(out), ref, f"replay {i}")
