@@ -3,6 +3,7 @@
 // kernel launches on the caller's stream.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 
 #include <mutex>
 #include <string>
@@ -301,7 +302,16 @@ int check_block(const ilw_block_params* p, int32_t batch, int32_t gh, int32_t gw
 // LayerNorm can be fused into the epilogue of the residual GEMM that
 // produces its input when one workgroup holds whole rows: 3 or 6 waves of 64
 // channels.
-bool ln_fusable(int32_t D) { return D == 192 || D == 384; }
+// ILW_FUSE_LN=0 runs every LayerNorm as its own kernel (same results; for
+// comparisons), read once.
+bool ln_fusable(int32_t D) {
+  static int on = -1;
+  if (on < 0) {
+    const char* e = getenv("ILW_FUSE_LN");
+    on = (e && e[0] == '0') ? 0 : 1;
+  }
+  return on && (D == 192 || D == 384);
+}
 
 GemmArgs with_ln(GemmArgs a, const int32_t* beta, const ilw_dyadic& out, int32_t iters,
                  int8_t* y2) {

@@ -73,15 +73,23 @@ __device__ __forceinline__ int32_t fdiv(int32_t n, int32_t d, float inv) {
   return q;
 }
 
-template <int WN, int WM, int EPI, bool KTAIL>
+// WN x WM waves per workgroup; each wave computes FI x FJ MFMA tiles of 16
+// channels x 16 tokens.  PF register slots of staged operands (PF > 1 is the
+// latency mode for small grids: PF K steps of loads in flight, and every
+// epilogue input -- channel constants, residual words -- loaded before the
+// main loop so that the kernel pays about one memory round trip).
+template <int WN, int WM, int FI, int FJ, int EPI, bool KTAIL, int PF>
 __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32_t tiles_n,
                                                               int64_t tiles_total) {
-  constexpr int TN = 64 * WN, TM = 64 * WM, NT = 64 * WN * WM;
+  constexpr int WTN = 16 * FI, WTM = 16 * FJ;  // wave tile
+  constexpr int TN = WTN * WN, TM = WTM * WM, NT = 64 * WN * WM;
+  constexpr bool LN = EPI == EPI_RESID_LN;
+  constexpr bool RES = EPI == EPI_RESID || LN;
+  constexpr bool EARLY = PF > 1;
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
-  __shared__ int8_t glut[256];
-  constexpr bool LN = EPI == EPI_RESID_LN;
-  __shared__ LnChan lnp[LN ? TN : 1];        // LayerNorm constants per channel
+  __shared__ int8_t glut[EPI == EPI_GELU ? 256 : 1];
+  __shared__ LnChan lnp[LN ? TN : 1];              // LayerNorm constants per channel
   __shared__ int32_t lnred[LN ? 2 * WN * TM : 1];  // per-wave row sums
 
   const int tid = threadIdx.x;
@@ -103,39 +111,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   const int8_t* __restrict__ W = a.w;
   const int64_t M = a.M;
   const int32_t N = a.N, K = a.K;
-
-  if (EPI == EPI_GELU) {
-    // SD-ShiftGELU of the requantized fc1 output is a function of one int8
-    // value: tabulate it (with its output requantization) once per workgroup.
-    for (int t = tid; t < 256; t += NT)
-      glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
-  }
-
-  int ln_wide = 0;
-  if (LN) {
-    // Stage the LayerNorm constants of the N (= TN) channels of the row.
-    for (int c = tid; c < TN; c += NT) {
-      const int q = a.ln_nq == 1 ? 0 : c;
-      LnChan p;
-      p.beta = a.ln_beta[c];
-      p.mult = a.ln_mult[q];
-      p.shift = a.ln_shift[q];
-      const float am = fabsf((float)p.mult);
-      const float bound =
-          am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
-      p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
-      lnp[c] = p;
-      ln_wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
-    }
-    ln_wide = __syncthreads_or(ln_wide);
-  }
-
   const v4i zero = {0, 0, 0, 0};
-  v4i acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = zero;
 
   // Global -> LDS staging: (TN + TM) rows of 64 bytes per K step, 16 bytes
   // per thread-chunk.  Rows past N or M are clamped onto the last valid row;
@@ -157,81 +133,111 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   }
 #pragma unroll
   for (int i = 0; i < (PW > PX ? PW : PX); ++i) kofs[i] = ((tid + i * NT) & 3) * 16;
-  v4i rw[PW], rx[PX];
-  auto gload = [&](int kt) {
+  // The loads of K step k go to register slot k % PF.
+  v4i rw[PF][PW], rx[PF][PX];
+  const int nk = (K + TK - 1) / TK;
+  auto gload = [&](int kt, int sl) {
     const int kb = kt * TK;
 #pragma unroll
     for (int i = 0; i < PW; ++i) {
       if (KTAIL) {
         const bool ok = kb + kofs[i] < K;
-        rw[i] = *(const v4i*)(wsrc[i] + (ok ? kb : 0));
-        if (!ok) rw[i] = zero;
+        rw[sl][i] = *(const v4i*)(wsrc[i] + (ok ? kb : 0));
+        if (!ok) rw[sl][i] = zero;
       } else {
-        rw[i] = *(const v4i*)(wsrc[i] + kb);
+        rw[sl][i] = *(const v4i*)(wsrc[i] + kb);
       }
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
       if (KTAIL) {
         const bool ok = kb + kofs[i] < K;
-        rx[i] = *(const v4i*)(xsrc[i] + (ok ? kb : 0));
-        if (!ok) rx[i] = zero;
+        rx[sl][i] = *(const v4i*)(xsrc[i] + (ok ? kb : 0));
+        if (!ok) rx[sl][i] = zero;
       } else {
-        rx[i] = *(const v4i*)(xsrc[i] + kb);
+        rx[sl][i] = *(const v4i*)(xsrc[i] + kb);
       }
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](int buf, int sl) {
 #pragma unroll
     for (int i = 0; i < PW; ++i) {
       const int c = tid + i * NT;
-      if (CW % NT == 0 || c < CW) *(v4i*)(&sW[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rw[i];
+      if (CW % NT == 0 || c < CW)
+        *(v4i*)(&sW[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rw[sl][i];
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
       const int c = tid + i * NT;
-      if (CX % NT == 0 || c < CX) *(v4i*)(&sX[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rx[i];
+      if (CX % NT == 0 || c < CX)
+        *(v4i*)(&sX[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rx[sl][i];
     }
   };
-  const int frag_off = (lane & 15) * LDS_ROW + (lane >> 4) * 16;
-  auto compute = [&](int buf) {
-    v4i fa[4], fb[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      fa[i] = *(const v4i*)(&sW[buf][(wn * 64 + i * 16) * LDS_ROW + frag_off]);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fb[j] = *(const v4i*)(&sX[buf][(wm * 64 + j * 16) * LDS_ROW + frag_off]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
-  };
 
-  const int nk = (K + TK - 1) / TK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(kt + 1);
-    compute(kt & 1);
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
-    __syncthreads();
+  // Operand loads first: everything below overlaps with their latency.
+  if constexpr (PF == 1) {
+    gload(0, 0);
+  } else {
+#pragma unroll
+    for (int d = 0; d < PF; ++d) gload(min(d, nk - 1), d);
   }
 
-  // Epilogue.  Lane holds channels n..n+3 (n = 4*(lane/16) within a 16-tile)
-  // of token lane%16 of each of the 4 x 4 tiles.
-  int64_t tok[4];      // per token: output row (STORE/GELU/RESID) or Q/K offset (QKV)
-  int64_t tokv[4];     // QKV: V^T offset of the token
-  bool tok_ok[4];
+  // Output coordinates.  Lane holds channels n..n+3 (n = 4*(lane/16) within a
+  // 16-tile) of token lane%16 of each of the FI x FJ tiles.
+  int32_t nch[FI];
+  bool ch_ok[FI];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t m = m0 + wm * 64 + j * 16 + (lane & 15);
+  for (int i = 0; i < FI; ++i) {
+    nch[i] = n0 + wn * WTN + i * 16 + (lane >> 4) * 4;
+    ch_ok[i] = nch[i] < N;  // N is a multiple of 16: the 4 channels are all valid
+  }
+  int64_t tok[FJ];   // per token: output row (STORE/GELU/RESID) or Q/K offset (QKV)
+  int64_t tokv[FJ];  // QKV: V^T offset of the token
+  bool tok_ok[FJ];
+#pragma unroll
+  for (int j = 0; j < FJ; ++j) {
+    const int64_t m = m0 + wm * WTM + j * 16 + (lane & 15);
     tok_ok[j] = m < M;
     tok[j] = m * N;
     tokv[j] = 0;
-    if (EPI == EPI_QKV && tok_ok[j]) {
+  }
+
+  // Channel constants and residual words (latency mode: loaded now).
+  int32_t pm[FI][4], ps[FI][4], pb[FI][4];
+  uint32_t rs[FI][FJ];
+  auto load_chan = [&](int i) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qi = a.nq == 1 ? 0 : min(nch[i], N - 4) + r;
+      pm[i][r] = a.mult[qi];
+      ps[i][r] = a.shift[qi];
+      pb[i][r] = a.bias ? a.bias[min(nch[i], N - 4) + r] : 0;
+    }
+  };
+  auto load_resid = [&](int i) {
+#pragma unroll
+    for (int j = 0; j < FJ; ++j)
+      rs[i][j] = *(const uint32_t*)(a.resid + min(tok[j], (M - 1) * N) + min(nch[i], N - 4));
+  };
+  if (EARLY) {
+#pragma unroll
+    for (int i = 0; i < FI; ++i) {
+      load_chan(i);
+      if (RES) load_resid(i);
+    }
+  }
+
+  if (EPI == EPI_GELU) {
+    // SD-ShiftGELU of the requantized fc1 output is a function of one int8
+    // value: tabulate it (with its output requantization) once per workgroup.
+    for (int t = tid; t < 256; t += NT)
+      glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
+  }
+  if (EPI == EPI_QKV) {
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) {
+      const int64_t m = m0 + wm * WTM + j * 16 + (lane & 15);
+      if (!tok_ok[j]) continue;
       const QkvLayout& Lq = a.qkv;
       const int32_t b = fdiv((int32_t)m, Lq.T, a.inv_T);
       const int32_t t = (int32_t)m - b * Lq.T;
@@ -244,21 +250,92 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       tokv[j] = bw * Lq.H * 64 * Lq.Twp + li;
     }
   }
-  uint32_t xw[4][4];  // RESID_LN: the residual outputs, 4 channels per word
+  int ln_wide = 0;
+  if (LN) {
+    // Stage the LayerNorm constants of the N (= TN) channels of the row.
+    for (int c = tid; c < TN; c += NT) {
+      const int q = a.ln_nq == 1 ? 0 : c;
+      LnChan p;
+      p.beta = a.ln_beta[c];
+      p.mult = a.ln_mult[q];
+      p.shift = a.ln_shift[q];
+      const float am = fabsf((float)p.mult);
+      const float bound =
+          am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
+      p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
+      lnp[c] = p;
+      ln_wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
+    }
+  }
+
+  v4i acc[FI][FJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) xw[i][j] = 0;
+    for (int j = 0; j < FJ; ++j) acc[i][j] = zero;
+  const int frag_off = (lane & 15) * LDS_ROW + (lane >> 4) * 16;
+  auto compute = [&](int buf) {
+    v4i fa[FI], fb[FJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int32_t n = n0 + wn * 64 + i * 16 + (lane >> 4) * 4;
-    if (n >= N) continue;  // N is a multiple of 16: the 4 channels are all valid
+    for (int i = 0; i < FI; ++i)
+      fa[i] = *(const v4i*)(&sW[buf][(wn * WTN + i * 16) * LDS_ROW + frag_off]);
+#pragma unroll
+    for (int j = 0; j < FJ; ++j)
+      fb[j] = *(const v4i*)(&sX[buf][(wm * WTM + j * 16) * LDS_ROW + frag_off]);
+#pragma unroll
+    for (int i = 0; i < FI; ++i)
+#pragma unroll
+      for (int j = 0; j < FJ; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+
+  if constexpr (PF == 1) {
+    sstore(0, 0);
+    if (LN) ln_wide = __syncthreads_or(ln_wide);
+    else __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 1 < nk) gload(kt + 1, 0);
+      compute(kt & 1);
+      if (kt + 1 < nk) sstore((kt + 1) & 1, 0);
+      __syncthreads();
+    }
+  } else {
+    // Loads are issued on every path (steps past the end re-read the last
+    // one), so the memory counter wait before each LDS store is exact: it
+    // leaves the younger slots' loads in flight.
+    sstore(0, 0);
+    if (LN) ln_wide = __syncthreads_or(ln_wide);
+    else __syncthreads();
+    gload(min(PF, nk - 1), 0);
+    for (int kt0 = 0; kt0 < nk; kt0 += PF) {
+#pragma unroll
+      for (int u = 0; u < PF; ++u) {
+        const int kt = kt0 + u;
+        if (kt < nk) compute(kt & 1);
+        sstore((kt + 1) & 1, (u + 1) % PF);
+        gload(min(kt + 1 + PF, nk - 1), (u + 1) % PF);
+        __syncthreads();
+      }
+    }
+  }
+
+  // Epilogue.
+  uint32_t xw[FI][FJ];  // RESID_LN: the residual outputs, 4 channels per word
+#pragma unroll
+  for (int i = 0; i < FI; ++i)
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) xw[i][j] = 0;
+#pragma unroll
+  for (int i = 0; i < FI; ++i) {
+    if (!ch_ok[i]) continue;
+    const int32_t n = nch[i];
+    if (!EARLY) {
+      load_chan(i);
+      if (RES) load_resid(i);
+    }
     ChanRq cr[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qi = a.nq == 1 ? 0 : n + r;
-      cr[r].init(a.mult[qi], a.shift[qi], a.bias ? a.bias[n + r] : 0);
-    }
+    for (int r = 0; r < 4; ++r) cr[r].init(pm[i][r], ps[i][r], pb[i][r]);
     int8_t* qk_base = nullptr;
     int64_t ch_qk = 0, ch_v = 0;
     bool is_v = false;
@@ -272,7 +349,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       ch_v = ((int64_t)h * 64 + c) * Lq.Twp;
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < FJ; ++j) {
       if (!tok_ok[j]) continue;
       int32_t v[4];
 #pragma unroll
@@ -282,8 +359,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       } else if (EPI == EPI_GELU) {
         *(uint32_t*)(a.y + tok[j] + n) = pack4(glut[v[0] + 128], glut[v[1] + 128],
                                                glut[v[2] + 128], glut[v[3] + 128]);
-      } else if (EPI == EPI_RESID || EPI == EPI_RESID_LN) {
-        const uint32_t s = *(const uint32_t*)(a.resid + tok[j] + n);
+      } else if (RES) {
+        const uint32_t s = rs[i][j];
         int32_t o[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -307,47 +384,53 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     // operator).  A token's N channels sit in 4 lanes of each of the WN waves
     // along the channels: reduce in the lane (byte dot products), across the
     // 4 lanes (shuffles), then across the waves (LDS).
-    int32_t S[4], SS[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      S[j] = 0;
-      SS[j] = 0;
+    for (int j = 0; j < FJ; ++j) {
+      int32_t S = 0, SS = 0;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        S[j] = __builtin_amdgcn_sdot4((int32_t)xw[i][j], 0x01010101, S[j], false);
-        SS[j] = __builtin_amdgcn_sdot4((int32_t)xw[i][j], (int32_t)xw[i][j], SS[j], false);
+      for (int i = 0; i < FI; ++i) {
+        S = __builtin_amdgcn_sdot4((int32_t)xw[i][j], 0x01010101, S, false);
+        SS = __builtin_amdgcn_sdot4((int32_t)xw[i][j], (int32_t)xw[i][j], SS, false);
       }
-      S[j] += __shfl_xor(S[j], 16, 64);
-      S[j] += __shfl_xor(S[j], 32, 64);
-      SS[j] += __shfl_xor(SS[j], 16, 64);
-      SS[j] += __shfl_xor(SS[j], 32, 64);
-      const int t = wm * 64 + j * 16 + (lane & 15);
+      S += __shfl_xor(S, 16, 64);
+      S += __shfl_xor(S, 32, 64);
+      SS += __shfl_xor(SS, 16, 64);
+      SS += __shfl_xor(SS, 32, 64);
+      const int t = wm * WTM + j * 16 + (lane & 15);
       if (lane < 16) {
-        lnred[(wn * TM + t) * 2 + 0] = S[j];
-        lnred[(wn * TM + t) * 2 + 1] = SS[j];
+        lnred[(wn * TM + t) * 2 + 0] = S;
+        lnred[(wn * TM + t) * 2 + 1] = SS;
       }
     }
     __syncthreads();
-    int32_t mu[4], F[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = wm * 64 + j * 16 + (lane & 15);
+    // Row statistics with one token per lane (the Newton steps form a serial
+    // dependency chain; one chain per lane keeps it short), then each lane
+    // fetches those of its FJ tokens.
+    int32_t mu_l, F_l;
+    {
+      const int t = wm * WTM + min(lane, WTM - 1);
       int32_t s = 0, ss = 0;
 #pragma unroll
       for (int w = 0; w < WN; ++w) {
         s += lnred[(w * TM + t) * 2 + 0];
         ss += lnred[(w * TM + t) * 2 + 1];
       }
-      mu[j] = mean_half_up(s, N);
-      const uint32_t V = (uint32_t)(ss - 2 * mu[j] * s + N * mu[j] * mu[j]);
+      mu_l = mean_half_up(s, N);
+      const uint32_t V = (uint32_t)(ss - 2 * mu_l * s + N * mu_l * mu_l);
       const uint32_t sigma = newton_isqrt_f64(V, a.ln_iters);
-      F[j] = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+      F_l = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+    }
+    int32_t mu[FJ], F[FJ];
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) {
+      mu[j] = __shfl(mu_l, j * 16 + (lane & 15), 64);
+      F[j] = __shfl(F_l, j * 16 + (lane & 15), 64);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int32_t n = wn * 64 + i * 16 + (lane >> 4) * 4;
+    for (int i = 0; i < FI; ++i) {
+      const int32_t n = wn * WTN + i * 16 + (lane >> 4) * 4;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < FJ; ++j) {
         if (!tok_ok[j]) continue;
         int32_t o[4];
 #pragma unroll
@@ -370,39 +453,60 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   }
 }
 
-template <int WN, int WM, bool KT>
-hipError_t launch_tile_k(int epi, const GemmArgs& a, hipStream_t s) {
-  constexpr int TN = 64 * WN, TM = 64 * WM;
+template <int WN, int WM, int FI, int FJ, bool KT, int PF>
+hipError_t launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
+  constexpr int TN = 16 * FI * WN, TM = 16 * FJ * WM;
   const int32_t tiles_n = (a.N + TN - 1) / TN;
   const int64_t tiles_m = (a.M + TM - 1) / TM;
   const int64_t total = tiles_m * tiles_n;
   dim3 grid((unsigned)total), block(64 * WN * WM);
-  if constexpr (WN == 6) {
-    // Only the fused LayerNorm epilogue of 384-channel rows uses 6 waves.
-    if (epi != EPI_RESID_LN) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID_LN, KT>), grid, block, 0, s, a, tiles_n, total);
-    return hipGetLastError();
-  }
-  if constexpr (WN != 3) {
-    if (epi == EPI_RESID_LN) return hipErrorInvalidValue;  // needs N = 64 * WN
-  }
+#define ILW_LAUNCH(E)                                                                   \
+  hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, FI, FJ, E, KT, PF>), grid, block, 0, s, a, \
+                     tiles_n, total)
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_STORE, KT>), grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_GELU, KT>), grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID, KT>), grid, block, 0, s, a, tiles_n, total); break;
-    case EPI_RESID_LN:
-      if constexpr (WN == 3)
-        hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_RESID_LN, KT>), grid, block, 0, s, a, tiles_n, total);
-      break;
-    default: hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, EPI_QKV, KT>), grid, block, 0, s, a, tiles_n, total); break;
+    case EPI_STORE: ILW_LAUNCH(EPI_STORE); break;
+    case EPI_GELU: ILW_LAUNCH(EPI_GELU); break;
+    case EPI_RESID: ILW_LAUNCH(EPI_RESID); break;
+    case EPI_QKV: ILW_LAUNCH(EPI_QKV); break;
+    default: return hipErrorInvalidValue;
   }
+#undef ILW_LAUNCH
   return hipGetLastError();
 }
 
-template <int WN, int WM>
+// Fused residual + LayerNorm: the workgroup holds whole rows (TN == N).
+template <int WN, int WM, int FI, int FJ, bool KT, int PF>
+hipError_t launch_ln(const GemmArgs& a, hipStream_t s) {
+  constexpr int TN = 16 * FI * WN, TM = 16 * FJ * WM;
+  if (a.N != TN) return hipErrorInvalidValue;
+  const int64_t total = (a.M + TM - 1) / TM;
+  hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, FI, FJ, EPI_RESID_LN, KT, PF>), dim3((unsigned)total),
+                     dim3(64 * WN * WM), 0, s, a, 1, total);
+  return hipGetLastError();
+}
+
+template <int WN, int WM, int FI, int FJ, int PF>
 hipError_t launch_tile(int epi, const GemmArgs& a, hipStream_t s) {
-  return a.K % TK == 0 ? launch_tile_k<WN, WM, false>(epi, a, s)
-                       : launch_tile_k<WN, WM, true>(epi, a, s);
+  return a.K % TK == 0 ? launch_cfg<WN, WM, FI, FJ, false, PF>(epi, a, s)
+                       : launch_cfg<WN, WM, FI, FJ, true, PF>(epi, a, s);
+}
+
+template <int WN, int WM, int FI, int FJ, int PF>
+hipError_t launch_ln_tile(const GemmArgs& a, hipStream_t s) {
+  return a.K % TK == 0 ? launch_ln<WN, WM, FI, FJ, false, PF>(a, s)
+                       : launch_ln<WN, WM, FI, FJ, true, PF>(a, s);
+}
+
+// Latency mode (ILW_GEMM_PF=1|3 forces it off or on): grids of at most about
+// one wave per SIMD with the throughput tiles.
+bool latency_mode(int64_t waves) {
+  static int ov = -1;
+  if (ov < 0) {
+    const char* e = getenv("ILW_GEMM_PF");
+    ov = (e && (atoi(e) == 1 || atoi(e) == 3)) ? atoi(e) : 0;
+  }
+  if (ov) return ov == 3;
+  return waves <= 1024;
 }
 
 }  // namespace
@@ -416,17 +520,24 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     a.inv_wh = 1.0f / (float)a.qkv.win_h;
     a.inv_ww = 1.0f / (float)a.qkv.win_w;
   }
+  const int64_t mt64 = (a.M + 63) / 64;
   if (epi == EPI_RESID_LN) {
     // The workgroup holds whole rows (N channels) so the LayerNorm statistics
-    // stay on chip: 64 tokens per wave row, two wave rows for big deep-K grids.
-    if (a.N == 192)
-      return (a.K >= 768 && (a.M + 127) / 128 * 2 >= 512) ? launch_tile<3, 2>(epi, a, s)
-                                                          : launch_tile<3, 1>(epi, a, s);
-    if (a.N == 384) return launch_tile<6, 1>(epi, a, s);
+    // stay on chip.
+    const bool lat = latency_mode(mt64 * (a.N / 64));
+    if (a.N == 192) {
+      if (lat) return launch_ln_tile<6, 1, 2, 1, 3>(a, s);  // 192 x 16 tokens
+      return (a.K >= 768 && (a.M + 127) / 128 * 2 >= 512) ? launch_ln_tile<3, 2, 4, 4, 1>(a, s)
+                                                          : launch_ln_tile<3, 1, 4, 4, 1>(a, s);
+    }
+    if (a.N == 384) {
+      if (lat) return launch_ln_tile<6, 1, 4, 1, 3>(a, s);  // 384 x 16 tokens
+      return launch_ln_tile<6, 1, 4, 4, 1>(a, s);
+    }
     return hipErrorInvalidValue;
   }
-  // Tile override for tuning: ILW_GEMM_TILE=<WN>x<WM> (waves along channels
-  // x waves along tokens), read once.
+  // Tile override for tuning: ILW_GEMM_TILE=<WN>x<WM> (waves of 64 x 64
+  // along channels x tokens), read once.
   static int ov_wn = -1, ov_wm = -1;
   if (ov_wn < 0) {
     const char* e = getenv("ILW_GEMM_TILE");
@@ -434,23 +545,24 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     if (e && sscanf(e, "%dx%d", &ov_wn, &ov_wm) != 2) ov_wn = ov_wm = 0;
   }
   if (ov_wn > 0) {
-    if (ov_wn == 1 && ov_wm == 1) return launch_tile<1, 1>(epi, a, s);
-    if (ov_wn == 1 && ov_wm == 4) return launch_tile<1, 4>(epi, a, s);
-    if (ov_wn == 2 && ov_wm == 2) return launch_tile<2, 2>(epi, a, s);
-    if (ov_wn == 2 && ov_wm == 4) return launch_tile<2, 4>(epi, a, s);
-    if (ov_wn == 3 && ov_wm == 1) return launch_tile<3, 1>(epi, a, s);
-    if (ov_wn == 3 && ov_wm == 2) return launch_tile<3, 2>(epi, a, s);
+    if (ov_wn == 1 && ov_wm == 1) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
+    if (ov_wn == 1 && ov_wm == 4) return launch_tile<1, 4, 4, 4, 1>(epi, a, s);
+    if (ov_wn == 2 && ov_wm == 2) return launch_tile<2, 2, 4, 4, 1>(epi, a, s);
+    if (ov_wn == 2 && ov_wm == 4) return launch_tile<2, 4, 4, 4, 1>(epi, a, s);
+    if (ov_wn == 3 && ov_wm == 1) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
+    if (ov_wn == 3 && ov_wm == 2) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   }
-  // Default tiles, from a sweep over the encoder shapes on MI355X: a single
-  // 64 x 64 wave per workgroup when the grid is small (batch 1); otherwise
-  // 192-channel tiles for the deep-K linears and N = 192, and 128 x 256
-  // tiles for the rest.
+  // Small grids: 64 x 64 workgroup tiles split over 4 waves of 32 x 32, with
+  // the latency-mode pipeline.  Otherwise, from a sweep over the encoder
+  // shapes on MI355X: 192-channel tiles for the deep-K linears and N = 192,
+  // and 128 x 256 tiles for the rest.
+  if (latency_mode(mt64 * ((a.N + 63) / 64))) return launch_tile<2, 2, 2, 2, 3>(epi, a, s);
   const int64_t big_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
-  if (big_tiles < 512) return launch_tile<1, 1>(epi, a, s);
-  if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2>(epi, a, s);
-  if (a.N == 192) return launch_tile<3, 1>(epi, a, s);
-  if (a.N % 128 == 0 && a.N >= 1536) return launch_tile<2, 2>(epi, a, s);
-  return launch_tile<2, 4>(epi, a, s);
+  if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
+  if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
+  if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
+  if (a.N % 128 == 0 && a.N >= 1536) return launch_tile<2, 2, 4, 4, 1>(epi, a, s);
+  return launch_tile<2, 4, 4, 4, 1>(epi, a, s);
 }
 
 }  // namespace ilw
