@@ -53,12 +53,17 @@ __device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
   return (uint32_t)q;
 }
 
-template <int R, int LPR, bool NARROW, bool RAGGED>
-__global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_row,
-                                                        int32_t clampL) {
+// NW waves per workgroup (4, 8 or 16): keys are split over all waves for the
+// scores, rows for the Shiftmax (R / NW rows per wave), and (channel group,
+// key range) pairs for P V, whose int32 partial sums are added through LDS.
+template <int R, int LPR, bool NARROW, bool RAGGED, int NW>
+__global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t lds_row,
+                                                            int32_t clampL) {
   extern __shared__ __attribute__((aligned(16))) int8_t sS[];  // [R][lds_row]
   __shared__ uint32_t elut[256];
-  __shared__ int32_t pmax[4][R];
+  __shared__ int32_t pmax[NW][R];
+  constexpr int KP = NW / 4;  // key ranges of the P V phase
+  __shared__ v4i ored[KP > 1 ? (KP - 1) * 4 * (R / 16) * 64 : 1];
 
   constexpr int NF = R / 16;  // query fragments of 16 rows
   const int tid = threadIdx.x, lane = tid & 63;
@@ -73,7 +78,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   const int8_t* __restrict__ Vt = a.vt + slice * 64 * Twp;
 
   // ShiftExp(-d) for d = 0..254 (entry 255 is never a valid max - score)
-  elut[tid] = tid < 255 ? (uint32_t)shift_exp(-tid, a.I0, a.k_inter) : 0u;
+  if (tid < 256) elut[tid] = tid < 255 ? (uint32_t)shift_exp(-tid, a.I0, a.k_inter) : 0u;
 
   // Query fragments (MFMA B operand: columns = query rows).  Rows past the
   // window are clamped to a valid row; their results are never stored.
@@ -113,24 +118,25 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
           pack_bytes(v[0], v[1], v[2], v[3]);
     }
   };
-  // A ring of four key fragments in flight: the load of block kb + 16 is
+  // A ring of four key fragments in flight: the load of block kb + 4 NW is
   // issued right after block kb has been consumed.  Loads past the last
   // block re-read the clamped last key and are never used.
-  v4i k0 = kload(wave), k1 = kload(wave + 4), k2 = kload(wave + 8), k3 = kload(wave + 12);
-  for (int32_t kb = wave; kb < nkb; kb += 16) {
+  v4i k0 = kload(wave), k1 = kload(wave + NW), k2 = kload(wave + 2 * NW),
+      k3 = kload(wave + 3 * NW);
+  for (int32_t kb = wave; kb < nkb; kb += 4 * NW) {
     scores(kb, k0);
-    k0 = kload(kb + 16);
-    if (kb + 4 >= nkb) break;
-    scores(kb + 4, k1);
-    k1 = kload(kb + 20);
-    if (kb + 8 >= nkb) break;
-    scores(kb + 8, k2);
-    k2 = kload(kb + 24);
-    if (kb + 12 >= nkb) break;
-    scores(kb + 12, k3);
-    k3 = kload(kb + 28);
+    k0 = kload(kb + 4 * NW);
+    if (kb + NW >= nkb) break;
+    scores(kb + NW, k1);
+    k1 = kload(kb + 5 * NW);
+    if (kb + 2 * NW >= nkb) break;
+    scores(kb + 2 * NW, k2);
+    k2 = kload(kb + 6 * NW);
+    if (kb + 3 * NW >= nkb) break;
+    scores(kb + 3 * NW, k3);
+    k3 = kload(kb + 7 * NW);
   }
-  // row maxima: combine the 4 lanes sharing a row, then the 4 waves
+  // row maxima: combine the 4 lanes sharing a row, then the waves
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     mx[f] = max(mx[f], __shfl_xor(mx[f], 16, 64));
@@ -148,10 +154,13 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
     const int sub = lane / LPR, k = lane % LPR;
     const int32_t nword = Twp >> 2;
     const int32_t pcap = (1 << (a.k_out - 1)) - 1;
-    for (int rr0 = wave * (R / 4); rr0 < (wave + 1) * (R / 4); rr0 += RG) {
+    static_assert(R / NW >= RG, "a wave must own at least RG rows");
+    for (int rr0 = wave * (R / NW); rr0 < (wave + 1) * (R / NW); rr0 += RG) {
       const int rr = rr0 + sub;
       uint32_t* row = (uint32_t*)(sS + rr * lds_row);
-      const int32_t m = max(max(pmax[0][rr], pmax[1][rr]), max(pmax[2][rr], pmax[3][rr]));
+      int32_t m = pmax[0][rr];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) m = max(m, pmax[w][rr]);
       const uint32_t m4 = (uint32_t)(m + 128) * 0x01010101u;
       uint32_t e[JW][4];
       uint64_t sum = 0;
@@ -198,13 +207,15 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
   }
   __syncthreads();
 
-  // ---- phase 3: O = P V.  Wave w owns channels 16w..16w+15; V^T is the A
-  // operand (rows = channels), P^T the B operand (columns = query rows), so a
-  // lane holds 4 consecutive channels of one query row.
+  // ---- phase 3: O = P V.  Wave w owns channels 16 (w % 4) .. + 15 over
+  // key range w / 4 (64-key blocks kp, kp + KP, ...); V^T is the A operand
+  // (rows = channels), P^T the B operand (columns = query rows), so a lane
+  // holds 4 consecutive channels of one query row.
   v4i o[NF];
 #pragma unroll
   for (int f = 0; f < NF; ++f) o[f] = zero;
-  const int32_t c0 = wave * 16;
+  const int cg = wave & 3, kp = wave >> 2;
+  const int32_t c0 = cg * 16;
   const int8_t* vrow = Vt + (int64_t)(c0 + (lane & 15)) * Twp + (lane >> 4) * 16;
   const int8_t* prow = sS + (lane & 15) * lds_row + (lane >> 4) * 16;
   const int32_t last = Twp - 64;  // loads past the end re-read the last block
@@ -217,19 +228,37 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a, int32_t lds_
     }
   };
   // four V^T fragments in flight, as for the keys
-  v4i v0 = vload(0), v1 = vload(64), v2 = vload(128), v3 = vload(192);
-  for (int32_t j0 = 0; j0 < Twp; j0 += 256) {
+  constexpr int32_t SJ = 64 * KP;  // key stride of one wave
+  const int32_t j00 = kp * 64;
+  v4i v0 = vload(j00), v1 = vload(j00 + SJ), v2 = vload(j00 + 2 * SJ), v3 = vload(j00 + 3 * SJ);
+  for (int32_t j0 = j00; j0 < Twp; j0 += 4 * SJ) {
     pv(j0, v0);
-    v0 = vload(j0 + 256);
-    if (j0 + 64 >= Twp) break;
-    pv(j0 + 64, v1);
-    v1 = vload(j0 + 320);
-    if (j0 + 128 >= Twp) break;
-    pv(j0 + 128, v2);
-    v2 = vload(j0 + 384);
-    if (j0 + 192 >= Twp) break;
-    pv(j0 + 192, v3);
-    v3 = vload(j0 + 448);
+    v0 = vload(j0 + 4 * SJ);
+    if (j0 + SJ >= Twp) break;
+    pv(j0 + SJ, v1);
+    v1 = vload(j0 + 5 * SJ);
+    if (j0 + 2 * SJ >= Twp) break;
+    pv(j0 + 2 * SJ, v2);
+    v2 = vload(j0 + 6 * SJ);
+    if (j0 + 3 * SJ >= Twp) break;
+    pv(j0 + 3 * SJ, v3);
+    v3 = vload(j0 + 7 * SJ);
+  }
+  if (KP > 1) {
+    // add the partial sums of the other key ranges into the kp = 0 waves
+    if (kp > 0) {
+#pragma unroll
+      for (int f = 0; f < NF; ++f) ored[(((kp - 1) * 4 + cg) * NF + f) * 64 + lane] = o[f];
+    }
+    __syncthreads();
+    if (kp > 0) return;
+#pragma unroll
+    for (int q = 0; q < KP - 1; ++q)
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        const v4i t = ored[((q * 4 + cg) * NF + f) * 64 + lane];
+        o[f] += t;
+      }
   }
   const int32_t b_img = bw / a.nW, w = bw % a.nW;
   const int32_t wy = w / a.nwx, wx = w % a.nwx;
@@ -274,11 +303,11 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(const int8_t* qkv, in
   }
 }
 
-template <int R, int LPR, bool NARROW, bool RAGGED>
+template <int R, int LPR, bool NARROW, bool RAGGED, int NW>
 hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   const int32_t lds_row = a.Twp + 16;
   const size_t smem = (size_t)R * lds_row;
-  auto kern = attention_kernel<R, LPR, NARROW, RAGGED>;
+  auto kern = attention_kernel<R, LPR, NARROW, RAGGED, NW>;
   static size_t configured = 0;
   if (smem > 65536 && smem > configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -286,28 +315,32 @@ hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
     if (e != hipSuccess) return e;
     configured = smem;
   }
-  dim3 grid((a.Tw + R - 1) / R, a.H, a.B * a.nW), block(256);
+  dim3 grid((a.Tw + R - 1) / R, a.H, a.B * a.nW), block(64 * NW);
   hipLaunchKernelGGL(kern, grid, block, smem, s, a, lds_row, clampL);
   return hipGetLastError();
 }
 
-template <int R, int LPR>
+template <int R, int LPR, int NW>
 hipError_t launch_rows(const AttnArgs& a, int32_t clampL, bool narrow, hipStream_t s) {
   const bool ragged = (a.Tw & 3) != 0;
   if (narrow) {
-    return ragged ? launch_variant<R, LPR, true, true>(a, clampL, s)
-                  : launch_variant<R, LPR, true, false>(a, clampL, s);
+    return ragged ? launch_variant<R, LPR, true, true, NW>(a, clampL, s)
+                  : launch_variant<R, LPR, true, false, NW>(a, clampL, s);
   }
-  return ragged ? launch_variant<R, LPR, false, true>(a, clampL, s)
-                : launch_variant<R, LPR, false, false>(a, clampL, s);
+  return ragged ? launch_variant<R, LPR, false, true, NW>(a, clampL, s)
+                : launch_variant<R, LPR, false, false, NW>(a, clampL, s);
 }
 
 template <int R>
-hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, hipStream_t s) {
+hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, int64_t wgs,
+                      hipStream_t s) {
   // a lane holds at most 8 words (32 scores) of its row
-  if (a.Twp <= 512) return launch_rows<R, 16>(a, clampL, narrow, s);
-  if (a.Twp <= 1024) return launch_rows<R, 32>(a, clampL, narrow, s);
-  return launch_rows<R, 64>(a, clampL, narrow, s);
+  if (a.Twp <= 512) return launch_rows<R, 16, 4>(a, clampL, narrow, s);
+  if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, narrow, s);
+  // Long rows (one row per 64 lanes): small grids split a 16-row block over
+  // 16 waves so that every SIMD holds several.
+  if (R == 16 && wgs * 4 <= 2048) return launch_rows<16, 64, 16>(a, clampL, narrow, s);
+  return launch_rows<R, 64, 4>(a, clampL, narrow, s);
 }
 
 }  // namespace
@@ -326,8 +359,9 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   // Fill the chip: fall back to 16-row blocks when 32-row blocks would give
   // fewer than two workgroups per CU.
   const int64_t wg32 = (int64_t)((a.Tw + 31) / 32) * a.H * a.B * a.nW;
-  if (wg32 < 512) return launch_lpr<16>(a, (int32_t)L, narrow, s);
-  return launch_lpr<32>(a, (int32_t)L, narrow, s);
+  const int64_t wg16 = (int64_t)((a.Tw + 15) / 16) * a.H * a.B * a.nW;
+  if (wg32 < 512) return launch_lpr<16>(a, (int32_t)L, narrow, wg16, s);
+  return launch_lpr<32>(a, (int32_t)L, narrow, wg32, s);
 }
 
 hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,

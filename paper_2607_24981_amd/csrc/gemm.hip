@@ -526,12 +526,16 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     // stay on chip.
     const bool lat = latency_mode(mt64 * (a.N / 64));
     if (a.N == 192) {
-      if (lat) return launch_ln_tile<6, 1, 2, 1, 3>(a, s);  // 192 x 16 tokens
+      if (lat)  // 192 x 16 tokens
+        return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
+                             : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
       return (a.K >= 768 && (a.M + 127) / 128 * 2 >= 512) ? launch_ln_tile<3, 2, 4, 4, 1>(a, s)
                                                           : launch_ln_tile<3, 1, 4, 4, 1>(a, s);
     }
     if (a.N == 384) {
-      if (lat) return launch_ln_tile<6, 1, 4, 1, 3>(a, s);  // 384 x 16 tokens
+      if (lat)  // 384 x 16 tokens
+        return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
+                             : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
       return launch_ln_tile<6, 1, 4, 4, 1>(a, s);
     }
     return hipErrorInvalidValue;
@@ -556,7 +560,9 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   // the latency-mode pipeline.  Otherwise, from a sweep over the encoder
   // shapes on MI355X: 192-channel tiles for the deep-K linears and N = 192,
   // and 128 x 256 tiles for the rest.
-  if (latency_mode(mt64 * ((a.N + 63) / 64))) return launch_tile<2, 2, 2, 2, 3>(epi, a, s);
+  if (latency_mode(mt64 * ((a.N + 63) / 64)))
+    return a.K >= 6 * TK ? launch_tile<2, 2, 2, 2, 6>(epi, a, s)
+                         : launch_tile<2, 2, 2, 2, 3>(epi, a, s);
   const int64_t big_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
   if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
