@@ -38,9 +38,10 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def stage_work(wl, B):
-    """Algorithmic work of one forward, per profiling stage:
-    (kind, amount) with kind 'ops' (int8 ops) or 'bytes' (HBM bytes)."""
+def stage_work(wl, B, launches):
+    """Algorithmic work of one forward, per profiling stage, given the number
+    of launches per forward of each stage: (kind, amount) with kind 'ops'
+    (int8 ops) or 'bytes' (HBM bytes)."""
     T, D, Hm = wl.tokens, wl.dim, wl.mlp_dim
     M = B * T
     nb = len(wl.windows)
@@ -48,24 +49,30 @@ def stage_work(wl, B):
     for wh, ww in wl.windows:
         tw = T if wh == 0 else wh * ww
         attn += 4 * (T // tw) * tw * tw * D * B
+    qkv, proj, mlp = 2 * M * 3 * D * D, 2 * M * D * D, 2 * M * Hm * D
+    n = lambda k: launches.get(k, 0)
     return {
-        "gemm_qkv": ("ops", nb * 2 * M * 3 * D * D),
+        "gemm_qkv": ("ops", n("gemm_qkv") * qkv),
         "attention": ("ops", attn),
-        "gemm_proj": ("ops", nb * 2 * M * D * D),
-        "gemm_fc1": ("ops", nb * 2 * M * Hm * D),
-        "gemm_fc2": ("ops", nb * 2 * M * D * Hm),
+        "gemm_proj": ("ops", n("gemm_proj") * proj),
+        "gemm_fc1": ("ops", n("gemm_fc1") * mlp),
+        "gemm_fc2": ("ops", n("gemm_fc2") * mlp),
+        # projection, fc1, fc2, and the QKV linear of the next block
+        "block_tail": ("ops", n("block_tail") * (proj + 2 * mlp) + (nb - n("gemm_qkv")) * qkv
+                       if n("block_tail") else 0),
         # int8 row in and out, plus beta / multiplier / shift per channel
-        "layernorm": ("bytes", nb * 2 * (2 * M * D + 12 * D)),
+        "layernorm": ("bytes", n("layernorm") * (2 * M * D + 12 * D)),
     }
 
 
 KERNEL_OF_STAGE = {
     "attention": ("attention_kernel", "paper_2607_24981_amd/csrc/attention.hip"),
-    "gemm_qkv": ("gemm_i8_kernel<3>", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "gemm_proj": ("gemm_i8_kernel<2>", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "gemm_fc1": ("gemm_i8_kernel<1>", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "gemm_fc2": ("gemm_i8_kernel<2>", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "layernorm": ("layernorm_kernel", "paper_2607_24981_amd/csrc/rowops.hip"),
+    "gemm_qkv": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "gemm_proj": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "gemm_fc1": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "gemm_fc2": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
+    "block_tail": ("block_tail_kernel", "paper_2607_24981_amd/csrc/block_tail.hip"),
+    "layernorm": ("layernorm_rows_kernel", "paper_2607_24981_amd/csrc/rowops.hip"),
 }
 
 
@@ -178,7 +185,7 @@ def main():
     torch.cuda.synchronize()
     prof = ilw.profile_read()
     ilw.profile_enable(False)
-    work = stage_work(wl, B)
+    work = stage_work(wl, B, {k: v[1] // args.profile_steps for k, v in prof.items()})
     stages = {}
     for name, (kind, amount) in work.items():
         ms, n = prof[name]

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ILW_ABI_VERSION 1
+#define ILW_ABI_VERSION 2
 
 typedef enum {
   ILW_OK = 0,
@@ -266,7 +266,8 @@ typedef enum {
   ILW_STAGE_GEMM_FC2 = 5,    /* fc2 + residual (+ next LN1) epilogue       */
   ILW_STAGE_RELAYOUT = 6,    /* token-major QKV -> window-major copy       */
   ILW_STAGE_DEFORM = 7,      /* deformable sampling                        */
-  ILW_NUM_STAGES = 8
+  ILW_STAGE_BLOCK_TAIL = 8,  /* projection ... next block's QKV, one launch */
+  ILW_NUM_STAGES = 9
 } ilw_stage;
 
 int ilw_profile_enable(int enable);

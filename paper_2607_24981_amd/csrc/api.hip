@@ -241,15 +241,18 @@ struct BlockLayout {
   size_t total;
 };
 
+// Workspace of one block: h | Q K V^T | att | x1 | g.  qkv_reserve (when
+// larger than this block's need) fixes the size of the Q K V^T region, so
+// that in an encoder every block's att buffer lies past every block's Q K V^T.
 size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
-                    int8_t* base, BlockLayout* out) {
+                    int8_t* base, BlockLayout* out, size_t qkv_reserve = 0) {
   const size_t M = (size_t)batch * g.T;
   size_t off = 0;
   BlockLayout L;
   L.h = base + off;
   off += align256(M * p->dim);
   size_t q = qkv_bytes(batch, g, p->dim, &L.qkv, base + off);
-  off += q;
+  off += q > qkv_reserve ? q : qkv_reserve;
   L.att = base + off;
   off += align256(M * p->dim);
   L.x1 = base + off;
@@ -324,19 +327,40 @@ GemmArgs with_ln(GemmArgs a, const int32_t* beta, const ilw_dyadic& out, int32_t
   return a;
 }
 
-// One encoder block: h = LN1(x) (unless h already holds it), attention,
-// x1 = Res(proj(att), x) with LN2 fused when possible, fc1 + GELU, and
-// y = Res(fc2(g), x1), which also leaves LN1 of `next` in h when fusable.
-int run_block(const ilw_block_params* p, const ilw_block_params* next, const int8_t* x,
-              int8_t* y, int32_t batch, const Geometry& g, const BlockLayout& L,
-              bool h_ready, hipStream_t s) {
+// The block tail kernel (projection ... next block's QKV in one launch) covers
+// dim 192 / MLP 768.  It pays off where launches dominate: by default for up
+// to 16384 tokens per call; ILW_TAIL=0 / 1 turns it off / on wherever it
+// applies (same results), read once.
+bool use_tail(const ilw_block_params* p, const ilw_block_params* next, int64_t M) {
+  static int mode = -1;
+  if (mode < 0) {
+    const char* e = getenv("ILW_TAIL");
+    mode = (e && e[0] == '0') ? 0 : ((e && e[0] == '1') ? 1 : 2);
+  }
+  if (mode == 0 || p->dim != 192 || p->mlp_dim != 768) return false;
+  if (next && next->dim != 192) return false;
+  return mode == 1 || M <= 16384;
+}
+
+// What the previous block already left for this one in the workspace.
+enum { READY_NONE = 0, READY_H = 1, READY_QKV = 2 };
+
+// One encoder block: h = LN1(x) and Q, K, V^T (unless already there),
+// attention, then either the block tail kernel (which also leaves the next
+// block's Q, K, V^T in next_qkv) or projection + residual (+ LN2), fc1 +
+// GELU and fc2 + residual (+ the next block's LN1 in h).
+int run_block(const ilw_block_params* p, const ilw_block_params* next,
+              const QkvLayout* next_qkv, const int8_t* x, int8_t* y, int32_t batch,
+              const Geometry& g, const BlockLayout& L, int ready, int* ready_out,
+              hipStream_t s) {
   const int64_t M = (int64_t)batch * g.T;
   const int32_t D = p->dim, Hm = p->mlp_dim;
   const bool fuse = ln_fusable(D);
   hipError_t he = hipSuccess;
+  *ready_out = READY_NONE;
 
   // h = LN1(x)
-  if (!h_ready) {
+  if (ready == READY_NONE) {
     StageTimer t(ILW_STAGE_LAYERNORM, s);
     he = launch_layernorm(x, L.h, M, D, p->ln1_beta, p->ln1_out.mult, p->ln1_out.shift,
                           p->ln1_out.n, p->ln_iters, s);
@@ -344,14 +368,15 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next, const int
     if (he != hipSuccess) return hip_status(he, "block LN1");
   }
   // q, k, v^T = QKV(h), scattered window-major
-  GemmArgs a = gemm_args(L.h, p->w_qkv, p->b_qkv, p->qkv, nullptr, M, 3 * D, D);
-  a.qkv = L.qkv;
-  {
+  GemmArgs a;
+  if (ready != READY_QKV) {
+    a = gemm_args(L.h, p->w_qkv, p->b_qkv, p->qkv, nullptr, M, 3 * D, D);
+    a.qkv = L.qkv;
     StageTimer t(ILW_STAGE_GEMM_QKV, s);
     he = launch_gemm(EPI_QKV, a, s);
     t.done();
+    if (he != hipSuccess) return hip_status(he, "block QKV");
   }
-  if (he != hipSuccess) return hip_status(he, "block QKV");
   // att = Attn(q, k, v)
   {
     StageTimer t(ILW_STAGE_ATTENTION, s);
@@ -359,6 +384,44 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next, const int
     t.done();
   }
   if (he != hipSuccess) return hip_status(he, "block attention");
+
+  if (use_tail(p, next_qkv ? next : nullptr, M)) {
+    TailArgs ta = {};
+    ta.att = L.att;
+    ta.x = x;
+    ta.y = y;
+    ta.M = M;
+    ta.w_proj = p->w_proj; ta.b_proj = p->b_proj; ta.proj_mult = p->proj.mult;
+    ta.proj_shift = p->proj.shift; ta.proj_nq = p->proj.n;
+    ta.res1_ma = p->res1_mult_a; ta.res1_mb = p->res1_mult_b; ta.res1_shift = p->res1_shift;
+    ta.ln2_beta = p->ln2_beta; ta.ln2_mult = p->ln2_out.mult; ta.ln2_shift = p->ln2_out.shift;
+    ta.ln2_nq = p->ln2_out.n; ta.ln2_iters = p->ln_iters;
+    ta.w_fc1 = p->w_fc1; ta.b_fc1 = p->b_fc1; ta.fc1_mult = p->fc1.mult;
+    ta.fc1_shift = p->fc1.shift; ta.fc1_nq = p->fc1.n;
+    ta.g_I0 = p->gelu_I0; ta.g_kinter = p->gelu_k_inter; ta.g_kout = p->gelu_k_out;
+    ta.g_mult = p->gelu_mult; ta.g_shift = p->gelu_shift;
+    ta.w_fc2 = p->w_fc2; ta.b_fc2 = p->b_fc2; ta.fc2_mult = p->fc2.mult;
+    ta.fc2_shift = p->fc2.shift; ta.fc2_nq = p->fc2.n;
+    ta.res2_ma = p->res2_mult_a; ta.res2_mb = p->res2_mult_b; ta.res2_shift = p->res2_shift;
+    if (next && next_qkv) {
+      ta.has_next = 1;
+      ta.ln1_beta = next->ln1_beta; ta.ln1_mult = next->ln1_out.mult;
+      ta.ln1_shift = next->ln1_out.shift; ta.ln1_nq = next->ln1_out.n;
+      ta.ln1_iters = next->ln_iters;
+      ta.w_qkv = next->w_qkv; ta.b_qkv = next->b_qkv; ta.qkv_mult = next->qkv.mult;
+      ta.qkv_shift = next->qkv.shift; ta.qkv_nq = next->qkv.n;
+      ta.qkv = *next_qkv;
+    }
+    {
+      StageTimer t(ILW_STAGE_BLOCK_TAIL, s);
+      he = launch_block_tail(ta, s);
+      t.done();
+    }
+    if (he != hipSuccess) return hip_status(he, "block tail");
+    *ready_out = ta.has_next ? READY_QKV : READY_NONE;
+    return ok();
+  }
+
   // x1 = Res(proj(att), x);  h = LN2(x1)
   a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
   a.resid = x;
@@ -407,6 +470,7 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next, const int
     t.done();
   }
   if (he != hipSuccess) return hip_status(he, "block fc2");
+  *ready_out = next && fuse ? READY_H : READY_NONE;
   return ok();
 }
 
@@ -428,13 +492,28 @@ int check_encoder(const ilw_block_params* blocks, int32_t n_blocks, const int32_
   return ILW_OK;
 }
 
+// Largest Q K V^T region over the blocks of an encoder.
+size_t encoder_qkv_reserve(const ilw_block_params* blocks, int32_t n_blocks,
+                           const int32_t* windows, int32_t batch, int32_t grid_h,
+                           int32_t grid_w) {
+  size_t q = 0;
+  for (int32_t b = 0; b < n_blocks; ++b) {
+    Geometry g;
+    check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
+    const size_t n = qkv_bytes(batch, g, blocks[b].dim, nullptr, nullptr);
+    q = n > q ? n : q;
+  }
+  return q;
+}
+
 size_t encoder_workspace(const ilw_block_params* blocks, int32_t n_blocks,
                          const int32_t* windows, int32_t batch, int32_t grid_h, int32_t grid_w) {
+  const size_t q = encoder_qkv_reserve(blocks, n_blocks, windows, batch, grid_h, grid_w);
   size_t need = 0;
   for (int32_t b = 0; b < n_blocks; ++b) {
     Geometry g;
     check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
-    const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr);
+    const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr, q);
     need = n > need ? n : need;
   }
   return need;
@@ -601,7 +680,9 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int
   REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
   BlockLayout L;
   block_layout(p, batch, g, (int8_t*)workspace, &L);
-  return run_block(p, nullptr, x, y, batch, g, L, false, (hipStream_t)stream);
+  int ready = READY_NONE;
+  return run_block(p, nullptr, nullptr, x, y, batch, g, L, READY_NONE, &ready,
+                   (hipStream_t)stream);
 }
 
 size_t ilw_encoder_workspace_bytes(const ilw_block_params* blocks, int32_t n_blocks,
@@ -626,20 +707,31 @@ int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
           "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
   REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
-  // Block b reads its input from x (b = 0) or y and writes y; LN1 of block
-  // b + 1 is produced by the fc2 epilogue of block b when it can be fused,
-  // into the workspace's h buffer, which sits at the same offset in every
-  // block's layout.
-  bool h_ready = false;
+  // Block b reads its input from x (b = 0) or y and writes y.  The workspace
+  // regions h and Q K V^T sit at the same offsets for every block, so block
+  // b can leave block b + 1's LN1 output (fused fc2 epilogue) or its Q, K,
+  // V^T (block tail kernel) there.
+  const size_t qres = encoder_qkv_reserve(blocks, n_blocks, windows, batch, grid_h, grid_w);
+  int ready = READY_NONE;
   for (int32_t b = 0; b < n_blocks; ++b) {
     Geometry g;
     check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
     BlockLayout L;
-    block_layout(&blocks[b], batch, g, (int8_t*)workspace, &L);
+    block_layout(&blocks[b], batch, g, (int8_t*)workspace, &L, qres);
     const ilw_block_params* next = b + 1 < n_blocks ? &blocks[b + 1] : nullptr;
-    if ((e = run_block(&blocks[b], next, b == 0 ? x : y, y, batch, g, L, h_ready, s)))
+    QkvLayout nq;
+    if (next) {
+      Geometry gn;
+      check_geometry(batch, grid_h, grid_w, windows[2 * b + 2], windows[2 * b + 3], &gn);
+      BlockLayout Ln;
+      block_layout(next, batch, gn, (int8_t*)workspace, &Ln, qres);
+      nq = Ln.qkv;
+    }
+    int ready_out = READY_NONE;
+    if ((e = run_block(&blocks[b], next, next ? &nq : nullptr, b == 0 ? x : y, y, batch, g, L,
+                       ready, &ready_out, s)))
       return e;
-    h_ready = next && ln_fusable(blocks[b].dim);
+    ready = ready_out;
   }
   return ok();
 }

@@ -36,43 +36,6 @@ constexpr int TK = 64;        // K bytes per step
 constexpr int LDS_ROW = 80;   // padded LDS row stride (bytes)
 constexpr int NXCD = 8;
 
-__device__ __forceinline__ uint32_t pack4(int32_t a, int32_t b, int32_t c, int32_t d) {
-  return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) |
-         ((uint32_t)(c & 0xff) << 16) | ((uint32_t)d << 24);
-}
-
-// Requantization of one channel with its accumulator bound L:
-// |acc| >= L saturates (|acc * mult| > 129 * 2^shift) and L * |mult| / 2^shift
-// stays far inside int32.  Any L in [129 * 2^s / |m| + 1, 2^30 * 2^s / |m|]
-// works, so an fp32 estimate with margin is exact enough.
-struct ChanRq {
-  int32_t L, mult, shift, bias;
-  int64_t rnd;
-  __device__ __forceinline__ void init(int32_t m, int32_t s, int32_t b) {
-    mult = m;
-    shift = s;
-    bias = b;
-    rnd = (int64_t)1 << (s - 1);
-    const float am = fabsf((float)m);
-    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) * __builtin_amdgcn_rcpf(am);
-    L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
-  }
-  __device__ __forceinline__ int32_t apply(int32_t acc) const {
-    int32_t a = acc + bias;
-    a = min(max(a, -L), L);
-    const int32_t v = (int32_t)(((int64_t)a * mult + rnd) >> shift);
-    return min(max(v, kQmin), kQmax);
-  }
-};
-
-// n / d for 0 <= n < 2^24 with an fp32 reciprocal and one correction step.
-__device__ __forceinline__ int32_t fdiv(int32_t n, int32_t d, float inv) {
-  int32_t q = (int32_t)((float)n * inv);
-  const int32_t r = n - q * d;
-  q += r < 0 ? -1 : (r >= d ? 1 : 0);
-  return q;
-}
-
 // WN x WM waves per workgroup; each wave computes FI x FJ MFMA tiles of 16
 // channels x 16 tokens.  PF register slots of staged operands (PF > 1 is the
 // latency mode for small grids: PF K steps of loads in flight, and every

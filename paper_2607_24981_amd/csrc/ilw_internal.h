@@ -187,6 +187,44 @@ struct LnChan {
 };
 
 // ---------------------------------------------------------------- launchers
+// ---- GEMM epilogue helpers (shared by the GEMM and block-tail kernels)
+__device__ __forceinline__ uint32_t pack4(int32_t a, int32_t b, int32_t c, int32_t d) {
+  return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) |
+         ((uint32_t)(c & 0xff) << 16) | ((uint32_t)d << 24);
+}
+
+// Requantization of one channel with its accumulator bound L:
+// |acc| >= L saturates (|acc * mult| > 129 * 2^shift) and L * |mult| / 2^shift
+// stays far inside int32.  Any L in [129 * 2^s / |m| + 1, 2^30 * 2^s / |m|]
+// works, so an fp32 estimate with margin is exact enough.
+struct ChanRq {
+  int32_t L, mult, shift, bias;
+  int64_t rnd;
+  __device__ __forceinline__ void init(int32_t m, int32_t s, int32_t b) {
+    mult = m;
+    shift = s;
+    bias = b;
+    rnd = (int64_t)1 << (s - 1);
+    const float am = fabsf((float)m);
+    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) * __builtin_amdgcn_rcpf(am);
+    L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
+  }
+  __device__ __forceinline__ int32_t apply(int32_t acc) const {
+    int32_t a = acc + bias;
+    a = min(max(a, -L), L);
+    const int32_t v = (int32_t)(((int64_t)a * mult + rnd) >> shift);
+    return min(max(v, kQmin), kQmax);
+  }
+};
+
+// n / d for 0 <= n < 2^24 with an fp32 reciprocal and one correction step.
+__device__ __forceinline__ int32_t fdiv(int32_t n, int32_t d, float inv) {
+  int32_t q = (int32_t)((float)n * inv);
+  const int32_t r = n - q * d;
+  q += r < 0 ? -1 : (r >= d ? 1 : 0);
+  return q;
+}
+
 enum GemmEpilogue {
   EPI_STORE = 0,     // y = rq(acc)
   EPI_GELU = 1,      // y = table[rq(acc)] (SD-ShiftGELU + its requantization)
@@ -227,6 +265,37 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+
+// The rest of an encoder block after attention, for one 16-token slab per
+// workgroup (dim 192, MLP 768): projection + residual, LayerNorm, fc1 +
+// SD-ShiftGELU, fc2 + residual, and optionally the next block's LayerNorm and
+// QKV linear scattered window-major.
+struct TailArgs {
+  const int8_t* att;  // [M, D] attention output
+  const int8_t* x;    // [M, D] block input (first residual)
+  int8_t* y;          // [M, D] block output
+  int64_t M;
+  const int8_t* w_proj; const int32_t* b_proj; const int32_t* proj_mult;
+  const int32_t* proj_shift; int32_t proj_nq;
+  int32_t res1_ma, res1_mb, res1_shift;
+  const int32_t* ln2_beta; const int32_t* ln2_mult; const int32_t* ln2_shift;
+  int32_t ln2_nq, ln2_iters;
+  const int8_t* w_fc1; const int32_t* b_fc1; const int32_t* fc1_mult;
+  const int32_t* fc1_shift; int32_t fc1_nq;
+  int32_t g_I0, g_kinter, g_kout, g_mult, g_shift;
+  const int8_t* w_fc2; const int32_t* b_fc2; const int32_t* fc2_mult;
+  const int32_t* fc2_shift; int32_t fc2_nq;
+  int32_t res2_ma, res2_mb, res2_shift;
+  // next block (has_next): LayerNorm 1 and QKV
+  int32_t has_next;
+  const int32_t* ln1_beta; const int32_t* ln1_mult; const int32_t* ln1_shift;
+  int32_t ln1_nq, ln1_iters;
+  const int8_t* w_qkv; const int32_t* b_qkv; const int32_t* qkv_mult;
+  const int32_t* qkv_shift; int32_t qkv_nq;
+  QkvLayout qkv;
+  float inv_T, inv_gw, inv_wh, inv_ww;
+};
+hipError_t launch_block_tail(const TailArgs& a, hipStream_t s);
 
 struct AttnArgs {
   const int8_t* q;

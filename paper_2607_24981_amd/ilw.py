@@ -16,7 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -348,7 +348,7 @@ def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
-          "relayout", "deform"]
+          "relayout", "deform", "block_tail"]
 
 
 def profile_enable(on: bool = True):

@@ -348,14 +348,18 @@ def test_encoder_shapes(D, H, Hm, grid, windows, B):
 
 @pytest.mark.parametrize("D,H", [(192, 3), (384, 6)])
 def test_encoder_fused_layernorm_edge_params(D, H):
-    """The fused LayerNorm epilogue with per-tensor output constants, |beta|
-    beyond 2^30 (the 64-bit output path) and one constant input row (zero
+    """The fused LayerNorms (block tail kernel at D = 192, GEMM epilogue at
+    D = 384) with per-tensor output constants, |beta| beyond 2^30 (the 64-bit
+    output path), per-tensor linear scales, and one constant input row (zero
     variance)."""
     say(f"encoder fused LN edge parameters D={D}")
-    blocks = _encoder_case(D, H, 2 * D, 3, 40 + D)
+    blocks = _encoder_case(D, H, 4 * D, 3, 40 + D)
     g = rng(D)
     blocks[1]["ln1_mult"] = blocks[1]["ln1_mult"][:1].copy()
     blocks[1]["ln1_shift"] = blocks[1]["ln1_shift"][:1].copy()
+    for k in ("proj", "fc2", "qkv"):
+        blocks[2][k + "_mult"] = blocks[2][k + "_mult"][:1].copy()
+        blocks[2][k + "_shift"] = blocks[2][k + "_shift"][:1].copy()
     blocks[1]["ln2_beta"] = g.integers(-2 ** 31 + 1, 2 ** 31 - 1, D).astype(np.int32)
     blocks[2]["ln1_beta"][:4] = [2 ** 31 - 1, -(2 ** 31) + 1, 2 ** 30 + 1, -(2 ** 30) - 1]
     grid, windows = (6, 9), [(3, 3), (0, 0), (2, 3)]
