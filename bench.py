@@ -20,7 +20,6 @@ Prints ONE JSON line on stdout:
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -65,33 +64,31 @@ def stage_work(wl, B, launches):
     }
 
 
+_INTERNAL = "paper_2607_24981_amd/csrc/ilw_internal.h"
 KERNEL_OF_STAGE = {
-    "attention": ("attention_kernel", "paper_2607_24981_amd/csrc/attention.hip"),
-    "gemm_qkv": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "gemm_proj": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "gemm_fc1": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "gemm_fc2": ("gemm_i8_kernel", "paper_2607_24981_amd/csrc/gemm.hip"),
-    "block_tail": ("block_tail_kernel", "paper_2607_24981_amd/csrc/block_tail.hip"),
-    "layernorm": ("layernorm_rows_kernel", "paper_2607_24981_amd/csrc/rowops.hip"),
+    "attention": ("attention_kernel", ["paper_2607_24981_amd/csrc/attention.hip", _INTERNAL]),
+    "gemm_qkv": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
+    "gemm_proj": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
+    "gemm_fc1": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
+    "gemm_fc2": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
+    "block_tail": ("block_tail_kernel", ["paper_2607_24981_amd/csrc/block_tail.hip", _INTERNAL]),
+    "layernorm": ("layernorm_rows_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
 }
 
 
-def source_digest(rel):
-    with open(os.path.join(ROOT, rel), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
-
-
 def measured_traffic(stage, workload):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, only
-    while the kernel source is unchanged since the counters were taken."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    (profiles/traffic.json), only while the kernel's sources are unchanged
+    since the counters were taken."""
+    from paper_2607_24981_amd.profsum import source_digest
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         table = json.load(f)
-    kernel, src = KERNEL_OF_STAGE[stage]
-    rec = table.get(workload, {}).get(kernel)
-    if not rec or rec.get("source_sha256_16") != source_digest(src):
+    kernel, srcs = KERNEL_OF_STAGE[stage]
+    rec = table.get(workload, {}).get(stage)
+    if not rec or rec.get("source_sha256_16") != source_digest(srcs):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -108,6 +105,9 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="first make one plain device-to-device copy of this many MiB "
+                         "(the known-size reference for rocprofv3 byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -128,6 +128,14 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a ROCm GPU", file=sys.stderr)
         sys.exit(1)
+
+    if args.calibration_copy_mib:
+        src = torch.ones(args.calibration_copy_mib << 20, dtype=torch.int8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"calibration copy of {args.calibration_copy_mib} MiB done")
 
     wl = synth.WORKLOADS[args.workload]
     B = wl.batch if args.batch is None else args.batch

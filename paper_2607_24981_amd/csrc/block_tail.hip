@@ -37,13 +37,11 @@ struct ChanC {
   int32_t L, mult, shift, bias;
 };
 
-__device__ __forceinline__ ChanC make_chan(const int32_t* mult, const int32_t* shift,
-                                           const int32_t* bias, int32_t nq, int32_t c) {
+__device__ __forceinline__ ChanC make_chan(int32_t mult, int32_t shift, int32_t bias) {
   ChanC r;
-  const int32_t q = nq == 1 ? 0 : c;
-  r.mult = mult[q];
-  r.shift = shift[q];
-  r.bias = bias ? bias[c] : 0;
+  r.mult = mult;
+  r.shift = shift;
+  r.bias = bias;
   const float am = fabsf((float)r.mult);
   const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)r.shift) * __builtin_amdgcn_rcpf(am);
   r.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
@@ -59,18 +57,14 @@ __device__ __forceinline__ int32_t rq_chan(int32_t acc, const ChanC& c) {
   return min(max(v, kQmin), kQmax);
 }
 
-__device__ __forceinline__ LnChan make_ln(const int32_t* beta, const int32_t* mult,
-                                          const int32_t* shift, int32_t nq, int32_t c,
-                                          int* wide) {
+__device__ __forceinline__ LnChan make_ln(int32_t beta, int32_t mult, int32_t shift) {
   LnChan p;
-  const int32_t q = nq == 1 ? 0 : c;
-  p.beta = beta[c];
-  p.mult = mult[q];
-  p.shift = shift[q];
+  p.beta = beta;
+  p.mult = mult;
+  p.shift = shift;
   const float am = fabsf((float)p.mult);
   const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
   p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
-  *wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
   return p;
 }
 
@@ -142,13 +136,55 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
   const int64_t mc = tok_ok ? m : M - 1;
   const v4i zero = {0, 0, 0, 0};
 
-  // ---- loads: attention slab, weights of the first two stages, residual
-  v4i att_chunk = zero;
-  if (tid < TS * D / 16) {
-    const int r = tid / (D / 16), c = tid % (D / 16);
-    att_chunk = *(const v4i*)(a.att + min(m0 + r, M - 1) * D + c * 16);
+  // ---- loads, smallest first: every load below is unconditional (indices
+  // are clamped, pointers chosen by wave-uniform selects), so the waits for
+  // the constants leave the weight loads in flight.
+  // (1) per-channel requantization constants.  The four segments start at
+  // multiples of 64 channels, so a wave's 64 channels lie in one segment.
+  constexpr int NC = NEXT ? NCH : NQKV, NIT = (NC + 64 * NWV - 1) / (64 * NWV);
+  int32_t cm[NIT], cs[NIT], cb[NIT];
+  bool hasb[NIT];
+#pragma unroll
+  for (int i = 0; i < NIT; ++i) {
+    const int c = min(tid + i * 64 * NWV, NC - 1);
+    const int cu = __builtin_amdgcn_readfirstlane(c) >> 6;
+    const int seg = (cu >= NFC1 / 64) + (cu >= NFC2 / 64) + (cu >= NQKV / 64);
+    const int32_t* mp = seg == 0 ? a.proj_mult : seg == 1 ? a.fc1_mult : seg == 2 ? a.fc2_mult : a.qkv_mult;
+    const int32_t* sp = seg == 0 ? a.proj_shift : seg == 1 ? a.fc1_shift : seg == 2 ? a.fc2_shift : a.qkv_shift;
+    const int32_t* bp = seg == 0 ? a.b_proj : seg == 1 ? a.b_fc1 : seg == 2 ? a.b_fc2 : a.b_qkv;
+    const int32_t nq = seg == 0 ? a.proj_nq : seg == 1 ? a.fc1_nq : seg == 2 ? a.fc2_nq : a.qkv_nq;
+    const int base = seg == 0 ? NPROJ : seg == 1 ? NFC1 : seg == 2 ? NFC2 : NQKV;
+    const int cc = c - base;
+    const int q = nq == 1 ? 0 : cc;
+    hasb[i] = bp != nullptr;
+    cm[i] = mp[q];
+    cs[i] = sp[q];
+    cb[i] = (bp ? bp : mp)[bp ? cc : q];
   }
+  // (2) LayerNorm constants: waves 0-2 LN2, waves 3-5 the next block's LN1
+  const int lrole = __builtin_amdgcn_readfirstlane(tid) / D;  // 0..3, wave-uniform
+  const bool l1 = NEXT && lrole == 1;
+  const int lc = tid % D;
+  int32_t lb, lm, ls;
+  {
+    const int32_t* bp = l1 ? a.ln1_beta : a.ln2_beta;
+    const int32_t* mp = l1 ? a.ln1_mult : a.ln2_mult;
+    const int32_t* sp = l1 ? a.ln1_shift : a.ln2_shift;
+    const int32_t nq = l1 ? a.ln1_nq : a.ln2_nq;
+    const int q = nq == 1 ? 0 : lc;
+    lb = bp[lc];
+    lm = mp[q];
+    ls = sp[q];
+  }
+  // (3) the attention slab and the residual input
+  const int ar = min(tid / (D / 16), TS - 1), ac = tid % (D / 16);
+  const v4i att_chunk = *(const v4i*)(a.att + min(m0 + ar, M - 1) * D + ac * 16);
   const int n1 = 16 * w + cq;  // the lane's projection / fc2 channels
+  const uint32_t xres = *(const uint32_t*)(a.x + mc * D + n1);
+  // (4) weights of the first two stages, issued after everything above (the
+  // compiler barrier keeps them last, so that waiting for the small loads
+  // leaves these in flight)
+  asm volatile("" ::: "memory");
   v4i wp[D / 64];
   {
     const int8_t* src = a.w_proj + (int64_t)(16 * w + tl) * D + kq;
@@ -163,26 +199,19 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
 #pragma unroll
       for (int s = 0; s < D / 64; ++s) w1[t][s] = *(const v4i*)(src + (int64_t)16 * t * D + s * 64);
   }
-  const uint32_t xres = *(const uint32_t*)(a.x + mc * D + n1);
 
-  // ---- per-channel constants into LDS
-  for (int c = tid; c < (NEXT ? NCH : NQKV); c += 64 * NWV) {
-    ChanC cc;
-    if (c < NFC1) cc = make_chan(a.proj_mult, a.proj_shift, a.b_proj, a.proj_nq, c - NPROJ);
-    else if (c < NFC2) cc = make_chan(a.fc1_mult, a.fc1_shift, a.b_fc1, a.fc1_nq, c - NFC1);
-    else if (c < NQKV) cc = make_chan(a.fc2_mult, a.fc2_shift, a.b_fc2, a.fc2_nq, c - NFC2);
-    else cc = make_chan(a.qkv_mult, a.qkv_shift, a.b_qkv, a.qkv_nq, c - NQKV);
-    chan[c] = cc;
+  // ---- constants into LDS
+#pragma unroll
+  for (int i = 0; i < NIT; ++i) {
+    const int c = tid + i * 64 * NWV;
+    if (c < NC) chan[c] = make_chan(cm[i], cs[i], hasb[i] ? cb[i] : 0);
   }
   int wide = 0;
-  if (tid < D) {
-    int wd = 0;
-    ln2p[tid] = make_ln(a.ln2_beta, a.ln2_mult, a.ln2_shift, a.ln2_nq, tid, &wd);
-    wide |= wd;
-  } else if (NEXT && tid < 2 * D) {
-    int wd = 0;
-    ln1p[tid - D] = make_ln(a.ln1_beta, a.ln1_mult, a.ln1_shift, a.ln1_nq, tid - D, &wd);
-    wide |= wd << 1;
+  if (lrole == 0 || l1) {
+    LnChan p = make_ln(lb, lm, ls);
+    wide = (lb > (1 << 30) || lb < -(1 << 30)) ? (l1 ? 2 : 1) : 0;
+    if (l1) ln1p[lc] = p;
+    else ln2p[lc] = p;
   }
   for (int t = tid; t < 256; t += 64 * NWV)
     glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
@@ -200,10 +229,7 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
     tq = (bw * Lq.H * Lq.Tw + li) * 64;
     tv = bw * Lq.H * 64 * Lq.Twp + li;
   }
-  if (tid < TS * D / 16) {
-    const int r = tid / (D / 16), c = tid % (D / 16);
-    *(v4i*)(bufX + r * XS + c * 16) = att_chunk;
-  }
+  if (tid < TS * D / 16) *(v4i*)(bufX + ar * XS + ac * 16) = att_chunk;
   // (__syncthreads_or only tells whether any thread's value is nonzero, so
   // each flag gets its own reduction)
   const bool wide2 = __syncthreads_or(wide & 1) != 0;
