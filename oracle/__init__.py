@@ -25,6 +25,7 @@ i8p = ctypes.POINTER(ctypes.c_int8)
 i16p = ctypes.POINTER(ctypes.c_int16)
 i32p = ctypes.POINTER(ctypes.c_int32)
 i64p = ctypes.POINTER(ctypes.c_int64)
+vpp = ctypes.POINTER(ctypes.c_void_p)
 c_i32 = ctypes.c_int32
 c_i64 = ctypes.c_int64
 
@@ -100,6 +101,10 @@ def lib():
                                   c_i32, i8p]),
             "orc_residual_tensor": (None, [i8p, i8p, i8p, c_i64, c_i32, c_i32,
                                            c_i32]),
+            "orc_split_conv_sum": (None, [c_i32, vpp, i32p, vpp, vpp, vpp, i32p, i32p,
+                                          c_i64, c_i32, i64p]),
+            "orc_split_conv": (None, [c_i32, vpp, i32p, vpp, vpp, vpp, i32p, i32p, c_i64,
+                                      c_i32, i32p, i32p, c_i32, i8p]),
             "orc_attention": (None, [i8p] + [c_i32] * 16 + [i8p]),
             "orc_block_forward": (None, [ctypes.POINTER(OrcBlock), i8p, i8p,
                                          c_i32, c_i32, c_i32, c_i32, c_i32]),
@@ -241,6 +246,49 @@ def linear(x, w, b, mult, shift):
     y = np.zeros((M, N), np.int8)
     lib().orc_linear(_p(x, i8p), _p(w, i8p), _p(b, i32p), M, N, K, _p(mult, i32p),
                      _p(shift, i32p), mult.shape[0], _p(y, i8p))
+    return y
+
+
+def _split_args(xs, ws, br_mults, br_shifts):
+    xs = [_arr(x, np.int8) for x in xs]
+    ws = [_arr(w, np.int8) for w in ws]
+    ms = [_arr(m, np.int32).reshape(-1) for m in br_mults]
+    ss = [_arr(v, np.int32).reshape(-1) for v in br_shifts]
+    nb = len(xs)
+    assert len(ws) == len(ms) == len(ss) == nb >= 1
+    M = xs[0].shape[0]
+    N = ws[0].shape[0]
+    for x, w, m, v in zip(xs, ws, ms, ss):
+        assert x.shape[0] == M and w.shape == (N, x.shape[1]) and m.shape == v.shape
+        assert m.shape[0] in (1, N)
+    ptrs = lambda arrs: (ctypes.c_void_p * nb)(*[a.ctypes.data for a in arrs])
+    ch = np.array([x.shape[1] for x in xs], np.int32)
+    nq = np.array([m.shape[0] for m in ms], np.int32)
+    keep = (xs, ws, ms, ss, ch, nq)
+    return keep, nb, M, N, ptrs(xs), ch, ptrs(ws), ptrs(ms), ptrs(ss), nq
+
+
+def split_conv_sum(xs, ws, br_mults, br_shifts, bias):
+    """A = bias + sum_b rescale_b(x_b W_b^T), int64 [M, N] (before the output
+    requantization)."""
+    keep, nb, M, N, px, ch, pw, pm, ps, nq = _split_args(xs, ws, br_mults, br_shifts)
+    b = None if bias is None else _arr(bias, np.int32)
+    A = np.zeros((M, N), np.int64)
+    lib().orc_split_conv_sum(nb, px, _p(ch, i32p), pw, pm, ps, _p(nq, i32p),
+                             None if b is None else _p(b, i32p), M, N, _p(A, i64p))
+    return A
+
+
+def split_conv(xs, ws, br_mults, br_shifts, bias, out_mult, out_shift):
+    """Scale-preserving split convolution (pointwise) -> int8 [M, N]."""
+    keep, nb, M, N, px, ch, pw, pm, ps, nq = _split_args(xs, ws, br_mults, br_shifts)
+    b = None if bias is None else _arr(bias, np.int32)
+    om = _arr(out_mult, np.int32).reshape(-1)
+    os_ = _arr(out_shift, np.int32).reshape(-1)
+    y = np.zeros((M, N), np.int8)
+    lib().orc_split_conv(nb, px, _p(ch, i32p), pw, pm, ps, _p(nq, i32p),
+                         None if b is None else _p(b, i32p), M, N, _p(om, i32p),
+                         _p(os_, i32p), om.shape[0], _p(y, i8p))
     return y
 
 

@@ -337,6 +337,62 @@ void orc_linear(const int8_t* x, const int8_t* w, const int32_t* b, int64_t M,
   free(acc);
 }
 
+/* Scale-preserving split convolution (Sec. 3.2.2): the projector's
+ * convolution over concatenated encoder feature maps is split into one
+ * convolution per map, so that each map keeps its own activation scale S_b.
+ * The int32 partial of branch b has scale S_b * S_w; it is brought to the
+ * common scale S_c = max_b S_b by the dyadic m_b / 2^s_b ~ S_b / S_c (an
+ * integer multiply-and-shift), and the rescaled partials are added in
+ * integers.  Readings: the convolution is pointwise (a linear layer over the
+ * tokens of the feature maps); the rescale rounds half up like every dyadic
+ * here and does not saturate; the bias is in the common scale. */
+void orc_split_conv_sum(int32_t n_branches, const int8_t* const* x,
+                        const int32_t* channels, const int8_t* const* w,
+                        const int32_t* const* br_mult, const int32_t* const* br_shift,
+                        const int32_t* br_nq, const int32_t* bias, int64_t M,
+                        int32_t N, int64_t* A) {
+  orc_require(n_branches >= 1, "at least one branch");
+  for (int64_t m = 0; m < M; m++)
+    for (int32_t n = 0; n < N; n++) {
+      __int128 total = bias ? bias[n] : 0;
+      for (int32_t b = 0; b < n_branches; b++) {
+        const int32_t C = channels[b];
+        int64_t acc = 0;
+        for (int32_t k = 0; k < C; k++)
+          acc += (int32_t)x[b][m * C + k] * (int32_t)w[b][(int64_t)n * C + k];
+        const int32_t q = br_nq[b] == 1 ? 0 : n;
+        const int32_t s = br_shift[b][q];
+        orc_require(s >= 1 && s <= 62, "branch rescale shift in [1, 62]");
+        total += floor_div((__int128)acc * br_mult[b][q] + pow2(s - 1), pow2(s));
+      }
+      orc_require(total >= INT64_MIN && total <= INT64_MAX, "sum fits int64");
+      A[m * N + n] = (int64_t)total;
+    }
+}
+
+void orc_split_conv(int32_t n_branches, const int8_t* const* x,
+                    const int32_t* channels, const int8_t* const* w,
+                    const int32_t* const* br_mult, const int32_t* const* br_shift,
+                    const int32_t* br_nq, const int32_t* bias, int64_t M, int32_t N,
+                    const int32_t* out_mult, const int32_t* out_shift, int32_t out_nq,
+                    int8_t* y) {
+  orc_require(out_nq == 1 || out_nq == N, "dyadic is per-tensor or per-channel");
+  int64_t* A = (int64_t*)malloc(sizeof(int64_t) * (size_t)N);
+  orc_require(A != NULL, "allocation");
+  for (int64_t m = 0; m < M; m++) {
+    const int8_t* xs[64];
+    orc_require(n_branches <= 64, "at most 64 branches");
+    for (int32_t b = 0; b < n_branches; b++) xs[b] = x[b] + m * channels[b];
+    orc_split_conv_sum(n_branches, xs, channels, w, br_mult, br_shift, br_nq, bias, 1, N,
+                       A);
+    for (int32_t n = 0; n < N; n++) {
+      const int32_t q = out_nq == 1 ? 0 : n;
+      y[m * N + n] = (int8_t)orc_requant(A[n], out_mult[q], out_shift[q]);
+    }
+  }
+  free(A);
+}
+
 void orc_residual_tensor(const int8_t* a, const int8_t* b, int8_t* y,
                          int64_t n, int32_t mult_a, int32_t mult_b,
                          int32_t shift) {

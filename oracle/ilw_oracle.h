@@ -70,6 +70,25 @@ void orc_residual_tensor(const int8_t* a, const int8_t* b, int8_t* y,
                          int64_t n, int32_t mult_a, int32_t mult_b,
                          int32_t shift);
 
+/* Scale-preserving split convolution of the projector (Sec. 3.2.2, Fig.
+ * projector_split_conv), pointwise: for each branch b (one encoder feature
+ * map with its own activation scale), acc_b = x_b W_b^T over its C_b
+ * channels; r_b = floor((acc_b * m_b + 2^(s_b - 1)) / 2^s_b) rescales the
+ * partial to the common scale (no saturation); A = bias + sum_b r_b; the
+ * output is y = sat8(rq(A; out)).  br_mult[b] / br_shift[b] hold br_nq[b]
+ * entries (1 or N).  orc_split_conv_sum returns A (int64, [M, N]). */
+void orc_split_conv_sum(int32_t n_branches, const int8_t* const* x,
+                        const int32_t* channels, const int8_t* const* w,
+                        const int32_t* const* br_mult, const int32_t* const* br_shift,
+                        const int32_t* br_nq, const int32_t* bias, int64_t M,
+                        int32_t N, int64_t* A);
+void orc_split_conv(int32_t n_branches, const int8_t* const* x,
+                    const int32_t* channels, const int8_t* const* w,
+                    const int32_t* const* br_mult, const int32_t* const* br_shift,
+                    const int32_t* br_nq, const int32_t* bias, int64_t M, int32_t N,
+                    const int32_t* out_mult, const int32_t* out_shift, int32_t out_nq,
+                    int8_t* y);
+
 /* Integer attention of one image: qkv is the int8 [T, 3*D] QKV output
  * (q | k | v, head-major inside each part), out is int8 [T, D]. */
 void orc_attention(const int8_t* qkv, int32_t grid_h, int32_t grid_w,
