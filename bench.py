@@ -73,6 +73,7 @@ KERNEL_OF_STAGE = {
     "gemm_fc2": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
     "block_tail": ("block_tail_kernel", ["paper_2607_24981_amd/csrc/block_tail.hip", _INTERNAL]),
     "layernorm": ("layernorm_rows_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
+    "split_conv": ("split_conv_kernel", ["paper_2607_24981_amd/csrc/split_conv.hip", _INTERNAL]),
 }
 
 
@@ -137,6 +138,8 @@ def main():
         del src, dst
         log(f"calibration copy of {args.calibration_copy_mib} MiB done")
 
+    if args.workload in synth.SPLIT_WORKLOADS:
+        return bench_split(args, synth.SPLIT_WORKLOADS[args.workload])
     wl = synth.WORKLOADS[args.workload]
     B = wl.batch if args.batch is None else args.batch
     log(f"workload {wl.name}: batch {B}, {wl.tokens} tokens, dim {wl.dim}, "
@@ -270,6 +273,110 @@ def main():
         "parity": parity,
         "stages": stages,
     }
+    print(json.dumps(line), flush=True)
+    if parity not in (None, "bit-exact"):
+        sys.exit(1)
+
+
+def _timed(step, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return (t1 - t0) * 1e3 / steps, ev0.elapsed_time(ev1) / steps
+
+
+def bench_split(args, wl):
+    """Stage three: the projector's scale-preserving split convolution."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24981_amd import ilw, synth
+    B = wl.batch if args.batch is None else args.batch
+    log(f"workload {wl.name}: batch {B}, {wl.tokens} tokens, branches {wl.branches} -> {wl.out}")
+    d = synth.split_conv_inputs(wl, args.seed, batch=B)
+    xs = [ilw.to_device(x) for x in d["xs"]]
+    ws = [ilw.to_device(w) for w in d["ws"]]
+    bm = [ilw.to_device(m) for m in d["branch_mults"]]
+    bs = [ilw.to_device(v) for v in d["branch_shifts"]]
+    bias, om, os_ = (ilw.to_device(d[k]) for k in ("bias", "out_mult", "out_shift"))
+    y = torch.empty((B * wl.tokens, wl.out), dtype=torch.int8, device="cuda")
+
+    def eager():
+        ilw.ilw_split_conv(xs, ws, bm, bs, bias, om, os_, y=y)
+
+    step = eager
+    if not args.no_graph:
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            for _ in range(3):
+                eager()
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            eager()
+        step = graph.replay
+    wall_ms, ev_ms = _timed(step, args.steps, args.warmup)
+    ops = wl.gemm_ops() * B // wl.batch
+    tops = ops / (wall_ms * 1e-3) / 1e12
+    log(f"timed {args.steps} steps: {wall_ms:.4f} ms/step wall, {ev_ms:.4f} ms/step events, "
+        f"{tops:.2f} TOPS, {B / (wall_ms * 1e-3):.1f} images/s")
+    result = y.cpu().numpy()
+
+    ilw.profile_enable(True)
+    for _ in range(args.profile_steps):
+        eager()
+    torch.cuda.synchronize()
+    ms, n = ilw.profile_read()["split_conv"]
+    ilw.profile_enable(False)
+    per_launch = ms / n
+    roof = {"bound": "mfma", "achieved": round(ops / (per_launch * 1e-3) / 1e12, 3),
+            "peak": PEAK_INT8_TOPS, "unit": "TOPS"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 5)
+    roof.update({"kernel": "split_conv_kernel", "stage": "split_conv",
+                 "ms_per_launch": round(per_launch, 5), "algorithmic_per_launch": ops,
+                 "traffic": measured_traffic("split_conv", wl.name)})
+    log(f"dominant stage split_conv: {json.dumps(roof)}")
+
+    cpu = parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        if not os.path.exists(oracle._SO):
+            oracle.build()
+        T = wl.tokens
+        c0 = time.perf_counter()
+        ref = oracle.split_conv([x[:T] for x in d["xs"]], d["ws"], d["branch_mults"],
+                                d["branch_shifts"], d["bias"], d["out_mult"], d["out_shift"])
+        c1 = time.perf_counter()
+        ops1 = wl.gemm_ops() // wl.batch
+        cpu = {"value": round(ops1 / (c1 - c0) / 1e12, 6), "unit": "TOPS",
+               "images_per_s": round(1 / (c1 - c0), 4), "cores": 1, "kind": "oracle",
+               "sample": f"one image (1 of {B}) of {wl.name}, {ops1 / 1e9:.3f} G int8 ops, "
+                         f"{c1 - c0:.2f} s"}
+        bad = int(np.count_nonzero(result[:T] != ref))
+        parity = "bit-exact" if bad == 0 else f"{bad} of {ref.size} outputs differ"
+        log(f"cpu baseline {cpu['value']} TOPS; parity of image 0: {parity}")
+
+    line = {"metric": METRIC, "value": round(tops, 3), "unit": "TOPS",
+            "images_per_s": round(B / (wall_ms * 1e-3), 2), "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(wall_ms, 5), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+            "config": {"workload": wl.name, "batch": B, "tokens": wl.tokens,
+                       "branches": list(wl.branches), "out_channels": wl.out,
+                       "launch": "eager" if args.no_graph else "hip graph",
+                       "gemm_ops_per_step": ops},
+            "roofline": roof, "cpu_baseline": cpu, "parity": parity}
     print(json.dumps(line), flush=True)
     if parity not in (None, "bit-exact"):
         sys.exit(1)

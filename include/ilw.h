@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ILW_ABI_VERSION 2
+#define ILW_ABI_VERSION 3
 
 typedef enum {
   ILW_OK = 0,
@@ -246,9 +246,31 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
                     int32_t mode, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Scale-preserving split convolution of the multi-scale projector (Sec.
+ * 3.2.2, Fig. projector_split_conv), pointwise (a linear layer over the
+ * tokens of the feature maps).  Branch b is one encoder feature map with its
+ * own activation scale S_b; its int32 partial is brought to the common scale
+ * (the largest S_b) by the branch's dyadic before the integer accumulation:
+ *   acc_b[m][n] = sum_k x[b][m][k] * w[b][n][k]
+ *   r_b         = floor((acc_b * m_b[n] + 2^(s_b[n]-1)) / 2^s_b[n])  (no saturation)
+ *   y[m][n]     = sat8(rq(bias[n] + sum_b r_b; out))   (sum in 64 bits)
+ *   n_branches  in [1, 8]
+ *   x, w, branch, channels: HOST arrays of n_branches entries; x[b] DEVICE
+ *               int8 [M, channels[b]], w[b] DEVICE int8 [N, channels[b]]
+ *               (both 16-byte aligned), branch[b] a dyadic with n = 1 or N
+ *               (m_b / 2^s_b ~ S_b / S_c), channels[b] a multiple of 64 in
+ *               [64, 65536]
+ *   bias        DEVICE int32 [N] in the common scale, or NULL
+ *   y           DEVICE int8 [M, N]; N a multiple of 16
+ */
+int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* channels,
+                   const int8_t* const* w, const ilw_dyadic* branch, const int32_t* bias,
+                   ilw_dyadic out, int8_t* y, int64_t M, int32_t N, void* stream);
+
+/* ------------------------------------------------------------------------
  * Per-stage kernel timing (tracing; off by default).  While enabled, every
- * kernel that ilw_block_forward, ilw_encoder_forward, ilw_attention and
- * ilw_deform_attn launch is bracketed by a pair of HIP events recorded on the
+ * kernel that ilw_block_forward, ilw_encoder_forward, ilw_attention,
+ * ilw_deform_attn and ilw_split_conv launch is bracketed by a pair of HIP events recorded on the
  * caller's stream, and the launch is attributed to one of the stages below.
  * Enabling (or disabling)
  * clears the records.  ilw_profile_read waits for the last recorded event and
@@ -267,7 +289,8 @@ typedef enum {
   ILW_STAGE_RELAYOUT = 6,    /* token-major QKV -> window-major copy       */
   ILW_STAGE_DEFORM = 7,      /* deformable sampling                        */
   ILW_STAGE_BLOCK_TAIL = 8,  /* projection ... next block's QKV, one launch */
-  ILW_NUM_STAGES = 9
+  ILW_STAGE_SPLIT_CONV = 9,  /* scale-preserving split convolution          */
+  ILW_NUM_STAGES = 10
 } ilw_stage;
 
 int ilw_profile_enable(int enable);

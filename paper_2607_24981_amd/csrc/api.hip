@@ -736,6 +736,58 @@ int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
   return ok();
 }
 
+int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* channels,
+                   const int8_t* const* w, const ilw_dyadic* branch, const int32_t* bias,
+                   ilw_dyadic out, int8_t* y, int64_t M, int32_t N, void* stream) {
+  REQUIRE(n_branches >= 1 && n_branches <= kMaxBranches, ILW_E_SHAPE,
+          "n_branches = %d must be in [1, %d]", n_branches, kMaxBranches);
+  REQUIRE(x && channels && w && branch, ILW_E_NULL,
+          "x, channels, w and branch (host arrays) must not be NULL");
+  REQUIRE(M >= 0 && N >= 16 && N % 16 == 0, ILW_E_SHAPE,
+          "M = %lld, N = %d invalid (N a positive multiple of 16)", (long long)M, N);
+  REQUIRE((M + 63) / 64 * ((N + 63) / 64) < (int64_t)1 << 31, ILW_E_UNSUPPORTED,
+          "too many tiles");
+  int e;
+  SplitArgs a = {};
+  a.nbr = n_branches;
+  int32_t ks = 0;
+  for (int32_t b = 0; b < n_branches; ++b) {
+    REQUIRE(channels[b] >= 64 && channels[b] <= 65536 && channels[b] % 64 == 0, ILW_E_SHAPE,
+            "channels[%d] = %d must be a multiple of 64 in [64, 65536]", b, channels[b]);
+    if ((e = check_dyadic(branch[b], N, "branch"))) return e;
+    a.C[b] = channels[b];
+    a.kstart[b] = ks;
+    ks += channels[b] / 64;
+    a.bmult[b] = branch[b].mult;
+    a.bshift[b] = branch[b].shift;
+    a.bnq[b] = branch[b].n;
+  }
+  a.kstart[n_branches] = ks;
+  if ((e = check_dyadic(out, N, "out"))) return e;
+  if (M == 0) return ok();
+  REQUIRE(y, ILW_E_NULL, "y must not be NULL");
+  REQUIRE(((uintptr_t)y & 3) == 0, ILW_E_PARAM, "y must be 4-byte aligned");
+  for (int32_t b = 0; b < n_branches; ++b) {
+    REQUIRE(x[b] && w[b], ILW_E_NULL, "x[%d] and w[%d] must not be NULL", b, b);
+    REQUIRE(aligned16(x[b]) && aligned16(w[b]), ILW_E_PARAM,
+            "x[%d] and w[%d] must be 16-byte aligned", b, b);
+    a.x[b] = x[b];
+    a.w[b] = w[b];
+  }
+  a.bias = bias;
+  a.omult = out.mult;
+  a.oshift = out.shift;
+  a.onq = out.n;
+  a.y = y;
+  a.M = M;
+  a.N = N;
+  hipStream_t s = (hipStream_t)stream;
+  StageTimer t(ILW_STAGE_SPLIT_CONV, s);
+  const hipError_t he = launch_split_conv(a, s);
+  t.done();
+  return hip_status(he, "ilw_split_conv");
+}
+
 int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
                     int32_t L, int32_t P, const int32_t* ref, const int16_t* offsets,
                     const int8_t* logits, int8_t* out, int32_t B, int32_t Q, int32_t heads,

@@ -297,6 +297,27 @@ struct TailArgs {
 };
 hipError_t launch_block_tail(const TailArgs& a, hipStream_t s);
 
+// Scale-preserving split convolution (pointwise), up to kMaxBranches branches.
+constexpr int kMaxBranches = 8;
+struct SplitArgs {
+  int32_t nbr;
+  const int8_t* x[kMaxBranches];   // [M, C_b]
+  const int8_t* w[kMaxBranches];   // [N, C_b]
+  int32_t C[kMaxBranches];
+  int32_t kstart[kMaxBranches + 1];  // first 64-channel K step of each branch
+  const int32_t* bmult[kMaxBranches];
+  const int32_t* bshift[kMaxBranches];
+  int32_t bnq[kMaxBranches];
+  const int32_t* bias;
+  const int32_t* omult;
+  const int32_t* oshift;
+  int32_t onq;
+  int8_t* y;  // [M, N]
+  int64_t M;
+  int32_t N;
+};
+hipError_t launch_split_conv(const SplitArgs& a, hipStream_t s);
+
 struct AttnArgs {
   const int8_t* q;
   const int8_t* k;

@@ -16,7 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -73,6 +73,8 @@ _SIGS = {
     "ilw_encoder_workspace_bytes": (c_size, [c_vp, c_i32, c_vp, c_i32, c_i32, c_i32]),
     "ilw_encoder_forward": (ctypes.c_int, [c_vp, c_i32, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32,
                                            c_vp, c_size, c_vp]),
+    "ilw_split_conv": (ctypes.c_int, [c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, Dyadic, c_vp,
+                                      c_i64, c_i32, c_vp]),
     "ilw_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "ilw_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(c_i32), c_i32]),
@@ -327,6 +329,27 @@ class Encoder:
         return out
 
 
+def ilw_split_conv(xs, ws, branch_mults, branch_shifts, bias, out_mult, out_shift, y=None):
+    """Scale-preserving split convolution: xs[b] int8 [M, C_b], ws[b] int8
+    [N, C_b], per-branch rescale dyadics, bias int32 [N] or None, output
+    dyadic -> int8 [M, N]."""
+    nb = len(xs)
+    assert len(ws) == len(branch_mults) == len(branch_shifts) == nb
+    M, N = xs[0].shape[0], ws[0].shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.int8, device=xs[0].device)
+    xp = (c_vp * nb)(*[_dev(x, torch.int8, "x") for x in xs])
+    wp = (c_vp * nb)(*[_dev(w, torch.int8, "w") for w in ws])
+    ch = (c_i32 * nb)(*[int(x.shape[1]) for x in xs])
+    br = (Dyadic * nb)(*[_dyadic(m, s_) for m, s_ in zip(branch_mults, branch_shifts)])
+    rc = lib().ilw_split_conv(nb, xp, ch, wp, br,
+                              None if bias is None else _dev(bias, torch.int32, "bias"),
+                              _dyadic(out_mult, out_shift), _dev(y, torch.int8, "y"), M, N,
+                              _stream())
+    _check(rc, "ilw_split_conv")
+    return y
+
+
 def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
                     out_shift, mode=0, s_d=-1, out=None):
     """value int8 [B, S, H, Dh]; ref int32 [B, Q, 2]; offsets int16 [B, Q, H, L, P, 2];
@@ -348,7 +371,7 @@ def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
-          "relayout", "deform", "block_tail"]
+          "relayout", "deform", "block_tail", "split_conv"]
 
 
 def profile_enable(on: bool = True):

@@ -79,6 +79,21 @@ class DeformWorkload:
     points: int
 
 
+@dataclass(frozen=True)
+class SplitConvWorkload:
+    """Projector input convolution: `branches` encoder feature maps of the
+    given channel counts, each with its own activation scale, to `out`
+    channels, over batch x tokens positions."""
+    name: str
+    batch: int
+    tokens: int
+    branches: tuple  # channels per branch
+    out: int
+
+    def gemm_ops(self) -> int:
+        return 2 * self.batch * self.tokens * self.out * sum(self.branches)
+
+
 def _alt(n, win):
     """n blocks alternating window / global, window first."""
     return tuple(win if i % 2 == 0 else (0, 0) for i in range(n))
@@ -103,6 +118,15 @@ WORKLOADS = {
 DEFORM_WORKLOADS = {
     "deform_q300_d256_b8": DeformWorkload("deform_q300_d256_b8", 8, 300, 256, 8, 32,
                                           ((80, 80), (40, 40), (20, 20)), 4),
+}
+
+# Stage three: the projector's split convolution over three 192-channel
+# feature maps of the tiny encoder (40x40 tokens) to 256 channels
+SPLIT_WORKLOADS = {
+    "splitconv_t1600_c3x192_n256_b1": SplitConvWorkload("splitconv_t1600_c3x192_n256_b1", 1,
+                                                        1600, (192, 192, 192), 256),
+    "splitconv_t1600_c3x192_n256_b32": SplitConvWorkload("splitconv_t1600_c3x192_n256_b32", 32,
+                                                         1600, (192, 192, 192), 256),
 }
 
 # Config order of the five workloads (encoder block, tiny encoder, medium
@@ -206,3 +230,32 @@ def deform_inputs(wl: DeformWorkload, seed: int, batch: int | None = None,
 def int8_tensor(seed: int, shape, lo: int = -127, hi: int = 127) -> np.ndarray:
     rng = np.random.Generator(np.random.PCG64(seed))
     return _u(rng, lo, hi, shape, np.int8)
+
+
+def split_conv_inputs(wl: SplitConvWorkload, seed: int, batch: int | None = None,
+                      per_channel: bool = False) -> dict:
+    """Inputs of the split convolution: int8 feature maps and weights per
+    branch; each branch's activation scale drawn in [0.005, 0.05], its rescale
+    dyadic m / 2^30 ~ S_b / max(S) (per-channel variant: a per-channel weight
+    scale ratio in [0.5, 1] on top); int32 bias; output dyadic with mult
+    U[2^29, 2^30] and shift U[40, 44]."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    B = wl.batch if batch is None else batch
+    M, N = B * wl.tokens, wl.out
+    xs = [_u(rng, -127, 127, (M, c), np.int8) for c in wl.branches]
+    ws = [_u(rng, -127, 127, (N, c), np.int8) for c in wl.branches]
+    scales = rng.uniform(0.005, 0.05, len(wl.branches))
+    top = scales.max()
+    bm, bs = [], []
+    for sb in scales:
+        ratio = sb / top
+        if per_channel:
+            ratio = ratio * rng.uniform(0.5, 1.0, N)
+        m = np.round(np.atleast_1d(ratio) * (1 << 30)).astype(np.int64)
+        bm.append(np.minimum(m, (1 << 30)).astype(np.int32))
+        bs.append(np.full(m.shape, 30, np.int32))
+    bias = _u(rng, -(1 << 15), 1 << 15, N)
+    om = _u(rng, 1 << 29, 1 << 30, N)
+    os_ = _u(rng, 40, 44, N)
+    return {"xs": xs, "ws": ws, "branch_mults": bm, "branch_shifts": bs, "bias": bias,
+            "out_mult": om, "out_shift": os_, "scales": scales}

@@ -211,3 +211,29 @@ def test_attention_and_deform_validation():
     assert call(Q=0) == OK
     assert L.ilw_deform_attn(FAKE, None, st, 3, 4, FAKE, FAKE, FAKE, FAKE, 8, 300, 8, 32, 16,
                              -1, 1 << 30, 34, 0, None) == E_NULL
+
+
+def test_split_conv_validation():
+    L = ilw.lib()
+    d = ilw.Dyadic(FAKE, FAKE, 1)
+
+    def call(nb=2, chans=(64, 128), N=64, M=10, br=None, out=None, x=True, w=True, y=FAKE):
+        xp = (ctypes.c_void_p * max(nb, 1))(*([FAKE] * max(nb, 1)))
+        wp = (ctypes.c_void_p * max(nb, 1))(*([FAKE] * max(nb, 1)))
+        ch = (ctypes.c_int32 * max(nb, 1))(*(list(chans) + [64] * max(nb, 1))[:max(nb, 1)])
+        bd = br if br is not None else (ilw.Dyadic * max(nb, 1))(*([d] * max(nb, 1)))
+        return L.ilw_split_conv(nb, xp if x else None, ch, wp if w else None, bd, None,
+                                out if out is not None else d, y, M, N, None)
+
+    assert call(nb=0) == E_SHAPE
+    assert call(nb=9, chans=(64,) * 9) == E_SHAPE
+    assert call(chans=(64, 100)) == E_SHAPE          # not a multiple of 64
+    assert call(chans=(64, 65600)) == E_SHAPE
+    assert call(N=40) == E_SHAPE                     # N % 16
+    assert call(x=False) == E_NULL
+    assert call(w=False) == E_NULL
+    assert call(br=(ilw.Dyadic * 2)(d, ilw.Dyadic(FAKE, FAKE, 7))) == E_SHAPE
+    assert call(br=(ilw.Dyadic * 2)(d, ilw.Dyadic(None, FAKE, 1))) == E_NULL
+    assert call(out=ilw.Dyadic(FAKE, FAKE, 3)) == E_SHAPE
+    assert call(M=0) == OK
+    assert call(y=FAKE + 2) == E_PARAM

@@ -409,6 +409,81 @@ def test_encoder_deterministic():
     assert_same(a, b, "determinism")
 
 
+# ------------------------------------------------------------------ split convolution
+def _split_case(g, M, N, chans, per_channel):
+    xs = [g.integers(-127, 128, (M, c)).astype(np.int8) for c in chans]
+    ws = [g.integers(-127, 128, (N, c)).astype(np.int8) for c in chans]
+    nq = N if per_channel else 1
+    bm = [g.integers(2 ** 27, 2 ** 30 + 1, nq).astype(np.int32) for _ in chans]
+    bs = [np.full(nq, 30, np.int32) for _ in chans]
+    bias = g.integers(-2 ** 15, 2 ** 15 + 1, N).astype(np.int32)
+    om = g.integers(2 ** 29, 2 ** 30 + 1, nq).astype(np.int32)
+    os_ = g.integers(38, 44, nq).astype(np.int32)
+    return xs, ws, bm, bs, bias, om, os_
+
+
+def _split_gpu(xs, ws, bm, bs, bias, om, os_):
+    return host(ilw.ilw_split_conv([dev(x) for x in xs], [dev(w) for w in ws],
+                                   [dev(m) for m in bm], [dev(v) for v in bs],
+                                   None if bias is None else dev(bias), dev(om), dev(os_)))
+
+
+@pytest.mark.parametrize("M,N,chans", [(1, 16, (64,)), (37, 48, (64, 128)),
+                                       (300, 256, (192, 192, 192)),
+                                       (1000, 144, (64,) * 8), (129, 32, (384, 64, 192))])
+@pytest.mark.parametrize("per_channel", [False, True])
+def test_split_conv_shapes(M, N, chans, per_channel):
+    say(f"split conv M={M} N={N} chans={chans} per_channel={per_channel}")
+    g = rng(M + N + len(chans) + per_channel)
+    args = _split_case(g, M, N, chans, per_channel)
+    ref = oracle.split_conv(*args)
+    assert_same(_split_gpu(*args), ref, "split conv")
+
+
+def test_split_conv_edge_params():
+    """No bias; a branch rescale far above 1 (64-bit running sums, outputs
+    saturated through the pre-clamp); a rescale of 1/2 (exact ties)."""
+    say("split conv edge parameters")
+    g = rng(77)
+    xs, ws, bm, bs, _, om, os_ = _split_case(g, 70, 64, (64, 128, 64), True)
+    bm[0][:] = 2 ** 31 - 1
+    bs[0][:] = 1
+    bm[1][:] = 1
+    bs[1][:] = 1
+    ref = oracle.split_conv(xs, ws, bm, bs, None, om, os_)
+    assert np.mean(np.abs(ref) == 127) > 0.5
+    assert_same(_split_gpu(xs, ws, bm, bs, None, om, os_), ref, "split conv edge")
+    bm[0][:] = 1 << 30
+    bs[0][:] = 30
+    ref = oracle.split_conv(xs, ws, bm, bs, None, om, os_)
+    assert_same(_split_gpu(xs, ws, bm, bs, None, om, os_), ref, "split conv ties")
+
+
+@pytest.mark.parametrize("per_channel", [False, True])
+def test_split_conv_projector_b1_full(per_channel):
+    wl = synth.SPLIT_WORKLOADS["splitconv_t1600_c3x192_n256_b1"]
+    say(f"{wl.name} per_channel={per_channel}")
+    d = synth.split_conv_inputs(wl, 5, per_channel=per_channel)
+    args = (d["xs"], d["ws"], d["branch_mults"], d["branch_shifts"], d["bias"],
+            d["out_mult"], d["out_shift"])
+    assert_same(_split_gpu(*args), oracle.split_conv(*args), "projector b1")
+
+
+def test_split_conv_projector_b32_sampled():
+    """Batch 32 (the large-tile launch): three images against the oracle."""
+    wl = synth.SPLIT_WORKLOADS["splitconv_t1600_c3x192_n256_b32"]
+    say(wl.name)
+    d = synth.split_conv_inputs(wl, 6)
+    got = _split_gpu(d["xs"], d["ws"], d["branch_mults"], d["branch_shifts"], d["bias"],
+                     d["out_mult"], d["out_shift"])
+    T = wl.tokens
+    for b in (0, 13, 31):
+        rows = slice(b * T, (b + 1) * T)
+        ref = oracle.split_conv([x[rows] for x in d["xs"]], d["ws"], d["branch_mults"],
+                                d["branch_shifts"], d["bias"], d["out_mult"], d["out_shift"])
+        assert_same(got[rows], ref, f"image {b}")
+
+
 # ------------------------------------------------------------------ deformable sampling
 @pytest.mark.parametrize("mode", [0, 1])
 def test_deform_c5_full(mode):
