@@ -90,6 +90,10 @@ def lib():
                                              c_i32, i32p]),
             "orc_shiftmax_rows": (None, [i8p, i8p, c_i64, c_i32, c_i32, c_i32,
                                          c_i32, c_i32, c_i32]),
+            "orc_shiftmax_ivit_rows": (None, [i8p, i8p, c_i64, c_i32, c_i32, c_i32,
+                                              c_i32, c_i32]),
+            "orc_shiftgelu_ivit_rows": (None, [i8p, i8p, c_i64, c_i32, c_i32, c_i32,
+                                               c_i32, c_i32, c_i32]),
             "orc_sdshiftgelu_tensor": (None, [i8p, i8p, c_i64, c_i32, c_i32,
                                               c_i32, c_i32, c_i32]),
             "orc_int_layernorm_row": (None, [i8p, c_i32, i32p, i32p, i32p, c_i32,
@@ -289,6 +293,25 @@ def split_conv(xs, ws, br_mults, br_shifts, bias, out_mult, out_shift):
     lib().orc_split_conv(nb, px, _p(ch, i32p), pw, pm, ps, _p(nq, i32p),
                          None if b is None else _p(b, i32p), M, N, _p(om, i32p),
                          _p(os_, i32p), om.shape[0], _p(y, i8p))
+    return y
+
+
+def shiftmax_ivit_rows(x, I0, M=31, k_inter=16, k_out=8):
+    """I-ViT Shiftmax (fixed division precision M) of every row of int8 x."""
+    x = _arr(x, np.int8)
+    rows, cols = x.reshape(-1, x.shape[-1]).shape
+    y = np.zeros_like(x)
+    lib().orc_shiftmax_ivit_rows(_p(x, i8p), _p(y, i8p), rows, cols, I0, k_inter, k_out, M)
+    return y
+
+
+def shiftgelu_ivit_rows(x, I0, out_mult, out_shift, k_inter=16, k_out=8):
+    """I-ViT ShiftGELU (row-maximum shift) of every row of int8 x, requantized."""
+    x = _arr(x, np.int8)
+    rows, cols = x.reshape(-1, x.shape[-1]).shape
+    y = np.zeros_like(x)
+    lib().orc_shiftgelu_ivit_rows(_p(x, i8p), _p(y, i8p), rows, cols, I0, k_inter, k_out,
+                                  out_mult, out_shift)
     return y
 
 

@@ -195,6 +195,46 @@ void orc_shiftmax_ivit_row(const int32_t* x, int32_t d, int32_t I0,
   }
 }
 
+void orc_shiftmax_ivit_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                            int32_t I0, int32_t k_inter, int32_t k_out, int32_t M) {
+  orc_require(M >= k_out && M <= 32, "division precision M in [k_out, 32]");
+  int32_t* in = (int32_t*)malloc(sizeof(int32_t) * (size_t)cols);
+  int32_t* out = (int32_t*)malloc(sizeof(int32_t) * (size_t)cols);
+  orc_require(in && out, "allocation");
+  for (int64_t r = 0; r < rows; r++) {
+    for (int32_t i = 0; i < cols; i++) in[i] = x[r * cols + i];
+    orc_shiftmax_ivit_row(in, cols, I0, k_inter, k_out, M, out);
+    for (int32_t i = 0; i < cols; i++) {
+      orc_require(out[i] >= 0 && out[i] <= 127, "I-ViT Shiftmax output fits int8");
+      y[r * cols + i] = (int8_t)out[i];
+    }
+  }
+  free(in);
+  free(out);
+}
+
+/* ShiftGELU of I-ViT over rows: the vector whose maximum shifts the sigmoid
+ * argument is the row (one token's channels).  Reading: the maximum is
+ * clamped at 0, which keeps every ShiftExp argument <= 0; a row with no
+ * positive I_p then gives exactly SD-ShiftGELU. */
+void orc_shiftgelu_ivit_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                             int32_t I0, int32_t k_inter, int32_t k_out,
+                             int32_t out_mult, int32_t out_shift) {
+  for (int64_t r = 0; r < rows; r++) {
+    int64_t max_ip = 0;
+    for (int32_t i = 0; i < cols; i++) {
+      const int64_t I = x[r * cols + i];
+      const int64_t Ip = I + (int64_t)floor_div(I, 2) + (int64_t)floor_div(I, 8) +
+                         (int64_t)floor_div(I, 16);
+      if (Ip > max_ip) max_ip = Ip;
+    }
+    for (int32_t i = 0; i < cols; i++)
+      y[r * cols + i] = (int8_t)orc_requant(
+          orc_ivit_shiftgelu(x[r * cols + i], (int32_t)max_ip, I0, k_inter, k_out),
+          out_mult, out_shift);
+  }
+}
+
 /* IntDiv, which Alg. 1 uses without defining.  Reading: the I-ViT integer
  * division of eq. shiftmax_original with M = M_hw = 31 applied to one
  * numerator, giving a k_out-bit ratio with scale 2^-(k_out-1):

@@ -50,6 +50,15 @@ void orc_shiftmax_ivit_row(const int32_t* x, int32_t d, int32_t I0,
 void orc_shiftmax_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
                        int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
                        int32_t s_d_static);
+/* I-ViT baselines over rows of int8 (the forms the paper's operators
+ * replace): Shiftmax with a fixed division precision M (eq.
+ * shiftmax_original), and ShiftGELU shifted by the row maximum of I_p
+ * (clamped at 0), requantized to int8 like SD-ShiftGELU. */
+void orc_shiftmax_ivit_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                            int32_t I0, int32_t k_inter, int32_t k_out, int32_t M);
+void orc_shiftgelu_ivit_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                             int32_t I0, int32_t k_inter, int32_t k_out,
+                             int32_t out_mult, int32_t out_shift);
 void orc_sdshiftgelu_tensor(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
                             int32_t k_inter, int32_t k_out, int32_t out_mult,
                             int32_t out_shift);
