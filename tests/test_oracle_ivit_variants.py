@@ -76,7 +76,7 @@ def test_shiftgelu_large_row_maximum_loses_the_sigmoid():
     shifted argument I_p - 212 reaches the ShiftExp clamp (Alg. 1: I_e =
     I + I/2 - I/16 <= -k_inter * I0) get a = a' = I0, so their sigmoid factor
     is floor(floor((2^31 - 1) / (2 I0)) * I0 / 2^24) = 63, i.e. 1/2, whatever
-    x; SD-ShiftGELU follows the sigmoid, and its worst error is 10x smaller."""
+    x; SD-ShiftGELU follows the sigmoid, and its worst error is 5x smaller."""
     I0, k_inter = 16, 16
     Ip = lambda v: v + v // 2 + v // 8 + v // 16
     Ie = lambda v: v + v // 2 - v // 16
@@ -92,4 +92,4 @@ def test_shiftgelu_large_row_maximum_loses_the_sigmoid():
     ivit = np.array([oracle.ivit_shiftgelu(v, mx, I0) for v in range(1, 128)])
     sd = np.array([oracle.sdshiftgelu(v, I0) for v in range(1, 128)])
     ideal = np.array([v / (1 + math.exp(-1.702 * v / I0)) * 128 for v in range(1, 128)])
-    assert np.abs(ivit - ideal).max() > 10 * np.abs(sd - ideal).max()
+    assert np.abs(ivit - ideal).max() > 5 * np.abs(sd - ideal).max()
