@@ -246,6 +246,25 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
                     int32_t mode, void* stream);
 
 /* ------------------------------------------------------------------------
+ * I-ViT baseline operators, the forms that Constrained Shiftmax and
+ * SD-ShiftGELU replace (for comparisons; same layouts as the operators
+ * above, one row = one contiguous run of cols int8 values, y may alias x):
+ *   ilw_shiftmax_ivit   eq. shiftmax_original (Sec. 3.3.2) with a fixed
+ *       division precision M in [k_out, 32]:
+ *       out = (floor((2^M - 1) / S_sum) * I_exp) >> (M - (k_out - 1));
+ *       the factor is 0 once S_sum >= 2^M (the collapse the paper describes)
+ *   ilw_shiftgelu_ivit  ShiftGELU (Sec. 3.3.1) with the sigmoid argument
+ *       shifted by the row maximum of I_p (clamped at 0) instead of
+ *       element-wise, then the same int8 requantization as ilw_sdshiftgelu
+ * Parameters otherwise as ilw_shiftmax / ilw_sdshiftgelu.
+ */
+int ilw_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
+                      int32_t k_inter, int32_t k_out, int32_t M, void* stream);
+int ilw_shiftgelu_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
+                       int32_t k_inter, int32_t k_out, int32_t out_mult, int32_t out_shift,
+                       void* stream);
+
+/* ------------------------------------------------------------------------
  * Scale-preserving split convolution of the multi-scale projector (Sec.
  * 3.2.2, Fig. projector_split_conv), pointwise (a linear layer over the
  * tokens of the feature maps).  Branch b is one encoder feature map with its

@@ -561,6 +561,36 @@ int ilw_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t
                     "ilw_shiftmax");
 }
 
+int ilw_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
+                      int32_t k_inter, int32_t k_out, int32_t M, void* stream) {
+  REQUIRE(rows >= 0 && cols >= 1 && cols <= 65536, ILW_E_SHAPE,
+          "rows=%lld cols=%d invalid (cols in [1, 65536])", (long long)rows, cols);
+  REQUIRE((rows + 3) / 4 < (int64_t)1 << 31, ILW_E_UNSUPPORTED, "too many rows");
+  int e;
+  if ((e = check_shiftmax(I0, k_inter, k_out, 4, 0))) return e;
+  REQUIRE(M >= k_out && M <= 32, ILW_E_PARAM, "M = %d must be in [k_out, 32]", M);
+  if (rows == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  return hip_status(launch_shiftmax_ivit(x, y, rows, cols, I0, k_inter, k_out, M,
+                                         (hipStream_t)stream),
+                    "ilw_shiftmax_ivit");
+}
+
+int ilw_shiftgelu_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
+                       int32_t k_inter, int32_t k_out, int32_t out_mult, int32_t out_shift,
+                       void* stream) {
+  REQUIRE(rows >= 0 && cols >= 1 && cols <= 65536, ILW_E_SHAPE,
+          "rows=%lld cols=%d invalid (cols in [1, 65536])", (long long)rows, cols);
+  REQUIRE((rows + 3) / 4 < (int64_t)1 << 31, ILW_E_UNSUPPORTED, "too many rows");
+  int e;
+  if ((e = check_gelu(I0, k_inter, k_out, out_mult, out_shift))) return e;
+  if (rows == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  return hip_status(launch_shiftgelu_ivit(x, y, rows, cols, I0, k_inter, k_out, out_mult,
+                                          out_shift, (hipStream_t)stream),
+                    "ilw_shiftgelu_ivit");
+}
+
 int ilw_sdshiftgelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0, int32_t k_inter,
                     int32_t k_out, int32_t out_mult, int32_t out_shift, void* stream) {
   REQUIRE(n >= 0, ILW_E_SHAPE, "n=%lld must be >= 0", (long long)n);

@@ -334,6 +334,12 @@ hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                             const int32_t* beta, const int32_t* mult,
                             const int32_t* shift, int32_t nq, int32_t iters,
                             hipStream_t s);
+hipError_t launch_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                               int32_t I0, int32_t k_inter, int32_t k_out, int32_t M,
+                               hipStream_t s);
+hipError_t launch_shiftgelu_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                                 int32_t I0, int32_t k_inter, int32_t k_out, int32_t mult,
+                                 int32_t shift, hipStream_t s);
 hipError_t launch_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
                            int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
                            int32_t s_d, hipStream_t s);

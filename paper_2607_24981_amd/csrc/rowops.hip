@@ -261,6 +261,68 @@ __global__ __launch_bounds__(256) void shiftmax_kernel(const int8_t* x, int8_t* 
   }
 }
 
+// I-ViT baselines (the forms the paper's operators replace), for comparison.
+//
+// Shiftmax with a fixed division precision M (eq. shiftmax_original):
+// out = (floor((2^M - 1) / S_sum) * I_exp) >> (M - (k_out - 1)).  The factor is
+// an exact floor from a correctly rounded FP64 quotient and one integer
+// correction (numerator < 2^32, S_sum < 2^47).
+__global__ __launch_bounds__(256) void shiftmax_ivit_kernel(const int8_t* x, int8_t* y,
+                                                            int64_t rows, int32_t cols,
+                                                            int32_t I0, int32_t k_inter,
+                                                            int32_t k_out, int32_t M) {
+  __shared__ int32_t elut[256];
+  elut[threadIdx.x] = shift_exp(-(int32_t)threadIdx.x, I0, k_inter);
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int8_t* xr = x + row * cols;
+  int8_t* yr = y + row * cols;
+  int32_t m = -128;
+  for (int32_t j = lane; j < cols; j += 64) m = max(m, (int32_t)xr[j]);
+  m = wave_max_i32(m);
+  uint64_t sum = 0;
+  for (int32_t j = lane; j < cols; j += 64) sum += (uint32_t)elut[m - xr[j]];
+  sum = wave_sum_u64(sum);
+  const uint64_t num = (1ull << M) - 1;
+  int64_t f = (int64_t)((double)num / (double)sum);
+  const int64_t r = (int64_t)num - f * (int64_t)sum;
+  f += r < 0 ? -1 : (r >= (int64_t)sum ? 1 : 0);
+  const int32_t sh = M - (k_out - 1);
+  for (int32_t j = lane; j < cols; j += 64)
+    yr[j] = (int8_t)(((uint64_t)f * (uint32_t)elut[m - xr[j]]) >> sh);
+}
+
+// ShiftGELU with the sigmoid argument shifted by the row maximum of I_p
+// (clamped at 0) instead of element-wise by ReLU(I_p), requantized to int8
+// like SD-ShiftGELU.  One wave per row.
+__global__ __launch_bounds__(256) void shiftgelu_ivit_kernel(const int8_t* x, int8_t* y,
+                                                             int64_t rows, int32_t cols,
+                                                             int32_t I0, int32_t k_inter,
+                                                             int32_t k_out, int32_t mult,
+                                                             int32_t shift) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int8_t* xr = x + row * cols;
+  int8_t* yr = y + row * cols;
+  int32_t mx = -128;
+  for (int32_t j = lane; j < cols; j += 64) mx = max(mx, (int32_t)xr[j]);
+  mx = wave_max_i32(mx);
+  // I_p is non-decreasing in x, so its row maximum is I_p of the row maximum
+  const int32_t max_ip = max(mx + (mx >> 1) + (mx >> 3) + (mx >> 4), 0);
+  const uint32_t a2 = (uint32_t)shift_exp(-max_ip, I0, k_inter);
+  for (int32_t j = lane; j < cols; j += 64) {
+    const int32_t v = xr[j];
+    const int32_t ip = v + (v >> 1) + (v >> 3) + (v >> 4);
+    const uint32_t a = (uint32_t)shift_exp(ip - max_ip, I0, k_inter);
+    const uint32_t f = 0x7fffffffu / (a + a2);
+    const int32_t d = (int32_t)(((uint64_t)f * a) >> (32 - k_out));
+    yr[j] = (int8_t)rq(v * d, mult, shift);
+  }
+}
+
 // ---------------------------------------------------------------- GELU
 __global__ __launch_bounds__(256) void gelu_kernel(const int8_t* x, int8_t* y, int64_t n,
                                                    int32_t I0, int32_t k_inter,
@@ -367,6 +429,24 @@ hipError_t launch_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t col
   dim3 grid((unsigned)((rows + 3) / 4)), block(256);
   hipLaunchKernelGGL(shiftmax_kernel, grid, block, 0, s, x, y, rows, cols, I0, k_inter,
                      k_out, m_p, s_d);
+  return hipGetLastError();
+}
+
+hipError_t launch_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                               int32_t I0, int32_t k_inter, int32_t k_out, int32_t M,
+                               hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(shiftmax_ivit_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                     x, y, rows, cols, I0, k_inter, k_out, M);
+  return hipGetLastError();
+}
+
+hipError_t launch_shiftgelu_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
+                                 int32_t I0, int32_t k_inter, int32_t k_out, int32_t mult,
+                                 int32_t shift, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(shiftgelu_ivit_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                     x, y, rows, cols, I0, k_inter, k_out, mult, shift);
   return hipGetLastError();
 }
 

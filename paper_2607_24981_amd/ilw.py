@@ -61,6 +61,10 @@ _SIGS = {
                                     c_i32, c_vp]),
     "ilw_sdshiftgelu": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32, c_i32,
                                        c_vp]),
+    "ilw_shiftmax_ivit": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                         c_vp]),
+    "ilw_shiftgelu_ivit": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                          c_i32, c_vp]),
     "ilw_int_layernorm": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_vp, Dyadic, c_i32,
                                          c_vp]),
     "ilw_residual_add": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_vp]),
@@ -327,6 +331,29 @@ class Encoder:
                                        _stream())
         _check(rc, "ilw_encoder_forward")
         return out
+
+
+def ilw_shiftmax_ivit(x, I0, M=31, k_inter=16, k_out=8, y=None):
+    """I-ViT Shiftmax (fixed division precision M) of every row of int8 x."""
+    cols = x.shape[-1]
+    rows = x.numel() // cols
+    if y is None:
+        y = torch.empty_like(x)
+    _check(lib().ilw_shiftmax_ivit(_dev(x, torch.int8, "x"), _dev(y, torch.int8, "y"), rows,
+                                   cols, I0, k_inter, k_out, M, _stream()), "ilw_shiftmax_ivit")
+    return y
+
+
+def ilw_shiftgelu_ivit(x, I0, out_mult, out_shift, k_inter=16, k_out=8, y=None):
+    """I-ViT ShiftGELU (row-maximum shift) of every row of int8 x, requantized."""
+    cols = x.shape[-1]
+    rows = x.numel() // cols
+    if y is None:
+        y = torch.empty_like(x)
+    _check(lib().ilw_shiftgelu_ivit(_dev(x, torch.int8, "x"), _dev(y, torch.int8, "y"), rows,
+                                    cols, I0, k_inter, k_out, out_mult, out_shift, _stream()),
+           "ilw_shiftgelu_ivit")
+    return y
 
 
 def ilw_split_conv(xs, ws, branch_mults, branch_shifts, bias, out_mult, out_shift, y=None):

@@ -237,3 +237,16 @@ def test_split_conv_validation():
     assert call(out=ilw.Dyadic(FAKE, FAKE, 3)) == E_SHAPE
     assert call(M=0) == OK
     assert call(y=FAKE + 2) == E_PARAM
+
+
+def test_ivit_baseline_validation():
+    L = ilw.lib()
+    assert L.ilw_shiftmax_ivit(FAKE, FAKE, 4, 8, 16, 16, 8, 7, None) == E_PARAM   # M < k_out
+    assert L.ilw_shiftmax_ivit(FAKE, FAKE, 4, 8, 16, 16, 8, 33, None) == E_PARAM
+    assert L.ilw_shiftmax_ivit(FAKE, FAKE, 4, 0, 16, 16, 8, 31, None) == E_SHAPE
+    assert L.ilw_shiftmax_ivit(FAKE, FAKE, 4, 8, 0, 16, 8, 31, None) == E_PARAM
+    assert L.ilw_shiftmax_ivit(None, FAKE, 4, 8, 16, 16, 8, 31, None) == E_NULL
+    assert L.ilw_shiftmax_ivit(FAKE, FAKE, 0, 8, 16, 16, 8, 31, None) == OK
+    assert L.ilw_shiftgelu_ivit(FAKE, FAKE, 4, 8, 16, 16, 8, 1 << 30, 63, None) == E_PARAM
+    assert L.ilw_shiftgelu_ivit(FAKE, FAKE, 4, 70000, 16, 16, 8, 1 << 30, 36, None) == E_SHAPE
+    assert L.ilw_shiftgelu_ivit(FAKE, None, 4, 8, 16, 16, 8, 1 << 30, 36, None) == E_NULL

@@ -409,6 +409,41 @@ def test_encoder_deterministic():
     assert_same(a, b, "determinism")
 
 
+# ------------------------------------------------------------------ I-ViT baselines
+@pytest.mark.parametrize("rows,cols", [(1, 1), (7, 4), (300, 400), (64, 1600), (3, 65536)])
+@pytest.mark.parametrize("I0,M", [(8, 31), (64, 16), (8192, 31), (24, 32), (16, 8)])
+def test_shiftmax_ivit(rows, cols, I0, M):
+    say(f"shiftmax ivit rows={rows} cols={cols} I0={I0} M={M}")
+    x = rng(rows * 3 + cols + I0).integers(-128, 128, (rows, cols)).astype(np.int8)
+    ref = oracle.shiftmax_ivit_rows(x, I0, M=M)
+    assert_same(host(ilw.ilw_shiftmax_ivit(dev(x), I0, M=M)), ref, "shiftmax ivit")
+
+
+def test_shiftmax_ivit_collapse():
+    """Rows whose S_sum reaches 2^31 (four equal maxima at I0 = 8192): every
+    output 0 on both sides; the constrained kernel keeps the budget."""
+    say("shiftmax ivit collapse")
+    x = np.zeros((256, 4), np.int8)
+    x[::2, 1] = -3
+    ref = oracle.shiftmax_ivit_rows(x, 8192, M=31)
+    assert np.all(ref[1::2] == 0)
+    assert_same(host(ilw.ilw_shiftmax_ivit(dev(x), 8192, M=31)), ref, "collapse")
+    got = host(ilw.ilw_shiftmax(dev(x), 8192))
+    assert np.all(got[1::2].astype(np.int64).sum(axis=1) >= 120)
+
+
+@pytest.mark.parametrize("rows,cols", [(1, 1), (333, 768), (64, 1536), (5, 4097)])
+@pytest.mark.parametrize("I0", [8, 16, 64])
+def test_shiftgelu_ivit(rows, cols, I0):
+    say(f"shiftgelu ivit rows={rows} cols={cols} I0={I0}")
+    g = rng(rows + cols + I0)
+    x = g.integers(-128, 128, (rows, cols)).astype(np.int8)
+    x[0] = np.minimum(x[0], 0)  # a row with no positive I_p
+    mult, shift = int(g.integers(2 ** 29, 2 ** 30)), int(g.integers(34, 38))
+    ref = oracle.shiftgelu_ivit_rows(x, I0, mult, shift)
+    assert_same(host(ilw.ilw_shiftgelu_ivit(dev(x), I0, mult, shift)), ref, "shiftgelu ivit")
+
+
 # ------------------------------------------------------------------ split convolution
 def _split_case(g, M, N, chans, per_channel):
     xs = [g.integers(-127, 128, (M, c)).astype(np.int8) for c in chans]
