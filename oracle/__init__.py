@@ -109,6 +109,9 @@ def lib():
                                           c_i64, c_i32, i64p]),
             "orc_split_conv": (None, [c_i32, vpp, i32p, vpp, vpp, vpp, i32p, i32p, c_i64,
                                       c_i32, i32p, i32p, c_i32, i8p]),
+            "orc_patch_embed": (None, [i8p, c_i32, c_i32, c_i32, c_i32, c_i32, i8p, i32p,
+                                       i32p, i32p, c_i32, i8p, c_i32, c_i32, c_i32, c_i32,
+                                       i8p]),
             "orc_attention": (None, [i8p] + [c_i32] * 16 + [i8p]),
             "orc_block_forward": (None, [ctypes.POINTER(OrcBlock), i8p, i8p,
                                          c_i32, c_i32, c_i32, c_i32, c_i32]),
@@ -312,6 +315,24 @@ def shiftgelu_ivit_rows(x, I0, out_mult, out_shift, k_inter=16, k_out=8):
     y = np.zeros_like(x)
     lib().orc_shiftgelu_ivit_rows(_p(x, i8p), _p(y, i8p), rows, cols, I0, k_inter, k_out,
                                   out_mult, out_shift)
+    return y
+
+
+def patch_embed(img, w, bias, mult, shift, pos, pos_ma, pos_mb, pos_shift, P=16):
+    """img int8 [B, C_in, H, W], w int8 [D, C_in*P*P] -> int8 [B, T, D]."""
+    img = _arr(img, np.int8)
+    w = _arr(w, np.int8)
+    mult, shift = _arr(mult, np.int32).reshape(-1), _arr(shift, np.int32).reshape(-1)
+    b = None if bias is None else _arr(bias, np.int32)
+    pos = _arr(pos, np.int8)
+    B, C, H, W = img.shape
+    D = w.shape[0]
+    T = (H // P) * (W // P)
+    assert w.shape[1] == C * P * P and pos.shape == (T, D)
+    y = np.zeros((B, T, D), np.int8)
+    lib().orc_patch_embed(_p(img, i8p), B, C, H, W, P, _p(w, i8p),
+                          None if b is None else _p(b, i32p), _p(mult, i32p), _p(shift, i32p),
+                          mult.shape[0], _p(pos, i8p), pos_ma, pos_mb, pos_shift, D, _p(y, i8p))
     return y
 
 

@@ -433,6 +433,40 @@ void orc_split_conv(int32_t n_branches, const int8_t* const* x,
   free(A);
 }
 
+/* Patch embedding (Table mappability: patch embedding is a convolution
+ * followed by an add; Sec. 3.2.1: convolutions follow the integer linear
+ * formulation with per-channel weight scales).  Readings: the positional
+ * embedding is an int8 table at its own scale, added to the requantized
+ * convolution output with the same two-input dyadic add as the residuals. */
+void orc_patch_embed(const int8_t* img, int32_t B, int32_t C_in, int32_t H, int32_t W,
+                     int32_t P, const int8_t* w, const int32_t* bias, const int32_t* mult,
+                     const int32_t* shift, int32_t nq, const int8_t* pos, int32_t pos_ma,
+                     int32_t pos_mb, int32_t pos_shift, int32_t D, int8_t* y) {
+  orc_require(P >= 1 && H % P == 0 && W % P == 0, "the patches tile the image");
+  orc_require(nq == 1 || nq == D, "dyadic is per-tensor or per-channel");
+  const int32_t gh = H / P, gw = W / P, T = gh * gw, K = C_in * P * P;
+  for (int32_t b = 0; b < B; b++)
+    for (int32_t py = 0; py < gh; py++)
+      for (int32_t px = 0; px < gw; px++) {
+        const int32_t t = py * gw + px;
+        for (int32_t n = 0; n < D; n++) {
+          int64_t acc = bias ? bias[n] : 0;
+          for (int32_t c = 0; c < C_in; c++)
+            for (int32_t ky = 0; ky < P; ky++)
+              for (int32_t kx = 0; kx < P; kx++) {
+                const int64_t pix =
+                    img[(((int64_t)b * C_in + c) * H + py * P + ky) * W + px * P + kx];
+                acc += pix * w[(int64_t)n * K + (c * P + ky) * P + kx];
+              }
+          orc_require(acc >= INT32_MIN && acc <= INT32_MAX, "accumulator fits int32");
+          const int32_t q = nq == 1 ? 0 : n;
+          const int32_t v = orc_requant(acc, mult[q], shift[q]);
+          y[((int64_t)b * T + t) * D + n] =
+              (int8_t)orc_residual(v, pos[(int64_t)t * D + n], pos_ma, pos_mb, pos_shift);
+        }
+      }
+}
+
 void orc_residual_tensor(const int8_t* a, const int8_t* b, int8_t* y,
                          int64_t n, int32_t mult_a, int32_t mult_b,
                          int32_t shift) {

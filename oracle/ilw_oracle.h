@@ -98,6 +98,17 @@ void orc_split_conv(int32_t n_branches, const int8_t* const* x,
                     const int32_t* out_mult, const int32_t* out_shift, int32_t out_nq,
                     int8_t* y);
 
+/* Patch embedding, the encoder's input layer (Table mappability: a
+ * convolution and an add): a P x P stride-P convolution of the int8 image
+ * [B, C_in, H, W] with weights [D, C_in * P * P] ((c, ky, kx) order), per-channel
+ * requantization to int8, then the int8 positional embedding pos [T, D]
+ * added with the two-input dyadic add.  Tokens are row-major over the
+ * (H/P) x (W/P) patch grid: y [B, T, D]. */
+void orc_patch_embed(const int8_t* img, int32_t B, int32_t C_in, int32_t H, int32_t W,
+                     int32_t P, const int8_t* w, const int32_t* bias, const int32_t* mult,
+                     const int32_t* shift, int32_t nq, const int8_t* pos, int32_t pos_ma,
+                     int32_t pos_mb, int32_t pos_shift, int32_t D, int8_t* y);
+
 /* Integer attention of one image: qkv is the int8 [T, 3*D] QKV output
  * (q | k | v, head-major inside each part), out is int8 [T, D]. */
 void orc_attention(const int8_t* qkv, int32_t grid_h, int32_t grid_w,
