@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ILW_ABI_VERSION 3
+#define ILW_ABI_VERSION 4
 
 typedef enum {
   ILW_OK = 0,
@@ -197,6 +197,26 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y,
                       void* stream);
 
 /* ------------------------------------------------------------------------
+ * Patch embedding, the encoder's input layer (Table mappability: a
+ * convolution plus an add; Sec. 3.2.1 integer linear formulation): a
+ * patch x patch stride-patch convolution of the int8 image, per-channel
+ * requantization to int8, then the int8 positional embedding added with the
+ * residual form  y = sat8(rq2(conv * pos_mult_a + pos * pos_mult_b; pos_shift)).
+ *   img  int8 [batch, channels, height, width] (per-tensor scale), 16-byte
+ *        aligned; height, width multiples of 16
+ *   w    int8 [dim, channels * patch * patch], K order (channel, ky, kx)
+ *   bias int32 [dim] or NULL; proj per-tensor or per-channel dyadic
+ *   pos  int8 [T, dim], T = (height/16) * (width/16), row-major patch grid
+ *   y    int8 [batch, T, dim]
+ * patch == 16 (the only size implemented); channels in [1, 256].
+ */
+int ilw_patch_embed(const int8_t* img, int32_t batch, int32_t channels, int32_t height,
+                    int32_t width, int32_t patch, const int8_t* w, const int32_t* bias,
+                    ilw_dyadic proj, const int8_t* pos, int32_t pos_mult_a,
+                    int32_t pos_mult_b, int32_t pos_shift, int8_t* y, int32_t dim,
+                    void* stream);
+
+/* ------------------------------------------------------------------------
  * A stack of n_blocks encoder blocks (the ViT encoder of LW-DETR, Sec. 3.1;
  * each block as ilw_block_forward), run in one call so that the LayerNorm
  * after each residual linear can be computed in that linear's epilogue
@@ -289,7 +309,7 @@ int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* ch
 /* ------------------------------------------------------------------------
  * Per-stage kernel timing (tracing; off by default).  While enabled, every
  * kernel that ilw_block_forward, ilw_encoder_forward, ilw_attention,
- * ilw_deform_attn and ilw_split_conv launch is bracketed by a pair of HIP events recorded on the
+ * ilw_deform_attn, ilw_split_conv and ilw_patch_embed launch is bracketed by a pair of HIP events recorded on the
  * caller's stream, and the launch is attributed to one of the stages below.
  * Enabling (or disabling)
  * clears the records.  ilw_profile_read waits for the last recorded event and
@@ -309,7 +329,8 @@ typedef enum {
   ILW_STAGE_DEFORM = 7,      /* deformable sampling                        */
   ILW_STAGE_BLOCK_TAIL = 8,  /* projection ... next block's QKV, one launch */
   ILW_STAGE_SPLIT_CONV = 9,  /* scale-preserving split convolution          */
-  ILW_NUM_STAGES = 10
+  ILW_STAGE_PATCH_EMBED = 10, /* patch embedding + positional embedding     */
+  ILW_NUM_STAGES = 11
 } ilw_stage;
 
 int ilw_profile_enable(int enable);

@@ -561,6 +561,47 @@ int ilw_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t
                     "ilw_shiftmax");
 }
 
+int ilw_patch_embed(const int8_t* img, int32_t batch, int32_t channels, int32_t height,
+                    int32_t width, int32_t patch, const int8_t* w, const int32_t* bias,
+                    ilw_dyadic proj, const int8_t* pos, int32_t pos_mult_a,
+                    int32_t pos_mult_b, int32_t pos_shift, int8_t* y, int32_t dim,
+                    void* stream) {
+  REQUIRE(patch == 16, ILW_E_UNSUPPORTED, "patch = %d: only 16 is implemented", patch);
+  REQUIRE(batch >= 0 && channels >= 1 && channels <= 256, ILW_E_SHAPE,
+          "batch = %d, channels = %d invalid (channels in [1, 256])", batch, channels);
+  REQUIRE(height >= 16 && width >= 16 && height % 16 == 0 && width % 16 == 0, ILW_E_SHAPE,
+          "image %dx%d must be a positive multiple of 16 in each side", height, width);
+  REQUIRE(dim >= 16 && dim % 16 == 0, ILW_E_SHAPE, "dim = %d must be a multiple of 16", dim);
+  const int64_t T = (int64_t)(height / 16) * (width / 16), M = (int64_t)batch * T;
+  REQUIRE(M < ((int64_t)1 << 31) && (int64_t)channels * height * width < ((int64_t)1 << 31),
+          ILW_E_UNSUPPORTED, "image or token count too large");
+  int e;
+  if ((e = check_dyadic(proj, dim, "proj"))) return e;
+  if ((e = check_mult(pos_mult_a, "pos_mult_a")) || (e = check_mult(pos_mult_b, "pos_mult_b")) ||
+      (e = check_shift(pos_shift, "pos_shift")))
+    return e;
+  if (batch == 0) return ok();
+  REQUIRE(img && w && pos && y, ILW_E_NULL, "img, w, pos and y must not be NULL");
+  REQUIRE(aligned16(img) && aligned16(w) && ((uintptr_t)pos & 3) == 0 &&
+              ((uintptr_t)y & 3) == 0,
+          ILW_E_PARAM, "img and w must be 16-byte aligned, pos and y 4-byte aligned");
+  GemmArgs a = gemm_args(img, w, bias, proj, y, M, dim, channels * 256);
+  a.resid = pos;
+  a.res_ma = pos_mult_a;
+  a.res_mb = pos_mult_b;
+  a.res_shift = pos_shift;
+  a.pC = channels;
+  a.pH = height;
+  a.pW = width;
+  a.pgw = width / 16;
+  a.pT = (int32_t)T;
+  hipStream_t s = (hipStream_t)stream;
+  StageTimer t(ILW_STAGE_PATCH_EMBED, s);
+  const hipError_t he = launch_gemm(EPI_PATCH, a, s);
+  t.done();
+  return hip_status(he, "ilw_patch_embed");
+}
+
 int ilw_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols, int32_t I0,
                       int32_t k_inter, int32_t k_out, int32_t M, void* stream) {
   REQUIRE(rows >= 0 && cols >= 1 && cols <= 65536, ILW_E_SHAPE,

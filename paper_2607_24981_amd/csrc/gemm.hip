@@ -47,7 +47,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   constexpr int WTN = 16 * FI, WTM = 16 * FJ;  // wave tile
   constexpr int TN = WTN * WN, TM = WTM * WM, NT = 64 * WN * WM;
   constexpr bool LN = EPI == EPI_RESID_LN;
-  constexpr bool RES = EPI == EPI_RESID || LN;
+  constexpr bool XP = EPI == EPI_PATCH;
+  constexpr bool RES = EPI == EPI_RESID || LN || XP;
   constexpr bool EARLY = PF > 1;
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
@@ -92,7 +93,15 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 #pragma unroll
   for (int i = 0; i < PX; ++i) {
     const int c = min(tid + i * NT, CX - 1);
-    xsrc[i] = X + min(m0 + (c >> 2), M - 1) * K + (c & 3) * 16;
+    const int64_t m = min(m0 + (c >> 2), M - 1);
+    if (XP) {
+      // top-left pixel of the token's patch; K offsets are added per step
+      const int32_t b = (int32_t)(m / a.pT), t = (int32_t)(m - (int64_t)b * a.pT);
+      const int32_t py = t / a.pgw, px = t - py * a.pgw;
+      xsrc[i] = X + ((int64_t)b * a.pC * a.pH + py * 16) * a.pW + px * 16;
+    } else {
+      xsrc[i] = X + m * K + (c & 3) * 16;
+    }
   }
 #pragma unroll
   for (int i = 0; i < (PW > PX ? PW : PX); ++i) kofs[i] = ((tid + i * NT) & 3) * 16;
@@ -113,7 +122,12 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      if (KTAIL) {
+      if (XP) {
+        // the chunk's 16 K values are pixels kx = 0..15 of row ky of channel c
+        const int32_t k = kb + kofs[i];
+        rx[sl][i] = *(const v4i*)(xsrc[i] + (int64_t)(k >> 8) * a.pH * a.pW +
+                                  ((k >> 4) & 15) * a.pW);
+      } else if (KTAIL) {
         const bool ok = kb + kofs[i] < K;
         rx[sl][i] = *(const v4i*)(xsrc[i] + (ok ? kb : 0));
         if (!ok) rx[sl][i] = zero;
@@ -156,6 +170,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   }
   int64_t tok[FJ];   // per token: output row (STORE/GELU/RESID) or Q/K offset (QKV)
   int64_t tokv[FJ];  // QKV: V^T offset of the token
+  int64_t rtok[FJ];  // RESID: row of the skip input (PATCH: of the positional table)
   bool tok_ok[FJ];
 #pragma unroll
   for (int j = 0; j < FJ; ++j) {
@@ -163,6 +178,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     tok_ok[j] = m < M;
     tok[j] = m * N;
     tokv[j] = 0;
+    const int64_t mc = min(m, M - 1);
+    rtok[j] = (XP ? mc % a.pT : mc) * N;
   }
 
   // Channel constants and residual words (latency mode: loaded now).
@@ -180,7 +197,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   auto load_resid = [&](int i) {
 #pragma unroll
     for (int j = 0; j < FJ; ++j)
-      rs[i][j] = *(const uint32_t*)(a.resid + min(tok[j], (M - 1) * N) + min(nch[i], N - 4));
+      rs[i][j] = *(const uint32_t*)(a.resid + rtok[j] + min(nch[i], N - 4));
   };
   if (EARLY) {
 #pragma unroll
@@ -431,6 +448,10 @@ hipError_t launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
     case EPI_GELU: ILW_LAUNCH(EPI_GELU); break;
     case EPI_RESID: ILW_LAUNCH(EPI_RESID); break;
     case EPI_QKV: ILW_LAUNCH(EPI_QKV); break;
+    case EPI_PATCH:
+      if constexpr (!KT) ILW_LAUNCH(EPI_PATCH);
+      else return hipErrorInvalidValue;  // K = 256 * channels has no tail
+      break;
     default: return hipErrorInvalidValue;
   }
 #undef ILW_LAUNCH

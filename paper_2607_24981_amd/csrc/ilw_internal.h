@@ -230,7 +230,8 @@ enum GemmEpilogue {
   EPI_GELU = 1,      // y = table[rq(acc)] (SD-ShiftGELU + its requantization)
   EPI_RESID = 2,     // y = Res(rq(acc), resid)
   EPI_QKV = 3,       // scatter rq(acc) into window-major Q, K, V^T
-  EPI_RESID_LN = 4   // EPI_RESID, and y2 = LayerNorm(y) (the tile holds whole rows)
+  EPI_RESID_LN = 4,  // EPI_RESID, and y2 = LayerNorm(y) (the tile holds whole rows)
+  EPI_PATCH = 5      // patch embedding: x gathered from an image, y = Res(rq(acc), pos)
 };
 
 // Window-major Q, K, V^T buffers used by the attention kernel:
@@ -262,6 +263,10 @@ struct GemmArgs {
   const int32_t* ln_mult;
   const int32_t* ln_shift;
   int32_t ln_nq, ln_iters;
+  // PATCH: x is an int8 image [B, pC, pH, pW] cut into 16 x 16 patches
+  // (pT per image, pgw per row of patches); resid (the positional table)
+  // is indexed by the token's position within its image
+  int32_t pC, pH, pW, pgw, pT;
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);

@@ -16,7 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -79,6 +79,8 @@ _SIGS = {
                                            c_vp, c_size, c_vp]),
     "ilw_split_conv": (ctypes.c_int, [c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, Dyadic, c_vp,
                                       c_i64, c_i32, c_vp]),
+    "ilw_patch_embed": (ctypes.c_int, [c_vp, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp,
+                                       Dyadic, c_vp, c_i32, c_i32, c_i32, c_vp, c_i32, c_vp]),
     "ilw_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "ilw_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(c_i32), c_i32]),
@@ -333,6 +335,24 @@ class Encoder:
         return out
 
 
+def ilw_patch_embed(img, w, bias, mult, shift, pos, pos_mult_a, pos_mult_b, pos_shift,
+                    patch=16, y=None):
+    """img int8 [B, C, H, W], w int8 [D, C*16*16] -> int8 [B, T, D] with the
+    positional embedding pos int8 [T, D] added."""
+    B, C, H, W = img.shape
+    D = w.shape[0]
+    T = (H // patch) * (W // patch)
+    if y is None:
+        y = torch.empty((B, T, D), dtype=torch.int8, device=img.device)
+    rc = lib().ilw_patch_embed(_dev(img, torch.int8, "img"), B, C, H, W, patch,
+                               _dev(w, torch.int8, "w"),
+                               None if bias is None else _dev(bias, torch.int32, "bias"),
+                               _dyadic(mult, shift), _dev(pos, torch.int8, "pos"), pos_mult_a,
+                               pos_mult_b, pos_shift, _dev(y, torch.int8, "y"), D, _stream())
+    _check(rc, "ilw_patch_embed")
+    return y
+
+
 def ilw_shiftmax_ivit(x, I0, M=31, k_inter=16, k_out=8, y=None):
     """I-ViT Shiftmax (fixed division precision M) of every row of int8 x."""
     cols = x.shape[-1]
@@ -398,7 +418,7 @@ def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
-          "relayout", "deform", "block_tail", "split_conv"]
+          "relayout", "deform", "block_tail", "split_conv", "patch_embed"]
 
 
 def profile_enable(on: bool = True):

@@ -259,3 +259,25 @@ def split_conv_inputs(wl: SplitConvWorkload, seed: int, batch: int | None = None
     os_ = _u(rng, 40, 44, N)
     return {"xs": xs, "ws": ws, "branch_mults": bm, "branch_shifts": bs, "bias": bias,
             "out_mult": om, "out_shift": os_, "scales": scales}
+
+
+def patch_embed_inputs(seed: int, batch: int, dim: int, height: int = 640, width: int = 640,
+                       channels: int = 3, shift_range=(40, 43)) -> dict:
+    """Patch-embedding inputs: an int8 image U[-127, 127] (a per-tensor
+    quantized RGB frame), 16x16 patch weights [dim, channels*256] with int32
+    bias and per-channel dyadic (mult U[2^29, 2^30], shift in shift_range),
+    an int8 positional table [T, dim] and its add (mults U[2^29, 2^30],
+    shift 31)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    T = (height // 16) * (width // 16)
+    return {
+        "img": _u(rng, -127, 127, (batch, channels, height, width), np.int8),
+        "w": _u(rng, -127, 127, (dim, channels * 256), np.int8),
+        "bias": _u(rng, -(1 << 15), 1 << 15, dim),
+        "mult": _u(rng, 1 << 29, 1 << 30, dim),
+        "shift": _u(rng, shift_range[0], shift_range[1], dim),
+        "pos": _u(rng, -127, 127, (T, dim), np.int8),
+        "pos_mult_a": int(_u(rng, 1 << 29, 1 << 30)),
+        "pos_mult_b": int(_u(rng, 1 << 29, 1 << 30)),
+        "pos_shift": 31,
+    }

@@ -409,6 +409,53 @@ def test_encoder_deterministic():
     assert_same(a, b, "determinism")
 
 
+# ------------------------------------------------------------------ patch embedding
+def _patch_args(d):
+    return (d["img"], d["w"], d["bias"], d["mult"], d["shift"], d["pos"], d["pos_mult_a"],
+            d["pos_mult_b"], d["pos_shift"])
+
+
+def _patch_gpu(d):
+    return host(ilw.ilw_patch_embed(dev(d["img"]), dev(d["w"]), dev(d["bias"]), dev(d["mult"]),
+                                    dev(d["shift"]), dev(d["pos"]), d["pos_mult_a"],
+                                    d["pos_mult_b"], d["pos_shift"]))
+
+
+@pytest.mark.parametrize("B,C,H,W,D", [(1, 3, 640, 640, 192), (2, 3, 48, 32, 32),
+                                       (3, 1, 64, 80, 48), (1, 3, 640, 640, 384)])
+def test_patch_embed(B, C, H, W, D):
+    say(f"patch embed B={B} C={C} {H}x{W} D={D}")
+    d = synth.patch_embed_inputs(B + C + D, B, D, H, W, C)
+    ref = oracle.patch_embed(*_patch_args(d))
+    assert np.std(ref.astype(np.float64)) > 5  # not a constant output
+    assert_same(_patch_gpu(d), ref, "patch embed")
+
+
+def test_patch_embed_b32_sampled():
+    """Batch 32 (throughput tiles): three images against the oracle."""
+    say("patch embed B=32")
+    d = synth.patch_embed_inputs(32, 32, 192)
+    got = _patch_gpu(d)
+    for b in (0, 15, 31):
+        db = dict(d, img=d["img"][b:b + 1])
+        assert_same(got[b:b + 1], oracle.patch_embed(*_patch_args(db)), f"image {b}")
+
+
+def test_encoder_from_image():
+    """Image -> patch embedding -> two encoder blocks, against the oracle chain."""
+    say("encoder from image")
+    d = synth.patch_embed_inputs(9, 2, 192, 160, 160)
+    blocks = _encoder_case(192, 3, 768, 2, 10)
+    windows = [(5, 5), (0, 0)]
+    x0 = oracle.patch_embed(*_patch_args(d))
+    ref = encoder_ref(blocks, windows, x0, 10, 10)
+    enc = ilw.Encoder(blocks, windows, 10, 10)
+    x0d = ilw.ilw_patch_embed(dev(d["img"]), dev(d["w"]), dev(d["bias"]), dev(d["mult"]),
+                              dev(d["shift"]), dev(d["pos"]), d["pos_mult_a"], d["pos_mult_b"],
+                              d["pos_shift"])
+    assert_same(host(enc.forward(x0d)), ref, "encoder from image")
+
+
 # ------------------------------------------------------------------ I-ViT baselines
 @pytest.mark.parametrize("rows,cols", [(1, 1), (7, 4), (300, 400), (64, 1600), (3, 65536)])
 @pytest.mark.parametrize("I0,M", [(8, 31), (64, 16), (8192, 31), (24, 32), (16, 8)])
