@@ -68,6 +68,39 @@ class OrcBlock(ctypes.Structure):
     ]
 
 
+def _linear_fields(stem):
+    return [("w_" + stem, i8p), ("b_" + stem, i32p), (stem + "_mult", i32p),
+            (stem + "_shift", i32p), (stem + "_nq", c_i32)]
+
+
+def _ln_fields(stem):
+    return [(stem + "_beta", i32p), (stem + "_mult", i32p), (stem + "_shift", i32p),
+            (stem + "_nq", c_i32)]
+
+
+class OrcDecoder(ctypes.Structure):
+    """Mirror of the oracle's own ``orc_decoder`` struct (ilw_oracle.h)."""
+    _fields_ = (
+        [(n, c_i32) for n in ("dim", "heads", "ffn_dim", "levels", "points", "ln_iters")]
+        + _linear_fields("qkv")
+        + [(n, c_i32) for n in ("score_mult", "score_shift", "smax_I0", "smax_k_inter",
+                                "smax_k_out", "smax_m_p", "smax_s_d", "pv_mult", "pv_shift")]
+        + _linear_fields("o")
+        + [(n, c_i32) for n in ("res1_mult_a", "res1_mult_b", "res1_shift")]
+        + _ln_fields("ln1")
+        + _linear_fields("val") + _linear_fields("off") + _linear_fields("attw")
+        + [(n, c_i32) for n in ("da_I0", "da_s_d", "da_out_mult", "da_out_shift", "da_mode")]
+        + _linear_fields("co")
+        + [(n, c_i32) for n in ("res2_mult_a", "res2_mult_b", "res2_shift")]
+        + _ln_fields("ln2")
+        + _linear_fields("fc1")
+        + [(n, c_i32) for n in ("gelu_I0", "gelu_k_inter", "gelu_k_out", "gelu_mult",
+                                "gelu_shift")]
+        + _linear_fields("fc2")
+        + [(n, c_i32) for n in ("res3_mult_a", "res3_mult_b", "res3_shift")]
+        + _ln_fields("ln3"))
+
+
 def lib():
     global _LIB
     if _LIB is None:
@@ -112,6 +145,8 @@ def lib():
             "orc_patch_embed": (None, [i8p, c_i32, c_i32, c_i32, c_i32, c_i32, i8p, i32p,
                                        i32p, i32p, c_i32, i8p, c_i32, c_i32, c_i32, c_i32,
                                        i8p]),
+            "orc_decoder_forward": (None, [ctypes.POINTER(OrcDecoder), i8p, i8p, i32p,
+                                           i32p, i32p, c_i32, c_i32, c_i32, i8p]),
             "orc_attention": (None, [i8p] + [c_i32] * 16 + [i8p]),
             "orc_block_forward": (None, [ctypes.POINTER(OrcBlock), i8p, i8p,
                                          c_i32, c_i32, c_i32, c_i32, c_i32]),
@@ -400,6 +435,42 @@ def block_forward(params: dict, x, grid_h, grid_w, win_h, win_w):
     s, keep = block_struct(params)
     lib().orc_block_forward(ctypes.byref(s), _p(x, i8p), _p(y, i8p), B, grid_h, grid_w,
                             win_h, win_w)
+    del keep
+    return y
+
+
+def decoder_struct(params: dict):
+    """Build the oracle's decoder struct from a parameter dict whose keys are
+    the struct's field names (the *_nq fields are taken from the lengths of
+    the multiplier arrays).  Returns the struct and the arrays to keep alive."""
+    keep = []
+    s = OrcDecoder()
+    for name, typ in OrcDecoder._fields_:
+        if name.endswith("_nq"):
+            setattr(s, name, int(np.asarray(params[name[:-3] + "_mult"]).shape[0]))
+        elif typ is c_i32:
+            setattr(s, name, int(params[name]))
+        else:
+            a = _arr(params[name], np.int8 if typ is i8p else np.int32)
+            keep.append(a)
+            setattr(s, name, _p(a, typ))
+    return s, keep
+
+
+def decoder_forward(params: dict, tgt, memory, ref, level_hw, level_start):
+    """tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 Q16 [B, Q, 2]
+    -> int8 [B, Q, D]."""
+    tgt = _arr(tgt, np.int8)
+    memory = _arr(memory, np.int8)
+    ref = _arr(ref, np.int32)
+    level_hw = _arr(level_hw, np.int32)
+    level_start = _arr(level_start, np.int32)
+    B, Q, D = tgt.shape
+    S = memory.shape[1]
+    y = np.zeros_like(tgt)
+    s, keep = decoder_struct(params)
+    lib().orc_decoder_forward(ctypes.byref(s), _p(tgt, i8p), _p(memory, i8p), _p(ref, i32p),
+                              _p(level_hw, i32p), _p(level_start, i32p), B, Q, S, _p(y, i8p))
     del keep
     return y
 

@@ -716,3 +716,77 @@ void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
   free(pw);
   free(acc);
 }
+
+/* Decoder layer (see the header).  Readings: post-norm sub-blocks as in the
+ * deformable decoder LW-DETR uses; the positional queries are already part
+ * of tgt; the offset linear yields int8 offsets in 1/16 pixel (a +-8 pixel
+ * range at 8 bits), widened to the sampler's Q8 by a factor 16; the sampler's
+ * Shiftmax uses k_inter = 16, k_out = 8, m_p = 4. */
+void orc_decoder_forward(const orc_decoder* p, const int8_t* tgt, const int8_t* memory,
+                         const int32_t* ref, const int32_t* level_hw,
+                         const int32_t* level_start, int32_t B, int32_t Q, int32_t S,
+                         int8_t* y) {
+  const int32_t D = p->dim, H = p->heads, F = p->ffn_dim, L = p->levels, P = p->points;
+  orc_require(D % H == 0, "dim is a multiple of heads");
+  const int32_t hd = D / H, NO = H * L * P * 2, NW = H * L * P;
+  const int64_t MQ = (int64_t)B * Q, MS = (int64_t)B * S;
+  int8_t* qkv = (int8_t*)malloc((size_t)(Q * 3 * D));
+  int8_t* att = (int8_t*)malloc((size_t)(MQ * D));
+  int8_t* tmp = (int8_t*)malloc((size_t)(MQ * (F > D ? F : D)));
+  int8_t* x = (int8_t*)malloc((size_t)(MQ * D));
+  int8_t* t1 = (int8_t*)malloc((size_t)(MQ * D));
+  int8_t* t2 = (int8_t*)malloc((size_t)(MQ * D));
+  int8_t* v = (int8_t*)malloc((size_t)(MS * D));
+  int8_t* off8 = (int8_t*)malloc((size_t)(MQ * NO));
+  int16_t* off = (int16_t*)malloc(sizeof(int16_t) * (size_t)(MQ * NO));
+  int8_t* lg = (int8_t*)malloc((size_t)(MQ * NW));
+  int8_t* smp = (int8_t*)malloc((size_t)(MQ * D));
+  int8_t* g = (int8_t*)malloc((size_t)(MQ * F));
+  orc_require(qkv && att && tmp && x && t1 && t2 && v && off8 && off && lg && smp && g,
+              "allocation");
+  /* self-attention: one global window of Q tokens per image */
+  for (int32_t b = 0; b < B; b++) {
+    orc_linear(tgt + (int64_t)b * Q * D, p->w_qkv, p->b_qkv, Q, 3 * D, D, p->qkv_mult,
+               p->qkv_shift, p->qkv_nq, qkv);
+    orc_attention(qkv, 1, Q, 0, 0, D, H, hd, p->score_mult, p->score_shift, p->smax_I0,
+                  p->smax_k_inter, p->smax_k_out, p->smax_m_p, p->smax_s_d, p->pv_mult,
+                  p->pv_shift, att + (int64_t)b * Q * D);
+  }
+  orc_linear(att, p->w_o, p->b_o, MQ, D, D, p->o_mult, p->o_shift, p->o_nq, tmp);
+  orc_residual_tensor(tmp, tgt, x, MQ * D, p->res1_mult_a, p->res1_mult_b, p->res1_shift);
+  orc_int_layernorm(x, t1, MQ, D, p->ln1_beta, p->ln1_mult, p->ln1_shift, p->ln1_nq,
+                    p->ln_iters);
+  /* cross-attention: deformable sampling of the projected encoder maps */
+  orc_linear(memory, p->w_val, p->b_val, MS, D, D, p->val_mult, p->val_shift, p->val_nq, v);
+  orc_linear(t1, p->w_off, p->b_off, MQ, NO, D, p->off_mult, p->off_shift, p->off_nq, off8);
+  for (int64_t i = 0; i < MQ * NO; i++) off[i] = (int16_t)(off8[i] * 16);
+  orc_linear(t1, p->w_attw, p->b_attw, MQ, NW, D, p->attw_mult, p->attw_shift, p->attw_nq,
+             lg);
+  orc_deform_attn(v, level_hw, level_start, L, P, ref, off, lg, smp, B, Q, H, hd, S,
+                  p->da_I0, 16, 8, 4, p->da_s_d, p->da_out_mult, p->da_out_shift,
+                  p->da_mode);
+  orc_linear(smp, p->w_co, p->b_co, MQ, D, D, p->co_mult, p->co_shift, p->co_nq, tmp);
+  orc_residual_tensor(tmp, t1, x, MQ * D, p->res2_mult_a, p->res2_mult_b, p->res2_shift);
+  orc_int_layernorm(x, t2, MQ, D, p->ln2_beta, p->ln2_mult, p->ln2_shift, p->ln2_nq,
+                    p->ln_iters);
+  /* FFN */
+  orc_linear(t2, p->w_fc1, p->b_fc1, MQ, F, D, p->fc1_mult, p->fc1_shift, p->fc1_nq, tmp);
+  orc_sdshiftgelu_tensor(tmp, g, MQ * F, p->gelu_I0, p->gelu_k_inter, p->gelu_k_out,
+                         p->gelu_mult, p->gelu_shift);
+  orc_linear(g, p->w_fc2, p->b_fc2, MQ, D, F, p->fc2_mult, p->fc2_shift, p->fc2_nq, tmp);
+  orc_residual_tensor(tmp, t2, x, MQ * D, p->res3_mult_a, p->res3_mult_b, p->res3_shift);
+  orc_int_layernorm(x, y, MQ, D, p->ln3_beta, p->ln3_mult, p->ln3_shift, p->ln3_nq,
+                    p->ln_iters);
+  free(qkv);
+  free(att);
+  free(tmp);
+  free(x);
+  free(t1);
+  free(t2);
+  free(v);
+  free(off8);
+  free(off);
+  free(lg);
+  free(smp);
+  free(g);
+}

@@ -109,6 +109,52 @@ void orc_patch_embed(const int8_t* img, int32_t B, int32_t C_in, int32_t H, int3
                      const int32_t* shift, int32_t nq, const int8_t* pos, int32_t pos_ma,
                      int32_t pos_mb, int32_t pos_shift, int32_t D, int8_t* y);
 
+/* One decoder layer (LW-DETR's deformable decoder made integer: Sec. 3.1.1
+ * nearest sampling, Sec. 3.3.2 Constrained Shiftmax, Sec. 3.3 I-LayerNorm
+ * with 20 Newton steps).  Post-norm:
+ *   t1 = LN1(Res(tgt, o(Attn(QKV(tgt)))))          self-attention, global over Q
+ *   v  = val(memory);  off = 16 * offl(t1);  w = attw(t1)
+ *   t2 = LN2(Res(t1, co(Deform(v, ref, off, w))))  cross-attention
+ *   y  = LN3(Res(t2, fc2(GELU(fc1(t2)))))          FFN
+ * All pointers are host memory.  head_dim = dim / heads. */
+typedef struct {
+  int32_t dim, heads, ffn_dim, levels, points, ln_iters;
+  const int8_t* w_qkv; const int32_t* b_qkv; const int32_t* qkv_mult;
+  const int32_t* qkv_shift; int32_t qkv_nq;
+  int32_t score_mult, score_shift, smax_I0, smax_k_inter, smax_k_out, smax_m_p,
+      smax_s_d, pv_mult, pv_shift;
+  const int8_t* w_o; const int32_t* b_o; const int32_t* o_mult;
+  const int32_t* o_shift; int32_t o_nq;
+  int32_t res1_mult_a, res1_mult_b, res1_shift;
+  const int32_t* ln1_beta; const int32_t* ln1_mult; const int32_t* ln1_shift;
+  int32_t ln1_nq;
+  const int8_t* w_val; const int32_t* b_val; const int32_t* val_mult;
+  const int32_t* val_shift; int32_t val_nq;
+  const int8_t* w_off; const int32_t* b_off; const int32_t* off_mult;
+  const int32_t* off_shift; int32_t off_nq;
+  const int8_t* w_attw; const int32_t* b_attw; const int32_t* attw_mult;
+  const int32_t* attw_shift; int32_t attw_nq;
+  int32_t da_I0, da_s_d, da_out_mult, da_out_shift, da_mode;
+  const int8_t* w_co; const int32_t* b_co; const int32_t* co_mult;
+  const int32_t* co_shift; int32_t co_nq;
+  int32_t res2_mult_a, res2_mult_b, res2_shift;
+  const int32_t* ln2_beta; const int32_t* ln2_mult; const int32_t* ln2_shift;
+  int32_t ln2_nq;
+  const int8_t* w_fc1; const int32_t* b_fc1; const int32_t* fc1_mult;
+  const int32_t* fc1_shift; int32_t fc1_nq;
+  int32_t gelu_I0, gelu_k_inter, gelu_k_out, gelu_mult, gelu_shift;
+  const int8_t* w_fc2; const int32_t* b_fc2; const int32_t* fc2_mult;
+  const int32_t* fc2_shift; int32_t fc2_nq;
+  int32_t res3_mult_a, res3_mult_b, res3_shift;
+  const int32_t* ln3_beta; const int32_t* ln3_mult; const int32_t* ln3_shift;
+  int32_t ln3_nq;
+} orc_decoder;
+
+void orc_decoder_forward(const orc_decoder* p, const int8_t* tgt, const int8_t* memory,
+                         const int32_t* ref, const int32_t* level_hw,
+                         const int32_t* level_start, int32_t B, int32_t Q, int32_t S,
+                         int8_t* y);
+
 /* Integer attention of one image: qkv is the int8 [T, 3*D] QKV output
  * (q | k | v, head-major inside each part), out is int8 [T, D]. */
 void orc_attention(const int8_t* qkv, int32_t grid_h, int32_t grid_w,

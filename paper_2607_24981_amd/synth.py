@@ -281,3 +281,100 @@ def patch_embed_inputs(seed: int, batch: int, dim: int, height: int = 640, width
         "pos_mult_b": int(_u(rng, 1 << 29, 1 << 30)),
         "pos_shift": 31,
     }
+
+
+@dataclass(frozen=True)
+class DecoderWorkload:
+    """One integer deformable decoder layer: queries of dim `dim` over the
+    stacked encoder maps of `levels`."""
+    name: str
+    batch: int
+    queries: int
+    dim: int
+    heads: int
+    ffn_dim: int
+    levels: tuple
+    points: int
+
+    def gemm_ops(self) -> int:
+        B, Q, D, H, F = self.batch, self.queries, self.dim, self.heads, self.ffn_dim
+        L, P = len(self.levels), self.points
+        S = sum(h * w for h, w in self.levels)
+        lin = 2 * B * Q * D * (3 * D + D + H * L * P * 3 + D + 2 * F) + 2 * B * S * D * D
+        attn = 4 * B * Q * Q * D
+        return lin + attn
+
+
+DECODER_WORKLOADS = {
+    "decoder_q300_d256_b8": DecoderWorkload("decoder_q300_d256_b8", 8, 300, 256, 8, 1024,
+                                            ((80, 80), (40, 40), (20, 20)), 4),
+}
+
+
+def decoder_params(rng: np.random.Generator, dim: int, heads: int, ffn_dim: int,
+                   levels: int, points: int, ln_iters: int = 20, mode: int = 0) -> dict:
+    """Parameters of one integer decoder layer, drawn in struct order (the
+    'wide' GEMM shifts so that most values stay inside int8; the offset
+    linear's shift spreads offsets over the int8 range, i.e. +-8 px at
+    1/16 px)."""
+    D, H, F, L, P = dim, heads, ffn_dim, levels, points
+    sh = SHIFTS["wide"]
+    p = {"dim": D, "heads": H, "ffn_dim": F, "levels": L, "points": P, "ln_iters": ln_iters}
+
+    def lin(stem, n, k, key="gemm"):
+        p["w_" + stem] = _u(rng, -127, 127, (n, k), np.int8)
+        p["b_" + stem] = _u(rng, -(1 << 15), 1 << 15, n)
+        p[stem + "_mult"], p[stem + "_shift"] = _dy(rng, n, sh[key])
+
+    def ln(stem):
+        p[stem + "_beta"] = _u(rng, -(1 << 26), 1 << 26, D)
+        mag = _u(rng, 1 << 29, 1 << 30, D)
+        sign = np.where(rng.integers(0, 8, size=D) == 0, -1, 1).astype(np.int32)
+        p[stem + "_mult"] = (mag * sign).astype(np.int32)
+        p[stem + "_shift"] = _u(rng, sh["ln"][0], sh["ln"][1], D)
+
+    def res(i):
+        p[f"res{i}_mult_a"] = int(_u(rng, 1 << 29, 1 << 30))
+        p[f"res{i}_mult_b"] = int(_u(rng, 1 << 29, 1 << 30))
+        p[f"res{i}_shift"] = 31
+
+    lin("qkv", 3 * D, D)
+    p["score_mult"], p["score_shift"] = (int(v[0]) for v in _dy(rng, 1, sh["score"]))
+    p["smax_I0"] = int(_u(rng, 8, 64))
+    p["smax_k_inter"], p["smax_k_out"], p["smax_m_p"], p["smax_s_d"] = 16, 8, 4, -1
+    p["pv_mult"], p["pv_shift"] = (int(v[0]) for v in _dy(rng, 1, sh["pv"]))
+    lin("o", D, D)
+    res(1)
+    ln("ln1")
+    lin("val", D, D)
+    lin("off", H * L * P * 2, D)
+    lin("attw", H * L * P, D)
+    p["da_I0"], p["da_s_d"] = 16, -1
+    p["da_out_mult"] = int(_u(rng, 1 << 29, 1 << 30))
+    p["da_out_shift"] = int(_u(rng, 33, 36))  # mode 1 adds the 16 bits of its weights itself
+    p["da_mode"] = mode
+    lin("co", D, D)
+    res(2)
+    ln("ln2")
+    lin("fc1", F, D)
+    p["gelu_I0"], p["gelu_k_inter"], p["gelu_k_out"] = int(_u(rng, 8, 64)), 16, 8
+    p["gelu_mult"], p["gelu_shift"] = (int(v[0]) for v in _dy(rng, 1, sh["gelu"]))
+    lin("fc2", D, F, "gemm_k4")
+    res(3)
+    ln("ln3")
+    return p
+
+
+def decoder_inputs(wl: DecoderWorkload, seed: int, batch: int | None = None, mode: int = 0):
+    """(params, tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 Q16
+    [B, Q, 2], level_hw [L, 2], level_start [L])."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    B = wl.batch if batch is None else batch
+    p = decoder_params(rng, wl.dim, wl.heads, wl.ffn_dim, len(wl.levels), wl.points, mode=mode)
+    hw = np.array(wl.levels, np.int32)
+    start = np.concatenate([[0], np.cumsum(hw[:, 0] * hw[:, 1])[:-1]]).astype(np.int32)
+    S = int((hw[:, 0] * hw[:, 1]).sum())
+    tgt = _u(rng, -127, 127, (B, wl.queries, wl.dim), np.int8)
+    memory = _u(rng, -127, 127, (B, S, wl.dim), np.int8)
+    ref = _u(rng, 0, 65535, (B, wl.queries, 2))
+    return p, tgt, memory, ref, hw, start
