@@ -110,6 +110,8 @@ def main():
     ap.add_argument("--from-image", action="store_true",
                     help="start each step from the int8 640x640x3 image: patch embedding and "
                          "positional embedding, then the encoder")
+    ap.add_argument("--mode", type=int, default=0,
+                    help="decoder workloads: deformable sampling 0 = nearest, 1 = bilinear-Q8")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="first make one plain device-to-device copy of this many MiB "
                          "(the known-size reference for rocprofv3 byte counters)")
@@ -144,6 +146,8 @@ def main():
 
     if args.workload in synth.SPLIT_WORKLOADS:
         return bench_split(args, synth.SPLIT_WORKLOADS[args.workload])
+    if args.workload in synth.DECODER_WORKLOADS:
+        return bench_decoder(args, synth.DECODER_WORKLOADS[args.workload])
     wl = synth.WORKLOADS[args.workload]
     B = wl.batch if args.batch is None else args.batch
     log(f"workload {wl.name}: batch {B}, {wl.tokens} tokens, dim {wl.dim}, "
@@ -399,6 +403,120 @@ def bench_split(args, wl):
                        "launch": "eager" if args.no_graph else "hip graph",
                        "gemm_ops_per_step": ops},
             "roofline": roof, "cpu_baseline": cpu, "parity": parity}
+    print(json.dumps(line), flush=True)
+    if parity not in (None, "bit-exact"):
+        sys.exit(1)
+
+
+def bench_decoder(args, wl):
+    """The integer deformable decoder layer around the deformable workload."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24981_amd import ilw, synth
+    B = wl.batch if args.batch is None else args.batch
+    log(f"workload {wl.name}: batch {B}, {wl.queries} queries, dim {wl.dim}, mode {args.mode}")
+    p, tgt, mem, ref, hw, start = synth.decoder_inputs(wl, args.seed, batch=B, mode=args.mode)
+    dd = ilw.DeviceDecoder(p)
+    tgt_d, mem_d, ref_d = ilw.to_device(tgt), ilw.to_device(mem), ilw.to_device(ref)
+    y = torch.empty_like(tgt_d)
+    S = mem.shape[1]
+    ws = torch.empty(dd.workspace_bytes(B, wl.queries, S), dtype=torch.int8, device="cuda")
+
+    def eager():
+        ilw.ilw_decoder_layer(dd, tgt_d, mem_d, ref_d, hw, start, y=y, workspace=ws)
+
+    step = eager
+    if not args.no_graph:
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            for _ in range(3):
+                eager()
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            eager()
+        step = graph.replay
+    wall_ms, ev_ms = _timed(step, args.steps, args.warmup)
+    ops = wl.gemm_ops() * B // wl.batch
+    tops = ops / (wall_ms * 1e-3) / 1e12
+    log(f"timed {args.steps} steps: {wall_ms:.4f} ms/step wall, {ev_ms:.4f} ms/step events, "
+        f"{tops:.2f} TOPS, {B / (wall_ms * 1e-3):.1f} images/s")
+    result = y.cpu().numpy()
+
+    ilw.profile_enable(True)
+    for _ in range(args.profile_steps):
+        eager()
+    torch.cuda.synchronize()
+    prof = ilw.profile_read()
+    ilw.profile_enable(False)
+    Q, D, H, F = wl.queries, wl.dim, wl.heads, wl.ffn_dim
+    L, P = len(wl.levels), wl.points
+    MQ, MS, NW = B * Q, B * S, H * L * P
+    work = {
+        "gemm_qkv": ("ops", 2 * MQ * 3 * D * D),
+        "attention": ("ops", 4 * B * Q * Q * D),
+        "decoder": ("ops", 2 * MQ * D * (2 * D + 3 * NW + 2 * F) + 2 * MS * D * D),
+        # gathered head slices, offsets (int16), logits, output
+        "deform": ("bytes", MQ * NW * (D // H) + MQ * 2 * NW * 2 + MQ * NW + MQ * D),
+        "layernorm": ("bytes", 3 * (2 * MQ * D + 12 * D)),
+    }
+    stages = {}
+    for name, (kind, amount) in work.items():
+        ms, n = prof[name]
+        if n == 0:
+            continue
+        per_step = ms / args.profile_steps
+        stages[name] = {"ms_per_step": round(per_step, 5),
+                        "launches_per_step": n // args.profile_steps,
+                        "ms_per_launch": round(ms / n, 5),
+                        ("TOPS" if kind == "ops" else "GBps"):
+                            round(amount / (per_step * 1e-3) / (1e12 if kind == "ops" else 1e9),
+                                  2)}
+    dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
+    kind, amount = work[dom]
+    achieved = amount / (stages[dom]["ms_per_step"] * 1e-3)
+    if kind == "ops":
+        roof = {"bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": PEAK_INT8_TOPS,
+                "unit": "TOPS"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(achieved / 1e9, 2), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 5)
+    roof.update({"stage": dom, "ms_per_launch": stages[dom]["ms_per_launch"],
+                 "algorithmic_per_step": amount, "traffic": None})
+    log(f"dominant stage {dom}: {json.dumps(roof)}")
+    log("stages: " + json.dumps(stages))
+
+    cpu = parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        if not os.path.exists(oracle._SO):
+            oracle.build()
+        c0 = time.perf_counter()
+        ref0 = oracle.decoder_forward(p, tgt[:1], mem[:1], ref[:1], hw, start)
+        c1 = time.perf_counter()
+        ops1 = wl.gemm_ops() // wl.batch
+        cpu = {"value": round(ops1 / (c1 - c0) / 1e12, 6), "unit": "TOPS",
+               "images_per_s": round(1 / (c1 - c0), 4), "cores": 1, "kind": "oracle",
+               "sample": f"one image (1 of {B}) of {wl.name}, mode {args.mode}: the whole "
+                         f"layer, {ops1 / 1e9:.2f} G int8 ops, {c1 - c0:.2f} s"}
+        bad = int(np.count_nonzero(result[:1] != ref0))
+        parity = "bit-exact" if bad == 0 else f"{bad} of {ref0.size} outputs differ"
+        log(f"cpu baseline {cpu['value']} TOPS; parity of image 0: {parity}")
+
+    line = {"metric": METRIC, "value": round(tops, 3), "unit": "TOPS",
+            "images_per_s": round(B / (wall_ms * 1e-3), 2), "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(wall_ms, 5), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+            "config": {"workload": wl.name, "batch": B, "queries": Q, "dim": D, "heads": H,
+                       "ffn_dim": F, "levels": [list(l) for l in wl.levels], "points": P,
+                       "sampling": "nearest" if args.mode == 0 else "bilinear-Q8",
+                       "launch": "eager" if args.no_graph else "hip graph",
+                       "gemm_ops_per_step": ops},
+            "roofline": roof, "cpu_baseline": cpu, "parity": parity, "stages": stages}
     print(json.dumps(line), flush=True)
     if parity not in (None, "bit-exact"):
         sys.exit(1)

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ILW_ABI_VERSION 4
+#define ILW_ABI_VERSION 6
 
 typedef enum {
   ILW_OK = 0,
@@ -141,9 +141,11 @@ int ilw_residual_add(const int8_t* a, const int8_t* b, int8_t* y, int64_t n,
  *       h*head_dim .. of each part.
  *   out int8 [batch, grid_h*grid_w, dim].
  * win_h == win_w == 0 selects global attention; otherwise win_h x win_w
- * windows tile the grid (LW-DETR's window attention).  head_dim == 64;
- * dim == heads * 64; tokens per window in [1, 2048].  The workspace
- * (ilw_attention_workspace_bytes) holds the window-major Q, K and V^T copies.
+ * windows tile the grid (LW-DETR's window attention).  head_dim 32 or 64
+ * (the decoder's 8 heads of 32 channels, the encoder's heads of 64);
+ * dim == heads * head_dim; tokens per window in [1, 2048].  The workspace
+ * (ilw_attention_workspace_bytes) holds the window-major Q, K and V^T copies,
+ * rows of 64 bytes per head.
  */
 typedef struct {
   int32_t score_mult, score_shift;  /* S -> int8 scores (folds 1/sqrt(d_h)) */
@@ -152,7 +154,8 @@ typedef struct {
 } ilw_attn_params;
 
 size_t ilw_attention_workspace_bytes(int32_t batch, int32_t grid_h, int32_t grid_w,
-                                     int32_t win_h, int32_t win_w, int32_t dim);
+                                     int32_t win_h, int32_t win_w, int32_t dim,
+                                     int32_t head_dim);
 int ilw_attention(const int8_t* qkv, int8_t* out, int32_t batch, int32_t grid_h,
                   int32_t grid_w, int32_t win_h, int32_t win_w, int32_t dim,
                   int32_t heads, int32_t head_dim, const ilw_attn_params* ap,
@@ -307,9 +310,56 @@ int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* ch
                    ilw_dyadic out, int8_t* y, int64_t M, int32_t N, void* stream);
 
 /* ------------------------------------------------------------------------
+ * One integer deformable decoder layer (LW-DETR's decoder made integer:
+ * Sec. 3.1.1 nearest sampling, Sec. 3.3.2 Constrained Shiftmax, Sec. 3.3
+ * I-LayerNorm with 20 Newton steps), post-norm:
+ *   t1 = LN1(Res1(tgt, o(Attn(QKV(tgt)))))        self-attention, one global
+ *                                                  window of the queries
+ *   v = val(memory); off = 16 * offl(t1) (int8 1/16 px -> Q8); w = attw(t1)
+ *   t2 = LN2(Res2(t1, co(Deform(v, ref, off, w)))) cross-attention (as
+ *                                                  ilw_deform_attn, mode 0/1)
+ *   y  = LN3(Res3(t2, fc2(GELU(fc1(t2)))))         FFN
+ *   tgt int8 [batch, queries, dim]; memory int8 [batch, value_tokens, dim],
+ *   the levels stacked as for ilw_deform_attn (level_hw, level_start: HOST
+ *   int32 [levels][2], [levels]); ref int32 Q16 [batch, queries, 2];
+ *   y int8 [batch, queries, dim] (must not alias tgt).
+ * The struct's arrays are DEVICE pointers.  head_dim = dim / heads in
+ * {32, 64}; dim, ffn_dim, heads*levels*points multiples of 16; queries in
+ * [1, 2048]; levels in [1, 8], levels*points <= 64.
+ */
+typedef struct {
+  int32_t dim, heads, ffn_dim, levels, points, ln_iters;
+  const int8_t* w_qkv; const int32_t* b_qkv; ilw_dyadic qkv;     /* [3*dim, dim] */
+  ilw_attn_params attn;
+  const int8_t* w_o; const int32_t* b_o; ilw_dyadic o;           /* [dim, dim]   */
+  int32_t res1_mult_a, res1_mult_b, res1_shift;
+  const int32_t* ln1_beta; ilw_dyadic ln1_out;
+  const int8_t* w_val; const int32_t* b_val; ilw_dyadic val;     /* [dim, dim]   */
+  const int8_t* w_off; const int32_t* b_off; ilw_dyadic off;     /* [heads*levels*points*2, dim] */
+  const int8_t* w_attw; const int32_t* b_attw; ilw_dyadic attw;  /* [heads*levels*points, dim]   */
+  int32_t da_I0, da_s_d, da_out_mult, da_out_shift, da_mode;
+  const int8_t* w_co; const int32_t* b_co; ilw_dyadic co;        /* [dim, dim]   */
+  int32_t res2_mult_a, res2_mult_b, res2_shift;
+  const int32_t* ln2_beta; ilw_dyadic ln2_out;
+  const int8_t* w_fc1; const int32_t* b_fc1; ilw_dyadic fc1;     /* [ffn, dim]   */
+  int32_t gelu_I0, gelu_k_inter, gelu_k_out, gelu_mult, gelu_shift;
+  const int8_t* w_fc2; const int32_t* b_fc2; ilw_dyadic fc2;     /* [dim, ffn]   */
+  int32_t res3_mult_a, res3_mult_b, res3_shift;
+  const int32_t* ln3_beta; ilw_dyadic ln3_out;
+} ilw_decoder_params;
+
+size_t ilw_decoder_workspace_bytes(const ilw_decoder_params* p, int32_t batch,
+                                   int32_t queries, int32_t value_tokens);
+int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8_t* memory,
+                      const int32_t* ref, const int32_t* level_hw, const int32_t* level_start,
+                      int8_t* y, int32_t batch, int32_t queries, int32_t value_tokens,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Per-stage kernel timing (tracing; off by default).  While enabled, every
  * kernel that ilw_block_forward, ilw_encoder_forward, ilw_attention,
- * ilw_deform_attn, ilw_split_conv and ilw_patch_embed launch is bracketed by a pair of HIP events recorded on the
+ * ilw_deform_attn, ilw_split_conv, ilw_patch_embed and ilw_decoder_layer
+ * launch is bracketed by a pair of HIP events recorded on the
  * caller's stream, and the launch is attributed to one of the stages below.
  * Enabling (or disabling)
  * clears the records.  ilw_profile_read waits for the last recorded event and
@@ -330,7 +380,8 @@ typedef enum {
   ILW_STAGE_BLOCK_TAIL = 8,  /* projection ... next block's QKV, one launch */
   ILW_STAGE_SPLIT_CONV = 9,  /* scale-preserving split convolution          */
   ILW_STAGE_PATCH_EMBED = 10, /* patch embedding + positional embedding     */
-  ILW_NUM_STAGES = 11
+  ILW_STAGE_DECODER = 11,    /* decoder linears, LayerNorms, offset widening */
+  ILW_NUM_STAGES = 12
 } ilw_stage;
 
 int ilw_profile_enable(int enable);

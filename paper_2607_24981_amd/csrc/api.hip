@@ -167,8 +167,9 @@ int check_attn(const ilw_attn_params* ap) {
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // Window-major Q/K/V^T buffers carved from a workspace.
-size_t qkv_bytes(int32_t batch, const Geometry& g, int32_t D, QkvLayout* L, int8_t* base) {
-  const int32_t H = D / 64;
+size_t qkv_bytes(int32_t batch, const Geometry& g, int32_t D, QkvLayout* L, int8_t* base,
+                 int32_t hd = 64) {
+  const int32_t H = D / hd;
   const size_t qk = (size_t)batch * g.nW * H * g.Tw * 64;
   const size_t vt = (size_t)batch * g.nW * H * 64 * g.Twp;
   if (L) {
@@ -185,6 +186,7 @@ size_t qkv_bytes(int32_t batch, const Geometry& g, int32_t D, QkvLayout* L, int8
     L->nW = g.nW;
     L->Tw = g.Tw;
     L->Twp = g.Twp;
+    L->hs = hd == 32 ? 5 : 6;
   }
   return 2 * align256(qk) + align256(vt);
 }
@@ -216,6 +218,7 @@ AttnArgs attn_args(const QkvLayout& L, int8_t* out, int32_t batch,
   a.s_d = ap.s_d;
   a.pv_mult = ap.pv_mult;
   a.pv_shift = ap.pv_shift;
+  a.hd = 1 << L.hs;
   return a;
 }
 
@@ -519,6 +522,95 @@ size_t encoder_workspace(const ilw_block_params* blocks, int32_t n_blocks,
   return need;
 }
 
+// ---- decoder layer -------------------------------------------------------
+struct DecoderLayout {
+  QkvLayout qkv;
+  int8_t *att, *x, *t1, *t2, *v, *off8, *lg, *smp, *g;
+  int16_t* off16;
+  size_t total;
+};
+
+size_t decoder_layout(const ilw_decoder_params* p, int32_t batch, int32_t Q, int32_t S,
+                      int8_t* base, DecoderLayout* out) {
+  Geometry g;
+  check_geometry(batch, 1, Q, 0, 0, &g);
+  const int32_t D = p->dim, NO = p->heads * p->levels * p->points * 2;
+  const size_t MQ = (size_t)batch * Q, MS = (size_t)batch * S;
+  DecoderLayout L;
+  size_t off = 0;
+  off += qkv_bytes(batch, g, D, &L.qkv, base, D / p->heads);
+  auto take = [&](size_t bytes) {
+    int8_t* ptr = base ? base + off : nullptr;
+    off += align256(bytes);
+    return ptr;
+  };
+  L.att = take(MQ * D);
+  L.x = take(MQ * D);
+  L.t1 = take(MQ * D);
+  L.t2 = take(MQ * D);
+  L.v = take(MS * D);
+  L.off8 = take(MQ * NO);
+  L.off16 = (int16_t*)take(MQ * NO * 2);
+  L.lg = take(MQ * NO / 2);
+  L.smp = take(MQ * D);
+  L.g = take(MQ * p->ffn_dim);
+  L.total = off;
+  if (out) *out = L;
+  return off;
+}
+
+int check_decoder(const ilw_decoder_params* p, int32_t batch, int32_t Q, int32_t S) {
+  REQUIRE(p, ILW_E_NULL, "decoder parameters must not be NULL");
+  REQUIRE(p->heads >= 1 && p->dim >= 16 && p->dim % p->heads == 0, ILW_E_SHAPE,
+          "dim = %d must be a multiple of heads = %d", p->dim, p->heads);
+  const int32_t hd = p->dim / p->heads;
+  REQUIRE(hd == 32 || hd == 64, ILW_E_UNSUPPORTED, "head_dim = %d: 32 and 64 are implemented",
+          hd);
+  REQUIRE(p->dim % 16 == 0 && p->ffn_dim >= 16 && p->ffn_dim % 16 == 0 &&
+              p->dim <= 16384 && p->ffn_dim <= 65536,
+          ILW_E_SHAPE, "dim = %d and ffn_dim = %d must be multiples of 16", p->dim,
+          p->ffn_dim);
+  REQUIRE(p->levels >= 1 && p->levels <= kMaxLevels && p->points >= 1 &&
+              p->levels * p->points <= 64,
+          ILW_E_SHAPE, "levels = %d, points = %d invalid", p->levels, p->points);
+  REQUIRE((p->heads * p->levels * p->points) % 16 == 0, ILW_E_SHAPE,
+          "heads*levels*points = %d must be a multiple of 16",
+          p->heads * p->levels * p->points);
+  REQUIRE(p->ln_iters >= 1 && p->ln_iters <= 64, ILW_E_PARAM,
+          "ln_iters = %d must be in [1, 64]", p->ln_iters);
+  REQUIRE(batch >= 0 && Q >= 1 && Q <= 2048 && S >= 1, ILW_E_SHAPE,
+          "batch = %d, queries = %d (in [1, 2048]), value_tokens = %d invalid", batch, Q, S);
+  REQUIRE((int64_t)batch * S < ((int64_t)1 << 31), ILW_E_UNSUPPORTED, "too many value tokens");
+  REQUIRE(p->w_qkv && p->w_o && p->w_val && p->w_off && p->w_attw && p->w_co && p->w_fc1 &&
+              p->w_fc2 && p->ln1_beta && p->ln2_beta && p->ln3_beta,
+          ILW_E_NULL, "weights and LayerNorm betas must not be NULL");
+  REQUIRE(aligned16(p->w_qkv) && aligned16(p->w_o) && aligned16(p->w_val) &&
+              aligned16(p->w_off) && aligned16(p->w_attw) && aligned16(p->w_co) &&
+              aligned16(p->w_fc1) && aligned16(p->w_fc2),
+          ILW_E_PARAM, "weights must be 16-byte aligned");
+  const int32_t D = p->dim, NW = p->heads * p->levels * p->points;
+  int e;
+  if ((e = check_dyadic(p->qkv, 3 * D, "qkv")) || (e = check_dyadic(p->o, D, "o")) ||
+      (e = check_dyadic(p->ln1_out, D, "ln1_out")) || (e = check_dyadic(p->val, D, "val")) ||
+      (e = check_dyadic(p->off, 2 * NW, "off")) || (e = check_dyadic(p->attw, NW, "attw")) ||
+      (e = check_dyadic(p->co, D, "co")) || (e = check_dyadic(p->ln2_out, D, "ln2_out")) ||
+      (e = check_dyadic(p->fc1, p->ffn_dim, "fc1")) || (e = check_dyadic(p->fc2, D, "fc2")) ||
+      (e = check_dyadic(p->ln3_out, D, "ln3_out")))
+    return e;
+  if ((e = check_attn(&p->attn))) return e;
+  if ((e = check_gelu(p->gelu_I0, p->gelu_k_inter, p->gelu_k_out, p->gelu_mult,
+                      p->gelu_shift)))
+    return e;
+  const int32_t* rm[9] = {&p->res1_mult_a, &p->res1_mult_b, &p->res2_mult_a, &p->res2_mult_b,
+                          &p->res3_mult_a, &p->res3_mult_b, &p->res1_shift, &p->res2_shift,
+                          &p->res3_shift};
+  for (int i = 0; i < 6; ++i)
+    if ((e = check_mult(*rm[i], "residual mult"))) return e;
+  for (int i = 6; i < 9; ++i)
+    if ((e = check_shift(*rm[i], "residual shift"))) return e;
+  return ILW_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -680,23 +772,25 @@ int ilw_residual_add(const int8_t* a, const int8_t* b, int8_t* y, int64_t n, int
 }
 
 size_t ilw_attention_workspace_bytes(int32_t batch, int32_t grid_h, int32_t grid_w,
-                                     int32_t win_h, int32_t win_w, int32_t dim) {
+                                     int32_t win_h, int32_t win_w, int32_t dim,
+                                     int32_t head_dim) {
   Geometry g;
   if (check_geometry(batch, grid_h, grid_w, win_h, win_w, &g)) return 0;
-  if (dim < 64 || dim % 64) {
-    fail(ILW_E_SHAPE, "dim = %d must be a positive multiple of 64", dim);
+  if ((head_dim != 32 && head_dim != 64) || dim < head_dim || dim % head_dim) {
+    fail(ILW_E_SHAPE, "dim = %d must be a positive multiple of head_dim = %d (32 or 64)", dim,
+         head_dim);
     return 0;
   }
   ok();
-  return qkv_bytes(batch, g, dim, nullptr, nullptr);
+  return qkv_bytes(batch, g, dim, nullptr, nullptr, head_dim);
 }
 
 int ilw_attention(const int8_t* qkv, int8_t* out, int32_t batch, int32_t grid_h,
                   int32_t grid_w, int32_t win_h, int32_t win_w, int32_t dim, int32_t heads,
                   int32_t head_dim, const ilw_attn_params* ap, void* workspace,
                   size_t workspace_bytes, void* stream) {
-  REQUIRE(head_dim == 64, ILW_E_UNSUPPORTED, "head_dim = %d: only 64 is implemented",
-          head_dim);
+  REQUIRE(head_dim == 32 || head_dim == 64, ILW_E_UNSUPPORTED,
+          "head_dim = %d: 32 and 64 are implemented", head_dim);
   REQUIRE(heads >= 1 && dim == heads * head_dim, ILW_E_SHAPE,
           "dim = %d must equal heads (%d) * head_dim", dim, heads);
   Geometry g;
@@ -707,12 +801,12 @@ int ilw_attention(const int8_t* qkv, int8_t* out, int32_t batch, int32_t grid_h,
   REQUIRE(qkv && out, ILW_E_NULL, "qkv and out must not be NULL");
   REQUIRE(aligned16(qkv) && aligned16(out), ILW_E_PARAM,
           "qkv and out must be 16-byte aligned");
-  const size_t need = qkv_bytes(batch, g, dim, nullptr, nullptr);
+  const size_t need = qkv_bytes(batch, g, dim, nullptr, nullptr, head_dim);
   REQUIRE(workspace && workspace_bytes >= need, ILW_E_WORKSPACE,
           "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
   REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
   QkvLayout L;
-  qkv_bytes(batch, g, dim, &L, (int8_t*)workspace);
+  qkv_bytes(batch, g, dim, &L, (int8_t*)workspace, head_dim);
   hipStream_t s = (hipStream_t)stream;
   hipError_t he;
   {
@@ -921,6 +1015,93 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t*
   hipError_t he = launch_deform(a, (hipStream_t)stream);
   t.done();
   return hip_status(he, "ilw_deform_attn");
+}
+
+size_t ilw_decoder_workspace_bytes(const ilw_decoder_params* p, int32_t batch,
+                                   int32_t queries, int32_t value_tokens) {
+  if (check_decoder(p, batch, queries, value_tokens)) return 0;
+  ok();
+  return decoder_layout(p, batch, queries, value_tokens, nullptr, nullptr);
+}
+
+int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8_t* memory,
+                      const int32_t* ref, const int32_t* level_hw, const int32_t* level_start,
+                      int8_t* y, int32_t batch, int32_t queries, int32_t value_tokens,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  int e;
+  if ((e = check_decoder(p, batch, queries, value_tokens))) return e;
+  if (batch == 0) return ok();
+  REQUIRE(tgt && memory && ref && y && level_hw && level_start, ILW_E_NULL,
+          "tgt, memory, ref, y, level_hw and level_start must not be NULL");
+  REQUIRE(aligned16(tgt) && aligned16(memory) && aligned16(y), ILW_E_PARAM,
+          "tgt, memory and y must be 16-byte aligned");
+  REQUIRE(y != tgt, ILW_E_PARAM, "y must not alias tgt");
+  const size_t need = decoder_layout(p, batch, queries, value_tokens, nullptr, nullptr);
+  REQUIRE(workspace && workspace_bytes >= need, ILW_E_WORKSPACE,
+          "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
+  DecoderLayout L;
+  decoder_layout(p, batch, queries, value_tokens, (int8_t*)workspace, &L);
+  hipStream_t s = (hipStream_t)stream;
+  const int32_t D = p->dim, H = p->heads, hd = D / H, F = p->ffn_dim;
+  const int32_t NW = H * p->levels * p->points, NO = 2 * NW;
+  const int64_t MQ = (int64_t)batch * queries, MS = (int64_t)batch * value_tokens;
+  hipError_t he = hipSuccess;
+  auto run = [&](int stage, auto&& launch) {
+    if (he != hipSuccess) return;
+    StageTimer t(stage, s);
+    he = launch();
+    t.done();
+  };
+  auto ln = [&](const int8_t* in, int8_t* out, const int32_t* beta, const ilw_dyadic& d) {
+    run(ILW_STAGE_LAYERNORM, [&] {
+      return launch_layernorm(in, out, MQ, D, beta, d.mult, d.shift, d.n, p->ln_iters, s);
+    });
+  };
+  auto resid = [&](GemmArgs a, const int8_t* skip, int32_t ma, int32_t mb, int32_t sh) {
+    a.resid = skip;
+    a.res_ma = ma;
+    a.res_mb = mb;
+    a.res_shift = sh;
+    run(ILW_STAGE_DECODER, [&] { return launch_gemm(EPI_RESID, a, s); });
+  };
+  auto plain = [&](const GemmArgs& a) {
+    run(ILW_STAGE_DECODER, [&] { return launch_gemm(EPI_STORE, a, s); });
+  };
+
+  // self-attention over the queries (one global window per image)
+  GemmArgs a = gemm_args(tgt, p->w_qkv, p->b_qkv, p->qkv, nullptr, MQ, 3 * D, D);
+  a.qkv = L.qkv;
+  run(ILW_STAGE_GEMM_QKV, [&] { return launch_gemm(EPI_QKV, a, s); });
+  run(ILW_STAGE_ATTENTION, [&] { return launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s); });
+  resid(gemm_args(L.att, p->w_o, p->b_o, p->o, L.x, MQ, D, D), tgt, p->res1_mult_a,
+        p->res1_mult_b, p->res1_shift);
+  ln(L.x, L.t1, p->ln1_beta, p->ln1_out);
+  // cross-attention: value projection, offsets (int8 1/16 px -> Q8), weights
+  plain(gemm_args(memory, p->w_val, p->b_val, p->val, L.v, MS, D, D));
+  plain(gemm_args(L.t1, p->w_off, p->b_off, p->off, L.off8, MQ, NO, D));
+  run(ILW_STAGE_DECODER, [&] { return launch_widen(L.off8, L.off16, MQ * NO, 4, s); });
+  plain(gemm_args(L.t1, p->w_attw, p->b_attw, p->attw, L.lg, MQ, NW, D));
+  if (he != hipSuccess) return hip_status(he, "ilw_decoder_layer");
+  if ((e = ilw_deform_attn(L.v, level_hw, level_start, p->levels, p->points, ref, L.off16,
+                           L.lg, L.smp, batch, queries, H, hd, p->da_I0, p->da_s_d,
+                           p->da_out_mult, p->da_out_shift, p->da_mode, stream)))
+    return e;
+  resid(gemm_args(L.smp, p->w_co, p->b_co, p->co, L.x, MQ, D, D), L.t1, p->res2_mult_a,
+        p->res2_mult_b, p->res2_shift);
+  ln(L.x, L.t2, p->ln2_beta, p->ln2_out);
+  // FFN
+  a = gemm_args(L.t2, p->w_fc1, p->b_fc1, p->fc1, L.g, MQ, F, D);
+  a.g_I0 = p->gelu_I0;
+  a.g_kinter = p->gelu_k_inter;
+  a.g_kout = p->gelu_k_out;
+  a.g_mult = p->gelu_mult;
+  a.g_shift = p->gelu_shift;
+  run(ILW_STAGE_DECODER, [&] { return launch_gemm(EPI_GELU, a, s); });
+  resid(gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, L.x, MQ, D, F), L.t2, p->res3_mult_a,
+        p->res3_mult_b, p->res3_shift);
+  ln(L.x, y, p->ln3_beta, p->ln3_out);
+  return hip_status(he, "ilw_decoder_layer");
 }
 
 int ilw_profile_enable(int enable) {

@@ -82,11 +82,15 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 
   // Query fragments (MFMA B operand: columns = query rows).  Rows past the
   // window are clamped to a valid row; their results are never stored.
+  // Past the head dimension (32-dim heads) the query fragment is zero, so
+  // the unused key bytes there contribute nothing.
+  const v4i zero4 = {0, 0, 0, 0};
   v4i qf[NF];
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int32_t r = min(i0 + f * 16 + (lane & 15), Tw - 1);
     qf[f] = *(const v4i*)(Q + (int64_t)r * 64 + (lane >> 4) * 16);
+    if ((lane >> 4) * 16 >= a.hd) qf[f] = zero4;
   }
 
   // ---- phase 1: scores.  Waves split the keys in blocks of 16; the key
@@ -263,6 +267,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   const int32_t b_img = bw / a.nW, w = bw % a.nW;
   const int32_t wy = w / a.nwx, wx = w % a.nwx;
   const int32_t c = c0 + (lane >> 4) * 4;
+  if (c0 >= a.hd) return;  // channel group past the head dimension
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int32_t i = i0 + f * 16 + (lane & 15);
@@ -272,7 +277,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       packed |= (uint32_t)(rq(o[f][r], a.pv_mult, a.pv_shift) & 0xff) << (8 * r);
-    *(uint32_t*)(a.out + ((int64_t)b_img * a.T + t) * a.D + h * 64 + c) = packed;
+    *(uint32_t*)(a.out + ((int64_t)b_img * a.T + t) * a.D + h * a.hd + c) = packed;
   }
 }
 
@@ -290,7 +295,7 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(const int8_t* qkv, in
   const int32_t w = (ty / L.win_h) * L.nwx + tx / L.win_w;
   const int32_t li = (ty % L.win_h) * L.win_w + tx % L.win_w;
   const int32_t part = n / L.D, rem_n = n % L.D;
-  const int32_t h = rem_n >> 6, c = rem_n & 63;
+  const int32_t h = rem_n >> L.hs, c = rem_n & ((1 << L.hs) - 1);
   const int64_t slice = ((int64_t)b * L.nW + w) * L.H + h;
   const v4i v = *(const v4i*)(qkv + m * 3 * L.D + n);
   if (part < 2) {

@@ -322,7 +322,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     if (EPI == EPI_QKV) {
       const QkvLayout& Lq = a.qkv;
       const int32_t part = n / Lq.D, rem_n = n - part * Lq.D;
-      const int32_t h = rem_n >> 6, c = rem_n & 63;
+      const int32_t h = rem_n >> Lq.hs, c = rem_n & ((1 << Lq.hs) - 1);
       is_v = part == 2;
       qk_base = part == 0 ? Lq.q : Lq.k;
       ch_qk = (int64_t)h * Lq.Tw * 64 + c;

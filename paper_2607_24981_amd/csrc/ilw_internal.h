@@ -236,11 +236,14 @@ enum GemmEpilogue {
 
 // Window-major Q, K, V^T buffers used by the attention kernel:
 //   Q, K [B, nW, H, Tw, 64],  V^T [B, nW, H, 64, Twp]  (Twp = Tw rounded to 64)
+// Window-major Q, K [B, nW, H, Tw, 64] and V^T [B, nW, H, 64, Twp]: rows of
+// 64 bytes per head whatever the head dimension (2^hs, 32 or 64); the bytes
+// past the head dimension are never written and never used.
 struct QkvLayout {
   int8_t* q;
   int8_t* k;
   int8_t* vt;
-  int32_t T, D, H, grid_w, win_h, win_w, nwx, nW, Tw, Twp;
+  int32_t T, D, H, grid_w, win_h, win_w, nwx, nW, Tw, Twp, hs;
 };
 
 struct GemmArgs {
@@ -330,6 +333,7 @@ struct AttnArgs {
   int8_t* out;       // [B, T, D] token-major
   int32_t B, T, D, H, grid_w, win_h, win_w, nwx, nW, Tw, Twp;
   int32_t score_mult, score_shift, I0, k_inter, k_out, m_p, s_d, pv_mult, pv_shift;
+  int32_t hd;        // head dimension: 32 or 64
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,
@@ -339,6 +343,7 @@ hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                             const int32_t* beta, const int32_t* mult,
                             const int32_t* shift, int32_t nq, int32_t iters,
                             hipStream_t s);
+hipError_t launch_widen(const int8_t* x, int16_t* y, int64_t n, int32_t shift, hipStream_t s);
 hipError_t launch_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
                                int32_t I0, int32_t k_inter, int32_t k_out, int32_t M,
                                hipStream_t s);

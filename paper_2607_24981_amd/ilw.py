@@ -16,7 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 4
+ABI_VERSION = 6
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -53,6 +53,29 @@ class BlockParams(ctypes.Structure):
     ]
 
 
+def _lin(stem):
+    return [("w_" + stem, c_vp), ("b_" + stem, c_vp), (stem, Dyadic)]
+
+
+class DecoderParams(ctypes.Structure):
+    _fields_ = (
+        [(n, c_i32) for n in ("dim", "heads", "ffn_dim", "levels", "points", "ln_iters")]
+        + _lin("qkv") + [("attn", AttnParams)] + _lin("o")
+        + [(n, c_i32) for n in ("res1_mult_a", "res1_mult_b", "res1_shift")]
+        + [("ln1_beta", c_vp), ("ln1_out", Dyadic)]
+        + _lin("val") + _lin("off") + _lin("attw")
+        + [(n, c_i32) for n in ("da_I0", "da_s_d", "da_out_mult", "da_out_shift", "da_mode")]
+        + _lin("co")
+        + [(n, c_i32) for n in ("res2_mult_a", "res2_mult_b", "res2_shift")]
+        + [("ln2_beta", c_vp), ("ln2_out", Dyadic)]
+        + _lin("fc1")
+        + [(n, c_i32) for n in ("gelu_I0", "gelu_k_inter", "gelu_k_out", "gelu_mult",
+                                "gelu_shift")]
+        + _lin("fc2")
+        + [(n, c_i32) for n in ("res3_mult_a", "res3_mult_b", "res3_shift")]
+        + [("ln3_beta", c_vp), ("ln3_out", Dyadic)])
+
+
 _SIGS = {
     "ilw_last_error": (ctypes.c_char_p, []),
     "ilw_abi_version": (ctypes.c_int, []),
@@ -68,7 +91,7 @@ _SIGS = {
     "ilw_int_layernorm": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_vp, Dyadic, c_i32,
                                          c_vp]),
     "ilw_residual_add": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_vp]),
-    "ilw_attention_workspace_bytes": (c_size, [c_i32] * 6),
+    "ilw_attention_workspace_bytes": (c_size, [c_i32] * 7),
     "ilw_attention": (ctypes.c_int, [c_vp, c_vp] + [c_i32] * 8 +
                       [ctypes.POINTER(AttnParams), c_vp, c_size, c_vp]),
     "ilw_block_workspace_bytes": (c_size, [ctypes.POINTER(BlockParams)] + [c_i32] * 5),
@@ -81,6 +104,10 @@ _SIGS = {
                                       c_i64, c_i32, c_vp]),
     "ilw_patch_embed": (ctypes.c_int, [c_vp, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp,
                                        Dyadic, c_vp, c_i32, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ilw_decoder_workspace_bytes": (c_size, [ctypes.POINTER(DecoderParams), c_i32, c_i32,
+                                             c_i32]),
+    "ilw_decoder_layer": (ctypes.c_int, [ctypes.POINTER(DecoderParams), c_vp, c_vp, c_vp, c_vp,
+                                         c_vp, c_vp, c_i32, c_i32, c_i32, c_vp, c_size, c_vp]),
     "ilw_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "ilw_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(c_i32), c_i32]),
@@ -208,7 +235,7 @@ def ilw_attention(qkv, grid_h, grid_w, win_h, win_w, heads, params: dict, out=No
     D = D3 // 3
     if out is None:
         out = torch.empty((B, T, D), dtype=torch.int8, device=qkv.device)
-    need = lib().ilw_attention_workspace_bytes(B, grid_h, grid_w, win_h, win_w, D)
+    need = lib().ilw_attention_workspace_bytes(B, grid_h, grid_w, win_h, win_w, D, D // heads)
     if need == 0 and B > 0:
         raise IlwError(f"ilw_attention_workspace_bytes: {last_error()}")
     if workspace is None:
@@ -376,6 +403,64 @@ def ilw_shiftgelu_ivit(x, I0, out_mult, out_shift, k_inter=16, k_out=8, y=None):
     return y
 
 
+class DeviceDecoder:
+    """Device copy of one decoder layer's parameters plus its ABI struct.
+    `p` is the parameter dict of the oracle's decoder (same keys)."""
+
+    def __init__(self, p: dict, device="cuda"):
+        self.p = p
+        self.t = {}
+        for k, v in p.items():
+            if isinstance(v, np.ndarray):
+                self.t[k] = to_device(v, device)
+        s = DecoderParams()
+        for n in ("dim", "heads", "ffn_dim", "levels", "points", "ln_iters", "da_I0", "da_s_d",
+                  "da_out_mult", "da_out_shift", "da_mode", "gelu_I0", "gelu_k_inter",
+                  "gelu_k_out", "gelu_mult", "gelu_shift", "res1_mult_a", "res1_mult_b",
+                  "res1_shift", "res2_mult_a", "res2_mult_b", "res2_shift", "res3_mult_a",
+                  "res3_mult_b", "res3_shift"):
+            setattr(s, n, int(p[n]))
+        for stem in ("qkv", "o", "val", "off", "attw", "co", "fc1", "fc2"):
+            setattr(s, "w_" + stem, self.t["w_" + stem].data_ptr())
+            setattr(s, "b_" + stem, self.t["b_" + stem].data_ptr())
+            setattr(s, stem, _dyadic(self.t[stem + "_mult"], self.t[stem + "_shift"]))
+        for stem in ("ln1", "ln2", "ln3"):
+            setattr(s, stem + "_beta", self.t[stem + "_beta"].data_ptr())
+            setattr(s, stem + "_out", _dyadic(self.t[stem + "_mult"], self.t[stem + "_shift"]))
+        s.attn = attn_params(p)
+        self.struct = s
+
+    def workspace_bytes(self, B, Q, S) -> int:
+        n = lib().ilw_decoder_workspace_bytes(ctypes.byref(self.struct), B, Q, S)
+        if n == 0 and B > 0:
+            raise IlwError(f"ilw_decoder_workspace_bytes: {last_error()}")
+        return n
+
+
+def ilw_decoder_layer(dec: DeviceDecoder, tgt, memory, ref, level_hw, level_start, y=None,
+                      workspace=None):
+    """tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 [B, Q, 2];
+    level_hw / level_start host arrays -> int8 [B, Q, D]."""
+    B, Q, D = tgt.shape
+    S = memory.shape[1]
+    L = dec.p["levels"]
+    hw = np.ascontiguousarray(np.asarray(level_hw, np.int32).reshape(L, 2))
+    st = np.ascontiguousarray(np.asarray(level_start, np.int32).reshape(L))
+    if y is None:
+        y = torch.empty_like(tgt)
+    if workspace is None:
+        workspace = torch.empty(max(dec.workspace_bytes(B, Q, S), 16), dtype=torch.int8,
+                                device=tgt.device)
+    rc = lib().ilw_decoder_layer(ctypes.byref(dec.struct), _dev(tgt, torch.int8, "tgt"),
+                                 _dev(memory, torch.int8, "memory"),
+                                 _dev(ref, torch.int32, "ref"), hw.ctypes.data_as(c_vp),
+                                 st.ctypes.data_as(c_vp), _dev(y, torch.int8, "y"), B, Q, S,
+                                 _dev(workspace, torch.int8, "workspace"), workspace.numel(),
+                                 _stream())
+    _check(rc, "ilw_decoder_layer")
+    return y
+
+
 def ilw_split_conv(xs, ws, branch_mults, branch_shifts, bias, out_mult, out_shift, y=None):
     """Scale-preserving split convolution: xs[b] int8 [M, C_b], ws[b] int8
     [N, C_b], per-branch rescale dyadics, bias int32 [N] or None, output
@@ -418,7 +503,7 @@ def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
-          "relayout", "deform", "block_tail", "split_conv", "patch_embed"]
+          "relayout", "deform", "block_tail", "split_conv", "patch_embed", "decoder"]
 
 
 def profile_enable(on: bool = True):

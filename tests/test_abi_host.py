@@ -185,9 +185,11 @@ def test_encoder_workspace_and_validation():
 def test_attention_and_deform_validation():
     L = ilw.lib()
     ap = ilw.AttnParams(1 << 30, 36, 16, 16, 8, 4, -1, 1 << 30, 36)
-    ws = L.ilw_attention_workspace_bytes(1, 16, 16, 0, 0, 192)
+    ws = L.ilw_attention_workspace_bytes(1, 16, 16, 0, 0, 192, 64)
+    assert L.ilw_attention_workspace_bytes(1, 16, 16, 0, 0, 192, 32) == 2 * ws
+    assert L.ilw_attention_workspace_bytes(1, 16, 16, 0, 0, 192, 48) == 0
     assert ws >= 3 * 256 * 192
-    assert L.ilw_attention(FAKE, FAKE, 1, 16, 16, 0, 0, 192, 3, 32, ctypes.byref(ap), FAKE,
+    assert L.ilw_attention(FAKE, FAKE, 1, 16, 16, 0, 0, 192, 12, 16, ctypes.byref(ap), FAKE,
                            ws, None) == E_UNSUP
     assert L.ilw_attention(FAKE, FAKE, 1, 16, 16, 0, 0, 192, 3, 64, ctypes.byref(ap), FAKE,
                            ws - 1, None) == E_WS

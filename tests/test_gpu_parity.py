@@ -239,6 +239,26 @@ def test_attention(case, s_d):
     assert_same(got, ref, "attention")
 
 
+@pytest.mark.parametrize("case", [(1, 1, 300, 0, 0, 8), (2, 6, 10, 3, 5, 4),
+                                  (1, 15, 20, 0, 0, 2), (3, 1, 37, 0, 0, 1),
+                                  (1, 40, 40, 0, 0, 2)])
+def test_attention_head_dim_32(case):
+    """32-channel heads (the decoder's self-attention: 300 queries, 8 heads)."""
+    B, gh, gw, wh, ww, H = case
+    say(f"attention hd32 B={B} grid={gh}x{gw} win={wh}x{ww} heads={H}")
+    g = rng(gh * 31 + gw + H)
+    D, T = 32 * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    p = {"score_mult": int(g.integers(2 ** 29, 2 ** 30)), "score_shift": 38,
+         "smax_I0": int(g.integers(8, 65)), "smax_s_d": -1,
+         "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 35}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, wh, ww, H, 32, p["score_mult"],
+                                     p["score_shift"], p["smax_I0"], p["pv_mult"],
+                                     p["pv_shift"]) for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
+    assert_same(got, ref, "attention hd32")
+
+
 # ------------------------------------------------------------------ encoder block
 @pytest.mark.parametrize("variant", ["wide", "baseline"])
 def test_block_c1(variant):
@@ -407,6 +427,34 @@ def test_encoder_deterministic():
     a = host(enc.forward(dev(x)))
     b = host(enc.forward(dev(x)))
     assert_same(a, b, "determinism")
+
+
+# ------------------------------------------------------------------ decoder layer
+def _decoder_gpu(p, tgt, mem, ref, hw, start):
+    dd = ilw.DeviceDecoder(p)
+    return host(ilw.ilw_decoder_layer(dd, dev(tgt), dev(mem), dev(ref), hw, start))
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("shape", [(2, 37, 64, 2, 128, ((9, 13), (4, 6)), 4),
+                                   (1, 100, 256, 8, 1024, ((20, 20), (10, 10)), 4),
+                                   (3, 16, 128, 2, 256, ((8, 8),), 8)])
+def test_decoder_layer_shapes(mode, shape):
+    B, Q, D, H, F, levels, P = shape
+    say(f"decoder B={B} Q={Q} D={D} H={H} F={F} levels={levels} P={P} mode={mode}")
+    wl = synth.DecoderWorkload("t", B, Q, D, H, F, levels, P)
+    args = synth.decoder_inputs(wl, Q + D + mode, mode=mode)
+    assert_same(_decoder_gpu(*args), oracle.decoder_forward(*args), "decoder")
+
+
+@pytest.mark.parametrize("mode,B", [(0, 8), (1, 2)])
+def test_decoder_layer_c5(mode, B):
+    """The decoder layer around the deformable workload: 300 queries, dim 256,
+    8 heads of 32, levels 80^2/40^2/20^2, 4 points; every output compared."""
+    wl = synth.DECODER_WORKLOADS["decoder_q300_d256_b8"]
+    say(f"{wl.name} mode={mode} B={B}")
+    args = synth.decoder_inputs(wl, 21 + mode, batch=B, mode=mode)
+    assert_same(_decoder_gpu(*args), oracle.decoder_forward(*args), "decoder c5")
 
 
 # ------------------------------------------------------------------ patch embedding
