@@ -342,9 +342,10 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, int64_t wg
   // a lane holds at most 8 words (32 scores) of its row
   if (a.Twp <= 512) return launch_rows<R, 16, 4>(a, clampL, narrow, s);
   if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, narrow, s);
-  // Long rows (one row per 64 lanes): small grids split a 16-row block over
-  // 16 waves so that every SIMD holds several.
-  if (R == 16 && wgs * 4 <= 2048) return launch_rows<16, 64, 16>(a, clampL, narrow, s);
+  // Long rows (one row per 64 lanes): small grids spread a 32-row block
+  // over 16 waves so that every SIMD holds several (measured best of 16 or
+  // 32 rows over 4, 8 or 16 waves for 1600-token rows at batch 1).
+  if (wgs * 4 <= 2048) return launch_rows<32, 64, 16>(a, clampL, narrow, s);
   return launch_rows<R, 64, 4>(a, clampL, narrow, s);
 }
 

@@ -513,14 +513,13 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
-      return (a.K >= 768 && (a.M + 127) / 128 * 2 >= 512) ? launch_ln_tile<3, 2, 4, 4, 1>(a, s)
-                                                          : launch_ln_tile<3, 1, 4, 4, 1>(a, s);
+      return launch_ln_tile<6, 2, 2, 4, 1>(a, s);  // 192 x 128 tokens, 12 waves of 32 x 64
     }
     if (a.N == 384) {
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
-      return launch_ln_tile<6, 1, 4, 4, 1>(a, s);
+      return launch_ln_tile<12, 1, 2, 4, 1>(a, s);  // 384 x 64 tokens, 12 waves of 32 x 64
     }
     return hipErrorInvalidValue;
   }
@@ -543,7 +542,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   // Small grids: 64 x 64 workgroup tiles split over 4 waves of 32 x 32, with
   // the latency-mode pipeline.  Otherwise, from a sweep over the encoder
   // shapes on MI355X: 192-channel tiles for the deep-K linears and N = 192,
-  // and 128 x 256 tiles for the rest.
+  // and 128 x 128 tiles over 8 waves of 32 x 64 for the rest.
   if (latency_mode(mt64 * ((a.N + 63) / 64)))
     return a.K >= 6 * TK ? launch_tile<2, 2, 2, 2, 6>(epi, a, s)
                          : launch_tile<2, 2, 2, 2, 3>(epi, a, s);
@@ -552,7 +551,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 128 == 0 && a.N >= 1536) return launch_tile<2, 2, 4, 4, 1>(epi, a, s);
-  return launch_tile<2, 4, 4, 4, 1>(epi, a, s);
+  return launch_tile<4, 2, 2, 4, 1>(epi, a, s);
 }
 
 }  // namespace ilw
