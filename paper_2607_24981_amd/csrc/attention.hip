@@ -35,6 +35,25 @@ __device__ __forceinline__ int32_t rq_clamped(int32_t acc, int32_t L, int32_t mu
   return min(max((int32_t)v, kQmin), kQmax);
 }
 
+// The same requantization in FP64, offset by 256 (the result is q + 256, in
+// [129, 383]; its low byte is q's).  |acc| <= 64 * 128 * 128 = 2^20 for a
+// 64-channel head, so for |acc * m / 2^s| < 2^9 the product acc * m is an
+// integer below 2^(s+9) and acc * m / 2^s + 256.5 is a multiple of 2^-s
+// below 2^10: exact in one FMA when s <= 43.  Past that range the rounded
+// value stays on the saturated side of 129 or 384 (rounding is monotone and
+// both bounds are representable), and truncation is the floor because the
+// unsaturated values are positive.  The host checks s <= 43 and that the
+// value cannot overflow the integer conversion.
+__device__ __forceinline__ int32_t rq_f64(int32_t acc, double scale) {
+  const double y = __builtin_fma((double)acc, scale, 256.5);
+  return min(max((int32_t)y, 256 + kQmin), 256 + kQmax);
+}
+
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
+
 // Bytes 0 of a, b, c, d packed into one word (a in the low byte).
 __device__ __forceinline__ uint32_t pack_bytes(int32_t a, int32_t b, int32_t c, int32_t d) {
   const uint32_t lo = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0400u);
@@ -56,7 +75,7 @@ __device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
 // NW waves per workgroup (4, 8 or 16): keys are split over all waves for the
 // scores, rows for the Shiftmax (R / NW rows per wave), and (channel group,
 // key range) pairs for P V, whose int32 partial sums are added through LDS.
-template <int R, int LPR, bool NARROW, bool RAGGED, int NW>
+template <int R, int LPR, bool NARROW, bool RAGGED, int NW, int JW>
 __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t lds_row,
                                                             int32_t clampL) {
   extern __shared__ __attribute__((aligned(16))) int8_t sS[];  // [R][lds_row]
@@ -95,57 +114,69 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 
   // ---- phase 1: scores.  Waves split the keys in blocks of 16; the key
   // fragment is the A operand, so a lane holds 4 consecutive keys of one row.
+  // The FP64 requantization (when the host found it exact) yields scores
+  // offset by 256; the maxima are corrected at the end.
   const v4i zero = {0, 0, 0, 0};
   const int32_t sm = a.score_mult, ss = a.score_shift;
   const int64_t srnd = (int64_t)1 << (ss - 1);
+  const double sscale = __builtin_ldexp((double)sm, -ss);
+  const int32_t moff = a.f64rq ? 256 : 0;
   int32_t mx[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) mx[f] = -128;
+  for (int f = 0; f < NF; ++f) mx[f] = -128 + moff;
   const int32_t nkb = (Tw + 15) >> 4;
   const int32_t kc = (lane >> 4) * 4;  // first of this lane's 4 keys in a block
   auto kload = [&](int32_t kb) {
     const int32_t key = min(kb * 16 + (lane & 15), Tw - 1);
     return *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
   };
-  auto scores = [&](int32_t kb, const v4i& kf) {
-    const int32_t col = kb * 16 + kc;
+  auto phase1 = [&](auto f64) {
+    auto scores = [&](int32_t kb, const v4i& kf) {
+      const int32_t col = kb * 16 + kc;
 #pragma unroll
-    for (int f = 0; f < NF; ++f) {
-      const v4i s = __builtin_amdgcn_mfma_i32_16x16x64_i8(kf, qf[f], zero, 0, 0, 0);
-      int32_t v[4];
+      for (int f = 0; f < NF; ++f) {
+        const v4i s = __builtin_amdgcn_mfma_i32_16x16x64_i8(kf, qf[f], zero, 0, 0, 0);
+        int32_t v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = rq_clamped(s[r], clampL, sm, srnd, ss);
-      // keys past the window repeat the last key (clamped rows), so they
-      // never raise the maximum
-      mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
-      *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + col) =
-          pack_bytes(v[0], v[1], v[2], v[3]);
+        for (int r = 0; r < 4; ++r)
+          v[r] = decltype(f64)::value ? rq_f64(s[r], sscale)
+                                      : rq_clamped(s[r], clampL, sm, srnd, ss);
+        // keys past the window repeat the last key (clamped rows), so they
+        // never raise the maximum
+        mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
+        *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + col) =
+            pack_bytes(v[0], v[1], v[2], v[3]);
+      }
+    };
+    // A ring of four key fragments in flight: the load of block kb + 4 NW is
+    // issued right after block kb has been consumed.  Loads past the last
+    // block re-read the clamped last key and are never used.
+    v4i k0 = kload(wave), k1 = kload(wave + NW), k2 = kload(wave + 2 * NW),
+        k3 = kload(wave + 3 * NW);
+    for (int32_t kb = wave; kb < nkb; kb += 4 * NW) {
+      scores(kb, k0);
+      k0 = kload(kb + 4 * NW);
+      if (kb + NW >= nkb) break;
+      scores(kb + NW, k1);
+      k1 = kload(kb + 5 * NW);
+      if (kb + 2 * NW >= nkb) break;
+      scores(kb + 2 * NW, k2);
+      k2 = kload(kb + 6 * NW);
+      if (kb + 3 * NW >= nkb) break;
+      scores(kb + 3 * NW, k3);
+      k3 = kload(kb + 7 * NW);
     }
   };
-  // A ring of four key fragments in flight: the load of block kb + 4 NW is
-  // issued right after block kb has been consumed.  Loads past the last
-  // block re-read the clamped last key and are never used.
-  v4i k0 = kload(wave), k1 = kload(wave + NW), k2 = kload(wave + 2 * NW),
-      k3 = kload(wave + 3 * NW);
-  for (int32_t kb = wave; kb < nkb; kb += 4 * NW) {
-    scores(kb, k0);
-    k0 = kload(kb + 4 * NW);
-    if (kb + NW >= nkb) break;
-    scores(kb + NW, k1);
-    k1 = kload(kb + 5 * NW);
-    if (kb + 2 * NW >= nkb) break;
-    scores(kb + 2 * NW, k2);
-    k2 = kload(kb + 6 * NW);
-    if (kb + 3 * NW >= nkb) break;
-    scores(kb + 3 * NW, k3);
-    k3 = kload(kb + 7 * NW);
-  }
+  if (a.f64rq)
+    phase1(Flag<true>{});
+  else
+    phase1(Flag<false>{});
   // row maxima: combine the 4 lanes sharing a row, then the waves
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     mx[f] = max(mx[f], __shfl_xor(mx[f], 16, 64));
     mx[f] = max(mx[f], __shfl_xor(mx[f], 32, 64));
-    if (lane < 16) pmax[wave][f * 16 + lane] = mx[f];
+    if (lane < 16) pmax[wave][f * 16 + lane] = mx[f] - moff;
   }
   __syncthreads();
 
@@ -154,7 +185,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   // registers between the sum and the normalization.
   {
     constexpr int RG = 64 / LPR;   // rows processed together by one wave
-    constexpr int JW = 8;          // words per lane (Twp / 4 <= 8 * LPR)
+    // JW words per lane: Twp / 4 <= JW * LPR
     const int sub = lane / LPR, k = lane % LPR;
     const int32_t nword = Twp >> 2;
     const int32_t pcap = (1 << (a.k_out - 1)) - 1;
@@ -308,11 +339,11 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(const int8_t* qkv, in
   }
 }
 
-template <int R, int LPR, bool NARROW, bool RAGGED, int NW>
+template <int R, int LPR, bool NARROW, bool RAGGED, int NW, int JW>
 hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   const int32_t lds_row = a.Twp + 16;
   const size_t smem = (size_t)R * lds_row;
-  auto kern = attention_kernel<R, LPR, NARROW, RAGGED, NW>;
+  auto kern = attention_kernel<R, LPR, NARROW, RAGGED, NW, JW>;
   static size_t configured = 0;
   if (smem > 65536 && smem > configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -325,27 +356,35 @@ hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int R, int LPR, int NW>
+template <int R, int LPR, int NW, int JW = 8>
 hipError_t launch_rows(const AttnArgs& a, int32_t clampL, bool narrow, hipStream_t s) {
   const bool ragged = (a.Tw & 3) != 0;
   if (narrow) {
-    return ragged ? launch_variant<R, LPR, true, true, NW>(a, clampL, s)
-                  : launch_variant<R, LPR, true, false, NW>(a, clampL, s);
+    return ragged ? launch_variant<R, LPR, true, true, NW, JW>(a, clampL, s)
+                  : launch_variant<R, LPR, true, false, NW, JW>(a, clampL, s);
   }
-  return ragged ? launch_variant<R, LPR, false, true, NW>(a, clampL, s)
-                : launch_variant<R, LPR, false, false, NW>(a, clampL, s);
+  return ragged ? launch_variant<R, LPR, false, true, NW, JW>(a, clampL, s)
+                : launch_variant<R, LPR, false, false, NW, JW>(a, clampL, s);
 }
 
 template <int R>
 hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, int64_t wgs,
                       hipStream_t s) {
-  // a lane holds at most 8 words (32 scores) of its row
-  if (a.Twp <= 512) return launch_rows<R, 16, 4>(a, clampL, narrow, s);
+  // Rows per wave: a lane holds JW words (4 JW scores) of its row, and the
+  // LPR lanes of a row combine their sums in log2(LPR) shuffle steps.  With
+  // 32-row blocks each wave normalizes 8 rows; doing them 8 (windows) or 2
+  // (long rows) at a time overlaps the rows' serial sum-shuffle-divide
+  // chains (measured against one row group of 16 or 64 lanes).
+  if (a.Twp <= 512) {
+    if constexpr (R == 32) return launch_rows<32, 8, 4, 16>(a, clampL, narrow, s);
+    return launch_rows<R, 16, 4>(a, clampL, narrow, s);
+  }
   if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, narrow, s);
-  // Long rows (one row per 64 lanes): small grids spread a 32-row block
-  // over 16 waves so that every SIMD holds several (measured best of 16 or
-  // 32 rows over 4, 8 or 16 waves for 1600-token rows at batch 1).
+  // Long rows: small grids spread a 32-row block over 16 waves so that every
+  // SIMD holds several (measured best of 16 or 32 rows over 4, 8 or 16 waves
+  // for 1600-token rows at batch 1).
   if (wgs * 4 <= 2048) return launch_rows<32, 64, 16>(a, clampL, narrow, s);
+  if constexpr (R == 32) return launch_rows<32, 32, 4, 16>(a, clampL, narrow, s);
   return launch_rows<R, 64, 4>(a, clampL, narrow, s);
 }
 
@@ -362,12 +401,16 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   // A lane sums at most 32 ShiftExp values: 32-bit partial sums are exact
   // while I0 * 2^k_inter < 2^27.
   const bool narrow = ((int64_t)a.I0 << a.k_inter) < ((int64_t)1 << 27);
+  // FP64 score requantization: exact for s <= 43, and |acc| <= 2^20 keeps
+  // |acc * m / 2^s| + 257 inside the int32 conversion.
+  AttnArgs b = a;
+  b.f64rq = a.score_shift <= 43 && ((am << 20) >> a.score_shift) + 257 < ((int64_t)1 << 31);
   // Fill the chip: fall back to 16-row blocks when 32-row blocks would give
   // fewer than two workgroups per CU.
   const int64_t wg32 = (int64_t)((a.Tw + 31) / 32) * a.H * a.B * a.nW;
   const int64_t wg16 = (int64_t)((a.Tw + 15) / 16) * a.H * a.B * a.nW;
-  if (wg32 < 512) return launch_lpr<16>(a, (int32_t)L, narrow, wg16, s);
-  return launch_lpr<32>(a, (int32_t)L, narrow, wg32, s);
+  if (wg32 < 512) return launch_lpr<16>(b, (int32_t)L, narrow, wg16, s);
+  return launch_lpr<32>(b, (int32_t)L, narrow, wg32, s);
 }
 
 hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,

@@ -550,7 +550,6 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
-  if (a.N % 128 == 0 && a.N >= 1536) return launch_tile<2, 2, 4, 4, 1>(epi, a, s);
   return launch_tile<4, 2, 2, 4, 1>(epi, a, s);
 }
 

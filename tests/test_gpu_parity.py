@@ -239,6 +239,37 @@ def test_attention(case, s_d):
     assert_same(got, ref, "attention")
 
 
+# (score_mult, score_shift): the FP64 score requantization covers shifts up
+# to 43 when |acc * m / 2^s| stays inside int32 (|acc| <= 2^20); the rest
+# take the 64-bit integer path.
+SCORE_RQ = [
+    (1, 13),                      # FP64: acc / 2^13, exact ties at acc = 4096 mod 8192
+    ((1 << 30) - 12345, 43),      # FP64 at its largest shift
+    (-((1 << 29) + 5), 40),       # FP64, negative scale
+    ((1 << 20) + 7, 22),          # FP64, mostly saturated
+    ((1 << 30) + 1, 44),          # integer path: shift past 43
+    ((1 << 31) - 1, 50),          # integer path: every score rounds to 0
+    (1 << 30, 12),                # integer path: the FP64 value would overflow int32
+]
+
+
+@pytest.mark.parametrize("case", [(1, 40, 40, 0, 0, 1), (2, 10, 10, 5, 5, 2)])
+@pytest.mark.parametrize("rqp", SCORE_RQ)
+def test_attention_score_requant_paths(case, rqp):
+    B, gh, gw, wh, ww, H = case
+    sm, ss = rqp
+    say(f"attention score rq m={sm} s={ss} B={B} grid={gh}x{gw} win={wh}x{ww} heads={H}")
+    g = rng(ss * 7 + gh)
+    D, T = 64 * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    p = {"score_mult": sm, "score_shift": ss, "smax_I0": int(g.integers(8, 65)),
+         "smax_s_d": -1, "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 36}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, wh, ww, H, 64, sm, ss, p["smax_I0"],
+                                     p["pv_mult"], p["pv_shift"]) for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
+    assert_same(got, ref, "attention score requant")
+
+
 @pytest.mark.parametrize("case", [(1, 1, 300, 0, 0, 8), (2, 6, 10, 3, 5, 4),
                                   (1, 15, 20, 0, 0, 2), (3, 1, 37, 0, 0, 1),
                                   (1, 40, 40, 0, 0, 2)])
