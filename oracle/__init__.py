@@ -89,7 +89,8 @@ class OrcDecoder(ctypes.Structure):
         + [(n, c_i32) for n in ("res1_mult_a", "res1_mult_b", "res1_shift")]
         + _ln_fields("ln1")
         + _linear_fields("val") + _linear_fields("off") + _linear_fields("attw")
-        + [(n, c_i32) for n in ("da_I0", "da_s_d", "da_out_mult", "da_out_shift", "da_mode")]
+        + [(n, c_i32) for n in ("da_I0", "da_s_d", "da_out_mult", "da_out_shift", "da_mode",
+                                "ref_dims")]
         + _linear_fields("co")
         + [(n, c_i32) for n in ("res2_mult_a", "res2_mult_b", "res2_shift")]
         + _ln_fields("ln2")
@@ -151,8 +152,9 @@ def lib():
             "orc_block_forward": (None, [ctypes.POINTER(OrcBlock), i8p, i8p,
                                          c_i32, c_i32, c_i32, c_i32, c_i32]),
             "orc_deform_nearest_index": (c_i64, [c_i32] * 6),
+            "orc_deform_box_nearest_index": (c_i64, [c_i32] * 9),
             "orc_deform_attn": (None, [i8p, i32p, i32p, c_i32, c_i32, i32p, i16p,
-                                       i8p, i8p] + [c_i32] * 13),
+                                       i8p, i8p] + [c_i32] * 14),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -448,6 +450,8 @@ def decoder_struct(params: dict):
     for name, typ in OrcDecoder._fields_:
         if name.endswith("_nq"):
             setattr(s, name, int(np.asarray(params[name[:-3] + "_mult"]).shape[0]))
+        elif name == "ref_dims":  # set from the reference array by decoder_forward
+            setattr(s, name, int(params.get(name, 2)))
         elif typ is c_i32:
             setattr(s, name, int(params[name]))
         else:
@@ -459,7 +463,7 @@ def decoder_struct(params: dict):
 
 def decoder_forward(params: dict, tgt, memory, ref, level_hw, level_start):
     """tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 Q16 [B, Q, 2]
-    -> int8 [B, Q, D]."""
+    (points) or [B, Q, 4] (boxes) -> int8 [B, Q, D]."""
     tgt = _arr(tgt, np.int8)
     memory = _arr(memory, np.int8)
     ref = _arr(ref, np.int32)
@@ -469,6 +473,7 @@ def decoder_forward(params: dict, tgt, memory, ref, level_hw, level_start):
     S = memory.shape[1]
     y = np.zeros_like(tgt)
     s, keep = decoder_struct(params)
+    s.ref_dims = ref.shape[-1]
     lib().orc_decoder_forward(ctypes.byref(s), _p(tgt, i8p), _p(memory, i8p), _p(ref, i32p),
                               _p(level_hw, i32p), _p(level_start, i32p), B, Q, S, _p(y, i8p))
     del keep
@@ -480,10 +485,16 @@ def deform_nearest_index(ref_x, ref_y, off_x, off_y, H, W):
                                           int(off_y), int(H), int(W))
 
 
+def deform_box_nearest_index(cx, cy, w, h, off_x, off_y, H, W, P):
+    return lib().orc_deform_box_nearest_index(*(int(v) for v in (cx, cy, w, h, off_x, off_y,
+                                                                 H, W, P)))
+
+
 def deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
                 out_shift, mode=0, k_inter=16, k_out=8, m_p=4, s_d=-1):
-    """value int8 [B, S, H, Dh]; ref int32 [B, Q, 2]; offsets int16
-    [B, Q, H, L, P, 2]; logits int8 [B, Q, H, L*P] -> out int8 [B, Q, H*Dh]."""
+    """value int8 [B, S, H, Dh]; ref int32 [B, Q, 2] (points) or [B, Q, 4]
+    (boxes); offsets int16 [B, Q, H, L, P, 2]; logits int8 [B, Q, H, L*P]
+    -> out int8 [B, Q, H*Dh]."""
     value = _arr(value, np.int8)
     level_hw = _arr(level_hw, np.int32)
     level_start = _arr(level_start, np.int32)
@@ -496,5 +507,5 @@ def deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult
     lib().orc_deform_attn(_p(value, i8p), _p(level_hw, i32p), _p(level_start, i32p),
                           L, P, _p(ref, i32p), _p(offsets, i16p), _p(logits, i8p),
                           _p(out, i8p), B, Q, H, Dh, S, I0, k_inter, k_out, m_p, s_d,
-                          out_mult, out_shift, mode)
+                          out_mult, out_shift, mode, ref.shape[-1])
     return out

@@ -628,21 +628,59 @@ void orc_block_forward(const orc_block* p, const int8_t* x, int8_t* y,
  *   ix = floor(X / 2^8)                      (pixel whose cell holds X)
  * which is the nearest pixel centre under the half-pixel convention.  A
  * sample outside the map contributes nothing (zero padding). */
-int64_t orc_deform_nearest_index(int32_t ref_x, int32_t ref_y, int32_t off_x,
-                                 int32_t off_y, int32_t H, int32_t W) {
-  int64_t X = (int64_t)floor_div((__int128)ref_x * W, 256) + off_x;
-  int64_t Y = (int64_t)floor_div((__int128)ref_y * H, 256) + off_y;
+/* Sampling location in Q8 pixels of a W x H level (pixel i spans
+ * [256 i, 256 (i+1)), its centre at 256 i + 128).
+ * Reference point (ref_dims 2: r = (x, y), Q16 fractions of the map): the
+ * reference lands at floor(x W / 2^8) and the offset is added in Q8 pixels.
+ * Reference box (ref_dims 4: r = (cx, cy, w, h), Q16 fractions): the offset
+ * is in units of the box, as in the deformable decoder with box references,
+ * location = c + (off / 2^8) / P * size / 2 as a fraction of the map; one
+ * floor of the exact value in Q8 pixels:
+ *   X = floor((cx * 2^9 * P + off_x * w) * W / (2^17 * P)). */
+static void deform_location(const int32_t* r, int32_t ref_dims, int32_t off_x,
+                            int32_t off_y, int32_t H, int32_t W, int32_t P,
+                            int64_t* X, int64_t* Y) {
+  if (ref_dims == 2) {
+    *X = (int64_t)floor_div((__int128)r[0] * W, 256) + off_x;
+    *Y = (int64_t)floor_div((__int128)r[1] * H, 256) + off_y;
+  } else {
+    const __int128 den = (__int128)131072 * P;
+    *X = (int64_t)floor_div(((__int128)r[0] * 512 * P + (__int128)off_x * r[2]) * W, den);
+    *Y = (int64_t)floor_div(((__int128)r[1] * 512 * P + (__int128)off_y * r[3]) * H, den);
+  }
+}
+
+static int64_t nearest_index(int64_t X, int64_t Y, int32_t H, int32_t W) {
   int64_t ix = (int64_t)floor_div(X, 256);
   int64_t iy = (int64_t)floor_div(Y, 256);
   if (ix < 0 || ix >= W || iy < 0 || iy >= H) return -1;
   return iy * W + ix;
 }
 
+int64_t orc_deform_nearest_index(int32_t ref_x, int32_t ref_y, int32_t off_x,
+                                 int32_t off_y, int32_t H, int32_t W) {
+  const int32_t r[2] = {ref_x, ref_y};
+  int64_t X, Y;
+  deform_location(r, 2, off_x, off_y, H, W, 1, &X, &Y);
+  return nearest_index(X, Y, H, W);
+}
+
+int64_t orc_deform_box_nearest_index(int32_t cx, int32_t cy, int32_t w, int32_t h,
+                                     int32_t off_x, int32_t off_y, int32_t H, int32_t W,
+                                     int32_t P) {
+  const int32_t r[4] = {cx, cy, w, h};
+  int64_t X, Y;
+  deform_location(r, 4, off_x, off_y, H, W, P, &X, &Y);
+  return nearest_index(X, Y, H, W);
+}
+
 /* Multi-scale deformable attention core (Sec. 3.1.1 with the decoder's
  * Softmax as Constrained Shiftmax, Sec. 3.3.2):
  *   value  int8  [B, S_total, heads, head_dim]  (levels stacked, level_start)
- *   ref    int32 [B, Q, 2]                      Q16 (x, y) in [0, 1)
- *   offsets int16 [B, Q, heads, L, P, 2]         Q8 pixels (x, y)
+ *   ref    int32 [B, Q, ref_dims]               Q16 fractions of the map:
+ *          points (x, y) or boxes (cx, cy, w, h)
+ *   offsets int16 [B, Q, heads, L, P, 2]         (x, y): Q8 pixels for points,
+ *          Q8 units of size / (2 P) for boxes (deform_location)
  *   logits int8  [B, Q, heads, L*P]  -> P = ConstrainedShiftmax per (b,q,h)
  *   out    int8  [B, Q, heads*head_dim] = sat8(rq(sum P * sampled value))
  * mode 0: nearest sampling (the paper's).  mode 1: a fixed-point bilinear
@@ -655,8 +693,9 @@ void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
                      int32_t heads, int32_t head_dim, int32_t S_total,
                      int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
                      int32_t s_d_static, int32_t out_mult, int32_t out_shift,
-                     int32_t mode) {
+                     int32_t mode, int32_t ref_dims) {
   orc_require(mode == 0 || mode == 1, "mode is 0 (nearest) or 1 (bilinear)");
+  orc_require(ref_dims == 2 || ref_dims == 4, "references are points (2) or boxes (4)");
   const int32_t LP = L * P;
   int32_t* lg = (int32_t*)malloc(sizeof(int32_t) * (size_t)LP);
   int32_t* pw = (int32_t*)malloc(sizeof(int32_t) * (size_t)LP);
@@ -670,16 +709,17 @@ void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
         orc_shiftmax_row(lg, LP, I0, k_inter, k_out, m_p, s_d_static, pw,
                          NULL);
         for (int32_t c = 0; c < head_dim; c++) acc[c] = 0;
-        int32_t rx = ref[((int64_t)b * Q + q) * 2 + 0];
-        int32_t ry = ref[((int64_t)b * Q + q) * 2 + 1];
+        const int32_t* r = ref + ((int64_t)b * Q + q) * ref_dims;
         for (int32_t l = 0; l < L; l++) {
           int32_t Hl = level_hw[2 * l + 0], Wl = level_hw[2 * l + 1];
           for (int32_t pt = 0; pt < P; pt++) {
             int64_t oidx = ((bqh * L + l) * P + pt) * 2;
             int32_t ox = offsets[oidx + 0], oy = offsets[oidx + 1];
             int32_t wgt = pw[l * P + pt];
+            int64_t X0, Y0;
+            deform_location(r, ref_dims, ox, oy, Hl, Wl, P, &X0, &Y0);
             if (mode == 0) {
-              int64_t idx = orc_deform_nearest_index(rx, ry, ox, oy, Hl, Wl);
+              int64_t idx = nearest_index(X0, Y0, Hl, Wl);
               if (idx < 0) continue;
               int64_t row = ((int64_t)b * S_total + level_start[l] + idx) *
                                 heads + h;
@@ -687,8 +727,7 @@ void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
                 acc[c] += (__int128)wgt * value[row * head_dim + c];
             } else {
               /* half-pixel grid: pixel centres sit at X = 256*i + 128 */
-              int64_t X = (int64_t)floor_div((__int128)rx * Wl, 256) + ox - 128;
-              int64_t Y = (int64_t)floor_div((__int128)ry * Hl, 256) + oy - 128;
+              int64_t X = X0 - 128, Y = Y0 - 128;
               int64_t x0 = (int64_t)floor_div(X, 256), fx = X - 256 * x0;
               int64_t y0 = (int64_t)floor_div(Y, 256), fy = Y - 256 * y0;
               for (int32_t dy = 0; dy < 2; dy++)
@@ -764,7 +803,7 @@ void orc_decoder_forward(const orc_decoder* p, const int8_t* tgt, const int8_t* 
              lg);
   orc_deform_attn(v, level_hw, level_start, L, P, ref, off, lg, smp, B, Q, H, hd, S,
                   p->da_I0, 16, 8, 4, p->da_s_d, p->da_out_mult, p->da_out_shift,
-                  p->da_mode);
+                  p->da_mode, p->ref_dims);
   orc_linear(smp, p->w_co, p->b_co, MQ, D, D, p->co_mult, p->co_shift, p->co_nq, tmp);
   orc_residual_tensor(tmp, t1, x, MQ * D, p->res2_mult_a, p->res2_mult_b, p->res2_shift);
   orc_int_layernorm(x, t2, MQ, D, p->ln2_beta, p->ln2_mult, p->ln2_shift, p->ln2_nq,

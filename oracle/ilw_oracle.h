@@ -135,6 +135,7 @@ typedef struct {
   const int8_t* w_attw; const int32_t* b_attw; const int32_t* attw_mult;
   const int32_t* attw_shift; int32_t attw_nq;
   int32_t da_I0, da_s_d, da_out_mult, da_out_shift, da_mode;
+  int32_t ref_dims;  /* 2: reference points (x, y); 4: reference boxes (cx, cy, w, h) */
   const int8_t* w_co; const int32_t* b_co; const int32_t* co_mult;
   const int32_t* co_shift; int32_t co_nq;
   int32_t res2_mult_a, res2_mult_b, res2_shift;
@@ -193,9 +194,14 @@ void orc_block_forward(const orc_block* p, const int8_t* x, int8_t* y,
                        int32_t win_h, int32_t win_w);
 
 /* Deformable sampling location of one sample: returns the flat pixel index
- * y*W + x inside the level, or -1 when the sample falls outside the map. */
+ * y*W + x inside the level, or -1 when the sample falls outside the map.
+ * Point reference (x, y), offsets in Q8 pixels; box reference (cx, cy, w, h),
+ * offsets in Q8 units of size / (2 P) (see orc_deform_attn). */
 int64_t orc_deform_nearest_index(int32_t ref_x, int32_t ref_y, int32_t off_x,
                                  int32_t off_y, int32_t H, int32_t W);
+int64_t orc_deform_box_nearest_index(int32_t cx, int32_t cy, int32_t w, int32_t h,
+                                     int32_t off_x, int32_t off_y, int32_t H, int32_t W,
+                                     int32_t P);
 void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
                      const int32_t* level_start, int32_t L, int32_t P,
                      const int32_t* ref, const int16_t* offsets,
@@ -203,7 +209,7 @@ void orc_deform_attn(const int8_t* value, const int32_t* level_hw,
                      int32_t heads, int32_t head_dim, int32_t S_total,
                      int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
                      int32_t s_d_static, int32_t out_mult, int32_t out_shift,
-                     int32_t mode);
+                     int32_t mode, int32_t ref_dims);
 
 #ifdef __cplusplus
 }

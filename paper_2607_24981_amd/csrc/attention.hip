@@ -49,11 +49,6 @@ __device__ __forceinline__ int32_t rq_f64(int32_t acc, double scale) {
   return min(max((int32_t)y, 256 + kQmin), 256 + kQmax);
 }
 
-template <bool B>
-struct Flag {
-  static constexpr bool value = B;
-};
-
 // Bytes 0 of a, b, c, d packed into one word (a in the low byte).
 __device__ __forceinline__ uint32_t pack_bytes(int32_t a, int32_t b, int32_t c, int32_t d) {
   const uint32_t lo = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0400u);

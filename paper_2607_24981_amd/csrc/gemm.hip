@@ -53,6 +53,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
   __shared__ int8_t glut[EPI == EPI_GELU ? 256 : 1];
+  __shared__ RqF64 rqc[TN];                         // output requantization per channel
+  __shared__ int64_t qoff[EPI == EPI_QKV ? TM : 1][2];  // QKV: Q/K and V^T offsets per token
   __shared__ LnChan lnp[LN ? TN : 1];              // LayerNorm constants per channel
   __shared__ int32_t lnred[LN ? 2 * WN * TM : 1];  // per-wave row sums
 
@@ -199,12 +201,19 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     for (int j = 0; j < FJ; ++j)
       rs[i][j] = *(const uint32_t*)(a.resid + rtok[j] + min(nch[i], N - 4));
   };
-  if (EARLY) {
+  if (EARLY && RES) {
 #pragma unroll
-    for (int i = 0; i < FI; ++i) {
-      load_chan(i);
-      if (RES) load_resid(i);
-    }
+    for (int i = 0; i < FI; ++i) load_resid(i);
+  }
+  // Output requantization constants of the tile's channels, once per
+  // workgroup (a lane's channels are shared by 16 lanes of each wave row).
+  int rq_int = 0;
+  for (int c = tid; c < TN; c += NT) {
+    const int32_t n = min(n0 + c, N - 1);
+    RqF64 r;
+    rq_int |= r.init(a.mult[a.nq == 1 ? 0 : n], a.shift[a.nq == 1 ? 0 : n],
+                     a.bias ? a.bias[n] : 0);
+    rqc[c] = r;
   }
 
   if (EPI == EPI_GELU) {
@@ -214,20 +223,20 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
   }
   if (EPI == EPI_QKV) {
-#pragma unroll
-    for (int j = 0; j < FJ; ++j) {
-      const int64_t m = m0 + wm * WTM + j * 16 + (lane & 15);
-      if (!tok_ok[j]) continue;
+    // destination of each of the tile's tokens in the window-major layout,
+    // once per workgroup
+    for (int t = tid; t < TM; t += NT) {
+      const int64_t m = min(m0 + t, M - 1);
       const QkvLayout& Lq = a.qkv;
       const int32_t b = fdiv((int32_t)m, Lq.T, a.inv_T);
-      const int32_t t = (int32_t)m - b * Lq.T;
-      const int32_t ty = fdiv(t, Lq.grid_w, a.inv_gw), tx = t - ty * Lq.grid_w;
+      const int32_t tt = (int32_t)m - b * Lq.T;
+      const int32_t ty = fdiv(tt, Lq.grid_w, a.inv_gw), tx = tt - ty * Lq.grid_w;
       const int32_t wy = fdiv(ty, Lq.win_h, a.inv_wh), iy = ty - wy * Lq.win_h;
       const int32_t wx = fdiv(tx, Lq.win_w, a.inv_ww), ix = tx - wx * Lq.win_w;
       const int64_t bw = (int64_t)b * Lq.nW + wy * Lq.nwx + wx;
       const int32_t li = iy * Lq.win_w + ix;
-      tok[j] = (bw * Lq.H * Lq.Tw + li) * 64;
-      tokv[j] = bw * Lq.H * 64 * Lq.Twp + li;
+      qoff[t][0] = (bw * Lq.H * Lq.Tw + li) * 64;
+      qoff[t][1] = bw * Lq.H * 64 * Lq.Twp + li;
     }
   }
   int ln_wide = 0;
@@ -271,8 +280,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 
   if constexpr (PF == 1) {
     sstore(0, 0);
+    rq_int = __syncthreads_or(rq_int);
     if (LN) ln_wide = __syncthreads_or(ln_wide);
-    else __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + 1 < nk) gload(kt + 1, 0);
       compute(kt & 1);
@@ -284,8 +293,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     // one), so the memory counter wait before each LDS store is exact: it
     // leaves the younger slots' loads in flight.
     sstore(0, 0);
+    rq_int = __syncthreads_or(rq_int);
     if (LN) ln_wide = __syncthreads_or(ln_wide);
-    else __syncthreads();
     gload(min(PF, nk - 1), 0);
     for (int kt0 = 0; kt0 < nk; kt0 += PF) {
 #pragma unroll
@@ -299,66 +308,91 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     }
   }
 
-  // Epilogue.
+  // Epilogue.  The FP64 requantization serves every tile whose channels
+  // allow it (the usual case); otherwise the integer form with constants
+  // read per lane.
   uint32_t xw[FI][FJ];  // RESID_LN: the residual outputs, 4 channels per word
 #pragma unroll
   for (int i = 0; i < FI; ++i)
 #pragma unroll
     for (int j = 0; j < FJ; ++j) xw[i][j] = 0;
-#pragma unroll
-  for (int i = 0; i < FI; ++i) {
-    if (!ch_ok[i]) continue;
-    const int32_t n = nch[i];
-    if (!EARLY) {
-      load_chan(i);
-      if (RES) load_resid(i);
-    }
-    ChanRq cr[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) cr[r].init(pm[i][r], ps[i][r], pb[i][r]);
-    int8_t* qk_base = nullptr;
-    int64_t ch_qk = 0, ch_v = 0;
-    bool is_v = false;
-    if (EPI == EPI_QKV) {
-      const QkvLayout& Lq = a.qkv;
-      const int32_t part = n / Lq.D, rem_n = n - part * Lq.D;
-      const int32_t h = rem_n >> Lq.hs, c = rem_n & ((1 << Lq.hs) - 1);
-      is_v = part == 2;
-      qk_base = part == 0 ? Lq.q : Lq.k;
-      ch_qk = (int64_t)h * Lq.Tw * 64 + c;
-      ch_v = ((int64_t)h * 64 + c) * Lq.Twp;
-    }
+  if (EPI == EPI_QKV) {
 #pragma unroll
     for (int j = 0; j < FJ; ++j) {
-      if (!tok_ok[j]) continue;
-      int32_t v[4];
+      const int t = wm * WTM + j * 16 + (lane & 15);
+      tok[j] = qoff[t][0];
+      tokv[j] = qoff[t][1];
+    }
+  }
+  auto epilogue = [&](auto f64) {
+    constexpr bool F = decltype(f64)::value;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = cr[r].apply(acc[i][j][r]);
-      if (EPI == EPI_STORE) {
-        *(uint32_t*)(a.y + tok[j] + n) = pack4(v[0], v[1], v[2], v[3]);
-      } else if (EPI == EPI_GELU) {
-        *(uint32_t*)(a.y + tok[j] + n) = pack4(glut[v[0] + 128], glut[v[1] + 128],
-                                               glut[v[2] + 128], glut[v[3] + 128]);
-      } else if (RES) {
-        const uint32_t s = rs[i][j];
-        int32_t o[4];
+    for (int i = 0; i < FI; ++i) {
+      if (!ch_ok[i]) continue;
+      const int32_t n = nch[i];
+      if (!EARLY && RES) load_resid(i);
+      RqF64 rf[4];
+      ChanRq cr[4];
+      if constexpr (F) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          o[r] = rq2(v[r], (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
-        const uint32_t word = pack4(o[0], o[1], o[2], o[3]);
-        *(uint32_t*)(a.y + tok[j] + n) = word;
-        if (LN) xw[i][j] = word;
-      } else {  // EPI_QKV: scatter into window-major Q, K and V^T
-        if (!is_v) {
-          *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(v[0], v[1], v[2], v[3]);
-        } else {
-          int8_t* dst = a.qkv.vt + tokv[j] + ch_v;
+        for (int r = 0; r < 4; ++r) rf[r] = rqc[n - n0 + r];
+      } else {
+        load_chan(i);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(int64_t)r * a.qkv.Twp] = (int8_t)v[r];
+        for (int r = 0; r < 4; ++r) cr[r].init(pm[i][r], ps[i][r], pb[i][r]);
+      }
+      int8_t* qk_base = nullptr;
+      int64_t ch_qk = 0, ch_v = 0;
+      bool is_v = false;
+      if (EPI == EPI_QKV) {
+        const QkvLayout& Lq = a.qkv;
+        const int32_t part = n / Lq.D, rem_n = n - part * Lq.D;
+        const int32_t h = rem_n >> Lq.hs, c = rem_n & ((1 << Lq.hs) - 1);
+        is_v = part == 2;
+        qk_base = part == 0 ? Lq.q : Lq.k;
+        ch_qk = (int64_t)h * Lq.Tw * 64 + c;
+        ch_v = ((int64_t)h * 64 + c) * Lq.Twp;
+      }
+#pragma unroll
+      for (int j = 0; j < FJ; ++j) {
+        if (!tok_ok[j]) continue;
+        // u[r]: the requantized value + 256 (FP64 form) or the value itself;
+        // its low byte is the int8 output either way
+        int32_t u[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) u[r] = F ? rf[r].apply(acc[i][j][r]) : cr[r].apply(acc[i][j][r]);
+        constexpr int32_t off = F ? 256 : 0;
+        if (EPI == EPI_STORE) {
+          *(uint32_t*)(a.y + tok[j] + n) = pack4(u[0], u[1], u[2], u[3]);
+        } else if (EPI == EPI_GELU) {
+          *(uint32_t*)(a.y + tok[j] + n) =
+              pack4(glut[u[0] + 128 - off], glut[u[1] + 128 - off], glut[u[2] + 128 - off],
+                    glut[u[3] + 128 - off]);
+        } else if (RES) {
+          const uint32_t s = rs[i][j];
+          int32_t o[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            o[r] = rq2(u[r] - off, (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
+          const uint32_t word = pack4(o[0], o[1], o[2], o[3]);
+          *(uint32_t*)(a.y + tok[j] + n) = word;
+          if (LN) xw[i][j] = word;
+        } else {  // EPI_QKV: scatter into window-major Q, K and V^T
+          if (!is_v) {
+            *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(u[0], u[1], u[2], u[3]);
+          } else {
+            int8_t* dst = a.qkv.vt + tokv[j] + ch_v;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(int64_t)r * a.qkv.Twp] = (int8_t)u[r];
+          }
         }
       }
     }
-  }
+  };
+  if (rq_int)
+    epilogue(Flag<false>{});
+  else
+    epilogue(Flag<true>{});
   if (LN) {
     // LayerNorm of the residual output rows (same reading as the standalone
     // operator).  A token's N channels sit in 4 lanes of each of the WN waves
@@ -483,6 +517,11 @@ hipError_t launch_ln_tile(const GemmArgs& a, hipStream_t s) {
 
 // Latency mode (ILW_GEMM_PF=1|3 forces it off or on): grids of at most about
 // one wave per SIMD with the throughput tiles.
+int tp_pf() {  // XXX experiment
+  static int v = -1;
+  if (v < 0) { const char* e = getenv("ILW_X_TPPF"); v = e ? atoi(e) : 1; }
+  return v;
+}
 bool latency_mode(int64_t waves) {
   static int ov = -1;
   if (ov < 0) {
@@ -513,12 +552,16 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
+      if (tp_pf() == 3) return launch_ln_tile<6, 2, 2, 4, 3>(a, s);  // XXX
+      if (tp_pf() == 2) return launch_ln_tile<6, 2, 2, 4, 2>(a, s);  // XXX
       return launch_ln_tile<6, 2, 2, 4, 1>(a, s);  // 192 x 128 tokens, 12 waves of 32 x 64
     }
     if (a.N == 384) {
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
+      if (tp_pf() == 3) return launch_ln_tile<12, 1, 2, 4, 3>(a, s);  // XXX
+      if (tp_pf() == 2) return launch_ln_tile<12, 1, 2, 4, 2>(a, s);  // XXX
       return launch_ln_tile<12, 1, 2, 4, 1>(a, s);  // 384 x 64 tokens, 12 waves of 32 x 64
     }
     return hipErrorInvalidValue;
@@ -550,6 +593,8 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
+  if (tp_pf() == 3) return launch_tile<4, 2, 2, 4, 3>(epi, a, s);  // XXX
+  if (tp_pf() == 2) return launch_tile<4, 2, 2, 4, 2>(epi, a, s);  // XXX
   return launch_tile<4, 2, 2, 4, 1>(epi, a, s);
 }
 

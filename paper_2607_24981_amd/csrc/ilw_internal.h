@@ -189,8 +189,10 @@ struct LnChan {
 // ---------------------------------------------------------------- launchers
 // ---- GEMM epilogue helpers (shared by the GEMM and block-tail kernels)
 __device__ __forceinline__ uint32_t pack4(int32_t a, int32_t b, int32_t c, int32_t d) {
-  return (uint32_t)(a & 0xff) | ((uint32_t)(b & 0xff) << 8) |
-         ((uint32_t)(c & 0xff) << 16) | ((uint32_t)d << 24);
+  // byte 0 of each (two byte permutes and a shift-or)
+  const uint32_t lo = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0400u);
+  const uint32_t hi = __builtin_amdgcn_perm((uint32_t)d, (uint32_t)c, 0x0c0c0400u);
+  return lo | (hi << 16);
 }
 
 // Requantization of one channel with its accumulator bound L:
@@ -215,6 +217,50 @@ struct ChanRq {
     const int32_t v = (int32_t)(((int64_t)a * mult + rnd) >> shift);
     return min(max(v, kQmin), kQmax);
   }
+};
+
+// The same requantization in FP64, for the GEMM epilogues.  Per channel:
+// scale = m * 2^-s and c = bias * m * 2^-s + 256.5, both exact doubles when
+// s <= 43 and |bias| < 2^21 (bias * m < 2^52); the accumulator is clamped to
+// [lo, hi] = [-L - bias, L - bias], beyond which the result saturates, with L
+// <= 2^30 * 2^s / |m| (no clamp when even 2^31 cannot reach 2^30 after the
+// scaling).  Then fma(acc, scale, c) rounds the exact value
+// (acc + bias) * m / 2^s + 256.5 once: an unsaturated result is a multiple of
+// 2^-s below 2^10, hence exact, a saturated one stays on its side of 129 or
+// 384, and the value fits the int32 conversion.  The result is q + 256 in
+// [129, 383] (its low byte is q's).
+struct RqF64 {
+  double scale, c;
+  int32_t lo, hi;
+  // Returns true when the channel needs the integer form instead.
+  __device__ __forceinline__ bool init(int32_t m, int32_t s, int32_t b) {
+    scale = __builtin_ldexp((double)m, -s);
+    c = __builtin_fma((double)b, scale, 256.5);
+    const float am = fabsf((float)m);
+    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) * __builtin_amdgcn_rcpf(am);
+    if (bound >= 1073741824.f) {
+      lo = INT32_MIN;
+      hi = INT32_MAX;
+    } else {
+      const int32_t L = (int32_t)bound + 1;
+      lo = -L - b;
+      hi = L - b;
+    }
+    return s > 43 || b >= (1 << 21) || b <= -(1 << 21);
+  }
+  __device__ __forceinline__ int32_t apply(int32_t acc) const {  // q + 256
+    // the clamp as one median-of-three (lo < hi always holds; the compiler
+    // cannot see it and would emit a max and a min)
+    int32_t a;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(a) : "v"(acc), "v"(lo), "v"(hi));
+    const int32_t q = (int32_t)__builtin_fma((double)a, scale, c);
+    return min(max(q, 256 + kQmin), 256 + kQmax);
+  }
+};
+
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
 };
 
 // n / d for 0 <= n < 2^24 with an fp32 reciprocal and one correction step.

@@ -201,10 +201,13 @@ def encoder_inputs(wl: EncoderWorkload, seed: int, variant: str = "baseline",
 
 
 def deform_inputs(wl: DeformWorkload, seed: int, batch: int | None = None,
-                  queries: int | None = None) -> dict:
+                  queries: int | None = None, boxes: bool = False) -> dict:
     """Inputs of the deformable sampling core: value maps, Q16 reference
     points, Q8 pixel offsets (+-8 px, so some samples leave the map), logits
-    over the L*P samples, and the output requantization."""
+    over the L*P samples, and the output requantization.  With boxes, the
+    references are boxes (cx, cy, w, h): the same centres, sizes U[2^12, 2^15]
+    (1/16 to 1/2 of the map), drawn after everything else; the offsets are
+    then in Q8 units of size / (2 P), so +-8 units reach +-size / P."""
     rng = np.random.Generator(np.random.PCG64(seed))
     B = wl.batch if batch is None else batch
     Q = wl.queries if queries is None else queries
@@ -224,6 +227,8 @@ def deform_inputs(wl: DeformWorkload, seed: int, batch: int | None = None,
     }
     d["out_mult"] = int(_u(rng, 1 << 29, 1 << 30))
     d["out_shift"] = int(_u(rng, 33, 36))
+    if boxes:
+        d["ref"] = np.concatenate([d["ref"], _u(rng, 1 << 12, 1 << 15, (B, Q, 2))], axis=-1)
     return d
 
 
@@ -365,9 +370,12 @@ def decoder_params(rng: np.random.Generator, dim: int, heads: int, ffn_dim: int,
     return p
 
 
-def decoder_inputs(wl: DecoderWorkload, seed: int, batch: int | None = None, mode: int = 0):
+def decoder_inputs(wl: DecoderWorkload, seed: int, batch: int | None = None, mode: int = 0,
+                   boxes: bool = False):
     """(params, tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 Q16
-    [B, Q, 2], level_hw [L, 2], level_start [L])."""
+    [B, Q, 2], level_hw [L, 2], level_start [L]).  With boxes, ref is
+    [B, Q, 4] (cx, cy, w, h): the same centres, sizes U[2^12, 2^15] drawn
+    last."""
     rng = np.random.Generator(np.random.PCG64(seed))
     B = wl.batch if batch is None else batch
     p = decoder_params(rng, wl.dim, wl.heads, wl.ffn_dim, len(wl.levels), wl.points, mode=mode)
@@ -377,4 +385,7 @@ def decoder_inputs(wl: DecoderWorkload, seed: int, batch: int | None = None, mod
     tgt = _u(rng, -127, 127, (B, wl.queries, wl.dim), np.int8)
     memory = _u(rng, -127, 127, (B, S, wl.dim), np.int8)
     ref = _u(rng, 0, 65535, (B, wl.queries, 2))
+    if boxes:
+        ref = np.concatenate([ref, _u(rng, 1 << 12, 1 << 15, (B, wl.queries, 2))], axis=-1)
+    p["ref_dims"] = ref.shape[-1]
     return p, tgt, memory, ref, hw, start

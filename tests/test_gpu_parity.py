@@ -64,6 +64,42 @@ def test_linear(M, N, K, per_tensor):
     assert_same(got, ref, "linear")
 
 
+def _edge_channels(N, fallback):
+    """Per-channel (mult, shift, bias) at the edges of the FP64 epilogue form
+    (shift 43, |bias| = 2^21 - 1, m = 0, odd m at shift 1: exact ties, tiny
+    and huge scales); with fallback, every 64-channel group also holds a
+    channel that needs the integer form (shift above 43 or |bias| >= 2^21)."""
+    ms = [(1 << 31) - 1, -((1 << 31) - 1), 0, 1, 3, 1 << 29, -(1 << 30), 12345,
+          (1 << 30) + 7, -5]
+    ss = [43, 43, 30, 1, 1, 30, 31, 13, 40, 2]
+    bs = [(1 << 21) - 1, -((1 << 21) - 1), 77, -3, 4, 1 << 20, -(1 << 20), 0, 12, -9]
+    mult = np.array([ms[i % len(ms)] for i in range(N)], np.int32)
+    shift = np.array([ss[i % len(ss)] for i in range(N)], np.int32)
+    bias = np.array([bs[i % len(bs)] for i in range(N)], np.int32)
+    if fallback:
+        for g0 in range(0, N, 64):
+            mult[g0 + 5], shift[g0 + 5], bias[g0 + 5] = (1 << 30) + 1, 50, 1 << 25
+            mult[g0 + 17], shift[g0 + 17], bias[g0 + 17] = -(1 << 31) + 1, 44, -(1 << 21)
+            mult[g0 + 40], shift[g0 + 40] = (1 << 31) - 1, 62
+    return mult, shift, bias
+
+
+@pytest.mark.parametrize("M", [300, 40000])
+@pytest.mark.parametrize("fallback", [False, True])
+def test_linear_requant_forms(M, fallback):
+    """The epilogue's FP64 requantization at its edges, and tiles that fall
+    back to the integer form, at a small-grid and a large-grid tile shape."""
+    N, K = 256, 128
+    say(f"linear requant forms M={M} fallback={fallback}")
+    g = rng(M + fallback)
+    x = g.integers(-127, 128, (M, K)).astype(np.int8)
+    w = g.integers(-127, 128, (N, K)).astype(np.int8)
+    mult, shift, bias = _edge_channels(N, fallback)
+    ref = oracle.linear(x, w, bias, mult, shift)
+    got = host(ilw.ilw_linear(dev(x), dev(w), dev(bias), dev(mult), dev(shift)))
+    assert_same(got, ref, "linear requant forms")
+
+
 def test_linear_no_bias_and_empty():
     say("linear without bias, M=0")
     g = rng(5)
@@ -315,6 +351,25 @@ def test_block_shapes(dims, grid, win, B):
     t = dev(x)
     got = host(ilw.ilw_block_forward(blk, t, *grid, *win, y=t))  # in place
     assert_same(got, ref, "block in place")
+
+
+@pytest.mark.parametrize("dims", [(128, 2, 512), (384, 6, 1536)])
+def test_block_requant_fallback(dims):
+    """A block whose QKV, projection, fc1 and fc2 layers each hold one
+    channel that the FP64 epilogue form cannot take (shift above 43, or a
+    bias of 2^21 or more): those tiles use the integer form."""
+    D, H, Hm = dims
+    say(f"block requant fallback D={D}")
+    p = synth.block_params(rng(D + 5), D, H, 64, Hm, "wide", ln_iters=20, smax_s_d=-1)
+    p["qkv_shift"][7] = 44
+    p["proj_shift"][3] = 47
+    p["b_fc1"][100] = 1 << 22
+    p["fc2_shift"][5] = 45
+    p["b_fc2"][9] = -(1 << 21)
+    x = rng(8).integers(-127, 128, (2, 96, D)).astype(np.int8)
+    ref = oracle.block_forward(p, x, 8, 12, 4, 6)
+    got = host(ilw.ilw_block_forward(ilw.DeviceBlock(p), dev(x), 8, 12, 4, 6))
+    assert_same(got, ref, "block requant fallback")
 
 
 def encoder_ref(blocks, windows, x, gh, gw):

@@ -36,10 +36,12 @@ def chain(p, tgt, memory, ref, hw, start):
     return y.reshape(B, Q, D)
 
 
+@pytest.mark.parametrize("boxes", [False, True])
 @pytest.mark.parametrize("mode", [0, 1])
-def test_decoder_equals_operator_chain(mode):
+def test_decoder_equals_operator_chain(mode, boxes):
+    """Point references and reference boxes (the sampler's box form)."""
     wl = synth.DecoderWorkload("small", 2, 37, 64, 2, 128, ((9, 13), (4, 6), (2, 3)), 3)
-    p, tgt, mem, ref, hw, start = synth.decoder_inputs(wl, 11 + mode, mode=mode)
+    p, tgt, mem, ref, hw, start = synth.decoder_inputs(wl, 11 + mode, mode=mode, boxes=boxes)
     y = oracle.decoder_forward(p, tgt, mem, ref, hw, start)
     assert np.array_equal(y, chain(p, tgt, mem, ref, hw, start))
     assert np.std(y.astype(np.float64)) > 5
