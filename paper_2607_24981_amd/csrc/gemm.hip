@@ -20,10 +20,14 @@
 // weights in that XCD's L2.
 //
 // At K = 192 the exact requantization costs more VALU time than the MFMA work
-// of the tile, so the epilogue is kept to a few instructions per output: the
-// accumulator is clamped to a per-channel bound beyond which the result is
-// saturated anyway, after which one 64-bit multiply-add and one shift give the
-// exact rounded value inside int32.
+// of the tile, so the epilogue is kept to a few instructions per output.  Each
+// workgroup stages its channels' constants in LDS once (RqF64: scale and
+// bias-carrying addend as doubles, accumulator bounds); an output is then a
+// clamp, a conversion, one FP64 fma, a conversion and a clamp, exact by the
+// argument at RqF64.  Tiles holding a channel outside that form's range
+// (shift above 43, |bias| >= 2^21) take the integer form: the accumulator
+// clamped to a bound beyond which the result saturates, one 64-bit
+// multiply-add and one shift.
 #include <stdio.h>
 #include <stdlib.h>
 
@@ -517,11 +521,6 @@ hipError_t launch_ln_tile(const GemmArgs& a, hipStream_t s) {
 
 // Latency mode (ILW_GEMM_PF=1|3 forces it off or on): grids of at most about
 // one wave per SIMD with the throughput tiles.
-int tp_pf() {  // XXX experiment
-  static int v = -1;
-  if (v < 0) { const char* e = getenv("ILW_X_TPPF"); v = e ? atoi(e) : 1; }
-  return v;
-}
 bool latency_mode(int64_t waves) {
   static int ov = -1;
   if (ov < 0) {
@@ -552,16 +551,12 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
-      if (tp_pf() == 3) return launch_ln_tile<6, 2, 2, 4, 3>(a, s);  // XXX
-      if (tp_pf() == 2) return launch_ln_tile<6, 2, 2, 4, 2>(a, s);  // XXX
       return launch_ln_tile<6, 2, 2, 4, 1>(a, s);  // 192 x 128 tokens, 12 waves of 32 x 64
     }
     if (a.N == 384) {
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
-      if (tp_pf() == 3) return launch_ln_tile<12, 1, 2, 4, 3>(a, s);  // XXX
-      if (tp_pf() == 2) return launch_ln_tile<12, 1, 2, 4, 2>(a, s);  // XXX
       return launch_ln_tile<12, 1, 2, 4, 1>(a, s);  // 384 x 64 tokens, 12 waves of 32 x 64
     }
     return hipErrorInvalidValue;
@@ -593,8 +588,6 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
-  if (tp_pf() == 3) return launch_tile<4, 2, 2, 4, 3>(epi, a, s);  // XXX
-  if (tp_pf() == 2) return launch_tile<4, 2, 2, 4, 2>(epi, a, s);  // XXX
   return launch_tile<4, 2, 2, 4, 1>(epi, a, s);
 }
 
