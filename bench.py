@@ -112,6 +112,9 @@ def main():
                          "positional embedding, then the encoder")
     ap.add_argument("--mode", type=int, default=0,
                     help="decoder workloads: deformable sampling 0 = nearest, 1 = bilinear-Q8")
+    ap.add_argument("--boxes", action="store_true",
+                    help="decoder workloads: reference boxes (offsets relative to the box) "
+                         "instead of reference points")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="first make one plain device-to-device copy of this many MiB "
                          "(the known-size reference for rocprofv3 byte counters)")
@@ -415,8 +418,10 @@ def bench_decoder(args, wl):
 
     from paper_2607_24981_amd import ilw, synth
     B = wl.batch if args.batch is None else args.batch
-    log(f"workload {wl.name}: batch {B}, {wl.queries} queries, dim {wl.dim}, mode {args.mode}")
-    p, tgt, mem, ref, hw, start = synth.decoder_inputs(wl, args.seed, batch=B, mode=args.mode)
+    log(f"workload {wl.name}: batch {B}, {wl.queries} queries, dim {wl.dim}, mode {args.mode}, "
+        f"references {'boxes' if args.boxes else 'points'}")
+    p, tgt, mem, ref, hw, start = synth.decoder_inputs(wl, args.seed, batch=B, mode=args.mode,
+                                                       boxes=args.boxes)
     dd = ilw.DeviceDecoder(p)
     tgt_d, mem_d, ref_d = ilw.to_device(tgt), ilw.to_device(mem), ilw.to_device(ref)
     y = torch.empty_like(tgt_d)
@@ -459,8 +464,8 @@ def bench_decoder(args, wl):
         "gemm_qkv": ("ops", 2 * MQ * 3 * D * D),
         "attention": ("ops", 4 * B * Q * Q * D),
         "decoder": ("ops", 2 * MQ * D * (2 * D + 3 * NW + 2 * F) + 2 * MS * D * D),
-        # gathered head slices, offsets (int16), logits, output
-        "deform": ("bytes", MQ * NW * (D // H) + MQ * 2 * NW * 2 + MQ * NW + MQ * D),
+        # gathered head slices, offsets (int8, widened in the sampler), logits, output
+        "deform": ("bytes", MQ * NW * (D // H) + MQ * 2 * NW + MQ * NW + MQ * D),
         "layernorm": ("bytes", 3 * (2 * MQ * D + 12 * D)),
     }
     stages = {}
@@ -514,6 +519,7 @@ def bench_decoder(args, wl):
             "config": {"workload": wl.name, "batch": B, "queries": Q, "dim": D, "heads": H,
                        "ffn_dim": F, "levels": [list(l) for l in wl.levels], "points": P,
                        "sampling": "nearest" if args.mode == 0 else "bilinear-Q8",
+                       "references": "boxes" if args.boxes else "points",
                        "launch": "eager" if args.no_graph else "hip graph",
                        "gemm_ops_per_step": ops},
             "roofline": roof, "cpu_baseline": cpu, "parity": parity, "stages": stages}

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ILW_ABI_VERSION 6
+#define ILW_ABI_VERSION 7
 
 typedef enum {
   ILW_OK = 0,
@@ -268,6 +268,24 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
                     int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
                     int32_t mode, void* stream);
 
+/* The same sampler with reference boxes (Sec. 3.1.2: the decoder's
+ * references are the encoder's top-K boxes).  The paper gives no sampling
+ * rule; the one implemented takes the offsets relative to the box, as the
+ * deformable decoder with box references does:
+ *   ref     int32 [B, Q, 4]  (cx, cy, w, h), Q16 fractions of the map
+ *   offsets int16 [B, Q, heads, L, P, 2]  (x, y) in Q8 units of size / (2 P)
+ *   location = c + (off / 2^8) / P * size / 2, floored once in Q8 pixels:
+ *   X = floor((cx * 2^9 * P + off_x * w) * W_l / (2^17 * P)), likewise Y with
+ *   cy, h, H_l; then the nearest or bilinear rule of ilw_deform_attn.
+ * Other arguments, limits and errors as for ilw_deform_attn.
+ */
+int ilw_deform_attn_boxes(const int8_t* value, const int32_t* level_hw,
+                          const int32_t* level_start, int32_t L, int32_t P,
+                          const int32_t* ref, const int16_t* offsets, const int8_t* logits,
+                          int8_t* out, int32_t B, int32_t Q, int32_t heads, int32_t head_dim,
+                          int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
+                          int32_t mode, void* stream);
+
 /* ------------------------------------------------------------------------
  * I-ViT baseline operators, the forms that Constrained Shiftmax and
  * SD-ShiftGELU replace (for comparisons; same layouts as the operators
@@ -321,7 +339,7 @@ int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* ch
  *   y  = LN3(Res3(t2, fc2(GELU(fc1(t2)))))         FFN
  *   tgt int8 [batch, queries, dim]; memory int8 [batch, value_tokens, dim],
  *   the levels stacked as for ilw_deform_attn (level_hw, level_start: HOST
- *   int32 [levels][2], [levels]); ref int32 Q16 [batch, queries, 2];
+ *   int32 [levels][2], [levels]); ref int32 Q16 [batch, queries, ref_dims];
  *   y int8 [batch, queries, dim] (must not alias tgt).
  * The struct's arrays are DEVICE pointers.  head_dim = dim / heads in
  * {32, 64}; dim, ffn_dim, heads*levels*points multiples of 16; queries in
@@ -338,6 +356,7 @@ typedef struct {
   const int8_t* w_off; const int32_t* b_off; ilw_dyadic off;     /* [heads*levels*points*2, dim] */
   const int8_t* w_attw; const int32_t* b_attw; ilw_dyadic attw;  /* [heads*levels*points, dim]   */
   int32_t da_I0, da_s_d, da_out_mult, da_out_shift, da_mode;
+  int32_t ref_dims;  /* 2: ref holds points (ilw_deform_attn); 4: boxes (ilw_deform_attn_boxes) */
   const int8_t* w_co; const int32_t* b_co; ilw_dyadic co;        /* [dim, dim]   */
   int32_t res2_mult_a, res2_mult_b, res2_shift;
   const int32_t* ln2_beta; ilw_dyadic ln2_out;

@@ -316,7 +316,7 @@ bool ln_fusable(int32_t D) {
     const char* e = getenv("ILW_FUSE_LN");
     on = (e && e[0] == '0') ? 0 : 1;
   }
-  return on && (D == 192 || D == 384);
+  return on && (D == 192 || D == 256 || D == 384);
 }
 
 GemmArgs with_ln(GemmArgs a, const int32_t* beta, const ilw_dyadic& out, int32_t iters,
@@ -526,7 +526,6 @@ size_t encoder_workspace(const ilw_block_params* blocks, int32_t n_blocks,
 struct DecoderLayout {
   QkvLayout qkv;
   int8_t *att, *x, *t1, *t2, *v, *off8, *lg, *smp, *g;
-  int16_t* off16;
   size_t total;
 };
 
@@ -550,7 +549,6 @@ size_t decoder_layout(const ilw_decoder_params* p, int32_t batch, int32_t Q, int
   L.t2 = take(MQ * D);
   L.v = take(MS * D);
   L.off8 = take(MQ * NO);
-  L.off16 = (int16_t*)take(MQ * NO * 2);
   L.lg = take(MQ * NO / 2);
   L.smp = take(MQ * D);
   L.g = take(MQ * p->ffn_dim);
@@ -561,6 +559,8 @@ size_t decoder_layout(const ilw_decoder_params* p, int32_t batch, int32_t Q, int
 
 int check_decoder(const ilw_decoder_params* p, int32_t batch, int32_t Q, int32_t S) {
   REQUIRE(p, ILW_E_NULL, "decoder parameters must not be NULL");
+  REQUIRE(p->ref_dims == 2 || p->ref_dims == 4, ILW_E_PARAM,
+          "ref_dims = %d: references are points (2) or boxes (4)", p->ref_dims);
   REQUIRE(p->heads >= 1 && p->dim >= 16 && p->dim % p->heads == 0, ILW_E_SHAPE,
           "dim = %d must be a multiple of heads = %d", p->dim, p->heads);
   const int32_t hd = p->dim / p->heads;
@@ -953,12 +953,17 @@ int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* ch
   return hip_status(he, "ilw_split_conv");
 }
 
-int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
-                    int32_t L, int32_t P, const int32_t* ref, const int16_t* offsets,
-                    const int8_t* logits, int8_t* out, int32_t B, int32_t Q, int32_t heads,
-                    int32_t head_dim, int32_t I0, int32_t s_d, int32_t out_mult,
-                    int32_t out_shift, int32_t mode, void* stream) {
+namespace {
+// offsets: int16 Q8, or (offsets8 set) int8 values used as offsets8 << off_shift
+int deform_impl(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
+                int32_t L, int32_t P, const int32_t* ref, int32_t ref_dims,
+                const int16_t* offsets, const int8_t* logits, int8_t* out, int32_t B, int32_t Q,
+                int32_t heads, int32_t head_dim, int32_t I0, int32_t s_d, int32_t out_mult,
+                int32_t out_shift, int32_t mode, void* stream, const char* name,
+                const int8_t* offsets8 = nullptr, int32_t off_shift = 0) {
   REQUIRE(level_hw && level_start, ILW_E_NULL, "level_hw and level_start (host) required");
+  REQUIRE(ref_dims == 2 || ref_dims == 4, ILW_E_PARAM,
+          "ref_dims = %d: references are points (2) or boxes (4)", ref_dims);
   REQUIRE(L >= 1 && L <= kMaxLevels && P >= 1 && L * P <= 64, ILW_E_SHAPE,
           "L=%d P=%d invalid (L in [1, 8], L*P in [1, 64])", L, P);
   REQUIRE(B >= 0 && Q >= 0 && heads >= 1, ILW_E_SHAPE, "B=%d Q=%d heads=%d invalid", B, Q,
@@ -990,7 +995,7 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t*
   REQUIRE((groups * (head_dim / 4) + 255) / 256 < (int64_t)1 << 31, ILW_E_UNSUPPORTED,
           "too many queries");
   if (groups == 0) return ok();
-  REQUIRE(value && ref && offsets && logits && out, ILW_E_NULL,
+  REQUIRE(value && ref && (offsets || offsets8) && logits && out, ILW_E_NULL,
           "value, ref, offsets, logits and out must not be NULL");
   REQUIRE(((uintptr_t)value & 3) == 0 && ((uintptr_t)out & 3) == 0, ILW_E_PARAM,
           "value and out must be 4-byte aligned");
@@ -1011,10 +1016,35 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t*
   a.out_mult = out_mult;
   a.out_shift = out_shift;
   a.mode = mode;
+  a.ref_dims = ref_dims;
+  a.offs8 = offsets8;
+  a.off_shift = off_shift;
   StageTimer t(ILW_STAGE_DEFORM, (hipStream_t)stream);
   hipError_t he = launch_deform(a, (hipStream_t)stream);
   t.done();
-  return hip_status(he, "ilw_deform_attn");
+  return hip_status(he, name);
+}
+}  // namespace
+
+int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
+                    int32_t L, int32_t P, const int32_t* ref, const int16_t* offsets,
+                    const int8_t* logits, int8_t* out, int32_t B, int32_t Q, int32_t heads,
+                    int32_t head_dim, int32_t I0, int32_t s_d, int32_t out_mult,
+                    int32_t out_shift, int32_t mode, void* stream) {
+  return deform_impl(value, level_hw, level_start, L, P, ref, 2, offsets, logits, out, B, Q,
+                     heads, head_dim, I0, s_d, out_mult, out_shift, mode, stream,
+                     "ilw_deform_attn");
+}
+
+int ilw_deform_attn_boxes(const int8_t* value, const int32_t* level_hw,
+                          const int32_t* level_start, int32_t L, int32_t P,
+                          const int32_t* ref, const int16_t* offsets, const int8_t* logits,
+                          int8_t* out, int32_t B, int32_t Q, int32_t heads, int32_t head_dim,
+                          int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
+                          int32_t mode, void* stream) {
+  return deform_impl(value, level_hw, level_start, L, P, ref, 4, offsets, logits, out, B, Q,
+                     heads, head_dim, I0, s_d, out_mult, out_shift, mode, stream,
+                     "ilw_deform_attn_boxes");
 }
 
 size_t ilw_decoder_workspace_bytes(const ilw_decoder_params* p, int32_t batch,
@@ -1068,28 +1098,44 @@ int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8
   auto plain = [&](const GemmArgs& a) {
     run(ILW_STAGE_DECODER, [&] { return launch_gemm(EPI_STORE, a, s); });
   };
+  // residual add and post-norm LayerNorm: one GEMM with the LayerNorm in its
+  // epilogue where the tile can hold whole rows, else GEMM then LayerNorm
+  const bool fuse = ln_fusable(D);
+  auto resid_ln = [&](GemmArgs a, const int8_t* skip, int32_t ma, int32_t mb, int32_t sh,
+                      const int32_t* beta, const ilw_dyadic& d, int8_t* out) {
+    if (!fuse) {
+      resid(a, skip, ma, mb, sh);
+      ln(a.y, out, beta, d);
+      return;
+    }
+    a.resid = skip;
+    a.res_ma = ma;
+    a.res_mb = mb;
+    a.res_shift = sh;
+    run(ILW_STAGE_DECODER,
+        [&] { return launch_gemm(EPI_RESID_LN, with_ln(a, beta, d, p->ln_iters, out), s); });
+  };
 
   // self-attention over the queries (one global window per image)
   GemmArgs a = gemm_args(tgt, p->w_qkv, p->b_qkv, p->qkv, nullptr, MQ, 3 * D, D);
   a.qkv = L.qkv;
   run(ILW_STAGE_GEMM_QKV, [&] { return launch_gemm(EPI_QKV, a, s); });
   run(ILW_STAGE_ATTENTION, [&] { return launch_attention(attn_args(L.qkv, L.att, batch, p->attn), s); });
-  resid(gemm_args(L.att, p->w_o, p->b_o, p->o, L.x, MQ, D, D), tgt, p->res1_mult_a,
-        p->res1_mult_b, p->res1_shift);
-  ln(L.x, L.t1, p->ln1_beta, p->ln1_out);
+  resid_ln(gemm_args(L.att, p->w_o, p->b_o, p->o, L.x, MQ, D, D), tgt, p->res1_mult_a,
+           p->res1_mult_b, p->res1_shift, p->ln1_beta, p->ln1_out, L.t1);
   // cross-attention: value projection, offsets (int8 1/16 px -> Q8), weights
   plain(gemm_args(memory, p->w_val, p->b_val, p->val, L.v, MS, D, D));
   plain(gemm_args(L.t1, p->w_off, p->b_off, p->off, L.off8, MQ, NO, D));
-  run(ILW_STAGE_DECODER, [&] { return launch_widen(L.off8, L.off16, MQ * NO, 4, s); });
   plain(gemm_args(L.t1, p->w_attw, p->b_attw, p->attw, L.lg, MQ, NW, D));
   if (he != hipSuccess) return hip_status(he, "ilw_decoder_layer");
-  if ((e = ilw_deform_attn(L.v, level_hw, level_start, p->levels, p->points, ref, L.off16,
-                           L.lg, L.smp, batch, queries, H, hd, p->da_I0, p->da_s_d,
-                           p->da_out_mult, p->da_out_shift, p->da_mode, stream)))
+  // the sampler reads the int8 offsets (1/16 px) and widens them to Q8 itself
+  if ((e = deform_impl(L.v, level_hw, level_start, p->levels, p->points, ref, p->ref_dims,
+                       nullptr, L.lg, L.smp, batch, queries, H, hd, p->da_I0, p->da_s_d,
+                       p->da_out_mult, p->da_out_shift, p->da_mode, stream,
+                       "ilw_decoder_layer sampler", L.off8, 4)))
     return e;
-  resid(gemm_args(L.smp, p->w_co, p->b_co, p->co, L.x, MQ, D, D), L.t1, p->res2_mult_a,
-        p->res2_mult_b, p->res2_shift);
-  ln(L.x, L.t2, p->ln2_beta, p->ln2_out);
+  resid_ln(gemm_args(L.smp, p->w_co, p->b_co, p->co, L.x, MQ, D, D), L.t1, p->res2_mult_a,
+           p->res2_mult_b, p->res2_shift, p->ln2_beta, p->ln2_out, L.t2);
   // FFN
   a = gemm_args(L.t2, p->w_fc1, p->b_fc1, p->fc1, L.g, MQ, F, D);
   a.g_I0 = p->gelu_I0;
@@ -1098,9 +1144,8 @@ int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8
   a.g_mult = p->gelu_mult;
   a.g_shift = p->gelu_shift;
   run(ILW_STAGE_DECODER, [&] { return launch_gemm(EPI_GELU, a, s); });
-  resid(gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, L.x, MQ, D, F), L.t2, p->res3_mult_a,
-        p->res3_mult_b, p->res3_shift);
-  ln(L.x, y, p->ln3_beta, p->ln3_out);
+  resid_ln(gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, L.x, MQ, D, F), L.t2, p->res3_mult_a,
+           p->res3_mult_b, p->res3_shift, p->ln3_beta, p->ln3_out, y);
   return hip_status(he, "ilw_decoder_layer");
 }
 

@@ -390,7 +390,6 @@ hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                             const int32_t* beta, const int32_t* mult,
                             const int32_t* shift, int32_t nq, int32_t iters,
                             hipStream_t s);
-hipError_t launch_widen(const int8_t* x, int16_t* y, int64_t n, int32_t shift, hipStream_t s);
 hipError_t launch_shiftmax_ivit(const int8_t* x, int8_t* y, int64_t rows, int32_t cols,
                                int32_t I0, int32_t k_inter, int32_t k_out, int32_t M,
                                hipStream_t s);
@@ -417,6 +416,9 @@ struct DeformArgs {
   int32_t hw[kMaxLevels][2];
   int32_t start[kMaxLevels];
   int32_t I0, s_d, out_mult, out_shift, mode;
+  int32_t ref_dims;  // 2: reference points (x, y); 4: reference boxes (cx, cy, w, h)
+  const int8_t* offs8;  // when set, int8 offsets used as offs8 << off_shift instead of offs
+  int32_t off_shift;
 };
 hipError_t launch_deform(const DeformArgs& a, hipStream_t s);
 

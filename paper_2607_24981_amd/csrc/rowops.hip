@@ -346,16 +346,6 @@ __global__ __launch_bounds__(256) void gelu_kernel(const int8_t* x, int8_t* y, i
   if (blockIdx.x == 0 && t < n) y[t] = lut[(int32_t)x[t] + 128];
 }
 
-// ---------------------------------------------------------------- widen
-// y = int16(x) * 2^shift: the decoder's int8 sampling offsets (1/16 pixel)
-// to the sampler's Q8 pixels.
-__global__ __launch_bounds__(256) void widen_kernel(const int8_t* x, int16_t* y, int64_t n,
-                                                    int32_t shift) {
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride)
-    y[i] = (int16_t)((int32_t)x[i] * (1 << shift));
-}
-
 // ---------------------------------------------------------------- residual
 __global__ __launch_bounds__(256) void residual_kernel(const int8_t* a, const int8_t* b,
                                                        int8_t* y, int64_t n, int32_t ma,
@@ -460,13 +450,7 @@ hipError_t launch_shiftgelu_ivit(const int8_t* x, int8_t* y, int64_t rows, int32
   return hipGetLastError();
 }
 
-hipError_t launch_widen(const int8_t* x, int16_t* y, int64_t n, int32_t shift, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  int64_t g = (n + 255) / 256;
-  if (g > 4096) g = 4096;
-  hipLaunchKernelGGL(widen_kernel, dim3((unsigned)g), dim3(256), 0, s, x, y, n, shift);
-  return hipGetLastError();
-}
+
 
 hipError_t launch_gelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0, int32_t k_inter,
                        int32_t k_out, int32_t mult, int32_t shift, hipStream_t s) {

@@ -16,7 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 6
+ABI_VERSION = 7
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -64,7 +64,8 @@ class DecoderParams(ctypes.Structure):
         + [(n, c_i32) for n in ("res1_mult_a", "res1_mult_b", "res1_shift")]
         + [("ln1_beta", c_vp), ("ln1_out", Dyadic)]
         + _lin("val") + _lin("off") + _lin("attw")
-        + [(n, c_i32) for n in ("da_I0", "da_s_d", "da_out_mult", "da_out_shift", "da_mode")]
+        + [(n, c_i32) for n in ("da_I0", "da_s_d", "da_out_mult", "da_out_shift", "da_mode",
+                                "ref_dims")]
         + _lin("co")
         + [(n, c_i32) for n in ("res2_mult_a", "res2_mult_b", "res2_shift")]
         + [("ln2_beta", c_vp), ("ln2_out", Dyadic)]
@@ -113,6 +114,8 @@ _SIGS = {
                                         ctypes.POINTER(c_i32), c_i32]),
     "ilw_deform_attn": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp,
                                        c_vp] + [c_i32] * 9 + [c_vp]),
+    "ilw_deform_attn_boxes": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp,
+                                             c_vp] + [c_i32] * 9 + [c_vp]),
 }
 
 _LIB = None
@@ -420,6 +423,7 @@ class DeviceDecoder:
                   "res1_shift", "res2_mult_a", "res2_mult_b", "res2_shift", "res3_mult_a",
                   "res3_mult_b", "res3_shift"):
             setattr(s, n, int(p[n]))
+        s.ref_dims = int(p.get("ref_dims", 2))
         for stem in ("qkv", "o", "val", "off", "attw", "co", "fc1", "fc2"):
             setattr(s, "w_" + stem, self.t["w_" + stem].data_ptr())
             setattr(s, "b_" + stem, self.t["b_" + stem].data_ptr())
@@ -439,10 +443,14 @@ class DeviceDecoder:
 
 def ilw_decoder_layer(dec: DeviceDecoder, tgt, memory, ref, level_hw, level_start, y=None,
                       workspace=None):
-    """tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 [B, Q, 2];
-    level_hw / level_start host arrays -> int8 [B, Q, D]."""
+    """tgt int8 [B, Q, D], memory int8 [B, S, D], ref int32 [B, Q, 2] (points)
+    or [B, Q, 4] (boxes, as the layer's ref_dims says); level_hw / level_start
+    host arrays -> int8 [B, Q, D]."""
     B, Q, D = tgt.shape
     S = memory.shape[1]
+    rd = dec.struct.ref_dims
+    if tuple(ref.shape) != (B, Q, rd):
+        raise ValueError(f"ref has shape {tuple(ref.shape)}, expected {(B, Q, rd)}")
     L = dec.p["levels"]
     hw = np.ascontiguousarray(np.asarray(level_hw, np.int32).reshape(L, 2))
     st = np.ascontiguousarray(np.asarray(level_start, np.int32).reshape(L))
@@ -482,24 +490,41 @@ def ilw_split_conv(xs, ws, branch_mults, branch_shifts, bias, out_mult, out_shif
     return y
 
 
-def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
-                    out_shift, mode=0, s_d=-1, out=None):
-    """value int8 [B, S, H, Dh]; ref int32 [B, Q, 2]; offsets int16 [B, Q, H, L, P, 2];
-    logits int8 [B, Q, H, L*P]; level_hw / level_start are host arrays."""
+def _deform(entry, ref_dims, value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
+            out_shift, mode, s_d, out):
     B, S, H, Dh = value.shape
     _, Q, _, L, P, _ = offsets.shape
+    if tuple(ref.shape) != (B, Q, ref_dims):
+        raise ValueError(f"ref has shape {tuple(ref.shape)}, expected {(B, Q, ref_dims)}")
     hw = np.ascontiguousarray(np.asarray(level_hw, np.int32).reshape(L, 2))
     st = np.ascontiguousarray(np.asarray(level_start, np.int32).reshape(L))
     if out is None:
         out = torch.empty((B, Q, H * Dh), dtype=torch.int8, device=value.device)
-    rc = lib().ilw_deform_attn(_dev(value, torch.int8, "value"),
+    rc = getattr(lib(), entry)(_dev(value, torch.int8, "value"),
                                hw.ctypes.data_as(c_vp), st.ctypes.data_as(c_vp), L, P,
                                _dev(ref, torch.int32, "ref"),
                                _dev(offsets, torch.int16, "offsets"),
                                _dev(logits, torch.int8, "logits"), _dev(out, torch.int8, "out"),
                                B, Q, H, Dh, I0, s_d, out_mult, out_shift, mode, _stream())
-    _check(rc, "ilw_deform_attn")
+    _check(rc, entry)
     return out
+
+
+def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
+                    out_shift, mode=0, s_d=-1, out=None):
+    """value int8 [B, S, H, Dh]; ref int32 [B, Q, 2] (points); offsets int16
+    [B, Q, H, L, P, 2]; logits int8 [B, Q, H, L*P]; level_hw / level_start are
+    host arrays."""
+    return _deform("ilw_deform_attn", 2, value, level_hw, level_start, ref, offsets, logits,
+                   I0, out_mult, out_shift, mode, s_d, out)
+
+
+def ilw_deform_attn_boxes(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
+                          out_shift, mode=0, s_d=-1, out=None):
+    """As ilw_deform_attn with reference boxes: ref int32 [B, Q, 4]
+    (cx, cy, w, h), offsets in Q8 units of size / (2 P)."""
+    return _deform("ilw_deform_attn_boxes", 4, value, level_hw, level_start, ref, offsets,
+                   logits, I0, out_mult, out_shift, mode, s_d, out)
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",

@@ -543,6 +543,19 @@ def test_decoder_layer_c5(mode, B):
     assert_same(_decoder_gpu(*args), oracle.decoder_forward(*args), "decoder c5")
 
 
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("B,wl_name", [(2, "t"), (8, "decoder_q300_d256_b8")])
+def test_decoder_layer_boxes(mode, B, wl_name):
+    """The decoder layer with reference boxes (offsets relative to the box),
+    at a small shape and at the full 300-query layer."""
+    wl = (synth.DECODER_WORKLOADS[wl_name] if wl_name != "t" else
+          synth.DecoderWorkload("t", B, 37, 64, 2, 128, ((9, 13), (4, 6)), 4))
+    say(f"decoder boxes {wl.name} mode={mode} B={B}")
+    args = synth.decoder_inputs(wl, 31 + mode, batch=B, mode=mode, boxes=True)
+    assert args[3].shape[-1] == 4
+    assert_same(_decoder_gpu(*args), oracle.decoder_forward(*args), "decoder boxes")
+
+
 # ------------------------------------------------------------------ patch embedding
 def _patch_args(d):
     return (d["img"], d["w"], d["bias"], d["mult"], d["shift"], d["pos"], d["pos_mult_a"],
@@ -731,6 +744,73 @@ def test_deform_shapes(mode, s_d):
                                    dev(d["ref"]), dev(offs), dev(d["logits"]), 77, 1 << 30,
                                    30, mode, s_d=s_d))
     assert_same(got, ref, "deform small")
+
+
+def _deform_boxes_pair(d, offs, mode, s_d=-1, I0=None, m=None, sh=None):
+    I0 = d["I0"] if I0 is None else I0
+    m = d["out_mult"] if m is None else m
+    sh = d["out_shift"] if sh is None else sh
+    ref = oracle.deform_attn(d["value"], d["level_hw"], d["level_start"], d["ref"], offs,
+                             d["logits"], I0, m, sh, mode, s_d=s_d)
+    got = host(ilw.ilw_deform_attn_boxes(dev(d["value"]), d["level_hw"], d["level_start"],
+                                         dev(d["ref"]), dev(offs), dev(d["logits"]), I0, m, sh,
+                                         mode, s_d=s_d))
+    return got, ref
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_deform_boxes_c5_full(mode):
+    """The deformable workload (300 queries, 8 heads, 80^2/40^2/20^2, 4
+    points, batch 8) with reference boxes."""
+    wl = synth.DEFORM_WORKLOADS["deform_q300_d256_b8"]
+    say(f"{wl.name} boxes mode={mode}")
+    d = synth.deform_inputs(wl, 55, boxes=True)
+    got, ref = _deform_boxes_pair(d, d["offsets"], mode)
+    assert_same(got, ref, "deform boxes")
+    assert 0 < np.mean(np.abs(ref) == 127) < 0.5
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("P", [5, 4])
+def test_deform_boxes_shapes(mode, P):
+    """Odd level sizes, P not a power of two, zero offsets, offsets far
+    outside, boxes of every size from one pixel to the whole map."""
+    say(f"deform boxes small shapes mode={mode} P={P}")
+    wl = synth.DeformWorkload("small", 3, 7, 48, 3, 16, ((9, 13), (4, 6), (1, 1), (2, 3)), P)
+    d = synth.deform_inputs(wl, 12 + P, boxes=True)
+    d["ref"][0, :, 2:] = 1          # tiny boxes
+    d["ref"][1, :, 2:] = 65536      # boxes the size of the map
+    offs = d["offsets"].copy()
+    offs[0, 0] = 0
+    offs[2, 3] = 32767
+    offs[2, 4] = -32768
+    got, ref = _deform_boxes_pair(d, offs, mode, s_d=2 if mode else -1, I0=77, m=1 << 30,
+                                  sh=30)
+    assert_same(got, ref, "deform boxes small")
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("boxes", [False, True])
+@pytest.mark.parametrize("dh,levels,P", [(16, ((9, 13), (4, 6), (2, 3)), 3),   # 4 lanes, 3 samples each
+                                          (32, ((9, 13), (4, 6), (2, 3), (1, 1)), 8),  # 8 lanes, 4 each
+                                          (64, ((7, 5),), 1),                  # 16 lanes, 1 each
+                                          (256, ((6, 6), (3, 3)), 32),         # 64 lanes, 1 each
+                                          (8, ((5, 5),), 2),                   # 2 lanes: general kernel
+                                          (48, ((5, 4), (2, 2)), 3)])          # 12 lanes: general kernel
+def test_deform_lane_groups(mode, boxes, dh, levels, P):
+    """Every way the sampler splits a (query, head) over lanes."""
+    say(f"deform lane groups dh={dh} levels={levels} P={P} mode={mode} boxes={boxes}")
+    heads = 3 if dh < 256 else 1
+    wl = synth.DeformWorkload("g", 2, 11, dh * heads, heads, dh, levels, P)
+    d = synth.deform_inputs(wl, dh + P, boxes=boxes)
+    entry = ilw.ilw_deform_attn_boxes if boxes else ilw.ilw_deform_attn
+    ref = oracle.deform_attn(d["value"], d["level_hw"], d["level_start"], d["ref"],
+                             d["offsets"], d["logits"], d["I0"], d["out_mult"],
+                             d["out_shift"], mode)
+    got = host(entry(dev(d["value"]), d["level_hw"], d["level_start"], dev(d["ref"]),
+                     dev(d["offsets"]), dev(d["logits"]), d["I0"], d["out_mult"],
+                     d["out_shift"], mode))
+    assert_same(got, ref, "deform lane groups")
 
 
 def test_encoder_graph_replay():
