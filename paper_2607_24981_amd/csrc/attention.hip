@@ -376,9 +376,10 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, int64_t wg
   }
   if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, narrow, s);
   // Long rows: small grids spread a 32-row block over 16 waves so that every
-  // SIMD holds several (measured best of 16 or 32 rows over 4, 8 or 16 waves
-  // for 1600-token rows at batch 1).
-  if (wgs * 4 <= 2048) return launch_rows<32, 64, 16>(a, clampL, narrow, s);
+  // SIMD holds several, each wave normalizing its 2 rows together (measured
+  // best of 16 or 32 rows over 4, 8 or 16 waves for 1600-token rows at
+  // batch 1).
+  if (wgs * 4 <= 2048) return launch_rows<32, 32, 16, 16>(a, clampL, narrow, s);
   if constexpr (R == 32) return launch_rows<32, 32, 4, 16>(a, clampL, narrow, s);
   return launch_rows<R, 64, 4>(a, clampL, narrow, s);
 }
