@@ -257,7 +257,7 @@ ATTN_CASES = [
 
 
 @pytest.mark.parametrize("case", ATTN_CASES)
-@pytest.mark.parametrize("s_d", [-1, 4])
+@pytest.mark.parametrize("s_d", [-1, 4, 25])  # 25: past the FP64 normalization's range
 def test_attention(case, s_d):
     B, gh, gw, wh, ww, H = case
     say(f"attention B={B} grid={gh}x{gw} win={wh}x{ww} heads={H} s_d={s_d}")
