@@ -350,9 +350,9 @@ class Encoder:
             self._ws = torch.empty(max(need, 16), dtype=torch.int8, device=self.device)
         return self._ws
 
-    def forward(self, x, out=None):
+    def forward(self, x, out=None, workspace=None):
         """x int8 [B, T, D] -> int8 [B, T, D] (out may be x)."""
-        ws = self.workspace(x.shape[0])
+        ws = self.workspace(x.shape[0]) if workspace is None else workspace
         if out is None:
             out = torch.empty_like(x)
         rc = lib().ilw_encoder_forward(ctypes.addressof(self._structs), len(self.blocks),
@@ -362,6 +362,32 @@ class Encoder:
                                        _dev(ws, torch.int8, "workspace"), ws.numel(),
                                        _stream())
         _check(rc, "ilw_encoder_forward")
+        return out
+
+    def forward_streams(self, x, out, parts: int):
+        """The batch split into `parts` image ranges, each run on its own
+        stream (forked from and joined back into the current stream), so that
+        one part's attention shares the GPU with another part's linears.
+        Each part has its own workspace.  Capturable into a HIP graph."""
+        B = x.shape[0]
+        bounds = [B * i // parts for i in range(parts + 1)]
+        if getattr(self, "_part_streams", None) is None or len(self._part_streams) != parts:
+            self._part_streams = [torch.cuda.Stream(device=x.device) for _ in range(parts)]
+            self._part_ws = [None] * parts
+        cur = torch.cuda.current_stream(x.device)
+        for i, st in enumerate(self._part_streams):
+            nb = bounds[i + 1] - bounds[i]
+            need = max(self.workspace_bytes(nb), 16)
+            if self._part_ws[i] is None or self._part_ws[i].numel() < need:
+                self._part_ws[i] = torch.empty(need, dtype=torch.int8, device=x.device)
+            st.wait_stream(cur)
+        for i, st in enumerate(self._part_streams):
+            b0, b1 = bounds[i], bounds[i + 1]
+            if b1 > b0:
+                with torch.cuda.stream(st):
+                    self.forward(x[b0:b1], out[b0:b1], workspace=self._part_ws[i])
+        for st in self._part_streams:
+            cur.wait_stream(st)
         return out
 
 

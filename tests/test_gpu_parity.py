@@ -813,6 +813,37 @@ def test_deform_lane_groups(mode, boxes, dh, levels, P):
     assert_same(got, ref, "deform lane groups")
 
 
+@pytest.mark.parametrize("parts,B", [(2, 4), (2, 3), (3, 5)])
+def test_encoder_batch_split_streams(parts, B):
+    """The batch split over streams (forked from and joined back into the
+    capturing stream), captured into a HIP graph: every replay equals the
+    one-stream eager forward, uneven splits included."""
+    wl = synth.WORKLOADS["encoder_t1600_d192_b1"]
+    say(f"encoder batch split over {parts} streams, B={B}")
+    blocks, x = synth.encoder_inputs(wl, 8, "wide", batch=B)
+    enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
+    xd = dev(x)
+    ref = host(enc.forward(xd)).copy()
+    out = torch.empty_like(xd)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        enc.forward_streams(xd, out, parts)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    assert_same(host(out), ref, "eager split")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        enc.forward_streams(xd, out, parts)
+    for i in range(3):
+        out.fill_(0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert_same(host(out), ref, f"split replay {i}")
+        enc.forward(dev(x[::-1].copy()))  # eager work between replays
+        torch.cuda.synchronize()
+
+
 def test_encoder_graph_replay():
     """The benchmark captures the encoder forward into a HIP graph: every
     replay, interleaved with eager work and synchronizations, must reproduce
