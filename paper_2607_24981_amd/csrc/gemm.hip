@@ -4,12 +4,14 @@
 //
 //   y[m][n] = epilogue( rq(bias[n] + sum_k x[m][k] * w[n][k]; mult[n], shift[n]) )
 //
-// Tiling: each wave computes 64 channels x 64 tokens as 4 x 4 tiles of
-// v_mfma_i32_16x16x64_i8; a workgroup holds WN x WM waves.  Global loads of
-// the next K step are issued before the MFMAs of the current one; they are
-// unconditional (out-of-range rows are clamped onto valid ones and only feed
-// outputs that are never stored), which keeps the memory counters exact and
-// the loads in flight across the MFMAs.  The
+// Tiling: each wave computes FI x FJ tiles of v_mfma_i32_16x16x64_i8 (16
+// channels x 16 tokens each); a workgroup holds WN x WM waves.  Large grids
+// use 32 x 64 per wave, small grids (latency mode) 32 x 32 or 32/64 x 16 with
+// PF K steps of loads in flight.  Global loads of the next K step are issued
+// before the MFMAs of the current one; they are unconditional (out-of-range
+// rows are clamped onto valid ones and only feed outputs that are never
+// stored), which keeps the memory counters exact and the loads in flight
+// across the MFMAs.  The
 // weight tile is the MFMA A operand (rows = channels) and the activation tile
 // the B operand (columns = tokens), so each lane ends up holding four
 // consecutive channels of one token and stores them as one 32-bit word.  K
