@@ -84,7 +84,7 @@ def _edge_channels(N, fallback):
     return mult, shift, bias
 
 
-@pytest.mark.parametrize("M", [300, 40000])
+@pytest.mark.parametrize("M", [300, 40000, 120000])  # 120000: more tiles than fit at once
 @pytest.mark.parametrize("fallback", [False, True])
 def test_linear_requant_forms(M, fallback):
     """The epilogue's FP64 requantization at its edges, and tiles that fall
