@@ -232,6 +232,8 @@ def main():
     tops = ops / (wall_ms * 1e-3) / 1e12
     log(f"timed {args.steps} steps: {wall_ms:.4f} ms/step wall, {ev_ms:.4f} ms/step events, "
         f"{tops:.2f} TOPS, {B / (wall_ms * 1e-3):.1f} images/s")
+    spread = _step_spread(step)
+    log(f"single steps p10 / median / p90: {spread} ms")
     result = out.cpu().numpy()
 
     # per-stage kernel time, HIP events around each launch (eager pass, one
@@ -318,6 +320,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(wall_ms, 5),
+        "ms_per_step_p10_p50_p90": spread,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -358,6 +361,22 @@ def _timed(step, steps, warmup):
     return (t1 - t0) * 1e3 / steps, ev0.elapsed_time(ev1) / steps
 
 
+def _step_spread(step, n=50):
+    """p10 / median / p90 of single-step times: one HIP event between
+    consecutive steps (a pass of its own, after the timed region)."""
+    import numpy as np
+    import torch
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    evs[0].record()
+    for i in range(n):
+        step()
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    t = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(n)])
+    return [round(float(v), 5) for v in np.percentile(t, [10, 50, 90])]
+
+
 def bench_split(args, wl):
     """Stage three: the projector's scale-preserving split convolution."""
     import numpy as np
@@ -395,6 +414,7 @@ def bench_split(args, wl):
     tops = ops / (wall_ms * 1e-3) / 1e12
     log(f"timed {args.steps} steps: {wall_ms:.4f} ms/step wall, {ev_ms:.4f} ms/step events, "
         f"{tops:.2f} TOPS, {B / (wall_ms * 1e-3):.1f} images/s")
+    spread = _step_spread(step)
     result = y.cpu().numpy()
 
     ilw.profile_enable(True)
@@ -436,7 +456,8 @@ def bench_split(args, wl):
 
     line = {"metric": METRIC, "value": round(tops, 3), "unit": "TOPS",
             "images_per_s": round(B / (wall_ms * 1e-3), 2), "n_gpus": 1, "steps": args.steps,
-            "warmup": args.warmup, "ms_per_step": round(wall_ms, 5), "higher_is_better": True,
+            "warmup": args.warmup, "ms_per_step": round(wall_ms, 5),
+            "ms_per_step_p10_p50_p90": spread, "higher_is_better": True,
             "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
             "config": {"workload": wl.name, "batch": B, "tokens": wl.tokens,
                        "branches": list(wl.branches), "out_channels": wl.out,
@@ -486,6 +507,7 @@ def bench_decoder(args, wl):
     tops = ops / (wall_ms * 1e-3) / 1e12
     log(f"timed {args.steps} steps: {wall_ms:.4f} ms/step wall, {ev_ms:.4f} ms/step events, "
         f"{tops:.2f} TOPS, {B / (wall_ms * 1e-3):.1f} images/s")
+    spread = _step_spread(step)
     result = y.cpu().numpy()
 
     ilw.profile_enable(True)
@@ -555,7 +577,8 @@ def bench_decoder(args, wl):
 
     line = {"metric": METRIC, "value": round(tops, 3), "unit": "TOPS",
             "images_per_s": round(B / (wall_ms * 1e-3), 2), "n_gpus": 1, "steps": args.steps,
-            "warmup": args.warmup, "ms_per_step": round(wall_ms, 5), "higher_is_better": True,
+            "warmup": args.warmup, "ms_per_step": round(wall_ms, 5),
+            "ms_per_step_p10_p50_p90": spread, "higher_is_better": True,
             "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
             "config": {"workload": wl.name, "batch": B, "queries": Q, "dim": D, "heads": H,
                        "ffn_dim": F, "levels": [list(l) for l in wl.levels], "points": P,

@@ -30,7 +30,6 @@
 // (shift above 43, |bias| >= 2^21) take the integer form: the accumulator
 // clamped to a bound beyond which the result saturates, one 64-bit
 // multiply-add and one shift.
-#include <stdio.h>
 #include <stdlib.h>
 
 #include "ilw_internal.h"
@@ -568,22 +567,6 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       return launch_ln_tile<12, 1, 2, 4, 1>(a, s);  // 384 x 64 tokens, 12 waves of 32 x 64
     }
     return hipErrorInvalidValue;
-  }
-  // Tile override for tuning: ILW_GEMM_TILE=<WN>x<WM> (waves of 64 x 64
-  // along channels x tokens), read once.
-  static int ov_wn = -1, ov_wm = -1;
-  if (ov_wn < 0) {
-    const char* e = getenv("ILW_GEMM_TILE");
-    ov_wn = ov_wm = 0;
-    if (e && sscanf(e, "%dx%d", &ov_wn, &ov_wm) != 2) ov_wn = ov_wm = 0;
-  }
-  if (ov_wn > 0) {
-    if (ov_wn == 1 && ov_wm == 1) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
-    if (ov_wn == 1 && ov_wm == 4) return launch_tile<1, 4, 4, 4, 1>(epi, a, s);
-    if (ov_wn == 2 && ov_wm == 2) return launch_tile<2, 2, 4, 4, 1>(epi, a, s);
-    if (ov_wn == 2 && ov_wm == 4) return launch_tile<2, 4, 4, 4, 1>(epi, a, s);
-    if (ov_wn == 3 && ov_wm == 1) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
-    if (ov_wn == 3 && ov_wm == 2) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   }
   // Small grids: 64 x 64 workgroup tiles split over 4 waves of 32 x 32, with
   // the latency-mode pipeline.  Otherwise, from a sweep over the encoder

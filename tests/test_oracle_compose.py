@@ -103,6 +103,35 @@ def test_block_equals_operator_chain(orc, variant, win):
     assert np.array_equal(orc.block_forward(p, x[1:], 8, 8, *win), y[1:])
 
 
+def test_saturation_per_requant_point(orc):
+    """Saturation at every requantization point of the 256-token block: the
+    baseline distributions (shifts 30-38) saturate most linear outputs, the
+    wide variant (shifts 38-43) keeps each point mostly inside int8, so the
+    wide parity runs exercise the rounding of every requantization."""
+    wl = synth.WORKLOADS["block_t256_d192"]
+    frac = {}
+    for variant in ("baseline", "wide"):
+        blocks, x = synth.encoder_inputs(wl, 101, variant)
+        p, xb = blocks[0], x[0]
+        sat = lambda t: float(np.mean(np.abs(t.astype(np.int64)) == 127))
+        h = orc.int_layernorm(xb, p["ln1_beta"], p["ln1_mult"], p["ln1_shift"], p["ln_iters"])
+        qkv = orc.linear(h, p["w_qkv"], p["b_qkv"], p["qkv_mult"], p["qkv_shift"])
+        a = orc.attention(qkv, 16, 16, 0, 0, p["heads"], p["head_dim"], p["score_mult"],
+                          p["score_shift"], p["smax_I0"], p["pv_mult"], p["pv_shift"])
+        pr = orc.linear(a, p["w_proj"], p["b_proj"], p["proj_mult"], p["proj_shift"])
+        x1 = orc.residual_tensor(pr, xb, p["res1_mult_a"], p["res1_mult_b"], p["res1_shift"])
+        h2 = orc.int_layernorm(x1, p["ln2_beta"], p["ln2_mult"], p["ln2_shift"], p["ln_iters"])
+        f1 = orc.linear(h2, p["w_fc1"], p["b_fc1"], p["fc1_mult"], p["fc1_shift"])
+        g = orc.sdshiftgelu_tensor(f1, p["gelu_I0"], p["gelu_mult"], p["gelu_shift"])
+        f2 = orc.linear(g, p["w_fc2"], p["b_fc2"], p["fc2_mult"], p["fc2_shift"])
+        frac[variant] = {"LN1": sat(h), "QKV": sat(qkv), "attention": sat(a),
+                         "projection": sat(pr), "LN2": sat(h2), "fc1": sat(f1), "GELU": sat(g),
+                         "fc2": sat(f2)}
+    for point in ("QKV", "projection", "fc1", "fc2"):
+        assert frac["baseline"][point] > 0.5
+    assert all(v < 0.25 for v in frac["wide"].values()), frac["wide"]
+
+
 def test_block_wide_variant_is_not_saturated(orc):
     """The wide parity variant keeps most requantized values inside int8, so
     block parity exercises the rounding paths, not only saturation."""
