@@ -434,8 +434,10 @@ def _encoder_case(D, H, Hm, depth, seed, variant="wide"):
     # 192 and 384 channels: LayerNorm fused into the residual linears
     (192, 3, 768, (9, 12), [(3, 4), (0, 0), (9, 6)], 2),
     (384, 6, 1536, (7, 10), [(0, 0), (7, 5), (0, 0)], 3),
-    # 256 channels: stand-alone LayerNorm kernels
+    # 256 channels: fused as well (256-channel LayerNorm tiles)
     (256, 4, 512, (6, 6), [(3, 3), (0, 0)], 2),
+    # 128 channels: stand-alone LayerNorm kernels
+    (128, 2, 512, (6, 8), [(3, 4), (0, 0)], 2),
     # one block: no next block to fuse LN1 into
     (192, 3, 384, (8, 8), [(4, 4)], 1),
 ])
