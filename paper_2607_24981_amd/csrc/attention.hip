@@ -352,7 +352,10 @@ hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
 }
 
 template <int R, int LPR, int NW, int JW = 8>
-hipError_t launch_rows(const AttnArgs& a, int32_t clampL, bool narrow, hipStream_t s) {
+hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStream_t s) {
+  // A lane sums at most 4 JW ShiftExp values, each at most emax = ShiftExp(0)
+  // = I0 * 2^k_inter: 32-bit partial sums are exact while 4 JW emax < 2^32.
+  const bool narrow = emax * 4 * JW < ((int64_t)1 << 32);
   const bool ragged = (a.Tw & 3) != 0;
   if (narrow) {
     return ragged ? launch_variant<R, LPR, true, true, NW, JW>(a, clampL, s)
@@ -363,7 +366,7 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, bool narrow, hipStream
 }
 
 template <int R>
-hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, int64_t wgs,
+hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t wgs,
                       hipStream_t s) {
   // Rows per wave: a lane holds JW words (4 JW scores) of its row, and the
   // LPR lanes of a row combine their sums in log2(LPR) shuffle steps.  With
@@ -371,17 +374,17 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, bool narrow, int64_t wg
   // (long rows) at a time overlaps the rows' serial sum-shuffle-divide
   // chains (measured against one row group of 16 or 64 lanes).
   if (a.Twp <= 512) {
-    if constexpr (R == 32) return launch_rows<32, 8, 4, 16>(a, clampL, narrow, s);
-    return launch_rows<R, 16, 4>(a, clampL, narrow, s);
+    if constexpr (R == 32) return launch_rows<32, 8, 4, 16>(a, clampL, emax, s);
+    return launch_rows<R, 16, 4>(a, clampL, emax, s);
   }
-  if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, narrow, s);
+  if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, emax, s);
   // Long rows: small grids spread a 32-row block over 16 waves so that every
   // SIMD holds several, each wave normalizing its 2 rows together (measured
   // best of 16 or 32 rows over 4, 8 or 16 waves for 1600-token rows at
   // batch 1).
-  if (wgs * 4 <= 2048) return launch_rows<32, 32, 16, 16>(a, clampL, narrow, s);
-  if constexpr (R == 32) return launch_rows<32, 32, 4, 16>(a, clampL, narrow, s);
-  return launch_rows<R, 64, 4>(a, clampL, narrow, s);
+  if (wgs * 4 <= 2048) return launch_rows<32, 32, 16, 16>(a, clampL, emax, s);
+  if constexpr (R == 32) return launch_rows<32, 32, 4, 16>(a, clampL, emax, s);
+  return launch_rows<R, 64, 4>(a, clampL, emax, s);
 }
 
 }  // namespace
@@ -394,9 +397,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int64_t am = a.score_mult < 0 ? -(int64_t)a.score_mult : (int64_t)a.score_mult;
   int64_t L = am == 0 ? 1 : (129 * ((int64_t)1 << a.score_shift)) / am + 1;
   if (L > ((int64_t)1 << 30)) L = (int64_t)1 << 30;
-  // A lane sums at most 32 ShiftExp values: 32-bit partial sums are exact
-  // while I0 * 2^k_inter < 2^27.
-  const bool narrow = ((int64_t)a.I0 << a.k_inter) < ((int64_t)1 << 27);
+  const int64_t emax = (int64_t)a.I0 << a.k_inter;  // ShiftExp(0), the largest value
   // FP64 score requantization: exact for s <= 43, and |acc| <= 2^20 keeps
   // |acc * m / 2^s| + 257 inside the int32 conversion.
   AttnArgs b = a;
@@ -405,8 +406,8 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   // fewer than two workgroups per CU.
   const int64_t wg32 = (int64_t)((a.Tw + 31) / 32) * a.H * a.B * a.nW;
   const int64_t wg16 = (int64_t)((a.Tw + 15) / 16) * a.H * a.B * a.nW;
-  if (wg32 < 512) return launch_lpr<16>(b, (int32_t)L, narrow, wg16, s);
-  return launch_lpr<32>(b, (int32_t)L, narrow, wg32, s);
+  if (wg32 < 512) return launch_lpr<16>(b, (int32_t)L, emax, wg16, s);
+  return launch_lpr<32>(b, (int32_t)L, emax, wg32, s);
 }
 
 hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,

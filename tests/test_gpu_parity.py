@@ -326,6 +326,33 @@ def test_attention_head_dim_32(case):
     assert_same(got, ref, "attention hd32")
 
 
+@pytest.mark.parametrize("case", [(4, 40, 40, 20, 20, 3), (1, 40, 40, 0, 0, 3),
+                                  (4, 40, 40, 0, 0, 3)])
+@pytest.mark.parametrize("I0", [1023, 1500, 2047])
+@pytest.mark.parametrize("zero_q", [False, True])
+def test_attention_large_I0(case, I0, zero_q):
+    """Large ShiftExp scales (ShiftExp(0) = I0 * 2^16 up to 2^27) on the
+    variants whose lanes sum up to 64 values of a row (32-row blocks of
+    400-token windows; 1600-token rows on small and large grids): 32-bit
+    partial sums are exact only up to I0 = 1023.  Zero queries make every
+    score equal, so every value is ShiftExp(0)."""
+    B, gh, gw, wh, ww, H = case
+    say(f"attention large I0={I0} zero_q={zero_q} B={B} grid={gh}x{gw} win={wh}x{ww}")
+    g = rng(I0 + gh * wh + B)
+    D, T = 64 * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    if zero_q:
+        qkv[:, :, :D] = 0
+    p = {"score_mult": int(g.integers(2 ** 29, 2 ** 30)), "score_shift": 39,
+         "smax_I0": I0, "smax_s_d": -1,
+         "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 36}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, wh, ww, H, 64, p["score_mult"],
+                                     p["score_shift"], I0, p["pv_mult"], p["pv_shift"])
+                    for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
+    assert_same(got, ref, "attention large I0")
+
+
 # ------------------------------------------------------------------ encoder block
 @pytest.mark.parametrize("variant", ["wide", "baseline"])
 def test_block_c1(variant):
