@@ -139,7 +139,9 @@ void orc_shiftmax_row(const int32_t* x, int32_t d, int32_t I0, int32_t k_inter,
 
   int32_t s_d = s_d_static >= 0 ? s_d_static
                                 : orc_calibrate_shift(S_sum, m_p, M_hw);
-  orc_require(s_d >= 0 && s_d <= 40, "s_d in [0, 40]");
+  /* CalibrateShift puts no upper limit on s_d (S_sum < 2^63 and m_p <= 31
+   * keep it below 64); every shift below is taken in __int128. */
+  orc_require(s_d >= 0 && s_d <= 90, "s_d in [0, 90]");
 
   /* quotient-remainder accumulation of the shifted denominator */
   int64_t sum_Q = 0, sum_r = 0;

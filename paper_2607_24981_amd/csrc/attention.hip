@@ -223,7 +223,9 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
       uint64_t sr = sum >> sd;
       sr = sr < 1 ? 1 : (sr > 0x7fffffffull ? 0x7fffffffull : sr);
       const uint32_t F = div_2p31m1((uint32_t)sr);
-      const int32_t sh = 32 - a.k_out + sd;
+      // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63, so
+      // the cap keeps the 64-bit shift defined (large m_p gives s_d up to 41)
+      const int32_t sh = min(32 - a.k_out + sd, 63);
 #pragma unroll
       for (int j = 0; j < JW; ++j) {
         const int32_t wd = k + j * LPR;

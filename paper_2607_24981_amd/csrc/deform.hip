@@ -48,7 +48,9 @@ __global__ __launch_bounds__(256) void deform_kernel(DeformArgs a) {
   for (int32_t i = 0; i < LP; ++i) sum += (uint32_t)elut[m - lg[i]];
   const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, 4);
   const uint32_t F = shiftmax_factor(sum, sd);
-  const int32_t sh = 24 + sd;  // 32 - k_out with k_out = 8
+  // 32 - k_out with k_out = 8; s_d <= 31 (static) or <= 9 (at most 64 values
+  // below 2^30 with m_p = 4) keeps the shift below 64
+  const int32_t sh = 24 + sd;
 
   const bool box = a.ref_dims == 4;
   const int32_t* r = a.ref + bq * a.ref_dims;
@@ -190,7 +192,9 @@ __global__ __launch_bounds__(256) void deform_group_kernel(DeformArgs a) {
   }
   const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, 4);
   const uint32_t F = shiftmax_factor(sum, sd);
-  const int32_t sh = 24 + sd;  // 32 - k_out with k_out = 8
+  // 32 - k_out with k_out = 8; s_d <= 31 (static) or <= 9 (at most 64 values
+  // below 2^30 with m_p = 4) keeps the shift below 64
+  const int32_t sh = 24 + sd;
 
   const bool box = a.ref_dims == 4;
   const int32_t* r = a.ref + bq * a.ref_dims;

@@ -253,7 +253,9 @@ __global__ __launch_bounds__(256) void shiftmax_kernel(const int8_t* x, int8_t* 
   sum = wave_sum_u64(sum);
   const int32_t sd = s_d >= 0 ? s_d : calibrate_shift(sum, m_p);
   const uint32_t F = shiftmax_factor(sum, sd);
-  const int32_t sh = 32 - k_out + sd;
+  // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63, so the cap
+  // keeps the 64-bit shift defined (long rows with large m_p: s_d up to 61)
+  const int32_t sh = min(32 - k_out + sd, 63);
   const uint64_t cap = (1u << (k_out - 1)) - 1;
   for (int32_t j = lane; j < cols; j += 64) {
     uint64_t p = ((uint64_t)(uint32_t)elut[m - xr[j]] * F) >> sh;

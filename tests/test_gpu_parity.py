@@ -142,6 +142,21 @@ def test_shiftmax_params(s_d, k_out, k_inter, m_p):
         assert_same(got, ref, f"shiftmax I0={I0}")
 
 
+@pytest.mark.parametrize("rows,cols", [(16, 20), (8, 40), (8, 1100), (4, 5000)])
+@pytest.mark.parametrize("m_p", [24, 31])
+def test_shiftmax_large_m_p(rows, cols, m_p):
+    """A large headroom m_p with I0 = 16383 (ShiftExp(0) near 2^30): the
+    dynamic s_d = M_req + m_p - 31 reaches 35 to 44, so the output shift
+    32 - k_out + s_d runs past 64 bits on the longer rows."""
+    say(f"shiftmax large m_p={m_p} rows={rows} cols={cols}")
+    g = rng(cols + m_p)
+    x = g.integers(-128, 128, (rows, cols)).astype(np.int8)
+    x[0, :] = 7
+    ref = oracle.shiftmax_rows(x, 16383, m_p=m_p)
+    got = host(ilw.ilw_shiftmax(dev(x), 16383, m_p=m_p))
+    assert_same(got, ref, "shiftmax large m_p")
+
+
 def test_shiftmax_in_place():
     say("shiftmax in place")
     x = synth.int8_tensor(9, (40, 333))
@@ -324,6 +339,27 @@ def test_attention_head_dim_32(case):
                                      p["pv_shift"]) for b in range(B)])
     got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
     assert_same(got, ref, "attention hd32")
+
+
+@pytest.mark.parametrize("case", [(1, 40, 40, 0, 0, 1), (2, 40, 40, 20, 20, 1),
+                                  (1, 6, 10, 3, 5, 1)])
+def test_attention_large_m_p(case):
+    """m_p = 31 with I0 = 16383: s_d reaches 41 on 1600-token rows, past the
+    64-bit range of the output shift."""
+    B, gh, gw, wh, ww, H = case
+    say(f"attention m_p=31 I0=16383 B={B} grid={gh}x{gw} win={wh}x{ww}")
+    g = rng(gh * gw + wh)
+    D, T = 64 * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    qkv[:, : T // 2, :D] = 0  # rows of equal scores beside random ones
+    p = {"score_mult": int(g.integers(2 ** 29, 2 ** 30)), "score_shift": 39,
+         "smax_I0": 16383, "smax_m_p": 31, "smax_s_d": -1,
+         "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 30}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, wh, ww, H, 64, p["score_mult"],
+                                     p["score_shift"], 16383, p["pv_mult"], p["pv_shift"],
+                                     m_p=31) for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
+    assert_same(got, ref, "attention large m_p")
 
 
 @pytest.mark.parametrize("case", [(4, 40, 40, 20, 20, 3), (1, 40, 40, 0, 0, 3),

@@ -238,6 +238,32 @@ def test_shiftmax_uniform_rows_closed_form(orc):
             assert math.floor(128 / d) - 1 <= out[0] <= math.floor(128 / d)
 
 
+def test_shiftmax_large_sd_closed_form(orc):
+    """A large headroom m_p makes CalibrateShift's s_d = M_req + m_p - 31
+    (Alg. 2) large.  With I0 = 16383 every I_exp is below 2^30 and F below
+    2^31, so from s_d = 37 on (k_out = 8, output shift 24 + s_d >= 61) every
+    output is 0; when S_sum >> s_d is 0 or 1 the clamp makes S_R = 1 and
+    F = 2^31 - 1 exactly."""
+    I0 = 16383
+    seen = set()
+    for d, m_p in ((20, 31), (40, 31), (300, 31), (1100, 31), (1600, 31), (3000, 30)):
+        x = np.zeros(d, np.int64)
+        x[::7] = -3
+        x[1::5] = -100
+        out, (S_sum, s_d, S_R, F) = orc.shiftmax_row(x, I0, m_p=m_p)
+        e = [orc.shiftexp(int(v), I0, 16) for v in x]  # the row maximum is 0
+        assert S_sum == sum(e) and max(e) < 2 ** 30
+        assert s_d == max((S_sum - 1).bit_length() + m_p - 31, 0)
+        seen.add(s_d)
+        if S_sum >> s_d <= 1:
+            assert S_R == 1 and F == 2 ** 31 - 1
+        if s_d >= 37:
+            assert not out.any()
+        else:
+            assert out.any()
+    assert max(seen) >= 41 and min(seen) <= 36
+
+
 def test_shiftmax_reduces_to_ivit_when_sd_zero(orc):
     """With s_d = 0 and S_sum within 31 bits the constrained form is the fixed
     M = 31 Shiftmax of I-ViT (eq. shiftmax_original), written here with exact
