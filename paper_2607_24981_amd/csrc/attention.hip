@@ -24,29 +24,26 @@
 namespace ilw {
 namespace {
 
-// Score requantization with a pre-clamped accumulator: clamping to [-L, L]
-// keeps every saturated result saturated and keeps the shifted value inside
-// int32, so the exact result is one 64-bit multiply-add, one 64-bit shift
-// and a clamp.
+// Score requantization, stored biased: the result is q + 128 in [1, 255]
+// (q in [-127, 127]).  c = 2^(s-1) + 128 * 2^s, so
+//   floor((acc * m + c) / 2^s) = floor((acc * m + 2^(s-1)) / 2^s) + 128,
+// exact in 64 bits (|acc| <= 64 * 128 * 128 = 2^20 for a 64-channel head,
+// |m| < 2^31 and s <= 54).  The host checks that this value always fits in
+// int32 (always true for s >= 32); then the low word of the 64-bit shift is
+// the value itself and one clamp finishes the job.
+__device__ __forceinline__ int32_t rq_fast(int32_t acc, int32_t mult, int64_t c, int32_t shift) {
+  const int64_t v = ((int64_t)acc * mult + c) >> shift;
+  return min(max((int32_t)v, 128 + kQmin), 128 + kQmax);
+}
+
+// Otherwise (any s up to 62) the accumulator is clamped to [-L, L] first:
+// that keeps every saturated result saturated and the shifted value inside
+// int32; rnd = 2^(s-1) and the bias is added after the shift.
 __device__ __forceinline__ int32_t rq_clamped(int32_t acc, int32_t L, int32_t mult,
                                               int64_t rnd, int32_t shift) {
   acc = min(max(acc, -L), L);
   const int64_t v = ((int64_t)acc * mult + rnd) >> shift;
-  return min(max((int32_t)v, kQmin), kQmax);
-}
-
-// The same requantization in FP64, offset by 256 (the result is q + 256, in
-// [129, 383]; its low byte is q's).  |acc| <= 64 * 128 * 128 = 2^20 for a
-// 64-channel head, so for |acc * m / 2^s| < 2^9 the product acc * m is an
-// integer below 2^(s+9) and acc * m / 2^s + 256.5 is a multiple of 2^-s
-// below 2^10: exact in one FMA when s <= 43.  Past that range the rounded
-// value stays on the saturated side of 129 or 384 (rounding is monotone and
-// both bounds are representable), and truncation is the floor because the
-// unsaturated values are positive.  The host checks s <= 43 and that the
-// value cannot overflow the integer conversion.
-__device__ __forceinline__ int32_t rq_f64(int32_t acc, double scale) {
-  const double y = __builtin_fma((double)acc, scale, 256.5);
-  return min(max((int32_t)y, 256 + kQmin), 256 + kQmax);
+  return min(max((int32_t)v, kQmin), kQmax) + 128;
 }
 
 // Bytes 0 of a, b, c, d packed into one word (a in the low byte).
@@ -109,23 +106,21 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 
   // ---- phase 1: scores.  Waves split the keys in blocks of 16; the key
   // fragment is the A operand, so a lane holds 4 consecutive keys of one row.
-  // The FP64 requantization (when the host found it exact) yields scores
-  // offset by 256; the maxima are corrected at the end.
+  // Scores and row maxima are kept biased (q + 128).
   const v4i zero = {0, 0, 0, 0};
   const int32_t sm = a.score_mult, ss = a.score_shift;
   const int64_t srnd = (int64_t)1 << (ss - 1);
-  const double sscale = __builtin_ldexp((double)sm, -ss);
-  const int32_t moff = a.f64rq ? 256 : 0;
+  const int64_t sc = srnd + (a.rq_fast ? (int64_t)128 << ss : 0);  // s <= 54 when fast
   int32_t mx[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) mx[f] = -128 + moff;
+  for (int f = 0; f < NF; ++f) mx[f] = 0;
   const int32_t nkb = (Tw + 15) >> 4;
   const int32_t kc = (lane >> 4) * 4;  // first of this lane's 4 keys in a block
   auto kload = [&](int32_t kb) {
     const int32_t key = min(kb * 16 + (lane & 15), Tw - 1);
     return *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
   };
-  auto phase1 = [&](auto f64) {
+  auto phase1 = [&](auto fast) {
     auto scores = [&](int32_t kb, const v4i& kf) {
       const int32_t col = kb * 16 + kc;
 #pragma unroll
@@ -134,8 +129,8 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
         int32_t v[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          v[r] = decltype(f64)::value ? rq_f64(s[r], sscale)
-                                      : rq_clamped(s[r], clampL, sm, srnd, ss);
+          v[r] = decltype(fast)::value ? rq_fast(s[r], sm, sc, ss)
+                                       : rq_clamped(s[r], clampL, sm, srnd, ss);
         // keys past the window repeat the last key (clamped rows), so they
         // never raise the maximum
         mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
@@ -162,7 +157,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
       k3 = kload(kb + 7 * NW);
     }
   };
-  if (a.f64rq)
+  if (a.rq_fast)
     phase1(Flag<true>{});
   else
     phase1(Flag<false>{});
@@ -171,7 +166,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   for (int f = 0; f < NF; ++f) {
     mx[f] = max(mx[f], __shfl_xor(mx[f], 16, 64));
     mx[f] = max(mx[f], __shfl_xor(mx[f], 32, 64));
-    if (lane < 16) pmax[wave][f * 16 + lane] = mx[f] - moff;
+    if (lane < 16) pmax[wave][f * 16 + lane] = mx[f];
   }
   __syncthreads();
 
@@ -180,7 +175,8 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   // registers between the sum and the normalization.
   {
     constexpr int RG = 64 / LPR;   // rows processed together by one wave
-    // JW words per lane: Twp / 4 <= JW * LPR
+    // JW words per lane: Twp / 4 <= JW * LPR (the host picks the smallest
+    // JW it has for the window)
     const int sub = lane / LPR, k = lane % LPR;
     const int32_t nword = Twp >> 2;
     const int32_t pcap = (1 << (a.k_out - 1)) - 1;
@@ -191,7 +187,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
       int32_t m = pmax[0][rr];
 #pragma unroll
       for (int w = 1; w < NW; ++w) m = max(m, pmax[w][rr]);
-      const uint32_t m4 = (uint32_t)(m + 128) * 0x01010101u;
+      const uint32_t m4 = (uint32_t)m * 0x01010101u;  // biased maximum per byte
       uint32_t e[JW][4];
       uint64_t sum = 0;
       uint32_t sum32 = 0;
@@ -199,10 +195,10 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
       for (int j = 0; j < JW; ++j) {
         const int32_t wd = k + j * LPR;
         const uint32_t word = row[min(wd, nword - 1)];  // always inside the row
-        // max - score per byte: every valid byte is >= 0, and a borrow from
-        // an invalid (higher) byte never reaches a valid one.  Words past the
-        // window index table entry 255, which is 0.
-        uint32_t d4 = m4 - (word ^ 0x80808080u);
+        // max - score per byte (both biased): every valid byte is >= 0, and a
+        // borrow from an invalid (higher) byte never reaches a valid one.
+        // Words past the window index table entry 255, which is 0.
+        uint32_t d4 = m4 - word;
         if (!RAGGED) d4 = wd * 4 < Tw ? d4 : 0xffffffffu;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
@@ -367,6 +363,17 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStrea
                 : launch_variant<R, LPR, false, false, NW, JW>(a, clampL, s);
 }
 
+// The 16-word variants with the smallest word count the window needs: 13
+// words cover 1600-token rows over 32 lanes, 14 the 448-byte padded
+// 400-token rows over 8 lanes.
+template <int R, int LPR, int NW>
+hipError_t launch_fit16(const AttnArgs& a, int32_t clampL, int64_t emax, hipStream_t s) {
+  const int32_t jw = ((a.Twp >> 2) + LPR - 1) / LPR;
+  if (jw <= 13) return launch_rows<R, LPR, NW, 13>(a, clampL, emax, s);
+  if (jw == 14) return launch_rows<R, LPR, NW, 14>(a, clampL, emax, s);
+  return launch_rows<R, LPR, NW, 16>(a, clampL, emax, s);
+}
+
 template <int R>
 hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t wgs,
                       hipStream_t s) {
@@ -376,7 +383,7 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t w
   // (long rows) at a time overlaps the rows' serial sum-shuffle-divide
   // chains (measured against one row group of 16 or 64 lanes).
   if (a.Twp <= 512) {
-    if constexpr (R == 32) return launch_rows<32, 8, 4, 16>(a, clampL, emax, s);
+    if constexpr (R == 32) return launch_fit16<32, 8, 4>(a, clampL, emax, s);
     return launch_rows<R, 16, 4>(a, clampL, emax, s);
   }
   if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, emax, s);
@@ -384,8 +391,8 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t w
   // SIMD holds several, each wave normalizing its 2 rows together (measured
   // best of 16 or 32 rows over 4, 8 or 16 waves for 1600-token rows at
   // batch 1).
-  if (wgs * 4 <= 2048) return launch_rows<32, 32, 16, 16>(a, clampL, emax, s);
-  if constexpr (R == 32) return launch_rows<32, 32, 4, 16>(a, clampL, emax, s);
+  if (wgs * 4 <= 2048) return launch_fit16<32, 32, 16>(a, clampL, emax, s);
+  if constexpr (R == 32) return launch_fit16<32, 32, 4>(a, clampL, emax, s);
   return launch_rows<R, 64, 4>(a, clampL, emax, s);
 }
 
@@ -400,10 +407,12 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   int64_t L = am == 0 ? 1 : (129 * ((int64_t)1 << a.score_shift)) / am + 1;
   if (L > ((int64_t)1 << 30)) L = (int64_t)1 << 30;
   const int64_t emax = (int64_t)a.I0 << a.k_inter;  // ShiftExp(0), the largest value
-  // FP64 score requantization: exact for s <= 43, and |acc| <= 2^20 keeps
-  // |acc * m / 2^s| + 257 inside the int32 conversion.
+  // The unclamped score form: |acc| <= 2^20 keeps the 64-bit value below
+  // 2^62 for s <= 54, and the shifted value (below 2^51 / 2^s + 129) inside
+  // int32 for s >= 32, or for smaller s when |m| 2^20 / 2^s is small enough.
   AttnArgs b = a;
-  b.f64rq = a.score_shift <= 43 && ((am << 20) >> a.score_shift) + 257 < ((int64_t)1 << 31);
+  b.rq_fast = a.score_shift <= 54 &&
+              (a.score_shift >= 32 || ((am << 20) >> a.score_shift) + 257 < ((int64_t)1 << 31));
   // Fill the chip: fall back to 16-row blocks when 32-row blocks would give
   // fewer than two workgroups per CU.
   const int64_t wg32 = (int64_t)((a.Tw + 31) / 32) * a.H * a.B * a.nW;

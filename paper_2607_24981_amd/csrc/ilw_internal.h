@@ -380,7 +380,7 @@ struct AttnArgs {
   int32_t B, T, D, H, grid_w, win_h, win_w, nwx, nW, Tw, Twp;
   int32_t score_mult, score_shift, I0, k_inter, k_out, m_p, s_d, pv_mult, pv_shift;
   int32_t hd;        // head dimension: 32 or 64
-  int32_t f64rq;     // set by launch_attention: score requantization in FP64 is exact
+  int32_t rq_fast;   // set by launch_attention: the score shift cannot overflow int32
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 hipError_t launch_qkv_relayout(const int8_t* qkv, int32_t B, const QkvLayout& L,

@@ -290,17 +290,21 @@ def test_attention(case, s_d):
     assert_same(got, ref, "attention")
 
 
-# (score_mult, score_shift): the FP64 score requantization covers shifts up
-# to 43 when |acc * m / 2^s| stays inside int32 (|acc| <= 2^20); the rest
-# take the 64-bit integer path.
+# (score_mult, score_shift): the unclamped score form covers shifts 32..54,
+# and smaller shifts when |acc * m / 2^s| stays inside int32 (|acc| <= 2^20);
+# the rest clamp the accumulator first.
 SCORE_RQ = [
-    (1, 13),                      # FP64: acc / 2^13, exact ties at acc = 4096 mod 8192
-    ((1 << 30) - 12345, 43),      # FP64 at its largest shift
-    (-((1 << 29) + 5), 40),       # FP64, negative scale
-    ((1 << 20) + 7, 22),          # FP64, mostly saturated
-    ((1 << 30) + 1, 44),          # integer path: shift past 43
-    ((1 << 31) - 1, 50),          # integer path: every score rounds to 0
-    (1 << 30, 12),                # integer path: the FP64 value would overflow int32
+    (1, 13),                      # unclamped: acc / 2^13, exact ties at acc = 4096 mod 8192
+    ((1 << 30) - 12345, 43),      # unclamped, shift >= 32
+    (-((1 << 29) + 5), 40),       # unclamped, negative scale
+    ((1 << 20) + 7, 22),          # unclamped below 32, mostly saturated
+    ((1 << 30) + 1, 31),          # unclamped at the largest shift below 32
+    ((1 << 30) + 1, 44),          # unclamped
+    ((1 << 31) - 1, 54),          # unclamped at its largest shift: every score rounds to 0
+    ((1 << 31) - 1, 32),          # unclamped at shift 32, mostly saturated
+    (-((1 << 31) - 1), 55),       # clamped: past 54
+    ((1 << 31) - 1, 62),          # clamped at the largest shift
+    (1 << 30, 12),                # clamped: the shifted value would overflow int32
 ]
 
 
