@@ -24,6 +24,8 @@
 namespace ilw {
 namespace {
 
+constexpr int kXcds = 8;  // accelerator complex dies, each with its own L2
+
 // Score requantization, stored biased: the result is q + 128 in [1, 255]
 // (q in [-127, 127]).  c = 2^(s-1) + 128 * 2^s, so
 //   floor((acc * m + c) / 2^s) = floor((acc * m + 2^(s-1)) / 2^s) + 128,
@@ -69,7 +71,8 @@ __device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
 // key range) pairs for P V, whose int32 partial sums are added through LDS.
 template <int R, int LPR, bool NARROW, bool RAGGED, int NW, int JW>
 __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t lds_row,
-                                                            int32_t clampL) {
+                                                            int32_t clampL, int32_t nrb,
+                                                            int64_t ntiles) {
   extern __shared__ __attribute__((aligned(16))) int8_t sS[];  // [R][lds_row]
   __shared__ uint32_t elut[256];
   __shared__ int32_t pmax[NW][R];
@@ -80,9 +83,16 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int32_t Tw = a.Tw, Twp = a.Twp;
-  const int32_t i0 = blockIdx.x * R;
-  const int32_t h = blockIdx.y;
-  const int32_t bw = blockIdx.z;  // image * nW + window
+  // Workgroups go to the 8 XCDs round-robin; XCD x takes the contiguous
+  // tiles x * per + min(x, rem) + ..., so the row blocks of one (window,
+  // head) share one XCD's L2 for their keys and values.
+  const int64_t bid = blockIdx.x;
+  const int64_t per = ntiles / kXcds, rem = ntiles % kXcds, xcd = bid % kXcds;
+  const int64_t tile = xcd * per + (xcd < rem ? xcd : rem) + bid / kXcds;
+  const int64_t hs = tile / nrb;  // bw * H + h
+  const int32_t i0 = (int32_t)(tile - hs * nrb) * R;
+  const int32_t h = (int32_t)(hs % a.H);
+  const int32_t bw = (int32_t)(hs / a.H);  // image * nW + window
   const int64_t slice = (int64_t)bw * a.H + h;
   const int8_t* __restrict__ Q = a.q + slice * Tw * 64;
   const int8_t* __restrict__ K = a.k + slice * Tw * 64;
@@ -222,14 +232,30 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
       // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63, so
       // the cap keeps the 64-bit shift defined (large m_p gives s_d up to 41)
       const int32_t sh = min(32 - a.k_out + sd, 63);
+      // With sh < 32 and F < 2^sh (the usual case: F is small once s_d > 0,
+      // and S_sum >= 2^16 bounds it otherwise), Fs = F 2^(32-sh) fits in 32
+      // bits and floor(e F / 2^sh) is the high word of e Fs: one multiply.
+      // Taken when every row of the wave qualifies (a uniform branch).
+      if (__all(sh < 32 && F < (1u << (sh & 31)))) {
+        const uint32_t Fs = F << ((32 - sh) & 31);
 #pragma unroll
-      for (int j = 0; j < JW; ++j) {
-        const int32_t wd = k + j * LPR;
-        uint32_t p[4];
+        for (int j = 0; j < JW; ++j) {
+          const int32_t wd = k + j * LPR;
+          uint32_t p[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
-          p[b] = min((uint32_t)(((uint64_t)e[j][b] * F) >> sh), (uint32_t)pcap);
-        if (wd < nword) row[wd] = pack_bytes(p[0], p[1], p[2], p[3]);  // padding -> 0
+          for (int b = 0; b < 4; ++b) p[b] = min(__umulhi(e[j][b], Fs), (uint32_t)pcap);
+          if (wd < nword) row[wd] = pack_bytes(p[0], p[1], p[2], p[3]);  // padding -> 0
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < JW; ++j) {
+          const int32_t wd = k + j * LPR;
+          uint32_t p[4];
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            p[b] = min((uint32_t)(((uint64_t)e[j][b] * F) >> sh), (uint32_t)pcap);
+          if (wd < nword) row[wd] = pack_bytes(p[0], p[1], p[2], p[3]);  // padding -> 0
+        }
       }
     }
   }
@@ -344,8 +370,10 @@ hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
     if (e != hipSuccess) return e;
     configured = smem;
   }
-  dim3 grid((a.Tw + R - 1) / R, a.H, a.B * a.nW), block(64 * NW);
-  hipLaunchKernelGGL(kern, grid, block, smem, s, a, lds_row, clampL);
+  const int32_t nrb = (a.Tw + R - 1) / R;
+  const int64_t ntiles = (int64_t)nrb * a.H * a.B * a.nW;
+  hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(64 * NW), smem, s, a, lds_row, clampL,
+                     nrb, ntiles);
   return hipGetLastError();
 }
 

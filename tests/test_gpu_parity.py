@@ -345,6 +345,44 @@ def test_attention_head_dim_32(case):
     assert_same(got, ref, "attention hd32")
 
 
+# (k_inter, k_out, I0, s_d): rows whose tiny S_sum makes F >= 2^(32 - k_out
+# + s_d) (k_inter = 4 with I0 = 1 or 2), output shifts on both sides of 32
+# (s_d = 7 and 9 at k_out = 8), and other output widths.
+SMAX_PARAMS = [(4, 8, 1, -1), (4, 8, 2, 0), (16, 5, 8, -1), (16, 2, 16, -1), (10, 8, 100, 3),
+               (16, 8, 24, 9), (16, 8, 24, 7)]
+
+
+@pytest.mark.parametrize("case", [(2, 10, 10, 5, 5, 2), (4, 40, 40, 20, 20, 3),
+                                  (1, 40, 40, 0, 0, 3)])
+@pytest.mark.parametrize("smax", SMAX_PARAMS)
+def test_attention_shiftmax_params(case, smax):
+    _attention_smax_case(case, smax)
+
+
+@pytest.mark.parametrize("smax", [SMAX_PARAMS[0], SMAX_PARAMS[5]])
+def test_attention_shiftmax_params_large_grid(smax):
+    _attention_smax_case((4, 40, 40, 0, 0, 3), smax)
+
+
+def _attention_smax_case(case, smax):
+    B, gh, gw, wh, ww, H = case
+    k_inter, k_out, I0, s_d = smax
+    say(f"attention smax k_inter={k_inter} k_out={k_out} I0={I0} s_d={s_d} B={B} "
+        f"grid={gh}x{gw} win={wh}x{ww} heads={H}")
+    g = rng(gh * 7 + wh + I0 + k_out)
+    D, T = 64 * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    p = {"score_mult": int(g.integers(2 ** 29, 2 ** 30)), "score_shift": 39, "smax_I0": I0,
+         "smax_k_inter": k_inter, "smax_k_out": k_out, "smax_s_d": s_d,
+         "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 30 + k_out}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, wh, ww, H, 64, p["score_mult"],
+                                     p["score_shift"], I0, p["pv_mult"], p["pv_shift"],
+                                     k_inter=k_inter, k_out=k_out, s_d=s_d)
+                    for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
+    assert_same(got, ref, "attention shiftmax params")
+
+
 @pytest.mark.parametrize("case", [(1, 40, 40, 0, 0, 1), (2, 40, 40, 20, 20, 1),
                                   (1, 6, 10, 3, 5, 1)])
 def test_attention_large_m_p(case):
