@@ -55,6 +55,20 @@ __device__ __forceinline__ uint32_t pack_bytes(int32_t a, int32_t b, int32_t c, 
   return lo | (hi << 16);
 }
 
+// Bytes 0 of a, b, c, d clamped to cap and packed (a in the low byte), for
+// a..d < 2^16: the pairs go into 16-bit halves, are clamped two at a time
+// (v_pk_min_u16) and their low bytes gathered: 5 instructions for 4 values.
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_min_bytes(uint32_t a, uint32_t b, uint32_t c, uint32_t d,
+                                                   u16x2 cap) {
+  u16x2 lo = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(b, a, 0x05040100u));
+  u16x2 hi = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(d, c, 0x05040100u));
+  lo = __builtin_elementwise_min(lo, cap);
+  hi = __builtin_elementwise_min(hi, cap);
+  return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo),
+                               0x06040200u);
+}
+
 // floor((2^31 - 1) / S_R) for S_R in [1, 2^31 - 1]: an FP64 reciprocal
 // estimate is within one of the quotient; one integer correction makes it
 // exact.
@@ -69,10 +83,14 @@ __device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
 // NW waves per workgroup (4, 8 or 16): keys are split over all waves for the
 // scores, rows for the Shiftmax (R / NW rows per wave), and (channel group,
 // key range) pairs for P V, whose int32 partial sums are added through LDS.
-template <int R, int LPR, bool NARROW, bool RAGGED, int NW, int JW>
+// MASK says which Shiftmax words may hold no key: 0 any word past the keys
+// (whole words, T_w % 4 == 0), 1 any byte past the keys (T_w % 4 != 0),
+// 2 only the last word step's (T_w = Twp and (JW - 1) LPR <= Twp / 4).
+template <int R, int LPR, bool NARROW, int MASK, int NW, int JW>
 __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t lds_row,
                                                             int32_t clampL, int32_t nrb,
                                                             int64_t ntiles) {
+  constexpr bool RAGGED = MASK == 1;
   extern __shared__ __attribute__((aligned(16))) int8_t sS[];  // [R][lds_row]
   __shared__ uint32_t elut[256];
   __shared__ int32_t pmax[NW][R];
@@ -190,6 +208,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
     const int sub = lane / LPR, k = lane % LPR;
     const int32_t nword = Twp >> 2;
     const int32_t pcap = (1 << (a.k_out - 1)) - 1;
+    const u16x2 pcap2 = {(unsigned short)pcap, (unsigned short)pcap};
     static_assert(R / NW >= RG, "a wave must own at least RG rows");
     for (int rr0 = wave * (R / NW); rr0 < (wave + 1) * (R / NW); rr0 += RG) {
       const int rr = rr0 + sub;
@@ -204,12 +223,13 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 #pragma unroll
       for (int j = 0; j < JW; ++j) {
         const int32_t wd = k + j * LPR;
-        const uint32_t word = row[min(wd, nword - 1)];  // always inside the row
+        const bool tail = MASK != 2 || j == JW - 1;  // a step that may pass the keys
+        const uint32_t word = row[tail ? min(wd, nword - 1) : wd];  // inside the row
         // max - score per byte (both biased): every valid byte is >= 0, and a
         // borrow from an invalid (higher) byte never reaches a valid one.
         // Words past the window index table entry 255, which is 0.
         uint32_t d4 = m4 - word;
-        if (!RAGGED) d4 = wd * 4 < Tw ? d4 : 0xffffffffu;
+        if (!RAGGED && tail) d4 = wd * 4 < Tw ? d4 : 0xffffffffu;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           uint32_t ev = elut[(d4 >> (8 * b)) & 255];
@@ -236,15 +256,17 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
       // and S_sum >= 2^16 bounds it otherwise), Fs = F 2^(32-sh) fits in 32
       // bits and floor(e F / 2^sh) is the high word of e Fs: one multiply.
       // Taken when every row of the wave qualifies (a uniform branch).
+      // Either way the quotient is below 2^k_out <= 2^8 (e F < 2^(32 + s_d)
+      // when S_sum >> s_d fits S_R; smaller when S_R is clamped), so the
+      // 16-bit clamp-and-pack holds it.
       if (__all(sh < 32 && F < (1u << (sh & 31)))) {
         const uint32_t Fs = F << ((32 - sh) & 31);
 #pragma unroll
         for (int j = 0; j < JW; ++j) {
           const int32_t wd = k + j * LPR;
-          uint32_t p[4];
-#pragma unroll
-          for (int b = 0; b < 4; ++b) p[b] = min(__umulhi(e[j][b], Fs), (uint32_t)pcap);
-          if (wd < nword) row[wd] = pack_bytes(p[0], p[1], p[2], p[3]);  // padding -> 0
+          const uint32_t pw = pack_min_bytes(__umulhi(e[j][0], Fs), __umulhi(e[j][1], Fs),
+                                             __umulhi(e[j][2], Fs), __umulhi(e[j][3], Fs), pcap2);
+          if ((MASK == 2 && j < JW - 1) || wd < nword) row[wd] = pw;  // padding -> 0
         }
       } else {
 #pragma unroll
@@ -252,9 +274,9 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
           const int32_t wd = k + j * LPR;
           uint32_t p[4];
 #pragma unroll
-          for (int b = 0; b < 4; ++b)
-            p[b] = min((uint32_t)(((uint64_t)e[j][b] * F) >> sh), (uint32_t)pcap);
-          if (wd < nword) row[wd] = pack_bytes(p[0], p[1], p[2], p[3]);  // padding -> 0
+          for (int b = 0; b < 4; ++b) p[b] = (uint32_t)(((uint64_t)e[j][b] * F) >> sh);
+          if ((MASK == 2 && j < JW - 1) || wd < nword)
+            row[wd] = pack_min_bytes(p[0], p[1], p[2], p[3], pcap2);  // padding -> 0
         }
       }
     }
@@ -358,11 +380,11 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(const int8_t* qkv, in
   }
 }
 
-template <int R, int LPR, bool NARROW, bool RAGGED, int NW, int JW>
+template <int R, int LPR, bool NARROW, int MASK, int NW, int JW>
 hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   const int32_t lds_row = a.Twp + 16;
   const size_t smem = (size_t)R * lds_row;
-  auto kern = attention_kernel<R, LPR, NARROW, RAGGED, NW, JW>;
+  auto kern = attention_kernel<R, LPR, NARROW, MASK, NW, JW>;
   static size_t configured = 0;
   if (smem > 65536 && smem > configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -382,13 +404,15 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStrea
   // A lane sums at most 4 JW ShiftExp values, each at most emax = ShiftExp(0)
   // = I0 * 2^k_inter: 32-bit partial sums are exact while 4 JW emax < 2^32.
   const bool narrow = emax * 4 * JW < ((int64_t)1 << 32);
-  const bool ragged = (a.Tw & 3) != 0;
+  const int mask = (a.Tw & 3) ? 1 : (a.Tw == a.Twp && (JW - 1) * LPR <= (a.Twp >> 2) ? 2 : 0);
   if (narrow) {
-    return ragged ? launch_variant<R, LPR, true, true, NW, JW>(a, clampL, s)
-                  : launch_variant<R, LPR, true, false, NW, JW>(a, clampL, s);
+    if (mask == 2) return launch_variant<R, LPR, true, 2, NW, JW>(a, clampL, s);
+    return mask ? launch_variant<R, LPR, true, 1, NW, JW>(a, clampL, s)
+                : launch_variant<R, LPR, true, 0, NW, JW>(a, clampL, s);
   }
-  return ragged ? launch_variant<R, LPR, false, true, NW, JW>(a, clampL, s)
-                : launch_variant<R, LPR, false, false, NW, JW>(a, clampL, s);
+  if (mask == 2) return launch_variant<R, LPR, false, 2, NW, JW>(a, clampL, s);
+  return mask ? launch_variant<R, LPR, false, 1, NW, JW>(a, clampL, s)
+              : launch_variant<R, LPR, false, 0, NW, JW>(a, clampL, s);
 }
 
 // The 16-word variants with the smallest word count the window needs: 13

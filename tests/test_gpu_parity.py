@@ -268,6 +268,7 @@ ATTN_CASES = [
     (1, 6, 10, 3, 5, 1),       # 15 tokens: fewer keys than one block
     (1, 1, 1, 0, 0, 1),        # a single token
     (1, 45, 45, 0, 0, 2),      # 2025 tokens: near the window limit
+    (1, 32, 64, 0, 0, 2),      # 2048 tokens: the limit, a multiple of 64
 ]
 
 
