@@ -362,6 +362,22 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
   hipError_t he = hipSuccess;
   *ready_out = READY_NONE;
 
+  // h = LN1(x) and Q, K, V^T in one launch where the tail kernel runs
+  if (ready == READY_NONE && use_tail(p, nullptr, M)) {
+    TailArgs ha = {};
+    ha.x = x;
+    ha.M = M;
+    ha.ln1_beta = p->ln1_beta; ha.ln1_mult = p->ln1_out.mult;
+    ha.ln1_shift = p->ln1_out.shift; ha.ln1_nq = p->ln1_out.n; ha.ln1_iters = p->ln_iters;
+    ha.w_qkv = p->w_qkv; ha.b_qkv = p->b_qkv; ha.qkv_mult = p->qkv.mult;
+    ha.qkv_shift = p->qkv.shift; ha.qkv_nq = p->qkv.n;
+    ha.qkv = L.qkv;
+    StageTimer t(ILW_STAGE_GEMM_QKV, s);
+    he = launch_block_head(ha, s);
+    t.done();
+    if (he != hipSuccess) return hip_status(he, "block LN1 + QKV");
+    ready = READY_QKV;
+  }
   // h = LN1(x)
   if (ready == READY_NONE) {
     StageTimer t(ILW_STAGE_LAYERNORM, s);

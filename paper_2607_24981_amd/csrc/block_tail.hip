@@ -114,6 +114,59 @@ __device__ __forceinline__ uint32_t slab_layernorm(uint32_t xw, int w, int lane,
   return pack4(o[0], o[1], o[2], o[3]);
 }
 
+// Window-major offsets of token m (a valid token) for the next attention:
+// its row of Q and K, and its column of V^T.
+__device__ __forceinline__ void qkv_dest(const TailArgs& a, int64_t m, int64_t& tq, int64_t& tv) {
+  const QkvLayout& Lq = a.qkv;
+  const int32_t b = fdiv((int32_t)m, Lq.T, a.inv_T);
+  const int32_t t = (int32_t)m - b * Lq.T;
+  const int32_t ty = fdiv(t, Lq.grid_w, a.inv_gw), tx = t - ty * Lq.grid_w;
+  const int32_t wy = fdiv(ty, Lq.win_h, a.inv_wh), iy = ty - wy * Lq.win_h;
+  const int32_t wx = fdiv(tx, Lq.win_w, a.inv_ww), ix = tx - wx * Lq.win_w;
+  const int64_t bw = (int64_t)b * Lq.nW + wy * Lq.nwx + wx;
+  const int32_t li = iy * Lq.win_w + ix;
+  tq = (bw * Lq.H * Lq.Tw + li) * 64;
+  tv = bw * Lq.H * 64 * Lq.Twp + li;
+}
+
+// QKV of the slab from h in bufX (wave w: channels 48w .. 48w + 47, weights
+// in wq), requantized with the staged constants qc[0 .. 3D) and scattered
+// window-major: the lane's token goes to (tq, tv).
+__device__ __forceinline__ void slab_qkv(const TailArgs& a, const v4i (&wq)[3][D / 64],
+                                         const int8_t* bufX, const ChanC* qc, int w, int tl,
+                                         int cq, int kq, bool tok_ok, int64_t tq, int64_t tv) {
+  const v4i zero = {0, 0, 0, 0};
+  v4i acc2[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) acc2[t] = zero;
+#pragma unroll
+  for (int s = 0; s < D / 64; ++s) {
+    const v4i fb = *(const v4i*)(bufX + tl * XS + s * 64 + kq);
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      acc2[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wq[t][s], fb, acc2[t], 0, 0, 0);
+  }
+  if (!tok_ok) return;
+  const QkvLayout& Lq = a.qkv;
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int n = 48 * w + 16 * t + cq;  // channel of q | k | v
+    int32_t v[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = rq_chan(acc2[t][r], qc[n + r]);
+    const int32_t part = n / D, rem_n = n - part * D;
+    const int32_t h = rem_n >> 6, c = rem_n & 63;
+    if (part < 2) {
+      int8_t* base = part == 0 ? Lq.q : Lq.k;
+      *(uint32_t*)(base + tq + (int64_t)h * Lq.Tw * 64 + c) = pack4(v[0], v[1], v[2], v[3]);
+    } else {
+      int8_t* dst = Lq.vt + tv + ((int64_t)h * 64 + c) * Lq.Twp;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[(int64_t)r * Lq.Twp] = (int8_t)v[r];
+    }
+  }
+}
+
 template <bool NEXT>
 __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
   __shared__ __attribute__((aligned(16))) int8_t bufX[TS * XS];  // att, then h2, then h
@@ -217,18 +270,7 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
     glut[t] = (int8_t)rq(sd_gelu(t - 128, a.g_I0, a.g_kinter, a.g_kout), a.g_mult, a.g_shift);
   // window-major destination of the lane's token for the next block's Q, K, V^T
   int64_t tq = 0, tv = 0;
-  if (NEXT && tok_ok) {
-    const QkvLayout& Lq = a.qkv;
-    const int32_t b = fdiv((int32_t)m, Lq.T, a.inv_T);
-    const int32_t t = (int32_t)m - b * Lq.T;
-    const int32_t ty = fdiv(t, Lq.grid_w, a.inv_gw), tx = t - ty * Lq.grid_w;
-    const int32_t wy = fdiv(ty, Lq.win_h, a.inv_wh), iy = ty - wy * Lq.win_h;
-    const int32_t wx = fdiv(tx, Lq.win_w, a.inv_ww), ix = tx - wx * Lq.win_w;
-    const int64_t bw = (int64_t)b * Lq.nW + wy * Lq.nwx + wx;
-    const int32_t li = iy * Lq.win_w + ix;
-    tq = (bw * Lq.H * Lq.Tw + li) * 64;
-    tv = bw * Lq.H * 64 * Lq.Twp + li;
-  }
+  if (NEXT && tok_ok) qkv_dest(a, m, tq, tv);
   if (tid < TS * D / 16) *(v4i*)(bufX + ar * XS + ac * 16) = att_chunk;
   // (__syncthreads_or only tells whether any thread's value is nonzero, so
   // each flag gets its own reduction)
@@ -324,38 +366,85 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
     *(uint32_t*)(bufX + tl * XS + n1) = hw;
   }
   __syncthreads();
-  v4i acc2[3];
-#pragma unroll
-  for (int t = 0; t < 3; ++t) acc2[t] = zero;
-#pragma unroll
-  for (int s = 0; s < D / 64; ++s) {
-    const v4i fb = *(const v4i*)(bufX + tl * XS + s * 64 + kq);
+  slab_qkv(a, wq, bufX, chan + NQKV, w, tl, cq, kq, tok_ok, tq, tv);
+}
+
+// The first block's h = LN1(x) and Q, K, V^T = rq(h Wq^T + bq), scattered
+// window-major, for one 16-token slab per workgroup: the tail kernel's last
+// stage applied to the encoder input, so the first block needs no separate
+// LayerNorm and QKV launches.  Same wave layout: wave w normalizes channels
+// 16w .. 16w + 15 and computes QKV channels 48w .. 48w + 47.
+__global__ __launch_bounds__(64 * NWV) void block_head_kernel(TailArgs a) {
+  __shared__ __attribute__((aligned(16))) int8_t bufX[TS * XS];  // h
+  __shared__ ChanC chan[3 * D];
+  __shared__ LnChan ln1p[D];
+  __shared__ int32_t lnred[NWV * TS * 2];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t M = a.M;
+  const int64_t m0 = (int64_t)blockIdx.x * TS;
+  const int tl = lane & (TS - 1);
+  const int cq = (lane >> 4) * 4;
+  const int kq = (lane >> 4) * 16;
+  const int64_t m = m0 + tl;
+  const bool tok_ok = m < M;
+  const int64_t mc = tok_ok ? m : M - 1;
+
+  // loads, smallest first and all unconditional (clamped indices): the QKV
+  // and LayerNorm constants, the lane's input word, then the QKV weights
+  static_assert(3 * D <= 64 * NWV, "one QKV channel per thread");
+  const int c = min(tid, 3 * D - 1);
+  const int32_t cm = a.qkv_mult[a.qkv_nq == 1 ? 0 : c];
+  const int32_t cs = a.qkv_shift[a.qkv_nq == 1 ? 0 : c];
+  const int32_t cb = a.b_qkv ? a.b_qkv[c] : 0;
+  const int lc = tid % D;
+  const int32_t lb = a.ln1_beta[lc];
+  const int32_t lm = a.ln1_mult[a.ln1_nq == 1 ? 0 : lc];
+  const int32_t ls = a.ln1_shift[a.ln1_nq == 1 ? 0 : lc];
+  const int n1 = 16 * w + cq;  // the lane's 4 LayerNorm channels
+  const uint32_t xw = *(const uint32_t*)(a.x + mc * D + n1);
+  asm volatile("" ::: "memory");
+  v4i wq[3][D / 64];
+  {
+    const int8_t* src = a.w_qkv + (int64_t)(48 * w + tl) * D + kq;
 #pragma unroll
     for (int t = 0; t < 3; ++t)
-      acc2[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wq[t][s], fb, acc2[t], 0, 0, 0);
+#pragma unroll
+      for (int s = 0; s < D / 64; ++s) wq[t][s] = *(const v4i*)(src + (int64_t)16 * t * D + s * 64);
   }
-  if (!tok_ok) return;
-  const QkvLayout& Lq = a.qkv;
-#pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int n = 48 * w + 16 * t + cq;  // channel of q | k | v
-    int32_t v[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) v[r] = rq_chan(acc2[t][r], chan[NQKV + n + r]);
-    const int32_t part = n / D, rem_n = n - part * D;
-    const int32_t h = rem_n >> 6, c = rem_n & 63;
-    if (part < 2) {
-      int8_t* base = part == 0 ? Lq.q : Lq.k;
-      *(uint32_t*)(base + tq + (int64_t)h * Lq.Tw * 64 + c) = pack4(v[0], v[1], v[2], v[3]);
-    } else {
-      int8_t* dst = Lq.vt + tv + ((int64_t)h * 64 + c) * Lq.Twp;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dst[(int64_t)r * Lq.Twp] = (int8_t)v[r];
-    }
+
+  if (tid < 3 * D) chan[tid] = make_chan(cm, cs, cb);
+  int wide = 0;
+  if (tid < D) {
+    ln1p[tid] = make_ln(lb, lm, ls);
+    wide = lb > (1 << 30) || lb < -(1 << 30);
   }
+  int64_t tq = 0, tv = 0;
+  if (tok_ok) qkv_dest(a, m, tq, tv);
+  const bool wide1 = __syncthreads_or(wide) != 0;  // also publishes chan and ln1p
+
+  {
+    const uint32_t hw = slab_layernorm(xw, w, lane, n1, lnred, ln1p, wide1, a.ln1_iters);
+    *(uint32_t*)(bufX + tl * XS + n1) = hw;
+  }
+  __syncthreads();
+  slab_qkv(a, wq, bufX, chan, w, tl, cq, kq, tok_ok, tq, tv);
 }
 
 }  // namespace
+
+hipError_t launch_block_head(const TailArgs& a_in, hipStream_t s) {
+  if (a_in.M == 0) return hipSuccess;
+  TailArgs a = a_in;
+  a.inv_T = 1.0f / (float)a.qkv.T;
+  a.inv_gw = 1.0f / (float)a.qkv.grid_w;
+  a.inv_wh = 1.0f / (float)a.qkv.win_h;
+  a.inv_ww = 1.0f / (float)a.qkv.win_w;
+  hipLaunchKernelGGL(block_head_kernel, dim3((unsigned)((a.M + TS - 1) / TS)), dim3(64 * NWV),
+                     0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_block_tail(const TailArgs& a_in, hipStream_t s) {
   if (a_in.M == 0) return hipSuccess;

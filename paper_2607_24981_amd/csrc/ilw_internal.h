@@ -350,6 +350,9 @@ struct TailArgs {
   float inv_T, inv_gw, inv_wh, inv_ww;
 };
 hipError_t launch_block_tail(const TailArgs& a, hipStream_t s);
+// h = LN1(x) and the window-major Q, K, V^T of the first block (dim 192), from
+// TailArgs' x, M, LN1, QKV and layout fields.
+hipError_t launch_block_head(const TailArgs& a, hipStream_t s);
 
 // Scale-preserving split convolution (pointwise), up to kMaxBranches branches.
 constexpr int kMaxBranches = 8;
