@@ -23,13 +23,12 @@
 //
 // At K = 192 the exact requantization costs more VALU time than the MFMA work
 // of the tile, so the epilogue is kept to a few instructions per output.  Each
-// workgroup stages its channels' constants in LDS once (RqF64: scale and
-// bias-carrying addend as doubles, accumulator bounds); an output is then a
-// clamp, a conversion, one FP64 fma, a conversion and a clamp, exact by the
-// argument at RqF64.  Tiles holding a channel outside that form's range
-// (shift above 43, |bias| >= 2^21) take the integer form: the accumulator
-// clamped to a bound beyond which the result saturates, one 64-bit
-// multiply-add and one shift.
+// workgroup stages its channels' constants in LDS once (RqI64: multiplier,
+// shift, a 64-bit addend carrying the bias and the rounding, accumulator
+// bounds); an output is then a clamp, one 64-bit multiply-add, one shift and
+// a clamp, exact by the argument at RqI64.  Tiles holding a channel with a
+// shift above 53 take the general integer form (bias added first, then the
+// clamp, the multiply-add and the shift).
 #include <stdlib.h>
 
 #include "ilw_internal.h"
@@ -58,7 +57,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
   __shared__ int8_t glut[EPI == EPI_GELU ? 256 : 1];
-  __shared__ RqF64 rqc[TN];                         // output requantization per channel
+  __shared__ RqI64 rqc[TN];                         // output requantization per channel
   __shared__ int64_t qoff[EPI == EPI_QKV ? TM : 1][2];  // QKV: Q/K and V^T offsets per token
   __shared__ LnChan lnp[LN ? TN : 1];              // LayerNorm constants per channel
   __shared__ int32_t lnred[LN ? 2 * WN * TM : 1];  // per-wave row sums
@@ -189,18 +188,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     rtok[j] = (XP ? mc % a.pT : mc) * N;
   }
 
-  // Channel constants and residual words (latency mode: loaded now).
-  int32_t pm[FI][4], ps[FI][4], pb[FI][4];
+  // Residual words (latency mode: loaded now).
   uint32_t rs[FI][FJ];
-  auto load_chan = [&](int i) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qi = a.nq == 1 ? 0 : min(nch[i], N - 4) + r;
-      pm[i][r] = a.mult[qi];
-      ps[i][r] = a.shift[qi];
-      pb[i][r] = a.bias ? a.bias[min(nch[i], N - 4) + r] : 0;
-    }
-  };
   auto load_resid = [&](int i) {
 #pragma unroll
     for (int j = 0; j < FJ; ++j)
@@ -212,12 +201,10 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   }
   // Output requantization constants of the tile's channels, once per
   // workgroup (a lane's channels are shared by 16 lanes of each wave row).
-  int rq_int = 0;
   for (int c = tid; c < TN; c += NT) {
     const int32_t n = min(n0 + c, N - 1);
-    RqF64 r;
-    rq_int |= r.init(a.mult[a.nq == 1 ? 0 : n], a.shift[a.nq == 1 ? 0 : n],
-                     a.bias ? a.bias[n] : 0);
+    RqI64 r;
+    r.init(a.mult[a.nq == 1 ? 0 : n], a.shift[a.nq == 1 ? 0 : n], a.bias ? a.bias[n] : 0);
     rqc[c] = r;
   }
 
@@ -285,7 +272,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 
   if constexpr (PF == 1) {
     sstore(0, 0);
-    rq_int = __syncthreads_or(rq_int);
+    __syncthreads();  // the first tile and the staged constants
     if (LN) ln_wide = __syncthreads_or(ln_wide);
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + 1 < nk) gload(kt + 1, 0);
@@ -298,7 +285,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     // one), so the memory counter wait before each LDS store is exact: it
     // leaves the younger slots' loads in flight.
     sstore(0, 0);
-    rq_int = __syncthreads_or(rq_int);
+    __syncthreads();  // the first tile and the staged constants
     if (LN) ln_wide = __syncthreads_or(ln_wide);
     gload(min(PF, nk - 1), 0);
     for (int kt0 = 0; kt0 < nk; kt0 += PF) {
@@ -313,9 +300,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     }
   }
 
-  // Epilogue.  The FP64 requantization serves every tile whose channels
-  // allow it (the usual case); otherwise the integer form with constants
-  // read per lane.
+  // Epilogue: the staged four-instruction requantization, then the
+  // epilogue's own work.
   uint32_t xw[FI][FJ];  // RESID_LN: the residual outputs, 4 channels per word
 #pragma unroll
   for (int i = 0; i < FI; ++i)
@@ -329,23 +315,15 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       tokv[j] = qoff[t][1];
     }
   }
-  auto epilogue = [&](auto f64) {
-    constexpr bool F = decltype(f64)::value;
+  {
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
       if (!ch_ok[i]) continue;
       const int32_t n = nch[i];
       if (!EARLY && RES) load_resid(i);
-      RqF64 rf[4];
-      ChanRq cr[4];
-      if constexpr (F) {
+      RqI64 rf[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) rf[r] = rqc[n - n0 + r];
-      } else {
-        load_chan(i);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) cr[r].init(pm[i][r], ps[i][r], pb[i][r]);
-      }
+      for (int r = 0; r < 4; ++r) rf[r] = rqc[n - n0 + r];
       int8_t* qk_base = nullptr;
       int64_t ch_qk = 0, ch_v = 0;
       bool is_v = false;
@@ -361,24 +339,20 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 #pragma unroll
       for (int j = 0; j < FJ; ++j) {
         if (!tok_ok[j]) continue;
-        // u[r]: the requantized value + 256 (FP64 form) or the value itself;
-        // its low byte is the int8 output either way
-        int32_t u[4];
+        int32_t u[4];  // the requantized outputs
 #pragma unroll
-        for (int r = 0; r < 4; ++r) u[r] = F ? rf[r].apply(acc[i][j][r]) : cr[r].apply(acc[i][j][r]);
-        constexpr int32_t off = F ? 256 : 0;
+        for (int r = 0; r < 4; ++r) u[r] = rf[r].apply(acc[i][j][r]);
         if (EPI == EPI_STORE) {
           *(uint32_t*)(a.y + tok[j] + n) = pack4(u[0], u[1], u[2], u[3]);
         } else if (EPI == EPI_GELU) {
           *(uint32_t*)(a.y + tok[j] + n) =
-              pack4(glut[u[0] + 128 - off], glut[u[1] + 128 - off], glut[u[2] + 128 - off],
-                    glut[u[3] + 128 - off]);
+              pack4(glut[u[0] + 128], glut[u[1] + 128], glut[u[2] + 128], glut[u[3] + 128]);
         } else if (RES) {
           const uint32_t s = rs[i][j];
           int32_t o[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            o[r] = rq2(u[r] - off, (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
+            o[r] = rq2(u[r], (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
           const uint32_t word = pack4(o[0], o[1], o[2], o[3]);
           *(uint32_t*)(a.y + tok[j] + n) = word;
           if (LN) xw[i][j] = word;
@@ -393,11 +367,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
         }
       }
     }
-  };
-  if (rq_int)
-    epilogue(Flag<false>{});
-  else
-    epilogue(Flag<true>{});
+  }
   if (LN) {
     // LayerNorm of the residual output rows (same reading as the standalone
     // operator).  A token's N channels sit in 4 lanes of each of the WN waves

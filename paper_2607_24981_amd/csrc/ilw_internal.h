@@ -219,42 +219,43 @@ struct ChanRq {
   }
 };
 
-// The same requantization in FP64, for the GEMM epilogues.  Per channel:
-// scale = m * 2^-s and c = bias * m * 2^-s + 256.5, both exact doubles when
-// s <= 43 and |bias| < 2^21 (bias * m < 2^52); the accumulator is clamped to
-// [lo, hi] = [-L - bias, L - bias], beyond which the result saturates, with L
-// <= 2^30 * 2^s / |m| (no clamp when even 2^31 cannot reach 2^30 after the
-// scaling).  Then fma(acc, scale, c) rounds the exact value
-// (acc + bias) * m / 2^s + 256.5 once: an unsaturated result is a multiple of
-// 2^-s below 2^10, hence exact, a saturated one stays on its side of 129 or
-// 384, and the value fits the int32 conversion.  The result is q + 256 in
-// [129, 383] (its low byte is q's).
-struct RqF64 {
-  double scale, c;
-  int32_t lo, hi;
-  // Returns true when the channel needs the integer form instead.
-  __device__ __forceinline__ bool init(int32_t m, int32_t s, int32_t b) {
-    scale = __builtin_ldexp((double)m, -s);
-    c = __builtin_fma((double)b, scale, 256.5);
+// The requantization of the GEMM epilogues in four instructions.  Per
+// channel, the bias and the rounding are folded into one 64-bit addend
+// c = bias * m + 2^(s-1), and the accumulator is clamped to [lo, hi] =
+// [-L - bias, L - bias] (saturated to int32), beyond which the result
+// saturates anyway: L >= 129 * 2^s / |m| + 1 from an fp32 estimate with
+// margin, no clamp when that exceeds 2^30.  Then
+//   (acc * m + c) >> s = floor(((acc + bias) m + 2^(s-1)) / 2^s)
+// exactly: with acc + bias inside int32 (the int32 accumulator) the clamped
+// product stays below about 2^61 in magnitude (|m| <= 130 * 2^(s-30) when
+// there is no clamp), |c| below 2^62 + 2^61, and the shifted value far
+// inside int32, for every shift in [1, 62].  A clamp, a 64-bit multiply-add,
+// a 64-bit shift and a clamp.
+struct RqI64 {
+  int64_t c;
+  int32_t mult, shift, lo, hi;
+  __device__ __forceinline__ void init(int32_t m, int32_t s, int32_t b) {
+    mult = m;
+    shift = s;
+    c = (int64_t)b * m + ((int64_t)1 << (s - 1));
     const float am = fabsf((float)m);
     const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)s) * __builtin_amdgcn_rcpf(am);
     if (bound >= 1073741824.f) {
       lo = INT32_MIN;
       hi = INT32_MAX;
     } else {
-      const int32_t L = (int32_t)bound + 1;
-      lo = -L - b;
-      hi = L - b;
+      const int64_t L = (int64_t)bound + 1;
+      lo = (int32_t)max(-L - (int64_t)b, (int64_t)INT32_MIN);
+      hi = (int32_t)min(L - (int64_t)b, (int64_t)INT32_MAX);
     }
-    return s > 43 || b >= (1 << 21) || b <= -(1 << 21);
   }
-  __device__ __forceinline__ int32_t apply(int32_t acc) const {  // q + 256
+  __device__ __forceinline__ int32_t apply(int32_t acc) const {
     // the clamp as one median-of-three (lo < hi always holds; the compiler
     // cannot see it and would emit a max and a min)
     int32_t a;
     asm("v_med3_i32 %0, %1, %2, %3" : "=v"(a) : "v"(acc), "v"(lo), "v"(hi));
-    const int32_t q = (int32_t)__builtin_fma((double)a, scale, c);
-    return min(max(q, 256 + kQmin), 256 + kQmax);
+    const int32_t v = (int32_t)(((int64_t)a * mult + c) >> shift);
+    return min(max(v, kQmin), kQmax);
   }
 };
 

@@ -65,10 +65,10 @@ def test_linear(M, N, K, per_tensor):
 
 
 def _edge_channels(N, fallback):
-    """Per-channel (mult, shift, bias) at the edges of the FP64 epilogue form
-    (shift 43, |bias| = 2^21 - 1, m = 0, odd m at shift 1: exact ties, tiny
-    and huge scales); with fallback, every 64-channel group also holds a
-    channel that needs the integer form (shift above 43 or |bias| >= 2^21)."""
+    """Per-channel (mult, shift, bias) at the edges of the epilogue's
+    requantization (shift 43, |bias| = 2^21 - 1, m = 0, odd m at shift 1:
+    exact ties, tiny and huge scales); with extra, every 64-channel group also
+    holds channels with shifts of 44, 50 and 62 and larger biases."""
     ms = [(1 << 31) - 1, -((1 << 31) - 1), 0, 1, 3, 1 << 29, -(1 << 30), 12345,
           (1 << 30) + 7, -5]
     ss = [43, 43, 30, 1, 1, 30, 31, 13, 40, 2]
@@ -87,8 +87,8 @@ def _edge_channels(N, fallback):
 @pytest.mark.parametrize("M", [300, 40000, 120000])  # 120000: more tiles than fit at once
 @pytest.mark.parametrize("fallback", [False, True])
 def test_linear_requant_forms(M, fallback):
-    """The epilogue's FP64 requantization at its edges, and tiles that fall
-    back to the integer form, at a small-grid and a large-grid tile shape."""
+    """The epilogue's requantization at its edges, including large shifts and
+    biases, at a small-grid and a large-grid tile shape."""
     N, K = 256, 128
     say(f"linear requant forms M={M} fallback={fallback}")
     g = rng(M + fallback)
@@ -273,7 +273,7 @@ ATTN_CASES = [
 
 
 @pytest.mark.parametrize("case", ATTN_CASES)
-@pytest.mark.parametrize("s_d", [-1, 4, 25])  # 25: past the FP64 normalization's range
+@pytest.mark.parametrize("s_d", [-1, 4, 25])  # 25: output shifts of 32 and more
 def test_attention(case, s_d):
     B, gh, gw, wh, ww, H = case
     say(f"attention B={B} grid={gh}x{gw} win={wh}x{ww} heads={H} s_d={s_d}")
@@ -461,9 +461,8 @@ def test_block_shapes(dims, grid, win, B):
 
 @pytest.mark.parametrize("dims", [(128, 2, 512), (384, 6, 1536)])
 def test_block_requant_fallback(dims):
-    """A block whose QKV, projection, fc1 and fc2 layers each hold one
-    channel that the FP64 epilogue form cannot take (shift above 43, or a
-    bias of 2^21 or more): those tiles use the integer form."""
+    """A block whose QKV, projection, fc1 and fc2 layers each hold a channel
+    with a large shift (44 to 47) or a bias of 2^21 or more."""
     D, H, Hm = dims
     say(f"block requant fallback D={D}")
     p = synth.block_params(rng(D + 5), D, H, 64, Hm, "wide", ln_iters=20, smax_s_d=-1)
@@ -476,6 +475,47 @@ def test_block_requant_fallback(dims):
     ref = oracle.block_forward(p, x, 8, 12, 4, 6)
     got = host(ilw.ilw_block_forward(ilw.DeviceBlock(p), dev(x), 8, 12, 4, 6))
     assert_same(got, ref, "block requant fallback")
+
+
+# Biases near the int32 limits that still keep b + sum(x w) inside int32
+# (the method's int32 accumulator; |sum| <= 1536 * 127^2 < 2^25 here).
+BIG_BIAS = [(1 << 31) - (1 << 25), -(1 << 31) + (1 << 25), 1 << 30, -(1 << 30), 1 << 21]
+
+
+def test_linear_extreme_biases():
+    """Biases near the int32 limits, with every shift form (30..43, 44..53,
+    62)."""
+    say("linear extreme biases")
+    g = rng(31)
+    M, N, K = 300, 128, 768
+    x = g.integers(-127, 128, (M, K)).astype(np.int8)
+    w = g.integers(-127, 128, (N, K)).astype(np.int8)
+    bias = g.integers(-2 ** 15, 2 ** 15 + 1, N).astype(np.int32)
+    mult = g.integers(2 ** 29, 2 ** 30 + 1, N).astype(np.int32)
+    shift = g.integers(30, 44, N).astype(np.int32)
+    for i in range(0, N, 7):
+        bias[i] = BIG_BIAS[(i // 7) % len(BIG_BIAS)]
+        shift[i] = (30, 37, 43, 50, 53, 62)[(i // 7) % 6]
+        mult[i] = (1 << 31) - 1 if i % 2 else 3
+    ref = oracle.linear(x, w, bias, mult, shift)
+    got = host(ilw.ilw_linear(dev(x), dev(w), dev(bias), dev(mult), dev(shift)))
+    assert_same(got, ref, "linear extreme biases")
+
+
+@pytest.mark.parametrize("dims", [(192, 3, 768), (384, 6, 1536)])
+def test_block_extreme_biases(dims):
+    """A block (192 channels: the head and tail kernels; 384: the linears)
+    whose QKV, projection, fc1 and fc2 biases include values near +-2^31."""
+    D, H, Hm = dims
+    say(f"block extreme biases D={D}")
+    p = synth.block_params(rng(D + 9), D, H, 64, Hm, "wide", ln_iters=10, smax_s_d=-1)
+    for k, n in (("b_qkv", 3 * D), ("b_proj", D), ("b_fc1", Hm), ("b_fc2", D)):
+        for j, b in enumerate(BIG_BIAS):
+            p[k][(j * 37 + 5) % n] = b
+    x = rng(9).integers(-127, 128, (1, 96, D)).astype(np.int8)
+    ref = oracle.block_forward(p, x, 8, 12, 4, 6)
+    got = host(ilw.ilw_block_forward(ilw.DeviceBlock(p), dev(x), 8, 12, 4, 6))
+    assert_same(got, ref, "block extreme biases")
 
 
 def encoder_ref(blocks, windows, x, gh, gw):

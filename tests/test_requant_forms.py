@@ -2,17 +2,17 @@
 half up, saturated to [-127, 127]), checked on the CPU against the integer
 definition q = sat(floor((v * m + 2^(s-1)) / 2^s)).
 
-* Linear epilogues, FP64 form.  Per channel, the accumulator is first
-  clamped to [-L - b, L - b] with L = floor(130 * 2^s / |m|) + 1 (past L the
-  result saturates anyway), then
+* Linear epilogues.  Per channel, c = b m + 2^(s-1) folds the bias and the
+  rounding into one 64-bit addend, and the accumulator is first clamped to
+  [lo, hi] = [-L - b, L - b] saturated to int32, with L = floor(130 * 2^s /
+  |m|) + 1 (past L the result saturates anyway; no clamp when L would exceed
+  2^30):
 
-      q + 256 = clamp(trunc(fma(acc, m 2^-s, c)), 129, 383),
-      c = fma(b, m 2^-s, 256.5),
+      q = sat(int32((clamp(acc) * m + c) >> s))
 
-  claimed exact for s <= 43 and |b| < 2^21: c is representable, and the
-  unsaturated values are multiples of 2^-s below 2^10.  A fused multiply-add
-  rounds its exact value once; float() of an exact Fraction rounds the same
-  way (to nearest, ties to even).
+  claimed exact for every shift in [1, 62], any multiplier and any bias with
+  acc + b inside int32 (the method's int32 accumulator): no intermediate
+  leaves int64 and the shifted value stays inside int32.
 * Attention scores, 64-bit form, stored biased:
 
       q + 128 = clamp(int32((acc * m + 2^(s-1) + 128 * 2^s) >> s), 1, 255),
@@ -27,95 +27,95 @@ import math
 import numpy as np
 import pytest
 
+I32 = (-(1 << 31), (1 << 31) - 1)
+I64 = (-(1 << 63), (1 << 63) - 1)
+
 
 def rq_exact(acc, m, s):
     v = (acc * m + (1 << (s - 1))) >> s
     return max(-127, min(127, v))
 
 
-# ------------------------------------------------------------------ FP64 form
-def clamp_bound(m, s):
-    """The accumulator bound: None when no clamp is needed (L >= 2^30)."""
-    if m == 0:
-        return 2
-    L = (130 << s) // abs(m) + 1
-    return None if L >= 1 << 30 else L
+def in_range(v, r):
+    return r[0] <= v <= r[1]
 
 
-def rq_fp64(acc, b, m, s):
-    L = clamp_bound(m, s)
-    a = acc if L is None else max(-L - b, min(L - b, acc))
-    scale = Fraction(m, 1 << s)            # a power-of-two scaling: exact
-    c = float(b * scale + Fraction(513, 2))  # one rounding
-    assert Fraction(c) == b * scale + Fraction(513, 2), "addend not representable"
-    y = float(a * scale + Fraction(c))     # the fma: one rounding
-    return max(129, min(383, math.trunc(y))) - 256
+# ------------------------------------------------------- linear epilogue form
+def clamp_bounds(m, b, s, margin=130):
+    """[lo, hi] for the accumulator; None when no clamp is needed."""
+    L = 2 if m == 0 else (margin << s) // abs(m) + 1
+    if L >= 1 << 30:
+        return None
+    return max(-L - b, I32[0]), min(L - b, I32[1])
 
 
-def f64_ok(b, s):
-    return s <= 43 and abs(b) < 1 << 21
+def rq_linear(acc, b, m, s, margin=130):
+    bounds = clamp_bounds(m, b, s, margin)
+    a = acc if bounds is None else max(bounds[0], min(bounds[1], acc))
+    c = b * m + (1 << (s - 1))
+    assert in_range(c, I64), "addend overflow"
+    x = a * m + c
+    assert in_range(x, I64), "int64 overflow"
+    v = x >> s                       # arithmetic shift: the floor
+    assert in_range(v, I32), "int32 overflow"
+    return max(-127, min(127, v))
 
 
-def fp64_cases(m, s, b, rng, n=300, kmax=1536):
-    """Random accumulators over a K = 1536 int8 dot product, the clamp
-    edges and every rounding and saturation boundary of acc + b."""
+def linear_cases(m, s, b, rng, n=300, kmax=1536):
+    """Random accumulators over a K = 1536 int8 dot product (kept so that
+    acc + b fits int32), the clamp edges and every rounding and saturation
+    boundary of acc + b."""
     amax = kmax * 127 * 127
-    accs = set(int(a) for a in rng.integers(-amax, amax + 1, n))
-    accs.update({0, 1, -1, amax, -amax})
-    L = clamp_bound(m, s)
-    if L is not None:
-        for e in (-L - b, L - b):
+    lo_ok, hi_ok = max(-amax, I32[0] - b), min(amax, I32[1] - b)
+    accs = set(int(a) for a in rng.integers(lo_ok, hi_ok + 1, n))
+    accs.update({0, 1, -1, lo_ok, hi_ok})
+    bounds = clamp_bounds(m, b, s)
+    if bounds is not None:
+        for e in bounds:
             accs.update({e - 1, e, e + 1})
     if m != 0:
         for q in list(range(-130, 131, 5)) + [-128, -127, 126, 127, 128]:
             t = Fraction((2 * q + 1) << s, 2 * m) - b  # acc + b at q + 1/2
             for a in (math.floor(t) - 1, math.floor(t), math.ceil(t), math.ceil(t) + 1):
-                if abs(a) <= amax:
-                    accs.add(a)
-    return sorted(accs)
+                accs.add(a)
+    return sorted(a for a in accs if lo_ok <= a <= hi_ok)
 
 
 LIN_PARAMS = [(1, 13, 0), (3, 1, -5), (1 << 29, 30, 12345), (-(1 << 30), 31, -(1 << 20)),
               (12345, 20, 77), ((1 << 30) - 12345, 43, (1 << 21) - 1),
               (-((1 << 29) + 5), 40, -((1 << 21) - 1)), ((1 << 31) - 1, 43, 1 << 15),
-              ((1 << 31) - 1, 36, -(1 << 15)), ((1 << 29) + 3, 38, 32768)]
+              ((1 << 31) - 1, 36, -(1 << 15)), ((1 << 29) + 3, 38, 32768),
+              ((1 << 31) - 1, 62, (1 << 31) - (1 << 25)), (1, 62, 5), (-3, 53, -(1 << 30)),
+              ((1 << 31) - 1, 1, 7), (0, 17, 1 << 30), ((1 << 30) + 1, 50, -(1 << 31) + (1 << 25))]
 
 
 @pytest.mark.parametrize("m,s,b", LIN_PARAMS)
-def test_linear_fp64_form_is_exact(m, s, b):
-    assert f64_ok(b, s)
-    rng = np.random.default_rng(abs(m) % 1000 + s)
-    for acc in fp64_cases(m, s, b, rng):
-        assert rq_fp64(acc, b, m, s) == rq_exact(acc + b, m, s), (acc, b, m, s)
+@pytest.mark.parametrize("margin", [129, 130])
+def test_linear_form_is_exact(m, s, b, margin):
+    """Any clamp bound L in [129 * 2^s / |m| + 1, 2^30] works (the kernel's
+    fp32 estimate of 130 * 2^s / |m| lies there)."""
+    rng = np.random.default_rng(abs(m) % 1000 + s + margin)
+    for acc in linear_cases(m, s, b, rng):
+        assert rq_linear(acc, b, m, s, margin) == rq_exact(acc + b, m, s), (acc, b, m, s)
 
 
-def test_linear_fp64_random_parameters():
+def test_linear_form_random_parameters():
     rng = np.random.default_rng(7)
-    for _ in range(60):
-        s = int(rng.integers(1, 44))
+    for _ in range(120):
+        s = int(rng.integers(1, 63))
         m = int(rng.integers(-(1 << 31) + 1, 1 << 31))
-        b = int(rng.integers(-(1 << 21) + 1, 1 << 21))
-        for acc in fp64_cases(m, s, b, rng, n=40):
-            assert rq_fp64(acc, b, m, s) == rq_exact(acc + b, m, s), (acc, b, m, s)
+        b = int(rng.integers(-(1 << 31) + 1, 1 << 31))
+        for acc in linear_cases(m, s, b, rng, n=40):
+            assert rq_linear(acc, b, m, s) == rq_exact(acc + b, m, s), (acc, b, m, s)
 
 
-def test_fp64_bound_is_needed():
-    """Past s = 43 one rounding can cross an integer.  At s = 51 an
-    accumulator near 2^20 and m = floor((2^50 - 1) / acc) put acc * m / 2^51
-    within 2^-45 below 1/2; 256.5 plus that rounds to 257 (the spacing of
-    doubles there is 2^-44), while the exact result is 0.  The host sends
-    such shifts to the integer form."""
-    s = 51
-    found = 0
-    for acc in range((1 << 20) - 50000, (1 << 20) + 1):
-        m = ((1 << (s - 1)) - 1) // acc
-        gap = (1 << (s - 1)) - acc * m  # 2^(s-1) - acc * m, in [1, acc]
-        if gap < 1 << (s - 45):
-            assert not f64_ok(0, s)
-            assert rq_exact(acc, m, s) == 0
-            y = float(Fraction(acc * m, 1 << s) + Fraction(513, 2))
-            found += math.trunc(y) - 256 != 0
-    assert found > 0
+def test_linear_clamp_is_needed():
+    """Without the clamp a small shift with a large multiplier leaves int32
+    after the shift (m = 2^31 - 1, s = 1, acc = 2^24 gives about 2^54)."""
+    m, s, acc = (1 << 31) - 1, 1, 1 << 24
+    v = (acc * m + (1 << (s - 1))) >> s
+    assert not in_range(v, I32)
+    assert rq_linear(acc, 0, m, s) == rq_exact(acc, m, s) == 127
 
 
 # ------------------------------------------------------------ 64-bit score form
