@@ -12,19 +12,22 @@
 // are rescaled into an int64 running sum and cleared.  Tiling as in the GEMM:
 // weights are the MFMA A operand (a lane ends with 4 consecutive channels of
 // one token), double-buffered LDS tiles with 80-byte rows, unconditional
-// loads with clamped rows, and two K steps of loads in flight.
+// loads with clamped rows, and PF (two) K steps of loads in flight.  The
+// loads walk the branches with a wave-uniform cursor whose pointers and row
+// offsets change only at branch boundaries, and the fold is triggered by a
+// step count, so a K step issues no scalar loads.
 #include "ilw_internal.h"
 
 namespace ilw {
 namespace {
 
-constexpr int TK = 64, LDS_ROW = 80, NXCD = 8, PF = 2;
+constexpr int TK = 64, LDS_ROW = 80, NXCD = 8;
 
 struct BrChan {
   int32_t mult, shift;
 };
 
-template <int WN, int WM, int FI, int FJ>
+template <int WN, int WM, int FI, int FJ, int PF>
 __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, int32_t tiles_n,
                                                                  int64_t tiles_total) {
   constexpr int WTN = 16 * FI, WTM = 16 * FJ;
@@ -66,19 +69,38 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
   for (int i = 0; i < (PW > PX ? PW : PX); ++i) cofs[i] = ((tid + i * NT) & 3) * 16;
 
   v4i rw[PF][PW], rx[PF][PX];
-  // loads of flattened K step s (steps past the end re-read the last one)
-  auto gload = [&](int s, int sl) {
-    s = min(s, S - 1);
-    int b = 0;
-    for (int q = 1; q < nbr; ++q) b += s >= a.kstart[q];
-    const int32_t C = a.C[b];
-    const int32_t kb = (s - a.kstart[b]) * TK;
-    const int8_t* W = a.w[b];
-    const int8_t* X = a.x[b];
+  // Loads go step by step through the branches: a wave-uniform cursor (the
+  // branch lb and the byte offset lk in its rows) whose branch pointers and
+  // per-lane row offsets change only at branch boundaries.  Once every step
+  // has been loaded the cursor stays on the last one (re-read, never used).
+  int lb = 0, lsteps = 0;
+  int32_t lk = 0, LC = a.C[0];
+  const int8_t* LW = a.w[0];
+  const int8_t* LX = a.x[0];
+  int64_t wo[PW], xo[PX];  // row * C + chunk offset, for the cursor's branch
+  auto set_rows = [&]() {
 #pragma unroll
-    for (int i = 0; i < PW; ++i) rw[sl][i] = *(const v4i*)(W + (int64_t)wrow[i] * C + kb + cofs[i]);
+    for (int i = 0; i < PW; ++i) wo[i] = (int64_t)wrow[i] * LC + cofs[i];
 #pragma unroll
-    for (int i = 0; i < PX; ++i) rx[sl][i] = *(const v4i*)(X + xrow[i] * C + kb + cofs[i]);
+    for (int i = 0; i < PX; ++i) xo[i] = xrow[i] * LC + cofs[i];
+  };
+  set_rows();
+  auto gload = [&](int sl) {
+#pragma unroll
+    for (int i = 0; i < PW; ++i) rw[sl][i] = *(const v4i*)(LW + wo[i] + lk);
+#pragma unroll
+    for (int i = 0; i < PX; ++i) rx[sl][i] = *(const v4i*)(LX + xo[i] + lk);
+    if (++lsteps < S) {
+      lk += TK;
+      if (lk == LC) {
+        ++lb;
+        lk = 0;
+        LW = a.w[lb];
+        LX = a.x[lb];
+        LC = a.C[lb];
+        set_rows();
+      }
+    }
   };
   auto sstore = [&](int buf, int sl) {
 #pragma unroll
@@ -98,7 +120,7 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
   // Operand loads first; then the branch rescale constants of the tile's
   // channels into LDS.
 #pragma unroll
-  for (int d = 0; d < PF; ++d) gload(d, d);
+  for (int d = 0; d < PF; ++d) gload(d);
   for (int e = tid; e < nbr * TN; e += NT) {
     const int b = e / TN, c = e % TN;
     const int32_t n = min(n0 + c, N - 1);
@@ -151,21 +173,23 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
 
   sstore(0, 0);
   __syncthreads();
-  gload(PF, 0);
-  int b = 0;  // branch of the current step
+  gload(0);
+  int b = 0, ck = 0, csteps = a.C[0] / TK;  // branch of the current step, its steps
   for (int s0 = 0; s0 < S; s0 += PF) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
       const int s = s0 + u;
       if (s < S) {
         compute(s & 1);
-        if (s + 1 == a.kstart[b + 1]) {
+        if (++ck == csteps) {
           fold(b);
           ++b;
+          ck = 0;
+          csteps = b < nbr ? a.C[b] / TK : 0;
         }
       }
       sstore((s + 1) & 1, (u + 1) % PF);
-      gload(s + 1 + PF, (u + 1) % PF);
+      gload((u + 1) % PF);
       __syncthreads();
     }
   }
@@ -201,12 +225,12 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
   }
 }
 
-template <int WN, int WM, int FI, int FJ>
+template <int WN, int WM, int FI, int FJ, int PF = 2>
 hipError_t launch_split_tile(const SplitArgs& a, hipStream_t s) {
   constexpr int TN = 16 * FI * WN, TM = 16 * FJ * WM;
   const int32_t tiles_n = (a.N + TN - 1) / TN;
   const int64_t total = ((a.M + TM - 1) / TM) * tiles_n;
-  hipLaunchKernelGGL((split_conv_kernel<WN, WM, FI, FJ>), dim3((unsigned)total),
+  hipLaunchKernelGGL((split_conv_kernel<WN, WM, FI, FJ, PF>), dim3((unsigned)total),
                      dim3(64 * WN * WM), 0, s, a, tiles_n, total);
   return hipGetLastError();
 }
