@@ -59,8 +59,11 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   __shared__ int8_t glut[EPI == EPI_GELU ? 256 : 1];
   __shared__ RqI64 rqc[TN];                         // output requantization per channel
   __shared__ int64_t qoff[EPI == EPI_QKV ? TM : 1][2];  // QKV: Q/K and V^T offsets per token
-  __shared__ LnChan lnp[LN ? TN : 1];              // LayerNorm constants per channel
-  __shared__ int32_t lnred[LN ? 2 * WN * TM : 1];  // per-wave row sums
+  __shared__ RqI64 lnq[LN ? TN : 1];  // LayerNorm output requantization per channel
+  // per-wave row sums of the LayerNorm epilogue: in the first weight tile,
+  // free once the K loop's last barrier has passed
+  static_assert(2 * WN * TM * 4 <= TN * LDS_ROW, "row sums fit one weight tile");
+  int32_t* const lnred = (int32_t*)&sW[0][0];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -231,21 +234,15 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       qoff[t][1] = bw * Lq.H * 64 * Lq.Twp + li;
     }
   }
-  int ln_wide = 0;
   if (LN) {
-    // Stage the LayerNorm constants of the N (= TN) channels of the row.
+    // Stage the LayerNorm output constants of the N (= TN) channels of the
+    // row: gamma-scaled n plus beta requantizes like an accumulator plus a
+    // bias (|n| < 2^30 and beta inside int32 keep RqI64's bounds).
     for (int c = tid; c < TN; c += NT) {
       const int q = a.ln_nq == 1 ? 0 : c;
-      LnChan p;
-      p.beta = a.ln_beta[c];
-      p.mult = a.ln_mult[q];
-      p.shift = a.ln_shift[q];
-      const float am = fabsf((float)p.mult);
-      const float bound =
-          am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
-      p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
-      lnp[c] = p;
-      ln_wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
+      RqI64 r;
+      r.init(a.ln_mult[q], a.ln_shift[q], a.ln_beta[c]);
+      lnq[c] = r;
     }
   }
 
@@ -273,7 +270,6 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   if constexpr (PF == 1) {
     sstore(0, 0);
     __syncthreads();  // the first tile and the staged constants
-    if (LN) ln_wide = __syncthreads_or(ln_wide);
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + 1 < nk) gload(kt + 1, 0);
       compute(kt & 1);
@@ -286,7 +282,6 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     // leaves the younger slots' loads in flight.
     sstore(0, 0);
     __syncthreads();  // the first tile and the staged constants
-    if (LN) ln_wide = __syncthreads_or(ln_wide);
     gload(min(PF, nk - 1), 0);
     for (int kt0 = 0; kt0 < nk; kt0 += PF) {
 #pragma unroll
@@ -424,17 +419,9 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
         int32_t o[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const LnChan p = lnp[n + r];
           const int32_t d = (int8_t)(xw[i][j] >> (8 * r)) - mu[j];
           const int32_t nn = (d * F[j]) >> 1;  // |d| <= sigma: |d * F| < 2^31
-          if (!ln_wide) {
-            const int32_t t = min(max(nn + p.beta, -p.L), p.L);
-            const int32_t v =
-                (int32_t)(((int64_t)t * p.mult + ((int64_t)1 << (p.shift - 1))) >> p.shift);
-            o[r] = min(max(v, kQmin), kQmax);
-          } else {
-            o[r] = ln_out((int64_t)nn + p.beta, p.mult, p.shift);
-          }
+          o[r] = lnq[n + r].apply(nn);
         }
         *(uint32_t*)(a.y2 + tok[j] + n) = pack4(o[0], o[1], o[2], o[3]);
       }

@@ -226,10 +226,11 @@ struct ChanRq {
 // saturates anyway: L >= 129 * 2^s / |m| + 1 from an fp32 estimate with
 // margin, no clamp when that exceeds 2^30.  Then
 //   (acc * m + c) >> s = floor(((acc + bias) m + 2^(s-1)) / 2^s)
-// exactly: with acc + bias inside int32 (the int32 accumulator) the clamped
-// product stays below about 2^61 in magnitude (|m| <= 130 * 2^(s-30) when
-// there is no clamp), |c| below 2^62 + 2^61, and the shifted value far
-// inside int32, for every shift in [1, 62].  A clamp, a 64-bit multiply-add,
+// exactly whenever |acc + bias| < 3 * 2^30 (a linear's int32 accumulator;
+// LayerNorm's |n| <= 2^30 plus an int32 beta), for every shift in [1, 62]:
+// the clamped sum is at most 2^30, an unclamped one comes with |m| <=
+// 130 * 2^(s-30) (and |m| < 2^31 anyway), so |(acc + bias) m| + 2^(s-1) <
+// 2^63, |c| < 2^62 + 2^61, and the shifted value stays far inside int32.  A clamp, a 64-bit multiply-add,
 // a 64-bit shift and a clamp.
 struct RqI64 {
   int64_t c;
