@@ -510,19 +510,19 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
-      return launch_ln_tile<6, 2, 2, 4, 1>(a, s);  // 192 x 128 tokens, 12 waves of 32 x 64
+      return launch_ln_tile<3, 4, 4, 2, 1>(a, s);  // 192 x 128 tokens, 12 waves of 64 x 32
     }
     if (a.N == 256) {
       if (lat)  // 256 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<8, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<8, 1, 2, 1, 3>(a, s);
-      return launch_ln_tile<8, 1, 2, 4, 1>(a, s);  // 256 x 64 tokens, 8 waves of 32 x 64
+      return launch_ln_tile<4, 2, 4, 2, 1>(a, s);  // 256 x 64 tokens, 8 waves of 64 x 32
     }
     if (a.N == 384) {
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
-      return launch_ln_tile<12, 1, 2, 4, 1>(a, s);  // 384 x 64 tokens, 12 waves of 32 x 64
+      return launch_ln_tile<6, 2, 4, 2, 1>(a, s);  // 384 x 64 tokens, 12 waves of 64 x 32
     }
     return hipErrorInvalidValue;
   }
