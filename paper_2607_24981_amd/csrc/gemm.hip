@@ -504,13 +504,17 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   const int64_t mt64 = (a.M + 63) / 64;
   if (epi == EPI_RESID_LN) {
     // The workgroup holds whole rows (N channels) so the LayerNorm statistics
-    // stay on chip.
+    // stay on chip.  These tiles fill few workgroups per CU (one at N = 384),
+    // so the deep-K linears (fc2) keep two K steps of loads in flight: 4-7%
+    // faster there, slower at K <= 384.
     const bool lat = latency_mode(mt64 * (a.N / 64));
     if (a.N == 192) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
-      return launch_ln_tile<3, 4, 4, 2, 1>(a, s);  // 192 x 128 tokens, 12 waves of 64 x 32
+      // 192 x 128 tokens, 12 waves of 64 x 32
+      return a.K >= 12 * TK ? launch_ln_tile<3, 4, 4, 2, 2>(a, s)
+                            : launch_ln_tile<3, 4, 4, 2, 1>(a, s);
     }
     if (a.N == 256) {
       if (lat)  // 256 x 16 tokens
@@ -522,7 +526,9 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
-      return launch_ln_tile<6, 2, 4, 2, 1>(a, s);  // 384 x 64 tokens, 12 waves of 64 x 32
+      // 384 x 64 tokens, 12 waves of 64 x 32
+      return a.K >= 12 * TK ? launch_ln_tile<6, 2, 4, 2, 2>(a, s)
+                            : launch_ln_tile<6, 2, 4, 2, 1>(a, s);
     }
     return hipErrorInvalidValue;
   }
