@@ -112,7 +112,10 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
     const float am = fabsf((float)p.mult);
     const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
     p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
-    prm[c] = p;
+    // chunk-transposed: channel 16 ch + i sits at i * n16 + ch, so the LPR
+    // lanes of a row (consecutive chunks ch) read consecutive entries instead
+    // of entries 256 bytes apart, all in one LDS bank
+    prm[(c & 15) * (C >> 4) + (c >> 4)] = p;
     wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
   }
   wide = __syncthreads_or(wide);
@@ -159,7 +162,7 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
         uint32_t ow = 0;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const LnChan p = prm[ch * 16 + w * 4 + b];
+          const LnChan p = prm[(w * 4 + b) * n16 + ch];
           const int32_t d = (int8_t)(xv[j][w] >> (8 * b)) - mu;
           const int32_t n = (d * F) >> 1;  // |d| <= sigma: |d * F| < 2^31
           int32_t r;
