@@ -62,6 +62,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // with 4 bytes each per store instruction; staged, an instruction writes
   // whole 128-byte row segments (the batch-32 fc1 20% faster).
   constexpr bool STAGED = PF == 1 && (EPI == EPI_STORE || EPI == EPI_GELU);
+  constexpr bool RSTAGED = PF == 1 && RES;  // residual outputs (and LayerNorm's) likewise
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
   // KB K bytes per step (one or two MFMA K chunks): CPR 16-byte chunks per
   // staged row, rows padded by 16 bytes (80 or 144: the 16 rows of a fragment
@@ -373,8 +374,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
           for (int r = 0; r < 4; ++r)
             o[r] = rq2(u[r], (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
           const uint32_t word = pack4(o[0], o[1], o[2], o[3]);
-          *(uint32_t*)(a.y + tok[j] + n) = word;
-          if (LN) xw[i][j] = word;
+          if (!RSTAGED) *(uint32_t*)(a.y + tok[j] + n) = word;
+          if (LN || RSTAGED) xw[i][j] = word;
         } else {  // EPI_QKV: scatter into window-major Q, K and V^T
           if (!is_v) {
             *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(u[0], u[1], u[2], u[3]);
@@ -387,8 +388,29 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       }
     }
   }
+  // A tile of output words in the accumulator lane layout, written through
+  // LDS as 16-byte row chunks of dst (row stride N).
+  auto stage_store = [&](int8_t* dst, const uint32_t(&wd)[FI][FJ]) {
+    uint32_t* so = (uint32_t*)&sW[0][0];
+    __syncthreads();  // the staging area (weight tiles, LayerNorm sums) is free
+#pragma unroll
+    for (int i = 0; i < FI; ++i)
+#pragma unroll
+      for (int j = 0; j < FJ; ++j)
+        so[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((nch[i] - n0) >> 2)] = wd[i][j];
+    __syncthreads();
+    constexpr int CPT = TN / 16;  // 16-byte chunks per token row
+    for (int c = tid; c < TM * CPT; c += NT) {
+      const int r = c / CPT, q = c - r * CPT;
+      const int64_t m = m0 + r;
+      const int32_t n = n0 + q * 16;
+      if (m < M && n < N) *(v4i*)(dst + m * N + n) = *(const v4i*)(so + r * OSTR + q * 4);
+    }
+  };
+  static_assert(!(STAGED || RSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
+                "the output tile fits the weight tiles");
+  if constexpr (RSTAGED && !LN) stage_store(a.y, xw);
   if constexpr (STAGED) {
-    static_assert(TM * OSTR * 4 <= 2 * TN * LROW, "the output tile fits the weight tiles");
     __syncthreads();
     const uint32_t* so = (const uint32_t*)&sW[0][0];
     constexpr int CPT = TN / 16;  // 16-byte chunks per token row
@@ -442,6 +464,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       F_l = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
     }
     int32_t mu[FJ], F[FJ];
+    uint32_t yw2[FI][FJ] = {};  // staged LayerNorm outputs
 #pragma unroll
     for (int j = 0; j < FJ; ++j) {
       mu[j] = __shfl(mu_l, j * 16 + (lane & 15), 64);
@@ -460,8 +483,13 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
           const int32_t nn = (d * F[j]) >> 1;  // |d| <= sigma: |d * F| < 2^31
           o[r] = lnq[n + r].apply(nn);
         }
-        *(uint32_t*)(a.y2 + tok[j] + n) = pack4(o[0], o[1], o[2], o[3]);
+        if (RSTAGED) yw2[i][j] = pack4(o[0], o[1], o[2], o[3]);
+        else *(uint32_t*)(a.y2 + tok[j] + n) = pack4(o[0], o[1], o[2], o[3]);
       }
+    }
+    if constexpr (RSTAGED) {
+      stage_store(a.y, xw);
+      stage_store(a.y2, yw2);
     }
   }
 }
