@@ -63,6 +63,9 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // whole 128-byte row segments (the batch-32 fc1 20% faster).
   constexpr bool STAGED = PF == 1 && (EPI == EPI_STORE || EPI == EPI_GELU);
   constexpr bool RSTAGED = PF == 1 && RES;  // residual outputs (and LayerNorm's) likewise
+  // QKV: the Q and K words likewise (a 16-channel chunk of a token lies in
+  // one head's 64-byte window-major row); V^T keeps its byte scatter
+  constexpr bool QSTAGED = PF == 1 && EPI == EPI_QKV;
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
   // KB K bytes per step (one or two MFMA K chunks): CPR 16-byte chunks per
   // staged row, rows padded by 16 bytes (80 or 144: the 16 rows of a fragment
@@ -378,7 +381,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
           if (LN || RSTAGED) xw[i][j] = word;
         } else {  // EPI_QKV: scatter into window-major Q, K and V^T
           if (!is_v) {
-            *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(u[0], u[1], u[2], u[3]);
+            if (QSTAGED) xw[i][j] = pack4(u[0], u[1], u[2], u[3]);
+            else *(uint32_t*)(qk_base + tok[j] + ch_qk) = pack4(u[0], u[1], u[2], u[3]);
           } else {
             int8_t* dst = a.qkv.vt + tokv[j] + ch_v;
 #pragma unroll
@@ -407,8 +411,30 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       if (m < M && n < N) *(v4i*)(dst + m * N + n) = *(const v4i*)(so + r * OSTR + q * 4);
     }
   };
-  static_assert(!(STAGED || RSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
+  static_assert(!(STAGED || RSTAGED || QSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
                 "the output tile fits the weight tiles");
+  if constexpr (QSTAGED) {
+    uint32_t* so = (uint32_t*)&sW[0][0];
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < FI; ++i)
+#pragma unroll
+      for (int j = 0; j < FJ; ++j)
+        so[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((nch[i] - n0) >> 2)] = xw[i][j];
+    __syncthreads();
+    const QkvLayout& Lq = a.qkv;
+    constexpr int CPT = TN / 16;
+    for (int c = tid; c < TM * CPT; c += NT) {
+      const int r = c / CPT, q = c - r * CPT;
+      const int32_t n = n0 + q * 16;
+      const int32_t part = n / Lq.D, rem_n = n - part * Lq.D;
+      if (m0 + r < M && n < N && part < 2) {
+        const int32_t h = rem_n >> Lq.hs, cc = rem_n & ((1 << Lq.hs) - 1);
+        int8_t* dst = (part == 0 ? Lq.q : Lq.k) + qoff[r][0] + (int64_t)h * Lq.Tw * 64 + cc;
+        *(v4i*)dst = *(const v4i*)(so + r * OSTR + q * 4);
+      }
+    }
+  }
   if constexpr (RSTAGED && !LN) stage_store(a.y, xw);
   if constexpr (STAGED) {
     __syncthreads();
