@@ -32,6 +32,9 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
                                                                  int64_t tiles_total) {
   constexpr int WTN = 16 * FI, WTM = 16 * FJ;
   constexpr int TN = WTN * WN, TM = WTM * WM, NT = 64 * WN * WM;
+  // output staging: OSTR words per token row, an odd multiple of 4
+  constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
+  static_assert(TM * OSTR * 4 <= 2 * TN * LDS_ROW, "the output tile fits the weight tiles");
   __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
   __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
   __shared__ BrChan brc[kMaxBranches][TN];
@@ -220,7 +223,22 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
         t = t < -(int64_t)cr[r].L ? -(int64_t)cr[r].L : (t > cr[r].L ? cr[r].L : t);
         v[r] = cr[r].apply((int32_t)t);
       }
-      *(uint32_t*)(a.y + m * N + n) = pack4(v[0], v[1], v[2], v[3]);
+      ((uint32_t*)&sW[0][0])[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((n - n0) >> 2)] =
+          pack4(v[0], v[1], v[2], v[3]);
+    }
+  }
+  // The output tile leaves through LDS (the weight tiles, free after the
+  // last step's barrier) as 16-byte row chunks: a lane's own words would put
+  // 16 rows of 4 bytes each into every store instruction.
+  __syncthreads();
+  {
+    const uint32_t* so = (const uint32_t*)&sW[0][0];
+    constexpr int CPT = TN / 16;
+    for (int c = tid; c < TM * CPT; c += NT) {
+      const int r = c / CPT, q = c - r * CPT;
+      const int64_t m = m0 + r;
+      const int32_t n = n0 + q * 16;
+      if (m < M && n < N) *(v4i*)(a.y + m * N + n) = *(const v4i*)(so + r * OSTR + q * 4);
     }
   }
 }
