@@ -639,6 +639,42 @@ def test_encoder_big_grid_sampled():
         assert_same(full[b:b + 1], ref, f"image {b}")
 
 
+def test_encoder_big_grid_384_sampled():
+    """384 channels on a grid large enough for the throughput tiles (the
+    128-byte-step LayerNorm tile, the staged QKV and GELU stores), with a
+    token count that is a multiple of neither 64 nor 128: sampled images
+    against the oracle."""
+    grid, windows = (20, 20), [(10, 10), (0, 0)]
+    B = 29  # 11600 tokens: more than 1024 waves of 64-token LayerNorm tiles
+    say(f"encoder big grid 384 channels B={B}")
+    blocks = _encoder_case(384, 6, 1536, 2, 79)
+    x = rng(80).integers(-127, 128, (B, 400, 384)).astype(np.int8)
+    enc = ilw.Encoder(blocks, windows, *grid)
+    full = host(enc.forward(dev(x)))
+    for b in (0, 14, 28):
+        ref = encoder_ref(blocks, windows, x[b:b + 1], *grid)
+        assert_same(full[b:b + 1], ref, f"image {b}")
+
+
+def test_linear_large_grid_ragged_sampled():
+    """A store-epilogue linear on the throughput tiles (output staged through
+    LDS) with ragged M and N: the first, last and sampled rows against the
+    oracle."""
+    M, N, K = 20001, 1040, 192
+    say(f"linear large grid M={M} N={N} K={K}")
+    g = rng(81)
+    x = g.integers(-127, 128, (M, K)).astype(np.int8)
+    w = g.integers(-127, 128, (N, K)).astype(np.int8)
+    b = g.integers(-2 ** 15, 2 ** 15 + 1, N).astype(np.int32)
+    mult = g.integers(2 ** 29, 2 ** 30 + 1, N).astype(np.int32)
+    shift = g.integers(36, 44, N).astype(np.int32)
+    got = host(ilw.ilw_linear(dev(x), dev(w), dev(b), dev(mult), dev(shift)))
+    rows = np.unique(np.concatenate([np.arange(70), np.arange(M - 200, M),
+                                     g.integers(0, M, 300)]))
+    ref = oracle.linear(x[rows], w, b, mult, shift)
+    assert_same(got[rows], ref, "linear large grid rows")
+
+
 def test_encoder_matches_block_by_block():
     """The encoder entry point (fused LayerNorms) and the block entry point
     give the same bytes."""
