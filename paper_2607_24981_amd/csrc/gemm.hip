@@ -15,7 +15,9 @@
 // across the MFMAs.  The
 // weight tile is the MFMA A operand (rows = channels) and the activation tile
 // the B operand (columns = tokens), so each lane ends up holding four
-// consecutive channels of one token and stores them as one 32-bit word.  K
+// consecutive channels of one token (one 32-bit word).  The throughput tiles
+// transpose their output words through LDS and store 16-byte row chunks; the
+// latency-mode tiles store each lane's words directly.  K
 // advances 64 bytes per step (128 for the 384-channel LayerNorm tile, which
 // runs one workgroup per CU) through double-buffered LDS tiles whose rows are
 // padded by 16 bytes, which keeps the 16-byte fragment reads of a wave free of
