@@ -43,6 +43,21 @@ namespace {
 constexpr int TK = 64;        // K bytes per step
 constexpr int NXCD = 8;
 
+// 16 bytes to dst, which the entry points require to be 4-byte aligned: one
+// 16-byte store when the output base is 16-byte aligned (a16), else four
+// word stores.
+__device__ __forceinline__ void store16(int8_t* dst, const v4i& v, bool a16) {
+  if (a16) {
+    *(v4i*)dst = v;
+  } else {
+    uint32_t* d = (uint32_t*)dst;
+    d[0] = (uint32_t)v[0];
+    d[1] = (uint32_t)v[1];
+    d[2] = (uint32_t)v[2];
+    d[3] = (uint32_t)v[3];
+  }
+}
+
 // WN x WM waves per workgroup; each wave computes FI x FJ MFMA tiles of 16
 // channels x 16 tokens.  PF register slots of staged operands (PF > 1 is the
 // latency mode for small grids: PF K steps of loads in flight, and every
@@ -398,6 +413,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // LDS as 16-byte row chunks of dst (row stride N).
   auto stage_store = [&](int8_t* dst, const uint32_t(&wd)[FI][FJ]) {
     uint32_t* so = (uint32_t*)&sW[0][0];
+    const bool a16 = ((uintptr_t)dst & 15) == 0;
     __syncthreads();  // the staging area (weight tiles, LayerNorm sums) is free
 #pragma unroll
     for (int i = 0; i < FI; ++i)
@@ -410,7 +426,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       const int r = c / CPT, q = c - r * CPT;
       const int64_t m = m0 + r;
       const int32_t n = n0 + q * 16;
-      if (m < M && n < N) *(v4i*)(dst + m * N + n) = *(const v4i*)(so + r * OSTR + q * 4);
+      if (m < M && n < N) store16(dst + m * N + n, *(const v4i*)(so + r * OSTR + q * 4), a16);
     }
   };
   static_assert(!(STAGED || RSTAGED || QSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
@@ -441,13 +457,14 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   if constexpr (STAGED) {
     __syncthreads();
     const uint32_t* so = (const uint32_t*)&sW[0][0];
+    const bool a16 = ((uintptr_t)a.y & 15) == 0;
     constexpr int CPT = TN / 16;  // 16-byte chunks per token row
     for (int c = tid; c < TM * CPT; c += NT) {
       const int r = c / CPT, q = c - r * CPT;
       const int64_t m = m0 + r;
       const int32_t n = n0 + q * 16;
       if (m < M && n < N)
-        *(v4i*)(a.y + m * N + n) = *(const v4i*)(so + r * OSTR + q * 4);
+        store16(a.y + m * N + n, *(const v4i*)(so + r * OSTR + q * 4), a16);
     }
   }
   if (LN) {

@@ -23,6 +23,21 @@ namespace {
 
 constexpr int TK = 64, LDS_ROW = 80, NXCD = 8;
 
+// 16 bytes to dst, which the entry points require to be 4-byte aligned: one
+// 16-byte store when the output base is 16-byte aligned (a16), else four
+// word stores.
+__device__ __forceinline__ void store16(int8_t* dst, const v4i& v, bool a16) {
+  if (a16) {
+    *(v4i*)dst = v;
+  } else {
+    uint32_t* d = (uint32_t*)dst;
+    d[0] = (uint32_t)v[0];
+    d[1] = (uint32_t)v[1];
+    d[2] = (uint32_t)v[2];
+    d[3] = (uint32_t)v[3];
+  }
+}
+
 struct BrChan {
   int32_t mult, shift;
 };
@@ -233,12 +248,13 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
   __syncthreads();
   {
     const uint32_t* so = (const uint32_t*)&sW[0][0];
+    const bool a16 = ((uintptr_t)a.y & 15) == 0;
     constexpr int CPT = TN / 16;
     for (int c = tid; c < TM * CPT; c += NT) {
       const int r = c / CPT, q = c - r * CPT;
       const int64_t m = m0 + r;
       const int32_t n = n0 + q * 16;
-      if (m < M && n < N) *(v4i*)(a.y + m * N + n) = *(const v4i*)(so + r * OSTR + q * 4);
+      if (m < M && n < N) store16(a.y + m * N + n, *(const v4i*)(so + r * OSTR + q * 4), a16);
     }
   }
 }

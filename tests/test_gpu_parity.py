@@ -772,6 +772,24 @@ def test_patch_embed_b32_sampled():
         assert_same(got[b:b + 1], oracle.patch_embed(*_patch_args(db)), f"image {b}")
 
 
+def test_patch_embed_offset_output_b16():
+    """Throughput tiles (staged residual output) with y only 4 bytes aligned:
+    two images against the oracle, guard bytes untouched."""
+    say("patch embed B=16, output at a 4-byte offset")
+    d = synth.patch_embed_inputs(33, 16, 192)
+    T = (d["img"].shape[2] // 16) * (d["img"].shape[3] // 16)
+    buf, y = _offset_output((16, T, 192))
+    ilw.ilw_patch_embed(dev(d["img"]), dev(d["w"]), dev(d["bias"]), dev(d["mult"]),
+                        dev(d["shift"]), dev(d["pos"]), d["pos_mult_a"], d["pos_mult_b"],
+                        d["pos_shift"], y=y)
+    got = host(y)
+    for b in (0, 15):
+        db = dict(d, img=d["img"][b:b + 1])
+        assert_same(got[b:b + 1], oracle.patch_embed(*_patch_args(db)), f"image {b}")
+    rest = host(buf)
+    assert np.all(rest[:4] == 0x5a) and np.all(rest[4 + got.size:] == 0x5a), "guard bytes"
+
+
 def test_encoder_from_image():
     """Image -> patch embedding -> two encoder blocks, against the oracle chain."""
     say("encoder from image")
@@ -870,6 +888,49 @@ def test_split_conv_edge_params():
     bs[0][:] = 30
     ref = oracle.split_conv(xs, ws, bm, bs, None, om, os_)
     assert_same(_split_gpu(xs, ws, bm, bs, None, om, os_), ref, "split conv ties")
+
+
+def _offset_output(shape, off=4):
+    """A poisoned device buffer and a view into it at a 4-byte (not 16-byte)
+    aligned offset, for outputs that only need 4-byte alignment."""
+    n = int(np.prod(shape))
+    buf = torch.full((n + 32,), 0x5a, dtype=torch.int8, device="cuda")
+    return buf, buf[off:off + n].view(*shape)
+
+
+def _check_offset_output(buf, got, ref, what, off=4):
+    assert_same(got, ref, what)
+    rest = host(buf)
+    n = ref.size
+    assert np.all(rest[:off] == 0x5a) and np.all(rest[off + n:] == 0x5a), f"{what}: guard bytes"
+
+
+def test_split_conv_offset_output():
+    """y only 4 bytes aligned: the staged output takes word stores."""
+    say("split conv, output at a 4-byte offset")
+    g = rng(83)
+    xs, ws, bm, bs, bias, om, os_ = _split_case(g, 300, 128, (64, 128), True)
+    ref = oracle.split_conv(xs, ws, bm, bs, bias, om, os_)
+    buf, y = _offset_output(ref.shape)
+    ilw.ilw_split_conv([dev(a) for a in xs], [dev(a) for a in ws],
+                       [dev(a) for a in bm], [dev(a) for a in bs], dev(bias), dev(om),
+                       dev(os_), y=y)
+    _check_offset_output(buf, host(y), ref, "split conv offset output")
+
+
+def test_linear_offset_output_large_grid():
+    """y only 4 bytes aligned on the throughput tiles (staged output)."""
+    M, N, K = 8192, 576, 192
+    say(f"linear offset output M={M} N={N} K={K}")
+    g = rng(84)
+    x = g.integers(-127, 128, (M, K)).astype(np.int8)
+    w = g.integers(-127, 128, (N, K)).astype(np.int8)
+    b = g.integers(-2 ** 15, 2 ** 15 + 1, N).astype(np.int32)
+    mult = g.integers(2 ** 29, 2 ** 30 + 1, N).astype(np.int32)
+    shift = g.integers(36, 44, N).astype(np.int32)
+    buf, y = _offset_output((M, N))
+    ilw.ilw_linear(dev(x), dev(w), dev(b), dev(mult), dev(shift), y=y)
+    _check_offset_output(buf, host(y), oracle.linear(x, w, b, mult, shift), "linear offset output")
 
 
 @pytest.mark.parametrize("per_channel", [False, True])
