@@ -409,19 +409,24 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       }
     }
   }
-  // A tile of output words in the accumulator lane layout, written through
-  // LDS as 16-byte row chunks of dst (row stride N).
-  auto stage_store = [&](int8_t* dst, const uint32_t(&wd)[FI][FJ]) {
+  // Output words in the accumulator lane layout, transposed into LDS token
+  // rows (the weight tiles, free after the K loop; LayerNorm's row sums are
+  // past their last read at the first barrier).
+  auto stage_words = [&](const uint32_t(&wd)[FI][FJ]) {
     uint32_t* so = (uint32_t*)&sW[0][0];
-    const bool a16 = ((uintptr_t)dst & 15) == 0;
-    __syncthreads();  // the staging area (weight tiles, LayerNorm sums) is free
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < FI; ++i)
 #pragma unroll
       for (int j = 0; j < FJ; ++j)
         so[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((nch[i] - n0) >> 2)] = wd[i][j];
     __syncthreads();
-    constexpr int CPT = TN / 16;  // 16-byte chunks per token row
+  };
+  // The staged tile out to dst (row stride N) in 16-byte row chunks.
+  constexpr int CPT = TN / 16;  // 16-byte chunks per token row
+  auto copy_rows = [&](int8_t* dst) {
+    const uint32_t* so = (const uint32_t*)&sW[0][0];
+    const bool a16 = ((uintptr_t)dst & 15) == 0;
     for (int c = tid; c < TM * CPT; c += NT) {
       const int r = c / CPT, q = c - r * CPT;
       const int64_t m = m0 + r;
@@ -431,17 +436,20 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   };
   static_assert(!(STAGED || RSTAGED || QSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
                 "the output tile fits the weight tiles");
+  if constexpr (STAGED) {  // the words went to LDS in the loop above
+    __syncthreads();
+    copy_rows(a.y);
+  }
+  if constexpr (RSTAGED && !LN) {
+    stage_words(xw);
+    copy_rows(a.y);
+  }
   if constexpr (QSTAGED) {
-    uint32_t* so = (uint32_t*)&sW[0][0];
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < FI; ++i)
-#pragma unroll
-      for (int j = 0; j < FJ; ++j)
-        so[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((nch[i] - n0) >> 2)] = xw[i][j];
-    __syncthreads();
+    // Q and K chunks to their window-major rows (16-byte aligned: the rows
+    // are 64 bytes, the workspace 16-byte aligned)
+    stage_words(xw);
+    const uint32_t* so = (const uint32_t*)&sW[0][0];
     const QkvLayout& Lq = a.qkv;
-    constexpr int CPT = TN / 16;
     for (int c = tid; c < TM * CPT; c += NT) {
       const int r = c / CPT, q = c - r * CPT;
       const int32_t n = n0 + q * 16;
@@ -451,20 +459,6 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
         int8_t* dst = (part == 0 ? Lq.q : Lq.k) + qoff[r][0] + (int64_t)h * Lq.Tw * 64 + cc;
         *(v4i*)dst = *(const v4i*)(so + r * OSTR + q * 4);
       }
-    }
-  }
-  if constexpr (RSTAGED && !LN) stage_store(a.y, xw);
-  if constexpr (STAGED) {
-    __syncthreads();
-    const uint32_t* so = (const uint32_t*)&sW[0][0];
-    const bool a16 = ((uintptr_t)a.y & 15) == 0;
-    constexpr int CPT = TN / 16;  // 16-byte chunks per token row
-    for (int c = tid; c < TM * CPT; c += NT) {
-      const int r = c / CPT, q = c - r * CPT;
-      const int64_t m = m0 + r;
-      const int32_t n = n0 + q * 16;
-      if (m < M && n < N)
-        store16(a.y + m * N + n, *(const v4i*)(so + r * OSTR + q * 4), a16);
     }
   }
   if (LN) {
@@ -533,8 +527,10 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       }
     }
     if constexpr (RSTAGED) {
-      stage_store(a.y, xw);
-      stage_store(a.y2, yw2);
+      stage_words(xw);
+      copy_rows(a.y);
+      stage_words(yw2);
+      copy_rows(a.y2);
     }
   }
 }
