@@ -85,7 +85,9 @@ __device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
 // key range) pairs for P V, whose int32 partial sums are added through LDS.
 // MASK says which Shiftmax words may hold no key: 0 any word past the keys
 // (whole words, T_w % 4 == 0), 1 any byte past the keys (T_w % 4 != 0),
-// 2 only the last word step's (T_w = Twp and (JW - 1) LPR <= Twp / 4).
+// 2 only the last word step's (T_w = Twp and (JW - 1) LPR <= Twp / 4),
+// 3 only the last two steps' (whole words, JW LPR = Twp / 4 and
+// (JW - 2) LPR <= T_w / 4: every step stays inside the row).
 template <int R, int LPR, bool NARROW, int MASK, int NW, int JW>
 __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t lds_row,
                                                             int32_t clampL, int32_t nrb,
@@ -223,8 +225,9 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 #pragma unroll
       for (int j = 0; j < JW; ++j) {
         const int32_t wd = k + j * LPR;
-        const bool tail = MASK != 2 || j == JW - 1;  // a step that may pass the keys
-        const uint32_t word = row[tail ? min(wd, nword - 1) : wd];  // inside the row
+        // a step that may pass the keys
+        const bool tail = MASK == 2 ? j == JW - 1 : (MASK == 3 ? j >= JW - 2 : true);
+        const uint32_t word = row[tail && MASK != 3 ? min(wd, nword - 1) : wd];  // inside the row
         // max - score per byte (both biased): every valid byte is >= 0, and a
         // borrow from an invalid (higher) byte never reaches a valid one.
         // Words past the window index table entry 255, which is 0.
@@ -266,7 +269,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
           const int32_t wd = k + j * LPR;
           const uint32_t pw = pack_min_bytes(__umulhi(e[j][0], Fs), __umulhi(e[j][1], Fs),
                                              __umulhi(e[j][2], Fs), __umulhi(e[j][3], Fs), pcap2);
-          if ((MASK == 2 && j < JW - 1) || wd < nword) row[wd] = pw;  // padding -> 0
+          if ((MASK == 2 && j < JW - 1) || MASK == 3 || wd < nword) row[wd] = pw;  // padding -> 0
         }
       } else {
 #pragma unroll
@@ -275,7 +278,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
           uint32_t p[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) p[b] = (uint32_t)(((uint64_t)e[j][b] * F) >> sh);
-          if ((MASK == 2 && j < JW - 1) || wd < nword)
+          if ((MASK == 2 && j < JW - 1) || MASK == 3 || wd < nword)
             row[wd] = pack_min_bytes(p[0], p[1], p[2], p[3], pcap2);  // padding -> 0
         }
       }
@@ -404,12 +407,16 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStrea
   // A lane sums at most 4 JW ShiftExp values, each at most emax = ShiftExp(0)
   // = I0 * 2^k_inter: 32-bit partial sums are exact while 4 JW emax < 2^32.
   const bool narrow = emax * 4 * JW < ((int64_t)1 << 32);
-  const int mask = (a.Tw & 3) ? 1 : (a.Tw == a.Twp && (JW - 1) * LPR <= (a.Twp >> 2) ? 2 : 0);
+  int mask = (a.Tw & 3) ? 1 : (a.Tw == a.Twp && (JW - 1) * LPR <= (a.Twp >> 2) ? 2 : 0);
+  // exact fit: mask only the last two word steps (the 400-token windows, 3%)
+  if (mask == 0 && JW * LPR == (a.Twp >> 2) && (JW - 2) * LPR <= (a.Tw >> 2)) mask = 3;
   if (narrow) {
+    if (mask == 3) return launch_variant<R, LPR, true, 3, NW, JW>(a, clampL, s);
     if (mask == 2) return launch_variant<R, LPR, true, 2, NW, JW>(a, clampL, s);
     return mask ? launch_variant<R, LPR, true, 1, NW, JW>(a, clampL, s)
                 : launch_variant<R, LPR, true, 0, NW, JW>(a, clampL, s);
   }
+  if (mask == 3) return launch_variant<R, LPR, false, 3, NW, JW>(a, clampL, s);
   if (mask == 2) return launch_variant<R, LPR, false, 2, NW, JW>(a, clampL, s);
   return mask ? launch_variant<R, LPR, false, 1, NW, JW>(a, clampL, s)
               : launch_variant<R, LPR, false, 0, NW, JW>(a, clampL, s);
