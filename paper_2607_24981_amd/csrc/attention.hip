@@ -424,10 +424,11 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStrea
 
 // The 16-word variants with the smallest word count the window needs: 13
 // words cover 1600-token rows over 32 lanes, 14 the 448-byte padded
-// 400-token rows over 8 lanes.
+// 400-token rows over 8 lanes, 10 the 320-byte padded 300-query rows.
 template <int R, int LPR, int NW>
 hipError_t launch_fit16(const AttnArgs& a, int32_t clampL, int64_t emax, hipStream_t s) {
   const int32_t jw = ((a.Twp >> 2) + LPR - 1) / LPR;
+  if (jw <= 10) return launch_rows<R, LPR, NW, 10>(a, clampL, emax, s);
   if (jw <= 13) return launch_rows<R, LPR, NW, 13>(a, clampL, emax, s);
   if (jw == 14) return launch_rows<R, LPR, NW, 14>(a, clampL, emax, s);
   return launch_rows<R, LPR, NW, 16>(a, clampL, emax, s);
@@ -443,6 +444,8 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t w
   // chains (measured against one row group of 16 or 64 lanes).
   if (a.Twp <= 512) {
     if constexpr (R == 32) return launch_fit16<32, 8, 4>(a, clampL, emax, s);
+    // 7 words over 16 lanes fit the 448-byte padded 400-token rows exactly
+    if ((a.Twp >> 2) <= 7 * 16) return launch_rows<R, 16, 4, 7>(a, clampL, emax, s);
     return launch_rows<R, 16, 4>(a, clampL, emax, s);
   }
   if (a.Twp <= 1024) return launch_rows<R, 32, 4>(a, clampL, emax, s);
