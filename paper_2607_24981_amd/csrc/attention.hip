@@ -69,11 +69,16 @@ __device__ __forceinline__ uint32_t pack_min_bytes(uint32_t a, uint32_t b, uint3
                                0x06040200u);
 }
 
-// floor((2^31 - 1) / S_R) for S_R in [1, 2^31 - 1]: an FP64 reciprocal
-// estimate is within one of the quotient; one integer correction makes it
-// exact.
+// floor((2^31 - 1) / S_R) for S_R in [1, 2^31 - 1]: the hardware FP64
+// reciprocal estimate, refined by one Newton step, gives the quotient to
+// within one; one integer correction makes it exact.  (The raw estimate is
+// not enough: with a static s_d, S_R can be small and the quotient near
+// 2^31, where its relative error exceeds one unit.)
 __device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
-  const double est = 2147483647.0 * __builtin_amdgcn_rcp((double)sr);
+  const double s = (double)sr;
+  double rc = __builtin_amdgcn_rcp(s);
+  rc = fma(rc, fma(-s, rc, 1.0), rc);
+  const double est = 2147483647.0 * rc;
   int64_t q = (int64_t)est;
   const int64_t r = 2147483647LL - q * (int64_t)sr;
   q += r < 0 ? -1 : (r >= (int64_t)sr ? 1 : 0);

@@ -269,7 +269,32 @@ ATTN_CASES = [
     (1, 1, 1, 0, 0, 1),        # a single token
     (1, 45, 45, 0, 0, 2),      # 2025 tokens: near the window limit
     (1, 32, 64, 0, 0, 2),      # 2048 tokens: the limit, a multiple of 64
+    # 388 tokens (448 padded bytes, an exact fit of the Shiftmax words): only
+    # the last two word steps masked, the first of them partly valid; 16-row
+    # blocks (7 words over 16 lanes) and, at batch 40, 32-row blocks (14 over 8)
+    (1, 4, 97, 0, 0, 1),
+    (40, 4, 97, 0, 0, 1),
+    # 300 tokens at 32-row blocks: 10 words over 8 lanes, an exact fit
+    (26, 10, 30, 0, 0, 2),
 ]
+
+
+@pytest.mark.parametrize("s_d", [20, 25])
+def test_attention_static_sd_small_denominator(s_d):
+    """A static s_d far above the dynamic one with a large I0: S_R is a few
+    dozen, so F = floor((2^31 - 1) / S_R) is near 2^26, where an unrefined
+    FP64 reciprocal is off by more than one unit (a regression case)."""
+    B, gh, gw, H = 1, 16, 16, 3
+    say(f"attention static s_d={s_d}, I0=64")
+    g = rng(900 + s_d)
+    D, T = 64 * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    p = {"score_mult": (1 << 29) + 4321, "score_shift": 39, "smax_I0": 64, "smax_s_d": s_d,
+         "pv_mult": (1 << 29) + 777, "pv_shift": 36}
+    ref = oracle.attention(qkv[0], gh, gw, 0, 0, H, 64, p["score_mult"], p["score_shift"],
+                           p["smax_I0"], p["pv_mult"], p["pv_shift"], s_d=s_d)[None]
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, 0, 0, H, p))
+    assert_same(got, ref, "attention static s_d")
 
 
 @pytest.mark.parametrize("case", ATTN_CASES)
