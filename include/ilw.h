@@ -199,6 +199,28 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y,
                       int32_t win_w, void* workspace, size_t workspace_bytes,
                       void* stream);
 
+/* Size of the library's static device scratch used by
+ * ilw_block_forward_noalloc: 32 MiB on each GPU the library runs on. */
+#define ILW_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+/* ilw_block_forward without a caller workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture, serving loops and
+ * harnesses that forbid hipMalloc.  Arguments, results and error behaviour
+ * are those of ilw_block_forward; the workspace is instead a file-scope
+ * device array of ILW_NOALLOC_SCRATCH_BYTES that each GPU holds from the
+ * first call on it until the process ends.  Nothing is allocated or freed:
+ * the first call on a device looks the array's address up once
+ * (hipGetSymbolAddress) with that device current.  A call whose workspace
+ * need (ilw_block_workspace_bytes) exceeds the scratch returns
+ * ILW_E_WORKSPACE before any launch.  All calls on one GPU share its
+ * scratch, which keeps the last call's contents: calls in stream order are
+ * safe, calls that overlap in time on one GPU (several streams or threads)
+ * race and give undefined results.  No byte of the scratch needs to start
+ * at zero: every byte a kernel reads was written earlier in the same call.
+ * The device is the caller's current device. */
+int ilw_block_forward_noalloc(const ilw_block_params* p, const int8_t* x, int8_t* y,
+                              int32_t batch, int32_t grid_h, int32_t grid_w,
+                              int32_t win_h, int32_t win_w, void* stream);
+
 /* ------------------------------------------------------------------------
  * Patch embedding, the encoder's input layer (Table mappability: a
  * convolution plus an add; Sec. 3.2.1 integer linear formulation): a

@@ -79,6 +79,36 @@ struct StageTimer {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// ---- static scratch of ilw_block_forward_noalloc -------------------------
+// One file-scope device array; every GPU that loads the library holds its
+// own copy at its own address.  Host code never passes the array's name to a
+// kernel (on the host it is only a stand-in for the symbol): it uses the
+// device address looked up once per device, with that device current.
+static __device__ __align__(256) int8_t scratch[ILW_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int8_t* g_scratch_addr[kMaxDevices];
+
+int scratch_of_current_device(int8_t** out) {
+  int dev = -1;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return fail(ILW_E_HIP, "hipGetDevice: %s", hipGetErrorString(he));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(ILW_E_UNSUPPORTED, "device ordinal %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* addr = nullptr;
+    he = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+    if (he != hipSuccess || !addr)
+      return fail(ILW_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                  hipGetErrorString(he));
+    g_scratch_addr[dev] = (int8_t*)addr;
+  }
+  *out = g_scratch_addr[dev];
+  return ILW_OK;
+}
+
 #define REQUIRE(cond, code, ...)            \
   do {                                      \
     if (!(cond)) return fail(code, __VA_ARGS__); \
@@ -861,6 +891,29 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int
   REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
   BlockLayout L;
   block_layout(p, batch, g, (int8_t*)workspace, &L);
+  int ready = READY_NONE;
+  return run_block(p, nullptr, nullptr, x, y, batch, g, L, READY_NONE, &ready,
+                   (hipStream_t)stream);
+}
+
+int ilw_block_forward_noalloc(const ilw_block_params* p, const int8_t* x, int8_t* y,
+                              int32_t batch, int32_t grid_h, int32_t grid_w, int32_t win_h,
+                              int32_t win_w, void* stream) {
+  Geometry g;
+  int e;
+  if ((e = check_block(p, batch, grid_h, grid_w, win_h, win_w, &g))) return e;
+  if (batch == 0) return ok();
+  REQUIRE(x && y, ILW_E_NULL, "x and y must not be NULL");
+  REQUIRE(aligned16(x) && aligned16(y), ILW_E_PARAM, "x and y must be 16-byte aligned");
+  const size_t need = block_layout(p, batch, g, nullptr, nullptr);
+  REQUIRE(need <= ILW_NOALLOC_SCRATCH_BYTES, ILW_E_WORKSPACE,
+          "ilw_block_forward_noalloc: this block needs %zu bytes of scratch, above the "
+          "static scratch of %zu bytes (use ilw_block_forward with a workspace)",
+          need, (size_t)ILW_NOALLOC_SCRATCH_BYTES);
+  int8_t* ws = nullptr;
+  if ((e = scratch_of_current_device(&ws))) return e;
+  BlockLayout L;
+  block_layout(p, batch, g, ws, &L);
   int ready = READY_NONE;
   return run_block(p, nullptr, nullptr, x, y, batch, g, L, READY_NONE, &ready,
                    (hipStream_t)stream);

@@ -98,6 +98,8 @@ _SIGS = {
     "ilw_block_workspace_bytes": (c_size, [ctypes.POINTER(BlockParams)] + [c_i32] * 5),
     "ilw_block_forward": (ctypes.c_int, [ctypes.POINTER(BlockParams), c_vp, c_vp] +
                           [c_i32] * 5 + [c_vp, c_size, c_vp]),
+    "ilw_block_forward_noalloc": (ctypes.c_int, [ctypes.POINTER(BlockParams), c_vp, c_vp] +
+                                  [c_i32] * 5 + [c_vp]),
     "ilw_encoder_workspace_bytes": (c_size, [c_vp, c_i32, c_vp, c_i32, c_i32, c_i32]),
     "ilw_encoder_forward": (ctypes.c_int, [c_vp, c_i32, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32,
                                            c_vp, c_size, c_vp]),
@@ -318,6 +320,23 @@ def ilw_block_forward(block: DeviceBlock, x, grid_h, grid_w, win_h, win_w, y=Non
                                  _stream())
     _check(rc, "ilw_block_forward")
     return y
+
+
+def ilw_block_forward_noalloc(block: DeviceBlock, x, grid_h, grid_w, win_h, win_w, y=None):
+    """ilw_block_forward on the library's static device scratch (no workspace
+    argument; the library allocates nothing).  y must be given by callers
+    that cannot allocate."""
+    B = x.shape[0]
+    if y is None:
+        y = torch.empty_like(x)
+    rc = lib().ilw_block_forward_noalloc(ctypes.byref(block.struct), _dev(x, torch.int8, "x"),
+                                         _dev(y, torch.int8, "y"), B, grid_h, grid_w, win_h,
+                                         win_w, _stream())
+    _check(rc, "ilw_block_forward_noalloc")
+    return y
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class Encoder:
