@@ -12,7 +12,9 @@
 // before the MFMAs of the current one; they are unconditional (out-of-range
 // rows are clamped onto valid ones and only feed outputs that are never
 // stored), which keeps the memory counters exact and the loads in flight
-// across the MFMAs.  The
+// across the MFMAs.  The workgroup barriers wait for LDS operations only
+// (lds_sync): __syncthreads() would also wait for every outstanding global
+// load and drain the PF-deep pipeline at each K step.  The
 // weight tile is the MFMA A operand (rows = channels) and the activation tile
 // the B operand (columns = tokens), so each lane ends up holding four
 // consecutive channels of one token (one 32-bit word).  The throughput tiles
@@ -63,7 +65,7 @@ __device__ __forceinline__ void store16(int8_t* dst, const v4i& v, bool a16) {
 // latency mode for small grids: PF K steps of loads in flight, and every
 // epilogue input -- channel constants, residual words -- loaded before the
 // main loop so that the kernel pays about one memory round trip).
-template <int WN, int WM, int FI, int FJ, int EPI, bool KTAIL, int PF, int KB = TK>
+template <int WN, int WM, int FI, int FJ, int EPI, bool KTAIL, int PF, int KB = TK, bool LAT = (PF > 1)>
 __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32_t tiles_n,
                                                               int64_t tiles_total) {
   constexpr int WTN = 16 * FI, WTM = 16 * FJ;  // wave tile
@@ -71,18 +73,18 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   constexpr bool LN = EPI == EPI_RESID_LN;
   constexpr bool XP = EPI == EPI_PATCH;
   constexpr bool RES = EPI == EPI_RESID || LN || XP;
-  constexpr bool EARLY = PF > 1;
+  constexpr bool EARLY = LAT;
   // Store and GELU epilogues of the throughput tiles go through LDS: the
   // tile's output words are transposed there (OSTR words per token row, an
   // odd multiple of 4: the 16 tokens of a fragment land on disjoint banks)
   // and leave as 16-byte row chunks.  A lane's own words would cover 16 rows
   // with 4 bytes each per store instruction; staged, an instruction writes
   // whole 128-byte row segments (the batch-32 fc1 20% faster).
-  constexpr bool STAGED = PF == 1 && (EPI == EPI_STORE || EPI == EPI_GELU);
-  constexpr bool RSTAGED = PF == 1 && RES;  // residual outputs (and LayerNorm's) likewise
+  constexpr bool STAGED = !LAT && (EPI == EPI_STORE || EPI == EPI_GELU);
+  constexpr bool RSTAGED = !LAT && RES;  // residual outputs (and LayerNorm's) likewise
   // QKV: the Q and K words likewise (a 16-channel chunk of a token lies in
   // one head's 64-byte window-major row); V^T keeps its byte scatter
-  constexpr bool QSTAGED = PF == 1 && EPI == EPI_QKV;
+  constexpr bool QSTAGED = !LAT && EPI == EPI_QKV;
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
   // KB K bytes per step (one or two MFMA K chunks): CPR 16-byte chunks per
   // staged row, rows padded by 16 bytes (80 or 144: the 16 rows of a fragment
@@ -288,9 +290,13 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 #pragma unroll
     for (int j = 0; j < FJ; ++j) acc[i][j] = zero;
   const int frag_off = (lane & 15) * LROW + (lane >> 4) * 16;
-  auto compute = [&](int buf) {
+  // compute(buf, kt): the MFMAs of K step kt; with a K tail, 64-byte halves
+  // of the last step that lie wholly past K are skipped (their chunks are
+  // zero-filled anyway)
+  auto compute = [&](int buf, int kt) {
 #pragma unroll
     for (int h = 0; h < KB / TK; ++h) {
+      if (KTAIL && h > 0 && kt * KB + h * TK >= K) break;
       v4i fa[FI], fb[FJ];
 #pragma unroll
       for (int i = 0; i < FI; ++i)
@@ -308,28 +314,28 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
 
   if constexpr (PF == 1) {
     sstore(0, 0);
-    __syncthreads();  // the first tile and the staged constants
+    lds_sync();  // the first tile and the staged constants
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + 1 < nk) gload(kt + 1, 0);
-      compute(kt & 1);
+      compute(kt & 1, kt);
       if (kt + 1 < nk) sstore((kt + 1) & 1, 0);
-      __syncthreads();
+      lds_sync();
     }
   } else {
     // Loads are issued on every path (steps past the end re-read the last
     // one), so the memory counter wait before each LDS store is exact: it
     // leaves the younger slots' loads in flight.
     sstore(0, 0);
-    __syncthreads();  // the first tile and the staged constants
+    lds_sync();  // the first tile and the staged constants
     gload(min(PF, nk - 1), 0);
     for (int kt0 = 0; kt0 < nk; kt0 += PF) {
 #pragma unroll
       for (int u = 0; u < PF; ++u) {
         const int kt = kt0 + u;
-        if (kt < nk) compute(kt & 1);
+        if (kt < nk) compute(kt & 1, kt);
         sstore((kt + 1) & 1, (u + 1) % PF);
         gload(min(kt + 1 + PF, nk - 1), (u + 1) % PF);
-        __syncthreads();
+        lds_sync();
       }
     }
   }
@@ -414,13 +420,13 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // past their last read at the first barrier).
   auto stage_words = [&](const uint32_t(&wd)[FI][FJ]) {
     uint32_t* so = (uint32_t*)&sW[0][0];
-    __syncthreads();
+    lds_sync();
 #pragma unroll
     for (int i = 0; i < FI; ++i)
 #pragma unroll
       for (int j = 0; j < FJ; ++j)
         so[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((nch[i] - n0) >> 2)] = wd[i][j];
-    __syncthreads();
+    lds_sync();
   };
   // The staged tile out to dst (row stride N) in 16-byte row chunks.
   constexpr int CPT = TN / 16;  // 16-byte chunks per token row
@@ -437,7 +443,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   static_assert(!(STAGED || RSTAGED || QSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
                 "the output tile fits the weight tiles");
   if constexpr (STAGED) {  // the words went to LDS in the loop above
-    __syncthreads();
+    lds_sync();
     copy_rows(a.y);
   }
   if constexpr (RSTAGED && !LN) {
@@ -484,7 +490,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
         lnred[(wn * TM + t) * 2 + 1] = SS;
       }
     }
-    __syncthreads();
+    lds_sync();
     // Row statistics with one token per lane (the Newton steps form a serial
     // dependency chain; one chain per lane keeps it short), then each lane
     // fetches those of its FJ tokens.
@@ -535,7 +541,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   }
 }
 
-template <int WN, int WM, int FI, int FJ, bool KT, int PF>
+template <int WN, int WM, int FI, int FJ, bool KT, int PF, int KB = TK, bool LAT = (PF > 1)>
 hipError_t launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
   constexpr int TN = 16 * FI * WN, TM = 16 * FJ * WM;
   const int32_t tiles_n = (a.N + TN - 1) / TN;
@@ -543,7 +549,7 @@ hipError_t launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
   const int64_t total = tiles_m * tiles_n;
   dim3 grid((unsigned)total), block(64 * WN * WM);
 #define ILW_LAUNCH(E)                                                                   \
-  hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, FI, FJ, E, KT, PF>), grid, block, 0, s, a, \
+  hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, FI, FJ, E, KT, PF, KB, LAT>), grid, block, 0, s, a, \
                      tiles_n, total)
   switch (epi) {
     case EPI_STORE: ILW_LAUNCH(EPI_STORE); break;
@@ -551,8 +557,8 @@ hipError_t launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
     case EPI_RESID: ILW_LAUNCH(EPI_RESID); break;
     case EPI_QKV: ILW_LAUNCH(EPI_QKV); break;
     case EPI_PATCH:
-      if constexpr (!KT) ILW_LAUNCH(EPI_PATCH);
-      else return hipErrorInvalidValue;  // K = 256 * channels has no tail
+      if constexpr (!KT && KB == TK) ILW_LAUNCH(EPI_PATCH);
+      else return hipErrorInvalidValue;  // K = 256 * channels: 64-byte steps, no tail
       break;
     default: return hipErrorInvalidValue;
   }
@@ -561,26 +567,26 @@ hipError_t launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
 }
 
 // Fused residual + LayerNorm: the workgroup holds whole rows (TN == N).
-template <int WN, int WM, int FI, int FJ, bool KT, int PF, int KB = TK>
+template <int WN, int WM, int FI, int FJ, bool KT, int PF, int KB = TK, bool LAT = (PF > 1)>
 hipError_t launch_ln(const GemmArgs& a, hipStream_t s) {
   constexpr int TN = 16 * FI * WN, TM = 16 * FJ * WM;
   if (a.N != TN) return hipErrorInvalidValue;
   const int64_t total = (a.M + TM - 1) / TM;
-  hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, FI, FJ, EPI_RESID_LN, KT, PF, KB>), dim3((unsigned)total),
-                     dim3(64 * WN * WM), 0, s, a, 1, total);
+  hipLaunchKernelGGL((gemm_i8_kernel<WN, WM, FI, FJ, EPI_RESID_LN, KT, PF, KB, LAT>),
+                     dim3((unsigned)total), dim3(64 * WN * WM), 0, s, a, 1, total);
   return hipGetLastError();
 }
 
-template <int WN, int WM, int FI, int FJ, int PF>
+template <int WN, int WM, int FI, int FJ, int PF, int KB = TK, bool LAT = (PF > 1)>
 hipError_t launch_tile(int epi, const GemmArgs& a, hipStream_t s) {
-  return a.K % TK == 0 ? launch_cfg<WN, WM, FI, FJ, false, PF>(epi, a, s)
-                       : launch_cfg<WN, WM, FI, FJ, true, PF>(epi, a, s);
+  return a.K % KB == 0 ? launch_cfg<WN, WM, FI, FJ, false, PF, KB, LAT>(epi, a, s)
+                       : launch_cfg<WN, WM, FI, FJ, true, PF, KB, LAT>(epi, a, s);
 }
 
-template <int WN, int WM, int FI, int FJ, int PF>
+template <int WN, int WM, int FI, int FJ, int PF, int KB = TK, bool LAT = (PF > 1)>
 hipError_t launch_ln_tile(const GemmArgs& a, hipStream_t s) {
-  return a.K % TK == 0 ? launch_ln<WN, WM, FI, FJ, false, PF>(a, s)
-                       : launch_ln<WN, WM, FI, FJ, true, PF>(a, s);
+  return a.K % KB == 0 ? launch_ln<WN, WM, FI, FJ, false, PF, KB, LAT>(a, s)
+                       : launch_ln<WN, WM, FI, FJ, true, PF, KB, LAT>(a, s);
 }
 
 // Latency mode (ILW_GEMM_PF=1|3 forces it off or on): grids of at most about
@@ -652,6 +658,10 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
+  // Wide QKV linears on 256-channel x 128-token tiles of 8 waves of 64 x 64
+  // (12% faster than 128 x 128 on the 1152-channel QKV of the 384-wide
+  // encoder at batch 8; slower for fc1)
+  if (epi == EPI_QKV && a.N >= 1024) return launch_tile<4, 2, 4, 4, 1>(epi, a, s);
   return launch_tile<2, 4, 4, 2, 1>(epi, a, s);
 }
 

@@ -70,6 +70,18 @@ __device__ __forceinline__ int32_t sd_gelu(int32_t x, int32_t I0, int32_t k_inte
   return x * d;
 }
 
+// Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
+// operations (lgkmcnt(0)), then s_barrier.  Unlike __syncthreads() it does
+// not wait for outstanding global loads (vmcnt), so loads issued for later K
+// steps stay in flight across it.  The empty asm statements keep the
+// compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void lds_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // vmcnt 63, expcnt 7: no wait; lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Wave-wide reductions (wave64).
 __device__ __forceinline__ int32_t wave_sum_i32(int32_t v) {
 #pragma unroll
