@@ -78,6 +78,9 @@ KERNEL_OF_STAGE = {
     "layernorm": ("layernorm_rows_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
     "split_conv": ("split_conv_kernel", ["paper_2607_24981_amd/csrc/split_conv.hip", _INTERNAL]),
     "patch_embed": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
+    "shiftmax": ("shiftmax_rows_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
+    "sdshiftgelu": ("gelu_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
+    "residual": ("residual_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
 }
 
 
@@ -171,6 +174,8 @@ def main():
 
     if args.workload in synth.SPLIT_WORKLOADS:
         return bench_split(args, synth.SPLIT_WORKLOADS[args.workload])
+    if args.workload in synth.ROWOP_WORKLOADS:
+        return bench_rowop(args, synth.ROWOP_WORKLOADS[args.workload])
     if args.workload in synth.DECODER_WORKLOADS:
         return bench_decoder(args, synth.DECODER_WORKLOADS[args.workload])
     wl = synth.WORKLOADS[args.workload]
@@ -524,6 +529,97 @@ def bench_split(args, wl):
                        "branches": list(wl.branches), "out_channels": wl.out,
                        "launch": "eager" if args.no_graph else f"hip graph, {G} steps per replay",
                        "gemm_ops_per_step": ops},
+            "roofline": roof, "cpu_baseline": cpu, "parity": parity}
+    print(json.dumps(line), flush=True)
+    if parity not in (None, "bit-exact"):
+        sys.exit(1)
+
+
+def bench_rowop(args, wl):
+    """A stand-alone row-wise or element-wise operator over the tensor it
+    sees in the encoder; reported as achieved HBM GB/s of its algorithmic
+    bytes (int8 in and out once) against the 8 TB/s peak."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24981_amd import ilw, synth
+    log(f"workload {wl.name}: {wl.op} over {wl.rows} x {wl.cols} int8")
+    d = synth.rowop_inputs(wl, args.seed)
+    x = ilw.to_device(d["x"])
+    y = torch.empty_like(x)
+    if wl.op == "shiftmax":
+        call = lambda: ilw.ilw_shiftmax(x, d["I0"], y=y)
+    elif wl.op == "sdshiftgelu":
+        call = lambda: ilw.ilw_sdshiftgelu(x, d["I0"], d["mult"], d["shift"], y=y)
+    elif wl.op == "layernorm":
+        beta, mult, shift = (ilw.to_device(d[k]) for k in ("beta", "mult", "shift"))
+        call = lambda: ilw.ilw_int_layernorm(x, beta, mult, shift, 10, y=y)
+    else:
+        b = ilw.to_device(d["b"])
+        call = lambda: ilw.ilw_residual_add(x, b, d["mult_a"], d["mult_b"], d["shift"], y=y)
+    G = 1 if args.no_graph or args.steps % args.steps_per_graph else args.steps_per_graph
+    step = call
+    if not args.no_graph:
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            for _ in range(3):
+                call()
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(G):
+                call()
+        step = graph.replay
+    wall_ms, ev_ms = _timed(step, args.steps // G, max(1, args.warmup // G))
+    wall_ms, ev_ms = wall_ms / G, ev_ms / G
+    nbytes = wl.bytes_moved()
+    gbs = nbytes / (ev_ms * 1e-3) / 1e9
+    log(f"timed {args.steps} calls ({G} per graph replay): {ev_ms * 1e3:.2f} us per call, "
+        f"{gbs:.1f} GB/s of {nbytes / 1e6:.2f} MB")
+    spread = [round(v / G, 5) for v in _step_spread(step)]
+    result = y.cpu().numpy()
+    roof = {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 5), "kernel": KERNEL_OF_STAGE[wl.op if wl.op
+                                                                             != "layernorm"
+                                                                             else "layernorm"][0],
+            "stage": wl.op, "ms_per_launch": round(ev_ms, 5), "algorithmic_per_launch": nbytes,
+            "traffic": measured_traffic(wl.op, wl.name)}
+
+    cpu = parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        if not os.path.exists(oracle._SO):
+            oracle.build()
+        n = min(wl.rows, max(1, (64 << 20) // (64 * wl.cols)))  # a sample of whole rows
+        xs = d["x"][:n]
+        c0 = time.perf_counter()
+        if wl.op == "shiftmax":
+            ref = oracle.shiftmax_rows(xs, d["I0"])
+        elif wl.op == "sdshiftgelu":
+            ref = oracle.sdshiftgelu_tensor(xs, d["I0"], d["mult"], d["shift"])
+        elif wl.op == "layernorm":
+            ref = oracle.int_layernorm(xs, d["beta"], d["mult"], d["shift"], 10)
+        else:
+            ref = oracle.residual_tensor(xs, d["b"][:n], d["mult_a"], d["mult_b"], d["shift"])
+        c1 = time.perf_counter()
+        sb = wl.bytes_moved() * n // wl.rows
+        cpu = {"value": round(sb / (c1 - c0) / 1e9, 4), "unit": "GB/s", "cores": 1,
+               "kind": "oracle", "cpu_model": cpu_model(),
+               "sample": f"the first {n} of {wl.rows} rows, {c1 - c0:.2f} s"}
+        bad = int(np.count_nonzero(result[:n] != ref))
+        parity = "bit-exact" if bad == 0 else f"{bad} of {ref.size} outputs differ"
+        log(f"cpu baseline {cpu['value']} GB/s; parity of the sampled rows: {parity}")
+
+    line = {"metric": f"HBM GB/s of the stand-alone {wl.op} operator", "value": round(gbs, 2),
+            "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(ev_ms, 5), "ms_per_step_p10_p50_p90": spread,
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+            "data": "synthetic",
+            "config": {"workload": wl.name, "op": wl.op, "rows": wl.rows, "cols": wl.cols,
+                       "launch": "eager" if args.no_graph else f"hip graph, {G} calls per replay",
+                       "algorithmic_bytes": nbytes},
             "roofline": roof, "cpu_baseline": cpu, "parity": parity}
     print(json.dumps(line), flush=True)
     if parity not in (None, "bit-exact"):

@@ -276,6 +276,10 @@ template <bool B>
 struct Flag {
   static constexpr bool value = B;
 };
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
 
 // n / d for 0 <= n < 2^24 with an fp32 reciprocal and one correction step.
 __device__ __forceinline__ int32_t fdiv(int32_t n, int32_t d, float inv) {

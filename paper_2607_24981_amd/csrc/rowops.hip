@@ -86,14 +86,17 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
   }
 }
 
-// LPR lanes per row for C a multiple of 16 with C / 16 <= 8 * LPR: the row
+// LPR lanes per row for C a multiple of 16 with C / 16 <= JC * LPR: the row
 // stays in registers (16-byte chunks), sum and sum of squares come from byte
 // dot products, and the per-channel constants are staged in LDS once per
 // workgroup.  V = sum (x - mu)^2 = sum x^2 - 2 mu sum x + C mu^2 (exact).
+// Each wave walks several row groups and loads the next group's rows before
+// working on the current one; the first group's loads are issued before the
+// constants are staged, so the kernel pays about one memory round trip.
 // When every |beta| <= 2^30 the output path stays in 32 bits:
 // |n| <= 2^30 so |n + beta| < 2^31, which is clamped to [-L, L] and then
 // requantized with one 64-bit multiply-add.
-template <int LPR>
+template <int LPR, int JC>
 __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, int8_t* y,
                                                              int64_t rows, int32_t C,
                                                              const int32_t* beta,
@@ -101,7 +104,22 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
                                                              const int32_t* shift, int32_t nq,
                                                              int32_t iters) {
   extern __shared__ LnChan prm[];
-  constexpr int RG = 64 / LPR, JC = 8;  // rows per wave, max chunks per lane
+  constexpr int RG = 64 / LPR;  // rows per wave and group
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane / LPR, k = lane % LPR;
+  const int32_t n16 = C >> 4;
+  const int64_t ngroups = (rows + RG - 1) / RG;
+  const int64_t gstride = (int64_t)gridDim.x * 4;
+  auto load = [&](int64_t g, v4i (&xv)[JC]) {
+    const int64_t row = min(g * RG + sub, rows - 1);
+    const v4i* xr = (const v4i*)(x + row * C);
+#pragma unroll
+    for (int j = 0; j < JC; ++j) xv[j] = xr[min(k + j * LPR, n16 - 1)];
+  };
+  int64_t g = (int64_t)blockIdx.x * 4 + wave;
+  v4i nxt[JC];
+  if (g < ngroups) load(g, nxt);
+
   int wide = 0;
   for (int32_t c = threadIdx.x; c < C; c += 256) {
     const int32_t q = nq == 1 ? 0 : c;
@@ -115,26 +133,22 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
     // chunk-transposed: channel 16 ch + i sits at i * n16 + ch, so the LPR
     // lanes of a row (consecutive chunks ch) read consecutive entries instead
     // of entries 256 bytes apart, all in one LDS bank
-    prm[(c & 15) * (C >> 4) + (c >> 4)] = p;
+    prm[(c & 15) * n16 + (c >> 4)] = p;
     wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
   }
   wide = __syncthreads_or(wide);
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int sub = lane / LPR, k = lane % LPR;
-  const int32_t n16 = C >> 4;
-  const int64_t ngroups = (rows + RG - 1) / RG;
-  for (int64_t g = (int64_t)blockIdx.x * 4 + wave; g < ngroups; g += (int64_t)gridDim.x * 4) {
+  for (; g < ngroups; g += gstride) {
+    v4i xv[JC];
+#pragma unroll
+    for (int j = 0; j < JC; ++j) xv[j] = nxt[j];
+    if (g + gstride < ngroups) load(g + gstride, nxt);
     const int64_t row = g * RG + sub;
     const bool live = row < rows;
-    const v4i* xr = (const v4i*)(x + (live ? row : rows - 1) * C);
-    v4i xv[JC];
     int32_t S = 0, SS = 0;
 #pragma unroll
     for (int j = 0; j < JC; ++j) {
-      const int32_t ch = k + j * LPR;
-      xv[j] = xr[min(ch, n16 - 1)];
-      if (ch < n16) {
+      if (k + j * LPR < n16) {
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
           S = __builtin_amdgcn_sdot4(xv[j][w], 0x01010101, S, false);
@@ -263,6 +277,97 @@ __global__ __launch_bounds__(256) void shiftmax_kernel(const int8_t* x, int8_t* 
   for (int32_t j = lane; j < cols; j += 64) {
     uint64_t p = ((uint64_t)(uint32_t)elut[m - xr[j]] * F) >> sh;
     yr[j] = (int8_t)(p > cap ? cap : p);
+  }
+}
+
+// Rows of 16-byte chunks (cols % 16 == 0, aligned rows): LPR lanes per row
+// hold the row in JC chunks each, so it is read from memory once and written
+// once.  Bytes are biased (x + 128, one XOR per word): max - x is then a
+// byte-wise subtraction without borrows, and ShiftExp of it is one lookup in
+// a 256-entry LDS table (S_sum >> s_d is exactly the quotient-remainder
+// denominator of Alg. 2).  The row maximum uses 16-bit packed maxima of the
+// even and odd bytes.
+template <int LPR, int JC>
+__global__ __launch_bounds__(256) void shiftmax_rows_kernel(const int8_t* x, int8_t* y,
+                                                            int64_t rows, int32_t cols,
+                                                            int32_t I0, int32_t k_inter,
+                                                            int32_t k_out, int32_t m_p,
+                                                            int32_t s_d) {
+  __shared__ uint32_t elut[256];
+  elut[threadIdx.x] = (uint32_t)shift_exp(-(int32_t)threadIdx.x, I0, k_inter);
+  __syncthreads();
+  constexpr int RG = 64 / LPR;
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane / LPR, k = lane % LPR;
+  const int32_t n16 = cols >> 4;
+  const int64_t ngroups = (rows + RG - 1) / RG;
+  for (int64_t g = (int64_t)blockIdx.x * 4 + wave; g < ngroups; g += (int64_t)gridDim.x * 4) {
+    const int64_t row = g * RG + sub;
+    const bool live = row < rows;
+    const v4i* xr = (const v4i*)(x + (live ? row : rows - 1) * cols);
+    uint32_t w[JC][4];
+    u16x2 mx = {0, 0};
+#pragma unroll
+    for (int j = 0; j < JC; ++j) {
+      const int32_t ch = k + j * LPR;
+      const v4i v = xr[min(ch, n16 - 1)];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // chunks past the row repeat the last one: they cannot raise the max
+        w[j][q] = (uint32_t)v[q] ^ 0x80808080u;
+        const u16x2 ev = __builtin_bit_cast(u16x2, w[j][q] & 0x00ff00ffu);
+        const u16x2 od = __builtin_bit_cast(u16x2, (w[j][q] >> 8) & 0x00ff00ffu);
+        mx = __builtin_elementwise_max(mx, __builtin_elementwise_max(ev, od));
+      }
+    }
+    uint32_t m = max((uint32_t)mx[0], (uint32_t)mx[1]);
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o, 64));
+    const uint32_t m4 = m * 0x01010101u;
+    uint64_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < JC; ++j) {
+      if (k + j * LPR >= n16) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t d4 = m4 - w[j][q];
+        uint32_t ws = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) ws += elut[(d4 >> (8 * b)) & 255];
+        sum += ws;  // 4 values of at most 2^30 each
+      }
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) {
+      const uint32_t lo = __shfl_xor((uint32_t)sum, o, 64);
+      const uint32_t hi = __shfl_xor((uint32_t)(sum >> 32), o, 64);
+      sum += ((uint64_t)hi << 32) | lo;
+    }
+    const int32_t sd = s_d >= 0 ? s_d : calibrate_shift(sum, m_p);
+    const uint32_t F = shiftmax_factor(sum, sd);
+    // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63
+    const int32_t sh = min(32 - k_out + sd, 63);
+    const uint32_t cap = (1u << (k_out - 1)) - 1;
+    v4i* yr = (v4i*)(y + (live ? row : rows - 1) * cols);
+#pragma unroll
+    for (int j = 0; j < JC; ++j) {
+      const int32_t ch = k + j * LPR;
+      if (ch >= n16) break;
+      v4i o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t d4 = m4 - w[j][q];
+        uint32_t ow = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const uint64_t p = ((uint64_t)elut[(d4 >> (8 * b)) & 255] * F) >> sh;
+          ow |= (uint32_t)(p > cap ? cap : p) << (8 * b);
+        }
+        o[q] = (int32_t)ow;
+      }
+      if (live) yr[ch] = o;
+    }
   }
 }
 
@@ -395,27 +500,27 @@ hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                             const int32_t* beta, const int32_t* mult, const int32_t* shift,
                             int32_t nq, int32_t iters, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  // Many rows of the encoder widths: one row per lane.  The 16-byte row
-  // loads need 16-byte aligned rows.
+  // Many rows of the encoder widths: LPR lanes per row holding JC 16-byte
+  // chunks each.  The 16-byte row loads need 16-byte aligned rows.
   if (C % 16 == 0 && C <= 2048 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 15) == 0) {
     const int32_t n16 = C / 16;
-    // few rows: more lanes per row so that more waves share the work
-    const int lpr = (n16 <= 32 && rows >= 16384) ? 4 : (n16 <= 64 && rows >= 16384 ? 8 : 16);
-    const int64_t groups = (rows + (64 / lpr) - 1) / (64 / lpr);
-    int64_t wgs = (groups + 3) / 4;
-    if (wgs > 1024) wgs = 1024;
     const size_t smem = (size_t)C * sizeof(LnChan);
-    dim3 grid((unsigned)wgs), block(256);
-    if (lpr == 4)
-      hipLaunchKernelGGL(layernorm_rows_kernel<4>, grid, block, smem, s, x, y, rows, C, beta,
-                         mult, shift, nq, iters);
-    else if (lpr == 8)
-      hipLaunchKernelGGL(layernorm_rows_kernel<8>, grid, block, smem, s, x, y, rows, C, beta,
-                         mult, shift, nq, iters);
-    else
-      hipLaunchKernelGGL(layernorm_rows_kernel<16>, grid, block, smem, s, x, y, rows, C, beta,
-                         mult, shift, nq, iters);
-    return hipGetLastError();
+    auto go = [&](auto lpr_c, auto jc_c) {
+      constexpr int LPR = decltype(lpr_c)::value, JC = decltype(jc_c)::value;
+      const int64_t groups = (rows + (64 / LPR) - 1) / (64 / LPR);
+      // a few row groups per wave (the next group's loads overlap the
+      // current one), and enough workgroups to cover the chip
+      int64_t wgs = (groups + 15) / 16;
+      if (wgs < 512) wgs = (groups + 3) / 4;
+      if (wgs > 2048) wgs = 2048;
+      hipLaunchKernelGGL((layernorm_rows_kernel<LPR, JC>), dim3((unsigned)wgs), dim3(256), smem,
+                         s, x, y, rows, C, beta, mult, shift, nq, iters);
+      return hipGetLastError();
+    };
+    if (n16 <= 3 * 4) return go(IntC<4>{}, IntC<3>{});    // up to 192 channels
+    if (n16 <= 3 * 8) return go(IntC<8>{}, IntC<3>{});    // up to 384
+    if (n16 <= 4 * 16) return go(IntC<16>{}, IntC<4>{});  // up to 1024
+    return go(IntC<16>{}, IntC<8>{});                     // up to 2048
   }
   const int32_t nw = C / 4;
   if (nw <= 16 * 4) return launch_ln<16, 4>(x, y, rows, C, beta, mult, shift, nq, iters, s);
@@ -431,6 +536,21 @@ hipError_t launch_shiftmax(const int8_t* x, int8_t* y, int64_t rows, int32_t col
                            int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
                            int32_t s_d, hipStream_t s) {
   if (rows == 0) return hipSuccess;
+  if (cols % 16 == 0 && cols <= 64 * 16 * 2 && (((uintptr_t)x | (uintptr_t)y) & 15) == 0) {
+    const int32_t n16 = cols / 16;
+    auto go = [&](auto lpr_c, auto jc_c) {
+      constexpr int LPR = decltype(lpr_c)::value, JC = decltype(jc_c)::value;
+      const int64_t groups = (rows + (64 / LPR) - 1) / (64 / LPR);
+      int64_t wgs = (groups + 3) / 4;
+      if (wgs > 4096) wgs = 4096;
+      hipLaunchKernelGGL((shiftmax_rows_kernel<LPR, JC>), dim3((unsigned)wgs), dim3(256), 0, s,
+                         x, y, rows, cols, I0, k_inter, k_out, m_p, s_d);
+      return hipGetLastError();
+    };
+    if (n16 <= 2 * 8) return go(IntC<8>{}, IntC<2>{});
+    if (n16 <= 2 * 32) return go(IntC<32>{}, IntC<2>{});
+    return go(IntC<64>{}, IntC<2>{});
+  }
   dim3 grid((unsigned)((rows + 3) / 4)), block(256);
   hipLaunchKernelGGL(shiftmax_kernel, grid, block, 0, s, x, y, rows, cols, I0, k_inter,
                      k_out, m_p, s_d);

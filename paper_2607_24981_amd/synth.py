@@ -389,3 +389,68 @@ def decoder_inputs(wl: DecoderWorkload, seed: int, batch: int | None = None, mod
         ref = np.concatenate([ref, _u(rng, 1 << 12, 1 << 15, (B, wl.queries, 2))], axis=-1)
     p["ref_dims"] = ref.shape[-1]
     return p, tgt, memory, ref, hw, start
+
+
+@dataclass(frozen=True)
+class RowOpWorkload:
+    """One stand-alone row-wise or element-wise operator over the tensor it
+    sees inside the encoder: `rows` x `cols` int8 values."""
+    name: str
+    op: str  # "shiftmax", "sdshiftgelu", "layernorm", "residual"
+    rows: int
+    cols: int
+
+    def bytes_moved(self) -> int:
+        """Algorithmic HBM bytes of one call: each int8 input read once and
+        each output written once (the residual add reads two inputs), plus
+        LayerNorm's per-channel beta, multiplier and shift (int32 each)."""
+        n = self.rows * self.cols
+        if self.op == "residual":
+            return 3 * n
+        if self.op == "layernorm":
+            return 2 * n + 12 * self.cols
+        return 2 * n
+
+
+ROWOP_WORKLOADS = {
+    # the score rows of one global attention layer of the tiny encoder at
+    # batch 32: 32 images x 3 heads x 1600 queries, rows of 1600 keys
+    "shiftmax_r153600_c1600": RowOpWorkload("shiftmax_r153600_c1600", "shiftmax", 153600, 1600),
+    # the fc1 output of the tiny encoder at batch 32 (51 200 tokens x 768)
+    "sdshiftgelu_r51200_c768": RowOpWorkload("sdshiftgelu_r51200_c768", "sdshiftgelu", 51200,
+                                             768),
+    # the LayerNorm rows of the medium encoder at batch 8 and of the tiny
+    # encoder at batch 32
+    "layernorm_r12800_c384": RowOpWorkload("layernorm_r12800_c384", "layernorm", 12800, 384),
+    "layernorm_r51200_c192": RowOpWorkload("layernorm_r51200_c192", "layernorm", 51200, 192),
+    # the residual add of the tiny encoder at batch 32
+    "residual_r51200_c192": RowOpWorkload("residual_r51200_c192", "residual", 51200, 192),
+}
+
+
+def rowop_inputs(wl: RowOpWorkload, seed: int) -> dict:
+    """int8 inputs U[-127, 127] and the operator's parameters, drawn as for
+    the encoder blocks: Shiftmax and GELU I0 U[8, 64] (k_inter 16, k_out 8,
+    m_p 4, dynamic s_d); GELU output dyadic mult U[2^29, 2^30], shift
+    U[35, 38]; LayerNorm beta U[-2^26, 2^26], per-channel mult +-U[2^29, 2^30]
+    (1 in 8 negative), shift U[49, 51], 10 Newton steps; residual mults
+    U[2^29, 2^30], shift 31."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    d = {"x": _u(rng, -127, 127, (wl.rows, wl.cols), np.int8)}
+    if wl.op == "shiftmax":
+        d["I0"] = int(_u(rng, 8, 64))
+    elif wl.op == "sdshiftgelu":
+        d["I0"] = int(_u(rng, 8, 64))
+        d["mult"], d["shift"] = int(_u(rng, 1 << 29, 1 << 30)), int(_u(rng, 35, 38))
+    elif wl.op == "layernorm":
+        C = wl.cols
+        d["beta"] = _u(rng, -(1 << 26), 1 << 26, C)
+        mag = _u(rng, 1 << 29, 1 << 30, C)
+        sign = np.where(rng.integers(0, 8, size=C) == 0, -1, 1).astype(np.int32)
+        d["mult"] = (mag * sign).astype(np.int32)
+        d["shift"] = _u(rng, 49, 51, C)
+    else:
+        d["b"] = _u(rng, -127, 127, (wl.rows, wl.cols), np.int8)
+        d["mult_a"], d["mult_b"] = int(_u(rng, 1 << 29, 1 << 30)), int(_u(rng, 1 << 29, 1 << 30))
+        d["shift"] = 31
+    return d

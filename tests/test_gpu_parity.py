@@ -185,6 +185,31 @@ def test_shiftmax_in_place():
     assert_same(host(t), ref, "shiftmax in place")
 
 
+@pytest.mark.parametrize("rows,cols", [(5, 16), (9, 32), (17, 256), (33, 272), (6, 1024),
+                                       (3, 2048), (1000, 1600), (4, 2064)])
+@pytest.mark.parametrize("s_d", [-1, 0, 9])
+def test_shiftmax_row_chunks(rows, cols, s_d):
+    """Rows of whole 16-byte chunks held in registers (8, 32 or 64 lanes per
+    row, partially filled lanes, several rows per wave, a row count that
+    leaves the last wave's rows partly past the end), with the full int8
+    range (-128 gives the 255-step table entry), static and dynamic s_d;
+    2064 columns take the byte-wise kernel."""
+    say(f"shiftmax row chunks rows={rows} cols={cols} s_d={s_d}")
+    g = rng(rows * 7 + cols + s_d)
+    x = g.integers(-128, 128, (rows, cols)).astype(np.int8)
+    x[0, :] = -128
+    x[0, 3] = 127
+    if rows > 2:
+        x[1, :] = 5
+    for I0 in (8, 64, 4000):
+        ref = oracle.shiftmax_rows(x, I0, s_d=s_d)
+        got = host(ilw.ilw_shiftmax(dev(x), I0, s_d=s_d))
+        assert_same(got, ref, f"shiftmax row chunks I0={I0}")
+    t = dev(x)
+    ilw.ilw_shiftmax(t, 30, s_d=s_d, y=t)
+    assert_same(host(t), oracle.shiftmax_rows(x, 30, s_d=s_d), "shiftmax row chunks in place")
+
+
 # ------------------------------------------------------------------ SD-ShiftGELU
 @pytest.mark.parametrize("I0", [1, 8, 16, 37, 64, 1000, 16383])
 def test_sdshiftgelu_exhaustive(I0):
@@ -249,6 +274,26 @@ def test_layernorm_many_rows(rows, C, iters, per_tensor):
     t = dev(x)
     got = host(ilw.ilw_int_layernorm(t, dev(beta), dev(mult), dev(shift), iters, y=t))
     assert_same(got, ref, "layernorm many rows")
+
+
+@pytest.mark.parametrize("rows,C", [(1, 16), (4097, 192), (5, 384), (12801, 384), (33, 1024),
+                                    (9, 2048), (3000, 64)])
+def test_layernorm_row_groups(rows, C):
+    """The row kernel's lane groupings (4 lanes x 3 chunks up to 192
+    channels, 8 x 3 up to 384, 16 x 4 up to 1024, 16 x 8 up to 2048), with
+    several row groups per wave (the next group's loads in flight) and a
+    last group partly past the end."""
+    say(f"layernorm row groups rows={rows} C={C}")
+    g = rng(rows * 3 + C)
+    x = g.integers(-128, 128, (rows, C)).astype(np.int8)
+    x[0, :] = 9
+    beta = g.integers(-2 ** 26, 2 ** 26, C).astype(np.int32)
+    mult = (g.integers(2 ** 29, 2 ** 30, C) * g.choice([-1, 1], C)).astype(np.int32)
+    shift = g.integers(49, 52, C).astype(np.int32)
+    for iters in (10, 20):
+        ref = oracle.int_layernorm(x, beta, mult, shift, iters)
+        got = host(ilw.ilw_int_layernorm(dev(x), dev(beta), dev(mult), dev(shift), iters))
+        assert_same(got, ref, f"layernorm row groups iters={iters}")
 
 
 def test_layernorm_in_place():
