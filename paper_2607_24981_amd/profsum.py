@@ -13,6 +13,18 @@ used by the library).
       for the plain device copy of N MiB that the profiled command made first
       (the __amd_rocclr_copyBuffer dispatch with the largest FETCH_SIZE);
       updates profiles/traffic.json and prints a text summary.
+  python -m paper_2607_24981_amd.profsum counters DIR [DIR ...] --title T --command C
+      --label NAME=PATTERN[@PREV][#GRID] [--label ...] [--ops NAME=OPS] [--units NAME=N:WHAT]
+      per labelled kernel, the mean of every counter over its dispatches from
+      DIR/**/*counter_collection.csv (one directory per --pmc pass), and the
+      derived figures: int8 MFMA ops (MOPS_I8 x 512) against the algorithmic
+      ops given with --ops, MFMA busy and VALU busy as fractions of the
+      SIMD-cycles of the dispatch (GRBM_GUI_ACTIVE is summed over the 8
+      XCDs), VALU instructions per wave and per unit (--units, e.g. scores or
+      outputs per dispatch), LDS busy and bank-conflict share, and the share
+      of wave time spent waiting.  A dispatch takes the first label whose
+      PATTERN is in its kernel name and, with @PREV, whose preceding dispatch
+      has PREV in its name (with #GRID: whose grid has GRID threads).
 """
 from __future__ import annotations
 
@@ -148,6 +160,106 @@ def traffic(args):
     print(f"HBM bytes per launch {(fetch_b + write_b) / 1e6:.3f} MB")
 
 
+MI355X_CUS, MI355X_SIMDS, MI355X_XCDS = 256, 1024, 8
+
+
+def counters(args):
+    import collections
+    per = collections.defaultdict(dict)  # (dir, dispatch) -> {counter: value}
+    meta = {}
+    for d in args.dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                key = (d, int(r["Dispatch_Id"]))
+                per[key][r["Counter_Name"]] = float(r["Counter_Value"])
+                meta[key] = (short(r["Kernel_Name"]), int(r["Grid_Size"]),
+                             int(r["Workgroup_Size"]), int(r["LDS_Block_Size"]),
+                             int(r["VGPR_Count"]), int(r["Accum_VGPR_Count"]),
+                             int(r["Scratch_Size"]))
+    rules = []
+    for spec in args.label:
+        name, pat = spec.split("=", 1)
+        pat, _, grid = pat.partition("#")
+        pat, _, prev = pat.partition("@")
+        rules.append((name, pat, prev, int(grid) if grid else 0))
+    ops = dict((k, float(v)) for k, v in (o.split("=", 1) for o in args.ops or []))
+    units = {}
+    for u in args.units or []:
+        k, v = u.split("=", 1)
+        n, _, what = v.partition(":")
+        units[k] = (float(n), what or "unit")
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    shape = {}
+    ndisp = collections.defaultdict(lambda: collections.Counter())
+    for d in args.dirs:
+        ids = sorted(i for (dd, i) in meta if dd == d)
+        prev = ""
+        for i in ids:
+            k = meta[(d, i)][0]
+            for name, pat, pv, gr in rules:
+                if pat in k and (not pv or pv in prev) and (not gr or gr == meta[(d, i)][1]):
+                    for c, v in per[(d, i)].items():
+                        agg[name][c].append(v)
+                    ndisp[name][d] += 1
+                    shape[name] = (k,) + meta[(d, i)][1:]
+                    break
+            prev = k
+    print(f"# {args.title}")
+    print(f"# command: {args.command}")
+    print("# source: rocprofv3 --pmc (one pass per counter group), counter_collection.csv; "
+          "per label the mean over its dispatches")
+    print(f"# MI355X: {MI355X_CUS} CUs, {MI355X_SIMDS} SIMDs, {MI355X_XCDS} XCDs; one "
+          "v_mfma_i32_16x16x64_i8 = 32768 int8 ops = 64 MOPS_I8 units = 16 MFMA-busy cycles")
+    for name, _, _, _ in rules:
+        if name not in agg:
+            continue
+        m = {c: statistics.mean(v) for c, v in agg[name].items()}
+        n = max(ndisp[name].values())  # dispatches per pass
+        k, grid, wg, lds, vgpr, agpr, scr = shape[name]
+        print(f"\n[{name}] {k}")
+        print(f"  dispatches {n}; grid {grid} threads, workgroup {wg}, LDS {lds} B, "
+              f"VGPR {vgpr}, AGPR {agpr}, scratch {scr}")
+        gui = m.get("GRBM_GUI_ACTIVE")
+        cyc = gui / MI355X_XCDS if gui else None
+        waves = m.get("SQ_WAVES")
+        if cyc:
+            print(f"  GRBM_GUI_ACTIVE {gui:.0f} (summed over XCDs) -> {cyc:.0f} cycles, "
+                  f"{cyc / 2.4e3:.2f} us at 2.4 GHz (counter run: dispatches serialized)")
+        if "SQ_INSTS_VALU_MFMA_MOPS_I8" in m:
+            mops = m["SQ_INSTS_VALU_MFMA_MOPS_I8"] * 512
+            line = f"  int8 MFMA ops {mops / 1e9:.4f} G"
+            if name in ops:
+                line += f" (algorithmic {ops[name] / 1e9:.4f} G, ratio {mops / ops[name]:.3f})"
+            print(line)
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in m and cyc:
+            print(f"  MFMA busy {m['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * MI355X_SIMDS):.4f} of "
+                  f"SIMD-cycles")
+        if "SQ_ACTIVE_INST_VALU" in m and cyc:
+            print(f"  VALU busy {m['SQ_ACTIVE_INST_VALU'] / (cyc * MI355X_CUS):.4f} "
+                  f"(SQ_ACTIVE_INST_VALU / (CUs x cycles))")
+        if waves:
+            for c in ("SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_INSTS_SALU",
+                      "SQ_INSTS_VALU_INT32", "SQ_INSTS_VALU_INT64", "SQ_INSTS_VMEM_RD",
+                      "SQ_INSTS_VMEM_WR"):
+                if c in m:
+                    extra = ""
+                    if c == "SQ_INSTS_VALU" and name in units:
+                        cnt, what = units[name]
+                        extra = f", {m[c] * 64 / cnt:.2f} lane-instructions per {what}"
+                    print(f"  {c} {m[c]:.0f} ({m[c] / waves:.1f} per wave{extra})")
+        if "SQ_LDS_IDX_ACTIVE" in m and cyc:
+            la = m["SQ_LDS_IDX_ACTIVE"]
+            print(f"  LDS busy {la / (cyc * MI355X_CUS):.4f}; bank-conflict cycles "
+                  f"{m.get('SQ_LDS_BANK_CONFLICT', 0) / la if la else 0:.4f} of LDS-active cycles")
+        if "SQ_WAIT_INST_ANY" in m and "SQ_WAVE_CYCLES" in m:
+            print(f"  waves waiting on instruction dependencies "
+                  f"{m['SQ_WAIT_INST_ANY'] / m['SQ_WAVE_CYCLES']:.4f} of wave-cycles"
+                  + (f" (LDS {m['SQ_WAIT_INST_LDS'] / m['SQ_WAVE_CYCLES']:.4f})"
+                     if "SQ_WAIT_INST_LDS" in m else ""))
+        rest = sorted(c for c in m if not c.startswith(("SQ_INSTS", "GRBM")))
+        print("  raw: " + ", ".join(f"{c} {m[c]:.4g}" for c in rest))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__,
                                  formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -165,8 +277,15 @@ def main():
     t.add_argument("--source", action="append", required=True)
     t.add_argument("--copy-mib", type=float, required=True)
     t.add_argument("--command", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("dirs", nargs="+")
+    c.add_argument("--title", required=True)
+    c.add_argument("--command", required=True)
+    c.add_argument("--label", action="append", required=True)
+    c.add_argument("--ops", action="append")
+    c.add_argument("--units", action="append")
     args = ap.parse_args()
-    kernels(args) if args.cmd == "kernels" else traffic(args)
+    {"kernels": kernels, "traffic": traffic, "counters": counters}[args.cmd](args)
 
 
 if __name__ == "__main__":
