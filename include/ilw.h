@@ -23,7 +23,14 @@
  *     (round half up), sat8 clamps to the symmetric int8 range [-127, 127].
  *   - int8 tensors and weights must be 16-byte aligned and their row lengths
  *     multiples of 16 where stated.
- *   - Thread-safe: the only global state is a thread-local error string.
+ *   - Thread-safe.  The error string is thread-local.  The rest of the
+ *     process-wide state is set up once under a lock or a static
+ *     initializer: the kernel-attribute cache (per device and kernel), the
+ *     device address of the allocation-free scratch (per device) and the
+ *     stage profiler (ilw_profile_*, guarded by a mutex).  The environment
+ *     switches ILW_FUSE_LN, ILW_TAIL and ILW_GEMM_PF, which select between
+ *     equivalent kernel variants for comparison runs, are read once, at the
+ *     first call that needs them.
  */
 #ifndef ILW_H
 #define ILW_H
@@ -35,7 +42,7 @@
 extern "C" {
 #endif
 
-#define ILW_ABI_VERSION 7
+#define ILW_ABI_VERSION 8
 
 typedef enum {
   ILW_OK = 0,
@@ -113,9 +120,14 @@ int ilw_sdshiftgelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
  *   sigma: k <- floor((k + floor(V/k)) / 2), newton_iters times from k = 2^16
  *   n_i = floor(y_i * floor((2^31 - 1) / sigma) / 2)     (0 when V == 0)
  *   out_i = sat8(rq(n_i + beta_i; out.mult_i, out.shift_i))
- * gamma is folded into the (signed) output multiplier; beta int32 [C] is at
- * the scale of n (DEVICE array).  C in [4, 16384], a multiple of 4;
- * newton_iters in [1, 64].  y may alias x.
+ * beta int32 [C] is at the scale of n (DEVICE array).  There is no gamma
+ * argument: the affine scale is folded into the per-channel (signed) output
+ * multiplier.  A model with an integer gamma_i and one output dyadic (m, s)
+ * passes mult_i = gamma_i * m and beta_i = b_i / gamma_i, which equals
+ * rq(n_i * gamma_i + b_i; m, s) exactly when gamma_i divides b_i (and
+ * |gamma_i * m| < 2^31); a float gamma is folded when the multipliers are
+ * derived, with no separate rounding of gamma.  C in [4, 16384], a multiple
+ * of 4; newton_iters in [1, 64].  y may alias x.
  */
 int ilw_int_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                       const int32_t* beta, ilw_dyadic out, int32_t newton_iters,
@@ -275,7 +287,8 @@ int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
  *   ref     int32 [B, Q, 2]  reference point (x, y), Q16 fraction of the map
  *   offsets int16 [B, Q, heads, L, P, 2]  (x, y) in Q8 pixels of level l
  *   logits  int8  [B, Q, heads, L*P] -> Constrained Shiftmax per (b, q, h)
- *           with I0, k_inter = 16, k_out = 8, m_p = 4, s_d (as ilw_shiftmax)
+ *           with I0, k_inter, k_out, m_p, s_d (ranges as ilw_shiftmax; the
+ *           decoder's defaults are k_inter = 16, k_out = 8, m_p = 4)
  *   out     int8  [B, Q, heads*head_dim] = sat8(rq(sum_{l,p} P * sample))
  * Location: X = floor(ref_x * W_l / 2^8) + off_x (Q8), pixel ix = floor(X/2^8);
  * samples outside the map contribute 0.  mode 0 = nearest (the paper);
@@ -287,8 +300,8 @@ int ilw_deform_attn(const int8_t* value, const int32_t* level_hw,
                     const int32_t* level_start, int32_t L, int32_t P,
                     const int32_t* ref, const int16_t* offsets, const int8_t* logits,
                     int8_t* out, int32_t B, int32_t Q, int32_t heads, int32_t head_dim,
-                    int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
-                    int32_t mode, void* stream);
+                    int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p, int32_t s_d,
+                    int32_t out_mult, int32_t out_shift, int32_t mode, void* stream);
 
 /* The same sampler with reference boxes (Sec. 3.1.2: the decoder's
  * references are the encoder's top-K boxes).  The paper gives no sampling
@@ -305,8 +318,8 @@ int ilw_deform_attn_boxes(const int8_t* value, const int32_t* level_hw,
                           const int32_t* level_start, int32_t L, int32_t P,
                           const int32_t* ref, const int16_t* offsets, const int8_t* logits,
                           int8_t* out, int32_t B, int32_t Q, int32_t heads, int32_t head_dim,
-                          int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
-                          int32_t mode, void* stream);
+                          int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p, int32_t s_d,
+                          int32_t out_mult, int32_t out_shift, int32_t mode, void* stream);
 
 /* ------------------------------------------------------------------------
  * I-ViT baseline operators, the forms that Constrained Shiftmax and
@@ -357,7 +370,8 @@ int ilw_split_conv(int32_t n_branches, const int8_t* const* x, const int32_t* ch
  *                                                  window of the queries
  *   v = val(memory); off = 16 * offl(t1) (int8 1/16 px -> Q8); w = attw(t1)
  *   t2 = LN2(Res2(t1, co(Deform(v, ref, off, w)))) cross-attention (as
- *                                                  ilw_deform_attn, mode 0/1)
+ *                                                  ilw_deform_attn, mode 0/1,
+ *                                                  k_inter 16, k_out 8, m_p 4)
  *   y  = LN3(Res3(t2, fc2(GELU(fc1(t2)))))         FFN
  *   tgt int8 [batch, queries, dim]; memory int8 [batch, value_tokens, dim],
  *   the levels stacked as for ilw_deform_attn (level_hw, level_start: HOST
@@ -406,8 +420,8 @@ int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8
  * clears the records.  ilw_profile_read waits for the last recorded event and
  * returns, per stage, the summed kernel time in milliseconds and the number of
  * launches (arrays of n_stages entries, HOST memory).  Do not enable it while
- * a stream is being captured into a graph.  Not thread-safe with respect to
- * concurrent launches from several threads while enabled.
+ * a stream is being captured into a graph.  Launches from several threads
+ * record under one lock; each launch is attributed to the stage it belongs to.
  */
 typedef enum {
   ILW_STAGE_LAYERNORM = 0,   /* stand-alone LayerNorm kernels              */

@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -42,15 +43,17 @@ struct ProfRecord {
   int stage;
   hipEvent_t start, stop;
 };
+// The tracing state is shared by every thread: the switch is an atomic read
+// on every launch, the event pool and the records are guarded by the mutex.
 struct Profiler {
   std::mutex mu;
-  bool on = false;
+  std::atomic<bool> on{false};
   std::vector<hipEvent_t> pool;
   size_t used = 0;
   std::vector<ProfRecord> recs;
 } g_prof;
 
-hipEvent_t prof_event() {
+hipEvent_t prof_event() {  // with g_prof.mu held
   if (g_prof.used == g_prof.pool.size()) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
@@ -65,13 +68,15 @@ struct StageTimer {
   hipStream_t s;
   hipEvent_t a = nullptr, b = nullptr;
   StageTimer(int st, hipStream_t str) : stage(st), s(str) {
-    if (!g_prof.on) return;
+    if (!g_prof.on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lk(g_prof.mu);
     a = prof_event();
     b = prof_event();
     if (a && b) (void)hipEventRecord(a, s);
   }
   void done() {
-    if (!g_prof.on || !a || !b) return;
+    if (!a || !b) return;
+    std::lock_guard<std::mutex> lk(g_prof.mu);
     (void)hipEventRecord(b, s);
     g_prof.recs.push_back({stage, a, b});
   }
@@ -341,11 +346,10 @@ int check_block(const ilw_block_params* p, int32_t batch, int32_t gh, int32_t gw
 // ILW_FUSE_LN=0 runs every LayerNorm as its own kernel (same results; for
 // comparisons), read once.
 bool ln_fusable(int32_t D) {
-  static int on = -1;
-  if (on < 0) {
+  static const bool on = [] {  // read once (thread-safe static initialisation)
     const char* e = getenv("ILW_FUSE_LN");
-    on = (e && e[0] == '0') ? 0 : 1;
-  }
+    return !(e && e[0] == '0');
+  }();
   return on && (D == 192 || D == 256 || D == 384);
 }
 
@@ -365,11 +369,10 @@ GemmArgs with_ln(GemmArgs a, const int32_t* beta, const ilw_dyadic& out, int32_t
 // to 16384 tokens per call; ILW_TAIL=0 / 1 turns it off / on wherever it
 // applies (same results), read once.
 bool use_tail(const ilw_block_params* p, const ilw_block_params* next, int64_t M) {
-  static int mode = -1;
-  if (mode < 0) {
+  static const int mode = [] {  // read once (thread-safe static initialisation)
     const char* e = getenv("ILW_TAIL");
-    mode = (e && e[0] == '0') ? 0 : ((e && e[0] == '1') ? 1 : 2);
-  }
+    return (e && e[0] == '0') ? 0 : ((e && e[0] == '1') ? 1 : 2);
+  }();
   if (mode == 0 || p->dim != 192 || p->mlp_dim != 768) return false;
   if (next && next->dim != 192) return false;
   return mode == 1 || M <= 16384;
@@ -1027,8 +1030,9 @@ namespace {
 int deform_impl(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
                 int32_t L, int32_t P, const int32_t* ref, int32_t ref_dims,
                 const int16_t* offsets, const int8_t* logits, int8_t* out, int32_t B, int32_t Q,
-                int32_t heads, int32_t head_dim, int32_t I0, int32_t s_d, int32_t out_mult,
-                int32_t out_shift, int32_t mode, void* stream, const char* name,
+                int32_t heads, int32_t head_dim, int32_t I0, int32_t k_inter, int32_t k_out,
+                int32_t m_p, int32_t s_d, int32_t out_mult, int32_t out_shift, int32_t mode,
+                void* stream, const char* name,
                 const int8_t* offsets8 = nullptr, int32_t off_shift = 0) {
   REQUIRE(level_hw && level_start, ILW_E_NULL, "level_hw and level_start (host) required");
   REQUIRE(ref_dims == 2 || ref_dims == 4, ILW_E_PARAM,
@@ -1040,9 +1044,8 @@ int deform_impl(const int8_t* value, const int32_t* level_hw, const int32_t* lev
   REQUIRE(head_dim >= 4 && head_dim <= 256 && head_dim % 4 == 0, ILW_E_SHAPE,
           "head_dim = %d must be a multiple of 4 in [4, 256]", head_dim);
   REQUIRE(mode == 0 || mode == 1, ILW_E_PARAM, "mode = %d must be 0 or 1", mode);
-  REQUIRE(I0 >= 1 && I0 < (1 << 14), ILW_E_PARAM, "I0 = %d must be in [1, 2^14 - 1]", I0);
-  REQUIRE(s_d >= -1 && s_d <= 31, ILW_E_PARAM, "s_d = %d must be -1 or in [0, 31]", s_d);
   int e;
+  if ((e = check_shiftmax(I0, k_inter, k_out, m_p, s_d))) return e;
   if ((e = check_mult(out_mult, "out_mult"))) return e;
   REQUIRE(out_shift >= 1 && out_shift <= (mode == 0 ? 62 : 46), ILW_E_PARAM,
           "out_shift = %d out of range for mode %d", out_shift, mode);
@@ -1081,6 +1084,9 @@ int deform_impl(const int8_t* value, const int32_t* level_hw, const int32_t* lev
   a.P = P;
   a.S = (int32_t)S;
   a.I0 = I0;
+  a.k_inter = k_inter;
+  a.k_out = k_out;
+  a.m_p = m_p;
   a.s_d = s_d;
   a.out_mult = out_mult;
   a.out_shift = out_shift;
@@ -1098,22 +1104,23 @@ int deform_impl(const int8_t* value, const int32_t* level_hw, const int32_t* lev
 int ilw_deform_attn(const int8_t* value, const int32_t* level_hw, const int32_t* level_start,
                     int32_t L, int32_t P, const int32_t* ref, const int16_t* offsets,
                     const int8_t* logits, int8_t* out, int32_t B, int32_t Q, int32_t heads,
-                    int32_t head_dim, int32_t I0, int32_t s_d, int32_t out_mult,
-                    int32_t out_shift, int32_t mode, void* stream) {
+                    int32_t head_dim, int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p,
+                    int32_t s_d, int32_t out_mult, int32_t out_shift, int32_t mode,
+                    void* stream) {
   return deform_impl(value, level_hw, level_start, L, P, ref, 2, offsets, logits, out, B, Q,
-                     heads, head_dim, I0, s_d, out_mult, out_shift, mode, stream,
-                     "ilw_deform_attn");
+                     heads, head_dim, I0, k_inter, k_out, m_p, s_d, out_mult, out_shift, mode,
+                     stream, "ilw_deform_attn");
 }
 
 int ilw_deform_attn_boxes(const int8_t* value, const int32_t* level_hw,
                           const int32_t* level_start, int32_t L, int32_t P,
                           const int32_t* ref, const int16_t* offsets, const int8_t* logits,
                           int8_t* out, int32_t B, int32_t Q, int32_t heads, int32_t head_dim,
-                          int32_t I0, int32_t s_d, int32_t out_mult, int32_t out_shift,
-                          int32_t mode, void* stream) {
+                          int32_t I0, int32_t k_inter, int32_t k_out, int32_t m_p, int32_t s_d,
+                          int32_t out_mult, int32_t out_shift, int32_t mode, void* stream) {
   return deform_impl(value, level_hw, level_start, L, P, ref, 4, offsets, logits, out, B, Q,
-                     heads, head_dim, I0, s_d, out_mult, out_shift, mode, stream,
-                     "ilw_deform_attn_boxes");
+                     heads, head_dim, I0, k_inter, k_out, m_p, s_d, out_mult, out_shift, mode,
+                     stream, "ilw_deform_attn_boxes");
 }
 
 size_t ilw_decoder_workspace_bytes(const ilw_decoder_params* p, int32_t batch,
@@ -1199,8 +1206,8 @@ int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8
   if (he != hipSuccess) return hip_status(he, "ilw_decoder_layer");
   // the sampler reads the int8 offsets (1/16 px) and widens them to Q8 itself
   if ((e = deform_impl(L.v, level_hw, level_start, p->levels, p->points, ref, p->ref_dims,
-                       nullptr, L.lg, L.smp, batch, queries, H, hd, p->da_I0, p->da_s_d,
-                       p->da_out_mult, p->da_out_shift, p->da_mode, stream,
+                       nullptr, L.lg, L.smp, batch, queries, H, hd, p->da_I0, 16, 8, 4,
+                       p->da_s_d, p->da_out_mult, p->da_out_shift, p->da_mode, stream,
                        "ilw_decoder_layer sampler", L.off8, 4)))
     return e;
   resid_ln(gemm_args(L.smp, p->w_co, p->b_co, p->co, L.x, MQ, D, D), L.t1, p->res2_mult_a,
@@ -1220,7 +1227,7 @@ int ilw_decoder_layer(const ilw_decoder_params* p, const int8_t* tgt, const int8
 
 int ilw_profile_enable(int enable) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
-  g_prof.on = enable != 0;
+  g_prof.on.store(enable != 0);
   g_prof.recs.clear();
   g_prof.used = 0;
   return ok();

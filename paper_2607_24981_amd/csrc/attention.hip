@@ -19,6 +19,10 @@
 // two matmuls are 256 int8 MFMA ops (about two VALU lane-ops at the chip's
 // MFMA:VALU ratio), so this kernel is bound by the VALU work of the exact
 // Shiftmax, not by the matrix cores.
+#include <map>
+#include <mutex>
+#include <utility>
+
 #include "ilw_internal.h"
 
 namespace ilw {
@@ -67,22 +71,6 @@ __device__ __forceinline__ uint32_t pack_min_bytes(uint32_t a, uint32_t b, uint3
   hi = __builtin_elementwise_min(hi, cap);
   return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo),
                                0x06040200u);
-}
-
-// floor((2^31 - 1) / S_R) for S_R in [1, 2^31 - 1]: the hardware FP64
-// reciprocal estimate, refined by one Newton step, gives the quotient to
-// within one; one integer correction makes it exact.  (The raw estimate is
-// not enough: with a static s_d, S_R can be small and the quotient near
-// 2^31, where its relative error exceeds one unit.)
-__device__ __forceinline__ uint32_t div_2p31m1(uint32_t sr) {
-  const double s = (double)sr;
-  double rc = __builtin_amdgcn_rcp(s);
-  rc = fma(rc, fma(-s, rc, 1.0), rc);
-  const double est = 2147483647.0 * rc;
-  int64_t q = (int64_t)est;
-  const int64_t r = 2147483647LL - q * (int64_t)sr;
-  q += r < 0 ? -1 : (r >= (int64_t)sr ? 1 : 0);
-  return (uint32_t)q;
 }
 
 // NW waves per workgroup (4, 8 or 16): keys are split over all waves for the
@@ -388,17 +376,31 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(const int8_t* qkv, in
   }
 }
 
+// Dynamic LDS above 64 KB must be allowed per kernel; the attribute is set
+// once per (device, kernel) and size high-water mark, under a lock so that
+// threads launching on several devices at once all see it set.
+hipError_t allow_dynamic_lds(const void* kern, size_t smem) {
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, size_t> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  size_t& have = done[{dev, kern}];
+  if (smem <= have) return hipSuccess;
+  e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  if (e == hipSuccess) have = smem;
+  return e;
+}
+
 template <int R, int LPR, bool NARROW, int MASK, int NW, int JW>
 hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   const int32_t lds_row = a.Twp + 16;
   const size_t smem = (size_t)R * lds_row;
   auto kern = attention_kernel<R, LPR, NARROW, MASK, NW, JW>;
-  static size_t configured = 0;
-  if (smem > 65536 && smem > configured) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  if (smem > 65536) {
+    const hipError_t e = allow_dynamic_lds((const void*)kern, smem);
     if (e != hipSuccess) return e;
-    configured = smem;
   }
   const int32_t nrb = (a.Tw + R - 1) / R;
   const int64_t ntiles = (int64_t)nrb * a.H * a.B * a.nW;

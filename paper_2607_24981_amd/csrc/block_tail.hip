@@ -95,7 +95,7 @@ __device__ __forceinline__ uint32_t slab_layernorm(uint32_t xw, int w, int lane,
   const int32_t mu = mean_half_up(s, D);
   const uint32_t V = (uint32_t)(ss - 2 * mu * s + D * mu * mu);
   const uint32_t sigma = newton_isqrt_f64(V, iters);
-  const int32_t F = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+  const int32_t F = sigma ? (int32_t)div_2p31m1(sigma) : 0;
   int32_t o[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {

@@ -27,7 +27,7 @@ __device__ __forceinline__ int64_t floor_div_pos(int64_t n, int64_t d) {
 
 __global__ __launch_bounds__(256) void deform_kernel(DeformArgs a) {
   __shared__ int32_t elut[256];
-  elut[threadIdx.x] = shift_exp(-(int32_t)threadIdx.x, a.I0, 16);
+  elut[threadIdx.x] = shift_exp(-(int32_t)threadIdx.x, a.I0, a.k_inter);
   __syncthreads();
 
   const int32_t G = a.Dh >> 2;  // lanes per (b, q, h)
@@ -46,11 +46,12 @@ __global__ __launch_bounds__(256) void deform_kernel(DeformArgs a) {
   for (int32_t i = 0; i < LP; ++i) m = max(m, (int32_t)lg[i]);
   uint64_t sum = 0;
   for (int32_t i = 0; i < LP; ++i) sum += (uint32_t)elut[m - lg[i]];
-  const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, 4);
+  const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, a.m_p);
   const uint32_t F = shiftmax_factor(sum, sd);
-  // 32 - k_out with k_out = 8; s_d <= 31 (static) or <= 9 (at most 64 values
-  // below 2^30 with m_p = 4) keeps the shift below 64
-  const int32_t sh = 24 + sd;
+  // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63, so the cap
+  // keeps the 64-bit shift defined (s_d reaches 36 with m_p = 31)
+  const int32_t sh = min(32 - a.k_out + sd, 63);
+  const uint64_t cap = (1u << (a.k_out - 1)) - 1;
 
   const bool box = a.ref_dims == 4;
   const int32_t* r = a.ref + bq * a.ref_dims;
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(256) void deform_kernel(DeformArgs a) {
       const int8_t* vl = vbase + (int64_t)a.start[ll] * head_stride;
       const int32_t ic = live ? i : LP - 1;
       const uint64_t pw = ((uint64_t)(uint32_t)elut[m - lg[ic]] * F) >> sh;
-      const int32_t wgt = live ? (int32_t)(pw > 127 ? 127 : pw) : 0;
+      const int32_t wgt = live ? (int32_t)(pw > cap ? cap : pw) : 0;
       const int64_t ox = offset(2 * ic), oy = offset(2 * ic + 1);
       const int64_t X = box ? box_loc((cxs + ox * bw) * Wl) : ((rx * Wl) >> 8) + ox;
       const int64_t Y = box ? box_loc((cys + oy * bh) * Hl) : ((ry * Hl) >> 8) + oy;
@@ -154,7 +155,7 @@ template <int MODE, int J>
 __global__ __launch_bounds__(256) void deform_group_kernel(DeformArgs a) {
   constexpr int NC = MODE == 0 ? 1 : 4;  // value rows per sample
   __shared__ int32_t elut[256];
-  elut[threadIdx.x] = shift_exp(-(int32_t)threadIdx.x, a.I0, 16);
+  elut[threadIdx.x] = shift_exp(-(int32_t)threadIdx.x, a.I0, a.k_inter);
   __syncthreads();
 
   const int32_t G = a.Dh >> 2;
@@ -190,11 +191,12 @@ __global__ __launch_bounds__(256) void deform_group_kernel(DeformArgs a) {
     const uint32_t hi = __shfl_xor((uint32_t)(sum >> 32), o, 64);
     sum += ((uint64_t)hi << 32) | lo;
   }
-  const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, 4);
+  const int32_t sd = a.s_d >= 0 ? a.s_d : calibrate_shift(sum, a.m_p);
   const uint32_t F = shiftmax_factor(sum, sd);
-  // 32 - k_out with k_out = 8; s_d <= 31 (static) or <= 9 (at most 64 values
-  // below 2^30 with m_p = 4) keeps the shift below 64
-  const int32_t sh = 24 + sd;
+  // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63, so the cap
+  // keeps the 64-bit shift defined (s_d reaches 36 with m_p = 31)
+  const int32_t sh = min(32 - a.k_out + sd, 63);
+  const uint64_t cap = (1u << (a.k_out - 1)) - 1;
 
   const bool box = a.ref_dims == 4;
   const int32_t* r = a.ref + bq * a.ref_dims;
@@ -222,7 +224,7 @@ __global__ __launch_bounds__(256) void deform_group_kernel(DeformArgs a) {
     const int32_t l = ic / a.P;
     const int32_t Hl = a.hw[l][0], Wl = a.hw[l][1], st = a.start[l];
     const uint64_t pw = ((uint64_t)(uint32_t)elut[m - lgv[j]] * F) >> sh;
-    const int32_t wgt = valid ? (int32_t)(pw > 127 ? 127 : pw) : 0;
+    const int32_t wgt = valid ? (int32_t)(pw > cap ? cap : pw) : 0;
     const int64_t ox = offset(2 * ic), oy = offset(2 * ic + 1);
     const int64_t X = box ? box_loc((cxs + ox * bw) * Wl) : ((rx * Wl) >> 8) + ox;
     const int64_t Y = box ? box_loc((cys + oy * bh) * Hl) : ((ry * Hl) >> 8) + oy;

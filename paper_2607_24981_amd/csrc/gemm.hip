@@ -506,7 +506,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       mu_l = mean_half_up(s, N);
       const uint32_t V = (uint32_t)(ss - 2 * mu_l * s + N * mu_l * mu_l);
       const uint32_t sigma = newton_isqrt_f64(V, a.ln_iters);
-      F_l = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+      F_l = sigma ? (int32_t)div_2p31m1(sigma) : 0;
     }
     int32_t mu[FJ], F[FJ];
     uint32_t yw2[FI][FJ] = {};  // staged LayerNorm outputs
@@ -592,11 +592,10 @@ hipError_t launch_ln_tile(const GemmArgs& a, hipStream_t s) {
 // Latency mode (ILW_GEMM_PF=1|3 forces it off or on): grids of at most about
 // one wave per SIMD with the throughput tiles.
 bool latency_mode(int64_t waves) {
-  static int ov = -1;
-  if (ov < 0) {
+  static const int ov = [] {  // read once (thread-safe static initialisation)
     const char* e = getenv("ILW_GEMM_PF");
-    ov = (e && (atoi(e) == 1 || atoi(e) == 3)) ? atoi(e) : 0;
-  }
+    return (e && (atoi(e) == 1 || atoi(e) == 3)) ? atoi(e) : 0;
+  }();
   if (ov) return ov == 3;
   return waves <= 1024;
 }

@@ -180,11 +180,20 @@ __device__ __forceinline__ uint32_t newton_isqrt_f64(uint32_t V, int32_t iters) 
   return (uint32_t)k;
 }
 
-// floor((2^31 - 1) / s) for s in [1, 2^31 - 1] from a refined FP64
-// reciprocal and one integer correction.
-__device__ __forceinline__ uint32_t div_2p31m1_ln(uint32_t s) {
-  double r = __builtin_amdgcn_rcp((double)s);
-  r = fma(r, fma(-(double)s, r, 1.0), r);
+// floor((2^31 - 1) / s), exact for every s in [1, 2^31 - 1] (the Shiftmax
+// factor F and LayerNorm's 1 / sigma both use it).
+// Error bound: the hardware FP64 reciprocal estimate has a relative error of
+// at most 2^29 ulp = 2^-23; one Newton step squares it, so with the fma
+// roundings |rc - 1/s| / (1/s) < 2^-45.  The product 2^31 * rc is then within
+// 2^-14 of the true quotient (plus one rounding of 2^-22 at most), so its
+// truncation q is floor - 1, floor or floor + 1, and the remainder
+// 2^31 - 1 - q s, taken exactly in int64, tells which: one correction step
+// lands on the floor.  Without the Newton step the error near s = 1 would be
+// 2^31 * 2^-23 = 2^8 units.
+__device__ __forceinline__ uint32_t div_2p31m1(uint32_t s) {
+  const double sd = (double)s;
+  double r = __builtin_amdgcn_rcp(sd);
+  r = fma(r, fma(-sd, r, 1.0), r);
   int64_t q = (int64_t)(2147483647.0 * r);
   const int64_t rem = 2147483647LL - q * (int64_t)s;
   q += rem < 0 ? -1 : (rem >= (int64_t)s ? 1 : 0);
@@ -436,7 +445,7 @@ struct DeformArgs {
   int32_t B, Q, H, Dh, L, P, S;
   int32_t hw[kMaxLevels][2];
   int32_t start[kMaxLevels];
-  int32_t I0, s_d, out_mult, out_shift, mode;
+  int32_t I0, k_inter, k_out, m_p, s_d, out_mult, out_shift, mode;
   int32_t ref_dims;  // 2: reference points (x, y); 4: reference boxes (cx, cy, w, h)
   const int8_t* offs8;  // when set, int8 offsets used as offs8 << off_shift instead of offs
   int32_t off_shift;

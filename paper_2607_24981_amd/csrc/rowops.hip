@@ -164,7 +164,7 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
     const int32_t mu = mean_half_up(S, C);
     const uint32_t V = (uint32_t)(SS - 2 * mu * S + C * mu * mu);
     const uint32_t sigma = newton_isqrt_f64(V, iters);
-    const int32_t F = sigma ? (int32_t)div_2p31m1_ln(sigma) : 0;
+    const int32_t F = sigma ? (int32_t)div_2p31m1(sigma) : 0;
     v4i* yr = (v4i*)(y + (live ? row : rows - 1) * C);
 #pragma unroll
     for (int j = 0; j < JC; ++j) {

@@ -16,7 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 7
+ABI_VERSION = 8
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -115,9 +115,9 @@ _SIGS = {
     "ilw_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(c_i32), c_i32]),
     "ilw_deform_attn": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp,
-                                       c_vp] + [c_i32] * 9 + [c_vp]),
+                                       c_vp] + [c_i32] * 12 + [c_vp]),
     "ilw_deform_attn_boxes": (ctypes.c_int, [c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp,
-                                             c_vp] + [c_i32] * 9 + [c_vp]),
+                                             c_vp] + [c_i32] * 12 + [c_vp]),
 }
 
 _LIB = None
@@ -536,7 +536,7 @@ def ilw_split_conv(xs, ws, branch_mults, branch_shifts, bias, out_mult, out_shif
 
 
 def _deform(entry, ref_dims, value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
-            out_shift, mode, s_d, out):
+            out_shift, mode, s_d, out, k_inter, k_out, m_p):
     B, S, H, Dh = value.shape
     _, Q, _, L, P, _ = offsets.shape
     if tuple(ref.shape) != (B, Q, ref_dims):
@@ -550,26 +550,28 @@ def _deform(entry, ref_dims, value, level_hw, level_start, ref, offsets, logits,
                                _dev(ref, torch.int32, "ref"),
                                _dev(offsets, torch.int16, "offsets"),
                                _dev(logits, torch.int8, "logits"), _dev(out, torch.int8, "out"),
-                               B, Q, H, Dh, I0, s_d, out_mult, out_shift, mode, _stream())
+                               B, Q, H, Dh, I0, k_inter, k_out, m_p, s_d, out_mult,
+                               out_shift, mode, _stream())
     _check(rc, entry)
     return out
 
 
 def ilw_deform_attn(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
-                    out_shift, mode=0, s_d=-1, out=None):
+                    out_shift, mode=0, s_d=-1, out=None, k_inter=16, k_out=8, m_p=4):
     """value int8 [B, S, H, Dh]; ref int32 [B, Q, 2] (points); offsets int16
     [B, Q, H, L, P, 2]; logits int8 [B, Q, H, L*P]; level_hw / level_start are
-    host arrays."""
+    host arrays; I0, k_inter, k_out, m_p, s_d are the Constrained Shiftmax
+    parameters of the sampling weights."""
     return _deform("ilw_deform_attn", 2, value, level_hw, level_start, ref, offsets, logits,
-                   I0, out_mult, out_shift, mode, s_d, out)
+                   I0, out_mult, out_shift, mode, s_d, out, k_inter, k_out, m_p)
 
 
 def ilw_deform_attn_boxes(value, level_hw, level_start, ref, offsets, logits, I0, out_mult,
-                          out_shift, mode=0, s_d=-1, out=None):
+                          out_shift, mode=0, s_d=-1, out=None, k_inter=16, k_out=8, m_p=4):
     """As ilw_deform_attn with reference boxes: ref int32 [B, Q, 4]
     (cx, cy, w, h), offsets in Q8 units of size / (2 P)."""
     return _deform("ilw_deform_attn_boxes", 4, value, level_hw, level_start, ref, offsets,
-                   logits, I0, out_mult, out_shift, mode, s_d, out)
+                   logits, I0, out_mult, out_shift, mode, s_d, out, k_inter, k_out, m_p)
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",

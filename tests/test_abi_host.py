@@ -197,22 +197,27 @@ def test_attention_and_deform_validation():
                            None) == E_NULL
     hw = (ctypes.c_int32 * 6)(80, 80, 40, 40, 20, 20)
     st = (ctypes.c_int32 * 3)(0, 6400, 8000)
-    args = dict(L=3, P=4, B=8, Q=300, heads=8, head_dim=32, I0=16, s_d=-1, m=1 << 30,
-                s=34, mode=0)
+    args = dict(L=3, P=4, B=8, Q=300, heads=8, head_dim=32, I0=16, k_inter=16, k_out=8,
+                m_p=4, s_d=-1, m=1 << 30, s=34, mode=0)
 
     def call(**o):
         a = {**args, **o}
         return L.ilw_deform_attn(FAKE, hw, st, a["L"], a["P"], FAKE, FAKE, FAKE, FAKE, a["B"],
-                                 a["Q"], a["heads"], a["head_dim"], a["I0"], a["s_d"], a["m"],
-                                 a["s"], a["mode"], None)
+                                 a["Q"], a["heads"], a["head_dim"], a["I0"], a["k_inter"],
+                                 a["k_out"], a["m_p"], a["s_d"], a["m"], a["s"], a["mode"], None)
     assert call(mode=2) == E_PARAM
     assert call(head_dim=30) == E_SHAPE
     assert call(P=30) == E_SHAPE
     assert call(I0=0) == E_PARAM
+    assert call(k_inter=17) == E_PARAM
+    assert call(k_out=9) == E_PARAM
+    assert call(k_out=1) == E_PARAM
+    assert call(m_p=32) == E_PARAM
+    assert call(s_d=32) == E_PARAM
     assert call(mode=1, s=50) == E_PARAM
     assert call(Q=0) == OK
     assert L.ilw_deform_attn(FAKE, None, st, 3, 4, FAKE, FAKE, FAKE, FAKE, 8, 300, 8, 32, 16,
-                             -1, 1 << 30, 34, 0, None) == E_NULL
+                             16, 8, 4, -1, 1 << 30, 34, 0, None) == E_NULL
 
 
 def test_split_conv_validation():

@@ -343,17 +343,26 @@ ATTN_CASES = [
 ]
 
 
-@pytest.mark.parametrize("s_d", [20, 25])
-def test_attention_static_sd_small_denominator(s_d):
-    """A static s_d far above the dynamic one with a large I0: S_R is a few
-    dozen, so F = floor((2^31 - 1) / S_R) is near 2^26, where an unrefined
-    FP64 reciprocal is off by more than one unit (a regression case)."""
-    B, gh, gw, H = 1, 16, 16, 3
-    say(f"attention static s_d={s_d}, I0=64")
-    g = rng(900 + s_d)
+@pytest.mark.parametrize("grid", [16, 4])
+@pytest.mark.parametrize("I0", [1, 64, 16383])
+@pytest.mark.parametrize("s_d", [20, 25, 31])
+def test_attention_static_sd_small_denominator(s_d, I0, grid):
+    """A static s_d far above the dynamic one: S_R = S_sum >> s_d is a few
+    dozen or less, so F = floor((2^31 - 1) / S_R) is near 2^26..2^31, where an
+    unrefined FP64 reciprocal is off by more than one unit (a regression
+    case).  I0 at both ends of its range: with I0 = 1 and s_d >= 25 the
+    shifted sum is 0 and clamps to 1 (F = 2^31 - 1); with I0 = 2^14 - 1 the
+    exponentials use all of their 30 bits, and the 16-key rows (4 x 4 grid)
+    keep the probabilities of nearly flat rows above one output unit.  Where
+    every probability rounds to 0 (I0 = 1 with s_d >= 25; s_d = 31 unless
+    I0 is large and the row short) the output is 0, a degenerate case the
+    kernel must reproduce as well."""
+    B, gh, gw, H = 1, grid, grid, 3
+    say(f"attention static s_d={s_d}, I0={I0}, grid {grid}x{grid}")
+    g = rng(900 + s_d + I0 + grid)
     D, T = 64 * H, gh * gw
     qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
-    p = {"score_mult": (1 << 29) + 4321, "score_shift": 39, "smax_I0": 64, "smax_s_d": s_d,
+    p = {"score_mult": (1 << 29) + 4321, "score_shift": 39, "smax_I0": I0, "smax_s_d": s_d,
          "pv_mult": (1 << 29) + 777, "pv_shift": 36}
     ref = oracle.attention(qkv[0], gh, gw, 0, 0, H, 64, p["score_mult"], p["score_shift"],
                            p["smax_I0"], p["pv_mult"], p["pv_shift"], s_d=s_d)[None]
@@ -1176,6 +1185,40 @@ def test_deform_lane_groups(mode, boxes, dh, levels, P):
                      dev(d["offsets"]), dev(d["logits"]), d["I0"], d["out_mult"],
                      d["out_shift"], mode))
     assert_same(got, ref, "deform lane groups")
+
+
+# (k_inter, k_out, m_p, s_d, I0) of the sampling weights' Constrained Shiftmax
+DEFORM_SMAX = [(16, 4, 4, -1, 16), (8, 2, 0, -1, 16), (12, 6, 31, -1, 16),
+               (16, 8, 4, 20, 16383), (16, 8, 4, 31, 16383), (1, 3, 4, 0, 1),
+               (16, 8, 31, -1, 1)]
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("dh,boxes", [(32, False), (32, True), (48, True)])
+@pytest.mark.parametrize("smax", DEFORM_SMAX)
+def test_deform_shiftmax_params(smax, dh, boxes, mode):
+    """Every Constrained Shiftmax parameter of the sampler away from the
+    decoder's defaults: k_out down to 2 (weights 0 or 1), m_p = 31 with the
+    per-row s_d (the output shift reaches the 64-bit cap), static s_d up to
+    31 with I0 at both ends of its range; the wave-group kernel (32 channels
+    per head) and the general one (48).  The output shift is the smallest in
+    [20, 40) at which the oracle saturates under a fifth of the outputs."""
+    k_inter, k_out, m_p, s_d, I0 = smax
+    say(f"deform smax k_inter={k_inter} k_out={k_out} m_p={m_p} s_d={s_d} I0={I0} "
+        f"dh={dh} boxes={boxes} mode={mode}")
+    levels, P = (((9, 13), (4, 6), (2, 3), (1, 1)), 8) if dh == 32 else (((5, 4), (2, 2)), 3)
+    wl = synth.DeformWorkload("g", 2, 11, dh * 3, 3, dh, levels, P)
+    d = synth.deform_inputs(wl, dh + P + k_inter + k_out, boxes=boxes)
+    entry = ilw.ilw_deform_attn_boxes if boxes else ilw.ilw_deform_attn
+    kw = dict(k_inter=k_inter, k_out=k_out, m_p=m_p, s_d=s_d)
+    for sh in range(20, 40):
+        ref = oracle.deform_attn(d["value"], d["level_hw"], d["level_start"], d["ref"],
+                                 d["offsets"], d["logits"], I0, 1 << 30, sh, mode, **kw)
+        if np.mean(np.abs(ref) == 127) < 0.2:
+            break
+    got = host(entry(dev(d["value"]), d["level_hw"], d["level_start"], dev(d["ref"]),
+                     dev(d["offsets"]), dev(d["logits"]), I0, 1 << 30, sh, mode, **kw))
+    assert_same(got, ref, "deform shiftmax params")
 
 
 @pytest.mark.parametrize("parts,B", [(2, 4), (2, 3), (3, 5)])

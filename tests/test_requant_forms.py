@@ -1,5 +1,7 @@
-"""The kernels' fast forms of the dyadic requantization (Sec. 3.1: round
-half up, saturated to [-127, 127]), checked on the CPU against the integer
+"""The kernels' fast forms of the dyadic requantization (Sec. 3.2.1, Eq. 1:
+the scales are applied after the integer accumulation, as a dyadic multiply
+and shift; rounding half up and saturation to [-127, 127] are the readings
+this implementation takes), checked on the CPU against the integer
 definition q = sat(floor((v * m + 2^(s-1)) / 2^s)).
 
 * Linear epilogues.  Per channel, c = b m + 2^(s-1) folds the bias and the
