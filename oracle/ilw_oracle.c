@@ -10,8 +10,8 @@
  *   Sec. 3.2.1 / eq. (linear_quant)  integer linear layer, dyadic rescale
  *   Sec. 3.2.2                       dyadic multiply-and-shift rescale
  *   Sec. 3.3 (opening paragraph)     I-ViT integer LayerNorm, Newton sqrt
- *   Sec. 3.3.1, Alg. 1               ShiftExp, SD-ShiftGELU
- *   Sec. 3.3.2, Alg. 2               Constrained Shiftmax, CalibrateShift
+ *   Sec. 3.3.1 (ShiftExp of I-ViT)   ShiftExp, SD-ShiftGELU
+ *   Sec. 3.3.2                       Constrained Shiftmax, denominator shift
  *   Sec. 3.1.1                       nearest-neighbour deformable sampling
  * Readings of points the paper leaves open are stated where they are used.
  *
@@ -77,46 +77,82 @@ int32_t orc_residual(int32_t a, int32_t b, int32_t mult_a, int32_t mult_b,
   return sat8(floor_div(v, pow2(shift)));
 }
 
-/* ShiftExp (Alg. 1, function ShiftExp), for a non-positive input I with
- * I0 = round(1/S) passed in as an integer.  Returns I_exp; the matching scale
- * is S / 2^k_inter. */
+/* ceil(a / b) for a >= 0, b >= 1. */
+static int64_t ceil_div_nonneg(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+/* The sigmoid argument of eq. gelu, 1.702 x, as x + x/2 + x/8 + x/16 with
+ * floor shifts (Sec. 3.3.1). */
+static int64_t gelu_sigmoid_arg(int64_t x) {
+  return x + (int64_t)floor_div(x, 2) + (int64_t)floor_div(x, 8) + (int64_t)floor_div(x, 16);
+}
+
+/* ShiftExp, the integer exponential of I-ViT that Sec. 3.3.1 and 3.3.2 build
+ * on (its steps are spelled out in the appendix, Alg. 1).  For an input
+ * I <= 0 at scale S = 1 / I0 it approximates exp(S I) = 2^(-z / I0) with
+ * z = -I log2(e):
+ *   - log2(e) ~ 1 + 1/2 - 1/16, applied with floor shifts to the negative
+ *     input, which for the magnitude a = -I rounds the two fractions up:
+ *     z = a + ceil(a / 2) - ceil(a / 16);
+ *   - z is capped at k_inter I0 (the exponential is clipped below at
+ *     2^-k_inter);
+ *   - z = n I0 + f with 0 <= f < I0, so 2^(-z/I0) = 2^-n 2^(-f/I0), and the
+ *     fractional power is the chord 1 - f / (2 I0), in units of 1/I0:
+ *     I0 - ceil(f / 2);
+ *   - the result carries k_inter extra bits: (I0 - ceil(f/2)) 2^(k_inter - n),
+ *     at scale S / 2^k_inter. */
 int64_t orc_shiftexp(int64_t I, int32_t I0, int32_t k_inter) {
   orc_require(I <= 0, "ShiftExp input must be <= 0");
   orc_require(I0 >= 1, "I0 >= 1");
   orc_require(k_inter >= 1 && k_inter <= 30, "k_inter in [1, 30]");
-  /* I * log2(e) approximated as I + I/2 - I/16 with floor shifts */
-  int64_t Ie = I + (int64_t)floor_div(I, 2) - (int64_t)floor_div(I, 16);
-  /* lower-bound clipping at k_inter * (-I0) */
-  int64_t lo = -(int64_t)k_inter * I0;
-  if (Ie < lo) Ie = lo;
-  /* integer part q = floor(Ie / (-I0)) and decimal part r */
-  int64_t q = (int64_t)floor_div(Ie, -(int64_t)I0);
-  int64_t r = -(Ie - q * (-(int64_t)I0));
-  orc_require(q >= 0 && q <= k_inter, "ShiftExp integer part in [0, k_inter]");
-  orc_require(r >= 0 && r < I0, "ShiftExp decimal part in [0, I0)");
-  /* 2^(-r/I0) approximated linearly: I_b = (-r >> 1) + I0 */
-  int64_t Ib = (int64_t)floor_div(-r, 2) + I0;
-  return (int64_t)((__int128)Ib * pow2(k_inter - (int32_t)q));
+  const int64_t a = -I;
+  int64_t z = a + ceil_div_nonneg(a, 2) - ceil_div_nonneg(a, 16);
+  const int64_t z_cap = (int64_t)k_inter * I0;
+  if (z > z_cap) z = z_cap;
+  const int64_t n = z / I0; /* z >= 0: C division is the floor */
+  const int64_t f = z - n * I0;
+  orc_require(n >= 0 && n <= k_inter, "whole powers of two in [0, k_inter]");
+  const int64_t chord = I0 - ceil_div_nonneg(f, 2);
+  return (int64_t)((__int128)chord * pow2(k_inter - (int32_t)n));
 }
 
-/* CalibrateShift (Alg. 2; Sec. 3.3.2 equations for M_req, M_target, s_d). */
+/* The denominator shift of Constrained Shiftmax (Sec. 3.3.2): the division
+ * needs M_req = ceil(log2 S_sum) bits, plus the margin m_p; whatever exceeds
+ * the hardware precision M_hw is shifted out of the denominator:
+ * s_d = max(M_req + m_p - M_hw, 0). */
 int32_t orc_calibrate_shift(int64_t s_sum, int32_t m_p, int32_t M_hw) {
   orc_require(s_sum >= 1, "S_sum >= 1");
-  /* M_req = ceil(log2(S_sum)): the smallest M with 2^M >= S_sum */
-  int32_t M_req = 0;
+  int32_t M_req = 0; /* smallest M with 2^M >= S_sum */
   while (pow2(M_req) < s_sum) M_req++;
-  int32_t M_target = M_req + m_p;
-  int32_t s_d = M_target - M_hw;
-  return s_d > 0 ? s_d : 0;
+  const int32_t excess = M_req + m_p - M_hw;
+  return excess > 0 ? excess : 0;
 }
 
-/* Constrained Shiftmax over one row (Alg. 2, ConstrainedShiftmax; Sec. 3.3.2).
- * s_d_static >= 0 uses that calibrated denominator shift (the text calibrates
- * one s_d per Shiftmax block); s_d_static == -1 recomputes it from the row's
- * own S_sum as the algorithm listing does.  The final output formula is the
- * one the section ends with (I_exp times F, then one shift that includes
- * s_d).  Reading: the result is stored as a signed k_out-bit integer, so it is
- * limited to 2^(k_out-1) - 1. */
+/* S_R of Sec. 3.3.2: the exponential sum reduced by s_d bits, accumulated as
+ * the quotients of every term by 2^s_d plus the floor of the summed
+ * remainders, which the section shows equals floor(S_sum / 2^s_d); the
+ * equality is checked here. */
+static int64_t reduced_denominator(const int64_t* e, int32_t d, int32_t s_d,
+                                   int64_t S_sum) {
+  int64_t quotients = 0, remainders = 0;
+  for (int32_t i = 0; i < d; i++) {
+    const int64_t Qi = (int64_t)floor_div(e[i], pow2(s_d));
+    quotients += Qi;
+    remainders += e[i] - (int64_t)(Qi * pow2(s_d));
+  }
+  const int64_t S_R = quotients + (int64_t)floor_div(remainders, pow2(s_d));
+  orc_require(S_R == (int64_t)floor_div(S_sum, pow2(s_d)),
+              "quotient-remainder sum equals floor(S_sum / 2^s_d)");
+  return S_R;
+}
+
+/* Constrained Shiftmax over one row (Sec. 3.3.2).  The exponentials are
+ * ShiftExp of the scores less the row maximum (I-ViT's Shiftmax input), their
+ * sum S_sum sets s_d (or s_d_static >= 0 is used as the calibrated value; the
+ * text calibrates one s_d per Shiftmax block, while -1 recomputes it from the
+ * row itself), S_R is clamped to [1, 2^31 - 1], F = floor((2^31 - 1) / S_R),
+ * and out_i = floor(I_exp_i F / 2^(31 - k_out + 1 + s_d)), the form the
+ * section ends with.  Reading: the result is stored as a signed k_out-bit
+ * integer, so it is limited to 2^(k_out-1) - 1. */
 void orc_shiftmax_row(const int32_t* x, int32_t d, int32_t I0, int32_t k_inter,
                       int32_t k_out, int32_t m_p, int32_t s_d_static,
                       int32_t* out, int64_t* diag) {
@@ -126,47 +162,29 @@ void orc_shiftmax_row(const int32_t* x, int32_t d, int32_t I0, int32_t k_inter,
   int64_t* e = (int64_t*)malloc(sizeof(int64_t) * (size_t)d);
   orc_require(e != NULL, "allocation");
 
-  int32_t I_max = x[0];
-  for (int32_t i = 1; i < d; i++)
-    if (x[i] > I_max) I_max = x[i];
-
+  int32_t row_max = x[0];
+  for (int32_t i = 1; i < d; i++) row_max = x[i] > row_max ? x[i] : row_max;
   int64_t S_sum = 0;
   for (int32_t i = 0; i < d; i++) {
-    int64_t I_delta = (int64_t)x[i] - I_max; /* <= 0 */
-    e[i] = orc_shiftexp(I_delta, I0, k_inter);
+    e[i] = orc_shiftexp((int64_t)x[i] - row_max, I0, k_inter);
     S_sum += e[i];
   }
 
-  int32_t s_d = s_d_static >= 0 ? s_d_static
-                                : orc_calibrate_shift(S_sum, m_p, M_hw);
-  /* CalibrateShift puts no upper limit on s_d (S_sum < 2^63 and m_p <= 31
-   * keep it below 64); every shift below is taken in __int128. */
+  const int32_t s_d = s_d_static >= 0 ? s_d_static : orc_calibrate_shift(S_sum, m_p, M_hw);
+  /* nothing bounds s_d from above (S_sum < 2^63 and m_p <= 31 keep it below
+   * 64); the shifts below are taken in __int128 */
   orc_require(s_d >= 0 && s_d <= 90, "s_d in [0, 90]");
 
-  /* quotient-remainder accumulation of the shifted denominator */
-  int64_t sum_Q = 0, sum_r = 0;
-  for (int32_t i = 0; i < d; i++) {
-    int64_t Q = (int64_t)floor_div(e[i], pow2(s_d));
-    int64_t r = e[i] - (int64_t)(Q * pow2(s_d));
-    sum_Q += Q;
-    sum_r += r;
-  }
-  int64_t S_R = sum_Q + (int64_t)floor_div(sum_r, pow2(s_d));
-  /* the decomposition recovers the exact shifted sum */
-  orc_require(S_R == (int64_t)floor_div(S_sum, pow2(s_d)),
-              "quotient-remainder sum equals floor(S_sum / 2^s_d)");
+  const int64_t hw_max = 2147483647; /* 2^31 - 1 */
+  int64_t S_R = reduced_denominator(e, d, s_d, S_sum);
+  S_R = S_R < 1 ? 1 : (S_R > hw_max ? hw_max : S_R);
+  const int64_t F = hw_max / S_R; /* both positive: C division is the floor */
 
-  const int64_t lim = 2147483647; /* 2^31 - 1 */
-  if (S_R < 1) S_R = 1;
-  if (S_R > lim) S_R = lim;
-  int64_t F = lim / S_R; /* both positive: C division is the floor */
-
-  int32_t out_shift = 31 - k_out + 1 + s_d;
-  int64_t out_max = (int64_t)pow2(k_out - 1) - 1;
+  const int32_t out_shift = 31 - k_out + 1 + s_d;
+  const int64_t out_cap = (int64_t)pow2(k_out - 1) - 1;
   for (int32_t i = 0; i < d; i++) {
-    __int128 v = floor_div((__int128)e[i] * F, pow2(out_shift));
-    if (v > out_max) v = out_max;
-    out[i] = (int32_t)v;
+    const __int128 v = floor_div((__int128)e[i] * F, pow2(out_shift));
+    out[i] = (int32_t)(v > out_cap ? out_cap : v);
   }
   if (diag) {
     diag[0] = S_sum;
@@ -225,9 +243,7 @@ void orc_shiftgelu_ivit_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t c
   for (int64_t r = 0; r < rows; r++) {
     int64_t max_ip = 0;
     for (int32_t i = 0; i < cols; i++) {
-      const int64_t I = x[r * cols + i];
-      const int64_t Ip = I + (int64_t)floor_div(I, 2) + (int64_t)floor_div(I, 8) +
-                         (int64_t)floor_div(I, 16);
+      const int64_t Ip = gelu_sigmoid_arg(x[r * cols + i]);
       if (Ip > max_ip) max_ip = Ip;
     }
     for (int32_t i = 0; i < cols; i++)
@@ -237,7 +253,7 @@ void orc_shiftgelu_ivit_rows(const int8_t* x, int8_t* y, int64_t rows, int32_t c
   }
 }
 
-/* IntDiv, which Alg. 1 uses without defining.  Reading: the I-ViT integer
+/* IntDiv, which the SD-ShiftGELU pseudo-code (Alg. 1) uses without defining.  Reading: the I-ViT integer
  * division of eq. shiftmax_original with M = M_hw = 31 applied to one
  * numerator, giving a k_out-bit ratio with scale 2^-(k_out-1):
  *   IntDiv(a, b) = (floor((2^31 - 1) / b) * a) >> (31 - (k_out - 1)).      */
@@ -248,21 +264,26 @@ int64_t orc_intdiv(int64_t a, int64_t b, int32_t k_out) {
   return (int64_t)floor_div(factor * a, pow2(31 - (k_out - 1)));
 }
 
-/* SD-ShiftGELU (Alg. 1; Sec. 3.3.1): GELU(x) ~ x * sigmoid(1.702 x) with a
- * sign-dependent sigmoid, so that each element is processed on its own.
- * Returns I_out = I_x * I_div, whose scale is S_x * 2^-(k_out-1). */
+/* SD-ShiftGELU (Sec. 3.3.1): GELU(x) ~ x sigmoid(z), z = 1.702 x, with the
+ * sigmoid taken in the sign-dependent form the section gives:
+ *   z >= 0:  1 / (1 + exp(-z)) = exp(0) / (exp(0) + exp(-z)),
+ *   z <  0:  exp(z) / (exp(z) + 1) = exp(z) / (exp(z) + exp(0)),
+ * so both ShiftExp arguments are <= 0 and each element stands alone.  The
+ * ratio goes through IntDiv; returns I_out = x * ratio at scale
+ * S_x 2^-(k_out-1). */
 int64_t orc_sdshiftgelu(int32_t x, int32_t I0, int32_t k_inter,
                         int32_t k_out) {
-  int64_t I = x;
-  /* 1.702 * I as I + I/2 + I/8 + I/16 with floor shifts */
-  int64_t Ip = I + (int64_t)floor_div(I, 2) + (int64_t)floor_div(I, 8) +
-               (int64_t)floor_div(I, 16);
-  int64_t Ishift = Ip > 0 ? Ip : 0; /* ReLU(I_p) */
-  int64_t Idelta = Ip - Ishift;     /* <= 0 */
-  int64_t a = orc_shiftexp(Idelta, I0, k_inter);
-  int64_t a2 = orc_shiftexp(-Ishift, I0, k_inter);
-  int64_t Idiv = orc_intdiv(a, a + a2, k_out);
-  return I * Idiv;
+  const int64_t z = gelu_sigmoid_arg(x);
+  const int64_t e_zero = orc_shiftexp(0, I0, k_inter);
+  int64_t numer, other;
+  if (z >= 0) {
+    numer = e_zero;
+    other = orc_shiftexp(-z, I0, k_inter);
+  } else {
+    numer = orc_shiftexp(z, I0, k_inter);
+    other = e_zero;
+  }
+  return (int64_t)x * orc_intdiv(numer, numer + other, k_out);
 }
 
 /* The I-ViT ShiftGELU that SD-ShiftGELU replaces (Sec. 3.3.1): the sigmoid
@@ -272,8 +293,7 @@ int64_t orc_ivit_shiftgelu(int32_t x, int32_t max_ip, int32_t I0,
                            int32_t k_inter, int32_t k_out) {
   orc_require(max_ip >= 0, "vector maximum of I_p must be >= 0");
   int64_t I = x;
-  int64_t Ip = I + (int64_t)floor_div(I, 2) + (int64_t)floor_div(I, 8) +
-               (int64_t)floor_div(I, 16);
+  int64_t Ip = gelu_sigmoid_arg(I);
   orc_require(Ip <= max_ip, "max_ip is the vector maximum");
   int64_t a = orc_shiftexp(Ip - max_ip, I0, k_inter);
   int64_t a2 = orc_shiftexp(-(int64_t)max_ip, I0, k_inter);

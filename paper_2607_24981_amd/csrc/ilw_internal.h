@@ -41,33 +41,33 @@ __device__ __forceinline__ int32_t rq2(int32_t a, int32_t b, int32_t ma, int32_t
 }
 
 // ---------------------------------------------------------------- ShiftExp
-// ShiftExp of a non-positive input (Alg. 1): the exponent I*log2(e) is
-// I + I/2 - I/16 (floor shifts), clipped at -k_inter*I0, split into an integer
-// part q and a remainder r of I0, and 2^(-r/I0) is taken as 1 - r/(2 I0):
-//   I_exp = (I0 - ceil(r/2)) << (k_inter - q)
-// Result < 2^30 for I0 < 2^14 and k_inter <= 16.
+// I-ViT's integer exponential for I <= 0 at scale 1/I0: exp(I / I0) =
+// 2^(-z / I0) with z = -I log2(e) ~ a + a/2 - a/16 for a = -I, the two
+// fractions rounded up (floor shifts of the negative input); z is capped at
+// k_inter I0, split as z = n I0 + f (0 <= f < I0), and 2^(-f/I0) is the chord
+// 1 - f / (2 I0).  Result (I0 - ceil(f/2)) 2^(k_inter - n) < 2^30 for
+// I0 < 2^14 and k_inter <= 16.
 __device__ __forceinline__ int32_t shift_exp(int32_t I, int32_t I0, int32_t k_inter) {
-  int32_t e = I + (I >> 1) - (I >> 4);
-  e = max(e, -k_inter * I0);
-  uint32_t a = (uint32_t)(-e);
-  uint32_t q = a / (uint32_t)I0;
-  uint32_t r = a - q * (uint32_t)I0;
-  int32_t base = I0 - (int32_t)((r + 1) >> 1);
-  return base << (k_inter - (int32_t)q);
+  const uint32_t a = (uint32_t)(-I);
+  const uint32_t z = min(a + ((a + 1) >> 1) - ((a + 15) >> 4), (uint32_t)(k_inter * I0));
+  const uint32_t n = z / (uint32_t)I0;
+  const uint32_t f = z - n * (uint32_t)I0;
+  return (I0 - (int32_t)((f + 1) >> 1)) << (k_inter - (int32_t)n);
 }
 
-// SD-ShiftGELU of one int8 value (Alg. 1): sign-dependent sigmoid of
-// 1.702*x ~ x + x/2 + x/8 + x/16, ratio taken with the M = 31 integer
-// division, times x.  Returns I_out (|I_out| <= 127 * 2^(k_out-1)).
+// SD-ShiftGELU of one int8 value (Sec. 3.3.1): x sigmoid(z), z = 1.702 x ~
+// x + x/2 + x/8 + x/16 (floor shifts), the sigmoid in its sign-dependent
+// form: exp(0) / (exp(0) + exp(-z)) for z >= 0, exp(z) / (exp(z) + exp(0))
+// for z < 0.  Both are t = exp(-|z|) and one = exp(0) = I0 2^k_inter over the
+// same sum; the ratio is floor((2^31 - 1) / sum) times the numerator, kept to
+// k_out - 1 fraction bits.  Returns x times it (|result| <= 127 2^(k_out-1)).
 __device__ __forceinline__ int32_t sd_gelu(int32_t x, int32_t I0, int32_t k_inter,
                                            int32_t k_out) {
-  int32_t ip = x + (x >> 1) + (x >> 3) + (x >> 4);
-  int32_t pos = max(ip, 0);
-  uint32_t a = (uint32_t)shift_exp(ip - pos, I0, k_inter);
-  uint32_t a2 = (uint32_t)shift_exp(-pos, I0, k_inter);
-  uint32_t f = 0x7fffffffu / (a + a2);
-  int32_t d = (int32_t)(((uint64_t)f * a) >> (32 - k_out));
-  return x * d;
+  const int32_t z = x + (x >> 1) + (x >> 3) + (x >> 4);
+  const uint32_t one = (uint32_t)I0 << k_inter;
+  const uint32_t t = (uint32_t)shift_exp(z < 0 ? z : -z, I0, k_inter);
+  const uint32_t f = 0x7fffffffu / (one + t);
+  return x * (int32_t)(((uint64_t)f * (z >= 0 ? one : t)) >> (32 - k_out));
 }
 
 // Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
