@@ -126,8 +126,10 @@ int ilw_sdshiftgelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0,
  * passes mult_i = gamma_i * m and beta_i = b_i / gamma_i, which equals
  * rq(n_i * gamma_i + b_i; m, s) exactly when gamma_i divides b_i (and
  * |gamma_i * m| < 2^31); a float gamma is folded when the multipliers are
- * derived, with no separate rounding of gamma.  C in [4, 16384], a multiple
- * of 4; newton_iters in [1, 64].  y may alias x.
+ * derived, with no separate rounding of gamma.  A gamma that differs across
+ * channels therefore needs a per-channel output dyadic (out.n = C): with one
+ * per-tensor multiplier (out.n = 1) gamma must be uniform.  C in [4, 16384],
+ * a multiple of 4; newton_iters in [1, 64].  y may alias x.
  */
 int ilw_int_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
                       const int32_t* beta, ilw_dyadic out, int32_t newton_iters,

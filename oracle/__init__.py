@@ -18,7 +18,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ilw_oracle.c")
-_SO = os.path.join(_HERE, "libilw_oracle.so")
+# ILW_ORACLE_LIBRARY names another build of the same source (the sanitizer
+# run of the test-suite loads an instrumented one).
+_SO = os.environ.get("ILW_ORACLE_LIBRARY") or os.path.join(_HERE, "libilw_oracle.so")
 _LIB = None
 
 i8p = ctypes.POINTER(ctypes.c_int8)
@@ -38,6 +40,15 @@ def build(force: bool = True) -> str:
                                "-Wall", "-Wextra", "-o", tmp, _SRC])
         os.replace(tmp, _SO)
     return _SO
+
+
+def build_sanitized(out: str, cc: str) -> str:
+    """Compile the oracle with AddressSanitizer and UndefinedBehaviorSanitizer
+    (clang, shared sanitizer runtime, abort on the first report) into `out`."""
+    subprocess.check_call([cc, "-O1", "-g", "-std=c11", "-fPIC", "-shared",
+                           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                           "-fno-omit-frame-pointer", "-shared-libsan", "-o", out, _SRC])
+    return out
 
 
 class OrcBlock(ctypes.Structure):

@@ -61,5 +61,50 @@ def build(verbose: bool = False) -> str:
     return SO
 
 
+# Host-side instrumentation for the sanitizer build: the device code is built
+# as usual, only the host pass of the source gets the sanitizers.
+SANITIZE_HOST = ("-Xarch_host -fsanitize=address,undefined "
+                 "-Xarch_host -fno-sanitize-recover=all "
+                 "-Xarch_host -fno-omit-frame-pointer").split()
+
+
+def build_sanitized(out: str, sources=("api.hip",)) -> str:
+    """Link a copy of the library at `out` whose `sources` (by default the
+    C ABI layer with all argument validation) have AddressSanitizer and
+    UndefinedBehaviorSanitizer in their host code; the other objects are the
+    regular ones.  The sanitizer runtime must be preloaded by the process
+    that loads it."""
+    cc = hipcc()
+    objdir = os.path.join(HERE, "_build")
+    regular = [os.path.join(objdir, src + ".o") for src in SOURCES if src not in sources]
+    if not all(os.path.exists(o) for o in regular):
+        build()
+    objs = []
+    for src in sources:
+        obj = out + "." + src + ".o"
+        cmd = [cc, *FLAGS, *SOURCE_FLAGS.get(src, []), *SANITIZE_HOST, "-g", "-c",
+               os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed on {src} (sanitized):\n{r.stderr}")
+        objs.append(obj)
+    subprocess.check_call([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out,
+                           *objs, *regular])
+    return out
+
+
+def sanitizer_runtime() -> str:
+    """Path of the compiler's shared AddressSanitizer runtime (it also carries
+    the UndefinedBehaviorSanitizer handlers)."""
+    import glob
+    root = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    for base in (root, "/opt/rocm"):
+        hits = sorted(glob.glob(os.path.join(base, "llvm", "lib", "clang", "*", "lib", "linux",
+                                             "libclang_rt.asan-x86_64.so")))
+        if hits:
+            return hits[-1]
+    raise RuntimeError("libclang_rt.asan-x86_64.so not found")
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

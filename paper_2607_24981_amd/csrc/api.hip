@@ -201,6 +201,10 @@ int check_attn(const ilw_attn_params* ap) {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// base + off inside a workspace; a null base (a size query) stays null, since
+// an offset from a null pointer is undefined.
+int8_t* carve(int8_t* base, size_t off) { return base ? base + off : nullptr; }
+
 // Window-major Q/K/V^T buffers carved from a workspace.
 size_t qkv_bytes(int32_t batch, const Geometry& g, int32_t D, QkvLayout* L, int8_t* base,
                  int32_t hd = 64) {
@@ -209,8 +213,8 @@ size_t qkv_bytes(int32_t batch, const Geometry& g, int32_t D, QkvLayout* L, int8
   const size_t vt = (size_t)batch * g.nW * H * 64 * g.Twp;
   if (L) {
     L->q = base;
-    L->k = base + align256(qk);
-    L->vt = base + 2 * align256(qk);
+    L->k = carve(base, align256(qk));
+    L->vt = carve(base, 2 * align256(qk));
     L->T = g.T;
     L->D = D;
     L->H = H;
@@ -287,15 +291,15 @@ size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
   const size_t M = (size_t)batch * g.T;
   size_t off = 0;
   BlockLayout L;
-  L.h = base + off;
+  L.h = carve(base, off);
   off += align256(M * p->dim);
-  size_t q = qkv_bytes(batch, g, p->dim, &L.qkv, base + off);
+  size_t q = qkv_bytes(batch, g, p->dim, &L.qkv, carve(base, off));
   off += q > qkv_reserve ? q : qkv_reserve;
-  L.att = base + off;
+  L.att = carve(base, off);
   off += align256(M * p->dim);
-  L.x1 = base + off;
+  L.x1 = carve(base, off);
   off += align256(M * p->dim);
-  L.g = base + off;
+  L.g = carve(base, off);
   off += align256(M * p->mlp_dim);
   L.total = off;
   if (out) *out = L;
@@ -588,7 +592,7 @@ size_t decoder_layout(const ilw_decoder_params* p, int32_t batch, int32_t Q, int
   size_t off = 0;
   off += qkv_bytes(batch, g, D, &L.qkv, base, D / p->heads);
   auto take = [&](size_t bytes) {
-    int8_t* ptr = base ? base + off : nullptr;
+    int8_t* ptr = carve(base, off);
     off += align256(bytes);
     return ptr;
   };

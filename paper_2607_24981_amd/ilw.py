@@ -15,7 +15,9 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libilw.so")
+# ILW_LIBRARY_PATH loads another build of the same sources instead (the
+# sanitizer run of the CPU test-suite uses a host-instrumented one).
+LIB_PATH = os.environ.get("ILW_LIBRARY_PATH") or os.path.join(_HERE, "libilw.so")
 ABI_VERSION = 8
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t

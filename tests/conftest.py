@@ -11,6 +11,8 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
     config.addinivalue_line("markers", "slow: long-running CPU oracle case")
+    config.addinivalue_line("markers", "sanitize: the CPU suite rebuilt and rerun under "
+                            "AddressSanitizer and UndefinedBehaviorSanitizer")
 
 
 @pytest.fixture(scope="session")
