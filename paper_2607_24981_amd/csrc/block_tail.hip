@@ -294,11 +294,16 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
   uint32_t x1w;
   {
     int32_t o[4];
+    auto res1 = [&](auto wide) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int32_t v = rq_chan(acc[r], chan[NPROJ + n1 + r]);
-      o[r] = rq2(v, (int8_t)(xres >> (8 * r)), a.res1_ma, a.res1_mb, a.res1_shift);
-    }
+      for (int r = 0; r < 4; ++r) {
+        const int32_t v = rq_chan(acc[r], chan[NPROJ + n1 + r]);
+        o[r] = rq2i8<decltype(wide)::value>(v, (int8_t)(xres >> (8 * r)), a.res1_ma, a.res1_mb,
+                                            a.res1_shift);
+      }
+    };
+    if (a.res1_shift < 9) res1(Flag<true>{});
+    else res1(Flag<false>{});
     x1w = pack4(o[0], o[1], o[2], o[3]);
   }
   // h2 = LN2(x1) -> bufX (every wave is past its stage-1 reads of bufX once
@@ -349,11 +354,16 @@ __global__ __launch_bounds__(64 * NWV) void block_tail_kernel(TailArgs a) {
   uint32_t yw;
   {
     int32_t o[4];
+    auto res2 = [&](auto wide) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int32_t v = rq_chan(acc[r], chan[NFC2 + n1 + r]);
-      o[r] = rq2(v, (int8_t)(x1w >> (8 * r)), a.res2_ma, a.res2_mb, a.res2_shift);
-    }
+      for (int r = 0; r < 4; ++r) {
+        const int32_t v = rq_chan(acc[r], chan[NFC2 + n1 + r]);
+        o[r] = rq2i8<decltype(wide)::value>(v, (int8_t)(x1w >> (8 * r)), a.res2_ma, a.res2_mb,
+                                            a.res2_shift);
+      }
+    };
+    if (a.res2_shift < 9) res2(Flag<true>{});
+    else res2(Flag<false>{});
     yw = pack4(o[0], o[1], o[2], o[3]);
   }
   if (tok_ok) *(uint32_t*)(a.y + m * D + n1) = yw;

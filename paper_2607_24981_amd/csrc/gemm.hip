@@ -355,7 +355,9 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       tokv[j] = qoff[t][1];
     }
   }
-  {
+  // The residual add has a 32-bit form for shifts >= 9 (uniform per launch):
+  // the loop below is instantiated for both and selected once.
+  auto requant_tile = [&](auto wide_res) {
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
       if (!ch_ok[i]) continue;
@@ -398,7 +400,8 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
           int32_t o[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            o[r] = rq2(u[r], (int8_t)(s >> (8 * r)), a.res_ma, a.res_mb, a.res_shift);
+            o[r] = rq2i8<decltype(wide_res)::value>(u[r], (int8_t)(s >> (8 * r)), a.res_ma,
+                                                    a.res_mb, a.res_shift);
           const uint32_t word = pack4(o[0], o[1], o[2], o[3]);
           if (!RSTAGED) *(uint32_t*)(a.y + tok[j] + n) = word;
           if (LN || RSTAGED) xw[i][j] = word;
@@ -414,7 +417,11 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
         }
       }
     }
-  }
+  };
+  if (RES && a.res_shift < 9)
+    requant_tile(Flag<true>{});
+  else
+    requant_tile(Flag<false>{});
   // Output words in the accumulator lane layout, transposed into LDS token
   // rows (the weight tiles, free after the K loop; LayerNorm's row sums are
   // past their last read at the first barrier).

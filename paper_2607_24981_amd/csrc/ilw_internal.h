@@ -40,6 +40,18 @@ __device__ __forceinline__ int32_t rq2(int32_t a, int32_t b, int32_t ma, int32_t
   return sat8(v >> shift);
 }
 
+// The same for int8 inputs and shift >= 9 (wide = false): |v| < 2^39 + 2^61
+// but v >> shift < 2^30 + 1 in magnitude, so the shifted value fits int32 and
+// one median clamps it.  wide = true is the general form above; the flag is
+// uniform across the launch, so callers branch on it outside their loops.
+template <bool WIDE>
+__device__ __forceinline__ int32_t rq2i8(int32_t a, int32_t b, int32_t ma, int32_t mb,
+                                         int32_t shift) {
+  if (WIDE) return rq2(a, b, ma, mb, shift);
+  const int64_t v = (int64_t)a * ma + (int64_t)b * mb + ((int64_t)1 << (shift - 1));
+  return min(max((int32_t)(v >> shift), kQmin), kQmax);
+}
+
 // ---------------------------------------------------------------- ShiftExp
 // I-ViT's integer exponential for I <= 0 at scale 1/I0: exp(I / I0) =
 // 2^(-z / I0) with z = -I log2(e) ~ a + a/2 - a/16 for a = -I, the two

@@ -753,6 +753,34 @@ def test_encoder_fused_layernorm_edge_params(D, H):
     assert_same(host(enc.forward(dev(x))), ref, "encoder LN edge parameters")
 
 
+@pytest.mark.parametrize("shift", [1, 8, 9])
+@pytest.mark.parametrize("D,H,B,grid,win", [(192, 3, 1, (16, 16), (8, 8)),
+                                            (192, 3, 2, (9, 12), (3, 4)),
+                                            (384, 6, 2, (7, 10), (7, 5)),
+                                            (128, 2, 2, (6, 8), (3, 4))])
+def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
+    """Residual adds with shifts below 9 (the general 64-bit saturation) and
+    at 9 (the smallest shift of the 32-bit form), in every residual epilogue:
+    the batch-1 block tail (D = 192), the LayerNorm-fused GEMM tiles (192,
+    384) and the plain residual tile (128).  Multipliers near 2^shift, except
+    one of 2^30 in the second block's first residual, which saturates almost
+    every output there."""
+    say(f"encoder residual shift {shift} D={D} B={B} grid={grid}")
+    windows = [win, (0, 0)]
+    blocks = _encoder_case(D, H, 4 * D, 2, 60 + D + shift + B)
+    g = rng(70 + shift + D)
+    for i, blk in enumerate(blocks):
+        blk["res1_shift"] = blk["res2_shift"] = shift
+        for k in ("res1_mult_a", "res1_mult_b", "res2_mult_a", "res2_mult_b"):
+            blk[k] = int(g.integers(1 << (shift - 1), 3 << (shift - 1)))
+        if i == 1:
+            blk["res1_mult_a"] = 1 << 30
+    x = g.integers(-127, 128, (B, grid[0] * grid[1], D)).astype(np.int8)
+    ref = encoder_ref(blocks, windows, x, *grid)
+    enc = ilw.Encoder(blocks, windows, *grid)
+    assert_same(host(enc.forward(dev(x))), ref, "encoder residual shift forms")
+
+
 def test_encoder_big_grid_sampled():
     """A grid large enough for the two-wave-row fused fc2 tile (192 channels,
     deep K), with a ragged token count: sampled images against the oracle."""
