@@ -81,7 +81,7 @@ __device__ __forceinline__ uint32_t pack_min_bytes(uint32_t a, uint32_t b, uint3
 // 2 only the last word step's (T_w = Twp and (JW - 1) LPR <= Twp / 4),
 // 3 only the last two steps' (whole words, JW LPR = Twp / 4 and
 // (JW - 2) LPR <= T_w / 4: every step stays inside the row).
-template <int R, int LPR, bool NARROW, int MASK, int NW, int JW>
+template <int R, int LPR, bool NARROW, int MASK, int NW, int JW, bool P3K>
 __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t lds_row,
                                                             int32_t clampL, int32_t nrb,
                                                             int64_t ntiles) {
@@ -144,16 +144,17 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
     return *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
   };
   auto phase1 = [&](auto fast) {
-    auto scores = [&](int32_t kb, const v4i& kf) {
+    // requantize block kb's products, fold them into the row maxima and store
+    // them biased as bytes
+    auto emit = [&](int32_t kb, const v4i(&sc4)[NF]) {
       const int32_t col = kb * 16 + kc;
 #pragma unroll
       for (int f = 0; f < NF; ++f) {
-        const v4i s = __builtin_amdgcn_mfma_i32_16x16x64_i8(kf, qf[f], zero, 0, 0, 0);
         int32_t v[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          v[r] = decltype(fast)::value ? rq_fast(s[r], sm, sc, ss)
-                                       : rq_clamped(s[r], clampL, sm, srnd, ss);
+          v[r] = decltype(fast)::value ? rq_fast(sc4[f][r], sm, sc, ss)
+                                       : rq_clamped(sc4[f][r], clampL, sm, srnd, ss);
         // keys past the window repeat the last key (clamped rows), so they
         // never raise the maximum
         mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
@@ -161,23 +162,39 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
             pack_bytes(v[0], v[1], v[2], v[3]);
       }
     };
-    // A ring of four key fragments in flight: the load of block kb + 4 NW is
-    // issued right after block kb has been consumed.  Loads past the last
-    // block re-read the clamped last key and are never used.
-    v4i k0 = kload(wave), k1 = kload(wave + NW), k2 = kload(wave + 2 * NW),
-        k3 = kload(wave + 3 * NW);
-    for (int32_t kb = wave; kb < nkb; kb += 4 * NW) {
-      scores(kb, k0);
-      k0 = kload(kb + 4 * NW);
-      if (kb + NW >= nkb) break;
-      scores(kb + NW, k1);
-      k1 = kload(kb + 5 * NW);
-      if (kb + 2 * NW >= nkb) break;
-      scores(kb + 2 * NW, k2);
-      k2 = kload(kb + 6 * NW);
-      if (kb + 3 * NW >= nkb) break;
-      scores(kb + 3 * NW, k3);
-      k3 = kload(kb + 7 * NW);
+    auto products = [&](v4i(&sc4)[NF], const v4i& kf) {
+#pragma unroll
+      for (int f = 0; f < NF; ++f) sc4[f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(kf, qf[f], zero, 0, 0, 0);
+    };
+    if (wave >= nkb) return;
+    // A ring of four key fragments in flight: slot u holds block kb + u NW
+    // and is reloaded with block kb + 4 NW once its products are issued.
+    // Loads past the last block re-read the clamped last key and are never
+    // used.  The products of the next block are issued before the current
+    // block is requantized, so the matrix core and the vector unit overlap;
+    // two product sets alternate.
+    v4i kr[4] = {kload(wave), kload(wave + NW), kload(wave + 2 * NW), kload(wave + 3 * NW)};
+    v4i s0[NF], s1[NF];
+    products(s0, kr[0]);
+    kr[0] = kload(wave + 4 * NW);
+    int32_t kb = wave;
+    // one block: kr slot U + 1 feeds the next block's products; true when kb
+    // was the last block
+    auto step = [&](auto U, v4i(&cur)[NF], v4i(&nxt)[NF]) {
+      constexpr int un = (decltype(U)::value + 1) & 3;
+      const bool more = kb + NW < nkb;
+      if (more) products(nxt, kr[un]);
+      emit(kb, cur);
+      if (!more) return true;
+      kr[un] = kload(kb + 5 * NW);
+      kb += NW;
+      return false;
+    };
+    for (;;) {
+      if (step(IntC<0>{}, s0, s1)) break;
+      if (step(IntC<1>{}, s1, s0)) break;
+      if (step(IntC<2>{}, s0, s1)) break;
+      if (step(IntC<3>{}, s1, s0)) break;
     }
   };
   if (a.rq_fast)
@@ -279,15 +296,87 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   }
   __syncthreads();
 
-  // ---- phase 3: O = P V.  Wave w owns channels 16 (w % 4) .. + 15 over
-  // key range w / 4 (64-key blocks kp, kp + KP, ...); V^T is the A operand
-  // (rows = channels), P^T the B operand (columns = query rows), so a lane
-  // holds 4 consecutive channels of one query row.
+  // ---- phase 3: O = P V.  V^T is the A operand (rows = channels), P^T the
+  // B operand (columns = query rows), so a lane holds 4 consecutive channels
+  // of one query row.  Two ways to split the work over the waves:
+  //  * P3K (4 waves, rows of at least 752 keys): wave w takes the 64-key
+  //    blocks w, w + 4, ... for all 64 channels, so P is read from LDS once
+  //    per workgroup; the four partial sums of each 16-channel group are then
+  //    added through LDS (the score rows, free by then) by the wave that
+  //    owns the group (channels 16 w .. 16 w + 15);
+  //  * otherwise wave w owns channels 16 (w % 4) .. + 15 over key range
+  //    w / 4 (64-key blocks kp, kp + KP, ...), reading all of its key range
+  //    of P.
   v4i o[NF];
 #pragma unroll
   for (int f = 0; f < NF; ++f) o[f] = zero;
-  const int cg = wave & 3, kp = wave >> 2;
+  const int cg = P3K ? wave : (wave & 3);
   const int32_t c0 = cg * 16;
+  if constexpr (P3K) {
+    static_assert(NW == 4, "one 16-channel group per wave");
+    v4i og[4][NF];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int f = 0; f < NF; ++f) og[g][f] = zero;
+    const int8_t* vrow = Vt + (int64_t)(lane & 15) * Twp + (lane >> 4) * 16;
+    const int8_t* prow = sS + (lane & 15) * lds_row + (lane >> 4) * 16;
+    const int32_t last = Twp - 64;  // loads past the end re-read the last block
+    auto vload4 = [&](v4i(&vf)[4], int32_t j0) {
+      const int32_t jj = min(j0, last);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) vf[g] = *(const v4i*)(vrow + (int64_t)g * 16 * Twp + jj);
+    };
+    auto pv4 = [&](int32_t j0, const v4i(&vf)[4]) {
+      v4i pf[NF];
+#pragma unroll
+      for (int f = 0; f < NF; ++f) pf[f] = *(const v4i*)(prow + f * 16 * lds_row + j0);
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+          og[g][f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(vf[g], pf[f], og[g][f], 0, 0, 0);
+    };
+    // the next block's V^T fragments are in flight while this one is used
+    v4i va[4], vb[4];
+    int32_t j0 = wave * 64;
+    vload4(va, j0);
+    for (;;) {
+      if (j0 >= Twp) break;
+      vload4(vb, j0 + 4 * 64);
+      pv4(j0, va);
+      j0 += 4 * 64;
+      if (j0 >= Twp) break;
+      vload4(va, j0 + 4 * 64);
+      pv4(j0, vb);
+      j0 += 4 * 64;
+    }
+    // partial sums of the other waves' groups to LDS: [wave][g][f][lane]
+    __syncthreads();  // every wave is past its reads of P
+    v4i* part = (v4i*)sS;
+    auto publish = [&](auto G) {
+      constexpr int g = decltype(G)::value;
+      if (g != wave) {
+#pragma unroll
+        for (int f = 0; f < NF; ++f) part[((wave * 4 + g) * NF + f) * 64 + lane] = og[g][f];
+      } else {
+#pragma unroll
+        for (int f = 0; f < NF; ++f) o[f] = og[g][f];
+      }
+    };
+    publish(IntC<0>{});
+    publish(IntC<1>{});
+    publish(IntC<2>{});
+    publish(IntC<3>{});
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q == wave) continue;
+#pragma unroll
+      for (int f = 0; f < NF; ++f) o[f] += part[((q * 4 + wave) * NF + f) * 64 + lane];
+    }
+  } else {
+  const int kp = wave >> 2;
   const int8_t* vrow = Vt + (int64_t)(c0 + (lane & 15)) * Twp + (lane >> 4) * 16;
   const int8_t* prow = sS + (lane & 15) * lds_row + (lane >> 4) * 16;
   const int32_t last = Twp - 64;  // loads past the end re-read the last block
@@ -331,6 +420,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
         const v4i t = ored[((q * 4 + cg) * NF + f) * 64 + lane];
         o[f] += t;
       }
+  }
   }
   const int32_t b_img = bw / a.nW, w = bw % a.nW;
   const int32_t wy = w / a.nwx, wx = w % a.nwx;
@@ -393,11 +483,13 @@ hipError_t allow_dynamic_lds(const void* kern, size_t smem) {
   return e;
 }
 
-template <int R, int LPR, bool NARROW, int MASK, int NW, int JW>
+template <int R, int LPR, bool NARROW, int MASK, int NW, int JW, bool P3K>
 hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   const int32_t lds_row = a.Twp + 16;
   const size_t smem = (size_t)R * lds_row;
-  auto kern = attention_kernel<R, LPR, NARROW, MASK, NW, JW>;
+  // the split-key P V exchange needs 16 KB per 16 query rows of score rows
+  if (P3K && lds_row < 1024) return hipErrorInvalidValue;
+  auto kern = attention_kernel<R, LPR, NARROW, MASK, NW, JW, P3K>;
   if (smem > 65536) {
     const hipError_t e = allow_dynamic_lds((const void*)kern, smem);
     if (e != hipSuccess) return e;
@@ -409,7 +501,7 @@ hipError_t launch_variant(const AttnArgs& a, int32_t clampL, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int R, int LPR, int NW, int JW = 8>
+template <int R, int LPR, int NW, int JW = 8, bool P3K = false>
 hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStream_t s) {
   // A lane sums at most 4 JW ShiftExp values, each at most emax = ShiftExp(0)
   // = I0 * 2^k_inter: 32-bit partial sums are exact while 4 JW emax < 2^32.
@@ -418,27 +510,27 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStrea
   // exact fit: mask only the last two word steps (the 400-token windows, 3%)
   if (mask == 0 && JW * LPR == (a.Twp >> 2) && (JW - 2) * LPR <= (a.Tw >> 2)) mask = 3;
   if (narrow) {
-    if (mask == 3) return launch_variant<R, LPR, true, 3, NW, JW>(a, clampL, s);
-    if (mask == 2) return launch_variant<R, LPR, true, 2, NW, JW>(a, clampL, s);
-    return mask ? launch_variant<R, LPR, true, 1, NW, JW>(a, clampL, s)
-                : launch_variant<R, LPR, true, 0, NW, JW>(a, clampL, s);
+    if (mask == 3) return launch_variant<R, LPR, true, 3, NW, JW, P3K>(a, clampL, s);
+    if (mask == 2) return launch_variant<R, LPR, true, 2, NW, JW, P3K>(a, clampL, s);
+    return mask ? launch_variant<R, LPR, true, 1, NW, JW, P3K>(a, clampL, s)
+                : launch_variant<R, LPR, true, 0, NW, JW, P3K>(a, clampL, s);
   }
-  if (mask == 3) return launch_variant<R, LPR, false, 3, NW, JW>(a, clampL, s);
-  if (mask == 2) return launch_variant<R, LPR, false, 2, NW, JW>(a, clampL, s);
-  return mask ? launch_variant<R, LPR, false, 1, NW, JW>(a, clampL, s)
-              : launch_variant<R, LPR, false, 0, NW, JW>(a, clampL, s);
+  if (mask == 3) return launch_variant<R, LPR, false, 3, NW, JW, P3K>(a, clampL, s);
+  if (mask == 2) return launch_variant<R, LPR, false, 2, NW, JW, P3K>(a, clampL, s);
+  return mask ? launch_variant<R, LPR, false, 1, NW, JW, P3K>(a, clampL, s)
+              : launch_variant<R, LPR, false, 0, NW, JW, P3K>(a, clampL, s);
 }
 
 // The 16-word variants with the smallest word count the window needs: 13
 // words cover 1600-token rows over 32 lanes, 14 the 448-byte padded
 // 400-token rows over 8 lanes, 10 the 320-byte padded 300-query rows.
-template <int R, int LPR, int NW>
+template <int R, int LPR, int NW, bool P3K = false>
 hipError_t launch_fit16(const AttnArgs& a, int32_t clampL, int64_t emax, hipStream_t s) {
   const int32_t jw = ((a.Twp >> 2) + LPR - 1) / LPR;
-  if (jw <= 10) return launch_rows<R, LPR, NW, 10>(a, clampL, emax, s);
-  if (jw <= 13) return launch_rows<R, LPR, NW, 13>(a, clampL, emax, s);
-  if (jw == 14) return launch_rows<R, LPR, NW, 14>(a, clampL, emax, s);
-  return launch_rows<R, LPR, NW, 16>(a, clampL, emax, s);
+  if (jw <= 10) return launch_rows<R, LPR, NW, 10, P3K>(a, clampL, emax, s);
+  if (jw <= 13) return launch_rows<R, LPR, NW, 13, P3K>(a, clampL, emax, s);
+  if (jw == 14) return launch_rows<R, LPR, NW, 14, P3K>(a, clampL, emax, s);
+  return launch_rows<R, LPR, NW, 16, P3K>(a, clampL, emax, s);
 }
 
 template <int R>
@@ -461,7 +553,8 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t w
   // best of 16 or 32 rows over 4, 8 or 16 waves for 1600-token rows at
   // batch 1).
   if (wgs * 4 <= 2048) return launch_fit16<32, 32, 16>(a, clampL, emax, s);
-  if constexpr (R == 32) return launch_fit16<32, 32, 4>(a, clampL, emax, s);
+  // (P V split by key blocks over the 4 waves: P read from LDS once)
+  if constexpr (R == 32) return launch_fit16<32, 32, 4, true>(a, clampL, emax, s);
   return launch_rows<R, 64, 4>(a, clampL, emax, s);
 }
 

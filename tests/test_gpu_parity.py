@@ -389,6 +389,33 @@ def test_attention(case, s_d):
     assert_same(got, ref, "attention")
 
 
+@pytest.mark.parametrize("case", [
+    # (B, grid_h, grid_w, heads, head_dim): grids of 32-row blocks large enough
+    # for the split-key P V phase (rows past 1024 keys, 4 waves)
+    (4, 40, 40, 3, 64),     # 1600 keys, 25 key blocks over 4 waves (7, 6, 6, 6)
+    (5, 45, 45, 2, 64),     # 2025 keys: a ragged last block, 2048 padded
+    (6, 26, 40, 3, 64),     # 1040 keys: 17 blocks, just past the threshold
+    (4, 40, 40, 3, 32),     # 32-channel heads: two of the four groups unused
+])
+def test_attention_split_pv(case):
+    B, gh, gw, H, hd = case
+    say(f"attention split P V B={B} grid={gh}x{gw} heads={H} head_dim={hd}")
+    g = rng(gh * 7 + gw + B + hd)
+    D, T = hd * H, gh * gw
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    # scores spread over about 30 units of the int8 scale with a small I0:
+    # peaked rows, so that Shiftmax leaves nonzero weights on 1000+ keys
+    p = {"score_mult": int(g.integers(2 ** 29, 2 ** 30)), "score_shift": 40 if hd == 64 else 39,
+         "smax_I0": int(g.integers(8, 17)), "smax_s_d": -1,
+         "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 34}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, 0, 0, H, hd, p["score_mult"],
+                                     p["score_shift"], p["smax_I0"], p["pv_mult"],
+                                     p["pv_shift"]) for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, 0, 0, H, p))
+    assert_same(got, ref, "attention split P V")
+    assert np.mean(ref == 0) < 0.1 and np.mean(np.abs(ref) == 127) < 0.5
+
+
 # (score_mult, score_shift): the unclamped score form covers shifts 32..54,
 # and smaller shifts when |acc * m / 2^s| stays inside int32 (|acc| <= 2^20);
 # the rest clamp the accumulator first.
