@@ -355,12 +355,21 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       tokv[j] = qoff[t][1];
     }
   }
-  // The residual add has a 32-bit form for shifts >= 9 (uniform per launch):
-  // the loop below is instantiated for both and selected once.
-  auto requant_tile = [&](auto wide_res) {
+  // The residual add has a 32-bit form for shifts >= 9 (uniform per launch),
+  // and tiles inside M x N need no per-lane validity tests (whose exec-mask
+  // branches would split the loop into blocks the compiler cannot
+  // interleave): the loop below is instantiated for each case and selected
+  // once per workgroup.
+  // (only for the 384-channel LayerNorm tile, which holds one workgroup per
+  // CU anyway: elsewhere the interleaved form's extra registers would cost
+  // workgroups per CU)
+  constexpr bool BRANCH_FREE = LN && RSTAGED && TN >= 384;
+  const bool full_tile = BRANCH_FREE && n0 + TN <= N && m0 + TM <= M;
+  auto requant_tile = [&](auto wide_res, auto full) {
+    constexpr bool FULL = decltype(full)::value;
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
-      if (!ch_ok[i]) continue;
+      if (!FULL && !ch_ok[i]) continue;
       const int32_t n = nch[i];
       if (!EARLY && RES) load_resid(i);
       RqI64 rf[4];
@@ -380,7 +389,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       }
 #pragma unroll
       for (int j = 0; j < FJ; ++j) {
-        if (!tok_ok[j]) continue;
+        if (!FULL && !tok_ok[j]) continue;
         int32_t u[4];  // the requantized outputs
 #pragma unroll
         for (int r = 0; r < 4; ++r) u[r] = rf[r].apply(acc[i][j][r]);
@@ -418,10 +427,21 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       }
     }
   };
-  if (RES && a.res_shift < 9)
-    requant_tile(Flag<true>{});
-  else
-    requant_tile(Flag<false>{});
+  if (RES && a.res_shift < 9) {
+    if constexpr (BRANCH_FREE) {
+      if (full_tile) requant_tile(Flag<true>{}, Flag<true>{});
+      else requant_tile(Flag<true>{}, Flag<false>{});
+    } else {
+      requant_tile(Flag<true>{}, Flag<false>{});
+    }
+  } else {
+    if constexpr (BRANCH_FREE) {
+      if (full_tile) requant_tile(Flag<false>{}, Flag<true>{});
+      else requant_tile(Flag<false>{}, Flag<false>{});
+    } else {
+      requant_tile(Flag<false>{}, Flag<false>{});
+    }
+  }
   // Output words in the accumulator lane layout, transposed into LDS token
   // rows (the weight tiles, free after the K loop; LayerNorm's row sums are
   // past their last read at the first barrier).
@@ -522,12 +542,14 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       mu[j] = __shfl(mu_l, j * 16 + (lane & 15), 64);
       F[j] = __shfl(F_l, j * 16 + (lane & 15), 64);
     }
+    // (the 384-channel tile stages its outputs, and those of tokens past M
+    // are never copied out: no per-lane test there)
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
       const int32_t n = wn * WTN + i * 16 + (lane >> 4) * 4;
 #pragma unroll
       for (int j = 0; j < FJ; ++j) {
-        if (!tok_ok[j]) continue;
+        if (!BRANCH_FREE && !tok_ok[j]) continue;
         int32_t o[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
