@@ -280,14 +280,79 @@ GemmArgs gemm_args(const int8_t* x, const int8_t* w, const int32_t* b, const ilw
 struct BlockLayout {
   QkvLayout qkv;
   int8_t *h, *att, *x1, *g;
+  // proj and fc2 weights packed in MFMA fragment order for the 384-channel
+  // LayerNorm-fused kernel, or null where that kernel does not run
+  int8_t *wp_proj, *wp_fc2;
   size_t total;
 };
+
+bool ln_fusable(int32_t D);
+
+// Which of the block's residual linears take the packed-weight kernel: the
+// projection (its LayerNorm is LN2) and fc2 when a next block's LN1 follows.
+bool packs_proj(const ilw_block_params* p, int64_t M) {
+  return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->dim);
+}
+bool packs_fc2(const ilw_block_params* p, bool has_next, int64_t M) {
+  return has_next && ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim);
+}
+size_t packed_bytes(const ilw_block_params* p, bool has_next, int64_t M) {
+  return (packs_proj(p, M) ? align256(packed_frag_bytes(p->dim, p->dim)) : 0) +
+         (packs_fc2(p, has_next, M) ? align256(packed_frag_bytes(p->dim, p->mlp_dim)) : 0);
+}
+// Carves the packed weights of a block from base + off; returns the bytes used.
+size_t packed_layout(const ilw_block_params* p, bool has_next, int64_t M, int8_t* base,
+                     size_t off, BlockLayout* L) {
+  size_t used = 0;
+  L->wp_proj = L->wp_fc2 = nullptr;
+  if (packs_proj(p, M)) {
+    L->wp_proj = carve(base, off);
+    used += align256(packed_frag_bytes(p->dim, p->dim));
+  }
+  if (packs_fc2(p, has_next, M)) {
+    L->wp_fc2 = carve(base, off + used);
+    used += align256(packed_frag_bytes(p->dim, p->mlp_dim));
+  }
+  return used;
+}
+// One launch packing the listed blocks' weights (in groups of kMaxPack).
+hipError_t pack_block_weights(const ilw_block_params* const* ps, const BlockLayout* Ls, int32_t n,
+                              hipStream_t s) {
+  PackList pl = {};
+  auto flush = [&]() -> hipError_t {
+    if (pl.n == 0) return hipSuccess;
+    const hipError_t e = launch_pack_frags(pl, s);
+    pl = PackList{};
+    return e;
+  };
+  auto add = [&](const int8_t* src, int8_t* dst, int32_t N, int32_t K) -> hipError_t {
+    if (pl.n == kMaxPack) {
+      const hipError_t e = flush();
+      if (e != hipSuccess) return e;
+    }
+    pl.src[pl.n] = src;
+    pl.dst[pl.n] = dst;
+    pl.K[pl.n] = K;
+    pl.start[pl.n + 1] = pl.start[pl.n] + (int64_t)N * K / 16;
+    ++pl.n;
+    return hipSuccess;
+  };
+  for (int32_t b = 0; b < n; ++b) {
+    hipError_t e = hipSuccess;
+    if (Ls[b].wp_proj) e = add(ps[b]->w_proj, Ls[b].wp_proj, ps[b]->dim, ps[b]->dim);
+    if (e == hipSuccess && Ls[b].wp_fc2)
+      e = add(ps[b]->w_fc2, Ls[b].wp_fc2, ps[b]->dim, ps[b]->mlp_dim);
+    if (e != hipSuccess) return e;
+  }
+  return flush();
+}
 
 // Workspace of one block: h | Q K V^T | att | x1 | g.  qkv_reserve (when
 // larger than this block's need) fixes the size of the Q K V^T region, so
 // that in an encoder every block's att buffer lies past every block's Q K V^T.
 size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
-                    int8_t* base, BlockLayout* out, size_t qkv_reserve = 0) {
+                    int8_t* base, BlockLayout* out, size_t qkv_reserve = 0,
+                    bool with_packed = true) {
   const size_t M = (size_t)batch * g.T;
   size_t off = 0;
   BlockLayout L;
@@ -301,6 +366,9 @@ size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
   off += align256(M * p->dim);
   L.g = carve(base, off);
   off += align256(M * p->mlp_dim);
+  // a single block has no next block: its fc2 takes the plain residual tile
+  L.wp_proj = L.wp_fc2 = nullptr;
+  if (with_packed) off += packed_layout(p, false, (int64_t)M, base, off, &L);
   L.total = off;
   if (out) *out = L;
   return off;
@@ -480,6 +548,7 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
 
   // x1 = Res(proj(att), x);  h = LN2(x1)
   a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
+  a.wp = fuse ? L.wp_proj : nullptr;
   a.resid = x;
   a.res_ma = p->res1_mult_a;
   a.res_mb = p->res1_mult_b;
@@ -513,6 +582,7 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
   if (he != hipSuccess) return hip_status(he, "block fc1");
   // y = Res(fc2(g), x1);  h = LN1'(y) of the next block
   a = gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
+  a.wp = next && fuse ? L.wp_fc2 : nullptr;
   a.resid = L.x1;
   a.res_ma = p->res2_mult_a;
   a.res_mb = p->res2_mult_b;
@@ -565,11 +635,28 @@ size_t encoder_qkv_reserve(const ilw_block_params* blocks, int32_t n_blocks,
 size_t encoder_workspace(const ilw_block_params* blocks, int32_t n_blocks,
                          const int32_t* windows, int32_t batch, int32_t grid_h, int32_t grid_w) {
   const size_t q = encoder_qkv_reserve(blocks, n_blocks, windows, batch, grid_h, grid_w);
+  size_t need = 0, packed = 0;
+  for (int32_t b = 0; b < n_blocks; ++b) {
+    Geometry g;
+    check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
+    const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr, q, false);
+    need = n > need ? n : need;
+    packed += packed_bytes(&blocks[b], b + 1 < n_blocks, (int64_t)batch * g.T);
+  }
+  // every block's packed weights after the shared per-block region
+  return need + packed;
+}
+
+// The encoder's packed weights: block b's after those of blocks 0 .. b - 1,
+// past the shared per-block region.
+size_t encoder_shared_bytes(const ilw_block_params* blocks, int32_t n_blocks,
+                            const int32_t* windows, int32_t batch, int32_t grid_h, int32_t grid_w) {
+  const size_t q = encoder_qkv_reserve(blocks, n_blocks, windows, batch, grid_h, grid_w);
   size_t need = 0;
   for (int32_t b = 0; b < n_blocks; ++b) {
     Geometry g;
     check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
-    const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr, q);
+    const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr, q, false);
     need = n > need ? n : need;
   }
   return need;
@@ -898,6 +985,8 @@ int ilw_block_forward(const ilw_block_params* p, const int8_t* x, int8_t* y, int
   REQUIRE(aligned16(workspace), ILW_E_PARAM, "workspace must be 16-byte aligned");
   BlockLayout L;
   block_layout(p, batch, g, (int8_t*)workspace, &L);
+  hipError_t he = pack_block_weights(&p, &L, 1, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_status(he, "ilw_block_forward weight packing");
   int ready = READY_NONE;
   return run_block(p, nullptr, nullptr, x, y, batch, g, L, READY_NONE, &ready,
                    (hipStream_t)stream);
@@ -921,6 +1010,8 @@ int ilw_block_forward_noalloc(const ilw_block_params* p, const int8_t* x, int8_t
   if ((e = scratch_of_current_device(&ws))) return e;
   BlockLayout L;
   block_layout(p, batch, g, ws, &L);
+  hipError_t he = pack_block_weights(&p, &L, 1, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_status(he, "ilw_block_forward_noalloc weight packing");
   int ready = READY_NONE;
   return run_block(p, nullptr, nullptr, x, y, batch, g, L, READY_NONE, &ready,
                    (hipStream_t)stream);
@@ -953,21 +1044,32 @@ int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
   // b can leave block b + 1's LN1 output (fused fc2 epilogue) or its Q, K,
   // V^T (block tail kernel) there.
   const size_t qres = encoder_qkv_reserve(blocks, n_blocks, windows, batch, grid_h, grid_w);
+  // the 384-channel LayerNorm-fused linears read their weights packed in
+  // MFMA fragment order: every block's are packed first, in one launch
+  const size_t shared = encoder_shared_bytes(blocks, n_blocks, windows, batch, grid_h, grid_w);
+  std::vector<BlockLayout> Ls((size_t)n_blocks);
+  std::vector<const ilw_block_params*> ps((size_t)n_blocks);
+  {
+    size_t off = shared;
+    for (int32_t b = 0; b < n_blocks; ++b) {
+      Geometry g;
+      check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
+      block_layout(&blocks[b], batch, g, (int8_t*)workspace, &Ls[b], qres, false);
+      off += packed_layout(&blocks[b], b + 1 < n_blocks, (int64_t)batch * g.T,
+                           (int8_t*)workspace, off, &Ls[b]);
+      ps[b] = &blocks[b];
+    }
+    const hipError_t he = pack_block_weights(ps.data(), Ls.data(), n_blocks, s);
+    if (he != hipSuccess) return hip_status(he, "ilw_encoder_forward weight packing");
+  }
   int ready = READY_NONE;
   for (int32_t b = 0; b < n_blocks; ++b) {
     Geometry g;
     check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
-    BlockLayout L;
-    block_layout(&blocks[b], batch, g, (int8_t*)workspace, &L, qres);
+    const BlockLayout& L = Ls[b];
     const ilw_block_params* next = b + 1 < n_blocks ? &blocks[b + 1] : nullptr;
     QkvLayout nq;
-    if (next) {
-      Geometry gn;
-      check_geometry(batch, grid_h, grid_w, windows[2 * b + 2], windows[2 * b + 3], &gn);
-      BlockLayout Ln;
-      block_layout(next, batch, gn, (int8_t*)workspace, &Ln, qres);
-      nq = Ln.qkv;
-    }
+    if (next) nq = Ls[b + 1].qkv;
     int ready_out = READY_NONE;
     if ((e = run_block(&blocks[b], next, next ? &nq : nullptr, b == 0 ? x : y, y, batch, g, L,
                        ready, &ready_out, s)))

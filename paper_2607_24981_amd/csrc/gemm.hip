@@ -85,6 +85,10 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // QKV: the Q and K words likewise (a 16-channel chunk of a token lies in
   // one head's 64-byte window-major row); V^T keeps its byte scatter
   constexpr bool QSTAGED = !LAT && EPI == EPI_QKV;
+  // The 384-channel LayerNorm tile holds one workgroup per CU: tiles inside
+  // M x N take an epilogue without per-lane validity tests there (elsewhere
+  // the extra registers would cost workgroups per CU).
+  constexpr bool BRANCH_FREE = LN && RSTAGED && TN >= 384;
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
   // KB K bytes per step (one or two MFMA K chunks): CPR 16-byte chunks per
   // staged row, rows padded by 16 bytes (80 or 144: the 16 rows of a fragment
@@ -360,10 +364,6 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // branches would split the loop into blocks the compiler cannot
   // interleave): the loop below is instantiated for each case and selected
   // once per workgroup.
-  // (only for the 384-channel LayerNorm tile, which holds one workgroup per
-  // CU anyway: elsewhere the interleaved form's extra registers would cost
-  // workgroups per CU)
-  constexpr bool BRANCH_FREE = LN && RSTAGED && TN >= 384;
   const bool full_tile = BRANCH_FREE && n0 + TN <= N && m0 + TM <= M;
   auto requant_tile = [&](auto wide_res, auto full) {
     constexpr bool FULL = decltype(full)::value;
@@ -631,6 +631,8 @@ bool latency_mode(int64_t waves) {
 
 }  // namespace
 
+bool gemm_latency_mode(int64_t M, int32_t N) { return latency_mode(((M + 63) / 64) * (N / 64)); }
+
 hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (a_in.M == 0) return hipSuccess;
   GemmArgs a = a_in;
@@ -662,6 +664,9 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       return launch_ln_tile<4, 2, 4, 2, 1>(a, s);  // 256 x 64 tokens, 8 waves of 64 x 32
     }
     if (a.N == 384) {
+      // weights packed in fragment order: the register-operand kernel
+      if (!lat && a.wp && ln384_packed_kernel_applies(a.M, a.N, a.K))
+        return launch_ln384_packed(a, s);
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);

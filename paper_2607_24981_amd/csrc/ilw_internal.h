@@ -355,9 +355,34 @@ struct GemmArgs {
   // (pT per image, pgw per row of patches); resid (the positional table)
   // is indexed by the token's position within its image
   int32_t pC, pH, pW, pgw, pT;
+  // RESID_LN with N = 384: the weights packed in MFMA fragment order (see
+  // PackList), or null for the row-major weights above
+  const int8_t* wp;
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+
+// Weights packed in MFMA fragment order: for each 16-channel group n16 and
+// 64-byte K chunk k64, 1 KB in which lane L's 16 bytes are
+// W[16 n16 + L % 16][64 k64 + 16 (L / 16) .. + 15]; chunks ordered n16 major.
+// One launch packs up to kMaxPack matrices (N x K row-major, K % 64 == 0,
+// N % 16 == 0); start[] are the prefix sums of their 16-byte chunk counts.
+constexpr int kMaxPack = 32;
+struct PackList {
+  const int8_t* src[kMaxPack];
+  int8_t* dst[kMaxPack];
+  int32_t K[kMaxPack];
+  int64_t start[kMaxPack + 1];
+  int32_t n;
+};
+size_t packed_frag_bytes(int32_t N, int32_t K);
+hipError_t launch_pack_frags(const PackList& L, hipStream_t s);
+// True where launch_gemm(EPI_RESID_LN) takes the packed-weight kernel when
+// GemmArgs::wp is set (N = 384, K a multiple of 128, a grid past the latency
+// mode).
+bool ln384_packed_kernel_applies(int64_t M, int32_t N, int32_t K);
+hipError_t launch_ln384_packed(const GemmArgs& a, hipStream_t s);
+bool gemm_latency_mode(int64_t M, int32_t N);
 
 // The rest of an encoder block after attention, for one 16-token slab per
 // workgroup (dim 192, MLP 768): projection + residual, LayerNorm, fc1 +
