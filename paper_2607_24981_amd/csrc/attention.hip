@@ -139,10 +139,13 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
   for (int f = 0; f < NF; ++f) mx[f] = 0;
   const int32_t nkb = (Tw + 15) >> 4;
   const int32_t kc = (lane >> 4) * 4;  // first of this lane's 4 keys in a block
-  auto kload = [&](int32_t kb) {
-    const int32_t key = min(kb * 16 + (lane & 15), Tw - 1);
-    return *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16);
-  };
+  // The nkf whole 16-key blocks go through a ring of loads from a per-lane
+  // base (block kb, wave-uniform, clamped to the last whole block); a
+  // partial last block (T_w % 16 != 0) is done on its own afterwards, its
+  // keys past the window clamped to the last key.
+  const int32_t nkf = Tw >> 4;
+  const int8_t* const kbase = K + (lane & 15) * 64 + (lane >> 4) * 16;
+  auto kload = [&](int32_t kb) { return *(const v4i*)(kbase + (int64_t)min(kb, nkf - 1) * 1024); };
   auto phase1 = [&](auto fast) {
     // requantize block kb's products, fold them into the row maxima and store
     // them biased as bytes
@@ -157,7 +160,8 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
                                        : rq_clamped(sc4[f][r], clampL, sm, srnd, ss);
         // keys past the window repeat the last key (clamped rows), so they
         // never raise the maximum
-        mx[f] = max(mx[f], max(max(v[0], v[1]), max(v[2], v[3])));
+        mx[f] = max(max(mx[f], v[0]), v[1]);
+        mx[f] = max(max(mx[f], v[2]), v[3]);
         *(uint32_t*)(sS + (f * 16 + (lane & 15)) * lds_row + col) =
             pack_bytes(v[0], v[1], v[2], v[3]);
       }
@@ -166,7 +170,13 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
 #pragma unroll
       for (int f = 0; f < NF; ++f) sc4[f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(kf, qf[f], zero, 0, 0, 0);
     };
-    if (wave >= nkb) return;
+    if (nkf < nkb && wave == nkf % NW) {  // the partial last block
+      const int32_t key = min(nkf * 16 + (lane & 15), Tw - 1);
+      v4i sp[NF];
+      products(sp, *(const v4i*)(K + (int64_t)key * 64 + (lane >> 4) * 16));
+      emit(nkf, sp);
+    }
+    if (wave >= nkf) return;
     // A ring of four key fragments in flight: slot u holds block kb + u NW
     // and is reloaded with block kb + 4 NW once its products are issued.
     // Loads past the last block re-read the clamped last key and are never
@@ -182,7 +192,7 @@ __global__ __launch_bounds__(64 * NW) void attention_kernel(AttnArgs a, int32_t 
     // was the last block
     auto step = [&](auto U, v4i(&cur)[NF], v4i(&nxt)[NF]) {
       constexpr int un = (decltype(U)::value + 1) & 3;
-      const bool more = kb + NW < nkb;
+      const bool more = kb + NW < nkf;
       if (more) products(nxt, kr[un]);
       emit(kb, cur);
       if (!more) return true;
