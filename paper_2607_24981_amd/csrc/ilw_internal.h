@@ -364,9 +364,12 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 
 // Weights packed in MFMA fragment order: for each 16-channel group n16 and
 // 64-byte K chunk k64, 1 KB in which lane L's 16 bytes are
-// W[16 n16 + L % 16][64 k64 + 16 (L / 16) .. + 15]; chunks ordered n16 major.
-// One launch packs up to kMaxPack matrices (N x K row-major, K % 64 == 0,
-// N % 16 == 0); start[] are the prefix sums of their 16-byte chunk counts.
+// W[16 n16 + L % 16][64 k64 + 16 (L / 16) .. + 15].  The fragments of the 2
+// channel groups a wave of the 384-channel kernel owns are packed together,
+// K chunk major: fragment (n16, k64) is the ((n16 / 2) KC 2 + 2 k64 + n16 % 2)-th
+// KB (KC = K / 64).  One launch packs up to kMaxPack matrices (N x K
+// row-major, K % 64 == 0, N % 32 == 0); start[] are the prefix sums of their
+// 16-byte chunk counts.
 constexpr int kMaxPack = 32;
 struct PackList {
   const int8_t* src[kMaxPack];

@@ -8,13 +8,22 @@
 // A workgroup holds 64 tokens x all 384 channels, so the LayerNorm
 // statistics of a token stay on chip.  Each weight fragment (16 channels x 64
 // K bytes) is used by exactly one wave, so the weights skip LDS: a wave loads
-// its fragments straight into MFMA A-operand registers, one K step ahead.
-// Packed, the 16 x 64 bytes of a fragment are 1 KB contiguous in lane order
-// (lane L holds channel L % 16, K bytes 16 (L / 16) .. + 15), so each load
-// instruction of the wave reads 1 KB contiguous.  Only the 64-token
+// its fragments straight into MFMA A-operand registers.  Packed, the 16 x 64
+// bytes of a fragment are 1 KB contiguous in lane order (lane L holds
+// channel L % 16, K bytes 16 (L / 16) .. + 15), so each load instruction of
+// the wave reads 1 KB contiguous, and the fragments of one wave are grouped
+// K-chunk-major, so that one K step of a wave (2 K chunks x 2 fragments) is
+// 4 KB contiguous: one address, four immediate offsets.  Only the 64-token
 // activation tile is staged through LDS (shared by all waves).  Measured
 // against the LDS-staged weight tile on MI355X: 27% less time in the K loop
 // of the 1536-deep fc2, 20% at K = 384.
+//
+// Weights are loaded two K steps ahead (a ring of three register sets) when
+// the step count is a multiple of 3 (K = 384, 768, 1152, 1536), one step
+// ahead otherwise: fc2 21.4 -> 19.3 us, projection 13.9 -> 13.4 us at batch
+// 8.  Every load of the ring is unconditional (the step index clamped to the
+// last step) and the loop body holds whole ring turns: with guarded loads the
+// compiler waited for each load and spilled the ring.
 //
 // 12 waves: wave w owns channels 32 w .. 32 w + 31 (2 fragments) of all 64
 // tokens (4 fragments); a lane ends up with 4 consecutive channels of token
@@ -29,16 +38,23 @@ namespace {
 constexpr int LN_N = 384, LN_TM = 64, LN_FJ = 4;
 constexpr int LN_KB = 128, LN_LROW = LN_KB + 16;  // 144-byte rows: conflict-free fragments
 constexpr int LN_OSTR = LN_N / 4 + 4;  // output staging: 100 words per token row (odd x 4)
-constexpr int LN_SBUF = 2 * LN_TM * LN_LROW > LN_TM * LN_OSTR * 4 ? 2 * LN_TM * LN_LROW
-                                                                  : LN_TM * LN_OSTR * 4;
+constexpr int LN_XBUF = 3;  // activation tile buffers (the ring's length at most)
+constexpr int LN_SBUF = LN_XBUF * LN_TM * LN_LROW > LN_TM * LN_OSTR * 4
+                            ? LN_XBUF * LN_TM * LN_LROW
+                            : LN_TM * LN_OSTR * 4;
 constexpr int NXCD_LN = 8;
 constexpr int LN_WAVES = 12;  // waves per workgroup: 12 x 32 channels
+constexpr int kPackGroup = LN_N / 16 / LN_WAVES;  // fragments per wave, packed together
 
-// LN_NW waves of LN_FI 16-channel fragments each (LN_NW * LN_FI = 24)
-template <bool WIDE_RES, int LN_NW>
+// LN_NW waves of LN_FI 16-channel fragments each (LN_NW * LN_FI = 24); RING
+// weight register sets (2: one K step ahead, any step count; 3: two steps
+// ahead, step count a multiple of 3)
+template <bool WIDE_RES, int LN_NW, int RING>
 __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_t tiles) {
   constexpr int LN_FI = LN_N / 16 / LN_NW;
   static_assert(LN_FI * LN_NW * 16 == LN_N, "whole fragments per wave");
+  static_assert(LN_FI == kPackGroup, "the packing groups this wave's fragments");
+  static_assert(RING == 2 || RING == 3, "ring of two or three weight sets");
   // X double buffer during the K loop; after it, the output staging rows
   __shared__ __attribute__((aligned(16))) int8_t sbuf[LN_SBUF];
   __shared__ RqI64 rqc[LN_N];    // linear output requantization per channel
@@ -61,18 +77,20 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   const int xo = (tid / 8) * LN_LROW + (tid % 8) * 16;
   static_assert(64 * LN_NW >= LN_TM * LN_KB / 16, "one activation chunk per thread at most");
   const bool xown = tid < LN_TM * LN_KB / 16;  // threads that stage an activation chunk
-  const int8_t* wb = a.wp + (int64_t)(wave * LN_FI) * KC * 1024 + lane * 16;
+  // this wave's fragments: K chunk k64, fragment i at (k64 LN_FI + i) KB
+  const int8_t* wb = a.wp + (int64_t)wave * KC * (LN_FI * 1024) + lane * 16;
   auto wload = [&](v4i(&wf)[2][LN_FI], int kt) {
+    const int8_t* p = wb + (int64_t)kt * (2 * LN_FI * 1024);
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < LN_FI; ++i)
-        wf[h][i] = *(const v4i*)(wb + ((int64_t)i * KC + kt * 2 + h) * 1024);
+      for (int i = 0; i < LN_FI; ++i) wf[h][i] = *(const v4i*)(p + (h * LN_FI + i) * 1024);
   };
-  v4i w0[2][LN_FI], w1[2][LN_FI];
+  v4i w[RING][2][LN_FI];
   v4i rx = {0, 0, 0, 0};
   if (xown) rx = *(const v4i*)xsrc;
-  wload(w0, 0);
+#pragma unroll
+  for (int u = 0; u < RING - 1; ++u) wload(w[u], min(u, nk - 1));
 
   // constants, while the first loads are in flight
   for (int c = tid; c < LN_N; c += 64 * LN_NW) {
@@ -90,8 +108,6 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   for (int i = 0; i < LN_FI; ++i)
 #pragma unroll
     for (int j = 0; j < LN_FJ; ++j) acc[i][j] = zero;
-  int8_t* const sX0 = sbuf;
-  int8_t* const sX1 = sbuf + LN_TM * LN_LROW;
   const int fo = (lane & 15) * LN_LROW + (lane >> 4) * 16;
   auto compute = [&](const int8_t* sx, const v4i(&wf)[2][LN_FI]) {
 #pragma unroll
@@ -106,26 +122,47 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
           acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wf[h][i], fb[j], acc[i][j], 0, 0, 0);
     }
   };
-  // K loop: step kt computes from LDS buffer kt % 2 and weight set kt % 2
-  // while step kt + 1 loads
-  if (xown) *(v4i*)(sX0 + xo) = rx;
+  if (xown) *(v4i*)(sbuf + xo) = rx;
   lds_sync();
-  for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 1 < nk) {
-      if (xown) rx = *(const v4i*)(xsrc + (kt + 1) * LN_KB);
-      wload(w1, kt + 1);
+  if constexpr (RING == 3) {
+    // nk is a multiple of 3.  Step k computes from LDS buffer k % 3 and
+    // weight set k % 3 and loads the activations of step k + 1 and the
+    // weights of step k + 2 (clamped to the last step: re-read, never used).
+    // Buffer (k + 1) % 3 was last read in step k - 2, before the previous
+    // barrier.
+    for (int kt = 0; kt < nk; kt += 3) {
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int k = kt + u;
+        if (xown) rx = *(const v4i*)(xsrc + min(k + 1, nk - 1) * LN_KB);
+        wload(w[(u + 2) % 3], min(k + 2, nk - 1));
+        compute(sbuf + u * LN_TM * LN_LROW, w[u]);
+        if (xown) *(v4i*)(sbuf + ((u + 1) % 3) * LN_TM * LN_LROW + xo) = rx;
+        lds_sync();
+      }
     }
-    compute(sX0, w0);
-    if (kt + 1 < nk && xown) *(v4i*)(sX1 + xo) = rx;
-    lds_sync();
-    if (kt + 1 >= nk) break;
-    if (kt + 2 < nk) {
-      if (xown) rx = *(const v4i*)(xsrc + (kt + 2) * LN_KB);
-      wload(w0, kt + 2);
+  } else {
+    // step kt computes from LDS buffer kt % 2 and weight set kt % 2 while
+    // step kt + 1 loads
+    int8_t* const sX0 = sbuf;
+    int8_t* const sX1 = sbuf + LN_TM * LN_LROW;
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt + 1 < nk) {
+        if (xown) rx = *(const v4i*)(xsrc + (kt + 1) * LN_KB);
+        wload(w[1], kt + 1);
+      }
+      compute(sX0, w[0]);
+      if (kt + 1 < nk && xown) *(v4i*)(sX1 + xo) = rx;
+      lds_sync();
+      if (kt + 1 >= nk) break;
+      if (kt + 2 < nk) {
+        if (xown) rx = *(const v4i*)(xsrc + (kt + 2) * LN_KB);
+        wload(w[0], kt + 2);
+      }
+      compute(sX1, w[1]);
+      if (kt + 2 < nk && xown) *(v4i*)(sX0 + xo) = rx;
+      lds_sync();
     }
-    compute(sX1, w1);
-    if (kt + 2 < nk && xown) *(v4i*)(sX0 + xo) = rx;
-    lds_sync();
   }
 
   // Epilogue.  Lane: channels n_i .. n_i + 3 of token t_j = 16 j + lane % 16.
@@ -250,9 +287,13 @@ __global__ __launch_bounds__(256) void pack_frags_kernel(PackList L) {
   const int64_t local = c - L.start[j];
   const int32_t K = L.K[j], KC = K / 64;
   const int32_t lane = (int32_t)(local % 64);
-  const int64_t blk = local / 64;  // n16 * KC + k64
-  const int64_t n16 = blk / KC;
-  const int32_t k64 = (int32_t)(blk - n16 * KC);
+  // fragment (n16, k64) at blk = (n16 / G) KC G + k64 G + n16 % G, G
+  // fragments per group (one wave's channels)
+  const int64_t blk = local / 64;
+  const int64_t g = blk / ((int64_t)KC * kPackGroup);
+  const int32_t rem = (int32_t)(blk - g * KC * kPackGroup);
+  const int32_t k64 = rem / kPackGroup;
+  const int64_t n16 = g * kPackGroup + rem % kPackGroup;
   const int8_t* src = L.src[j] + (n16 * 16 + lane % 16) * K + k64 * 64 + (lane / 16) * 16;
   *(v4i*)(L.dst[j] + local * 16) = *(const v4i*)src;
 }
@@ -272,20 +313,21 @@ hipError_t launch_pack_frags(const PackList& L, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int NW>
+template <int NW, int RING>
 hipError_t launch_ln384_nw(const GemmArgs& a, int64_t tiles, hipStream_t s) {
   if (a.res_shift < 9)
-    hipLaunchKernelGGL((ln384_wp_kernel<true, NW>), dim3((unsigned)tiles), dim3(64 * NW), 0, s, a,
-                       tiles);
+    hipLaunchKernelGGL((ln384_wp_kernel<true, NW, RING>), dim3((unsigned)tiles), dim3(64 * NW), 0,
+                       s, a, tiles);
   else
-    hipLaunchKernelGGL((ln384_wp_kernel<false, NW>), dim3((unsigned)tiles), dim3(64 * NW), 0, s,
-                       a, tiles);
+    hipLaunchKernelGGL((ln384_wp_kernel<false, NW, RING>), dim3((unsigned)tiles), dim3(64 * NW),
+                       0, s, a, tiles);
   return hipGetLastError();
 }
 
 hipError_t launch_ln384_packed(const GemmArgs& a, hipStream_t s) {
   const int64_t tiles = (a.M + LN_TM - 1) / LN_TM;
-  return launch_ln384_nw<LN_WAVES>(a, tiles, s);
+  if ((a.K / LN_KB) % 3 == 0) return launch_ln384_nw<LN_WAVES, 3>(a, tiles, s);
+  return launch_ln384_nw<LN_WAVES, 2>(a, tiles, s);
 }
 
 }  // namespace ilw

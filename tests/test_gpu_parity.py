@@ -808,17 +808,19 @@ def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
     assert_same(host(enc.forward(dev(x))), ref, "encoder residual shift forms")
 
 
-@pytest.mark.parametrize("variant", ["baseline", "wide"])
-def test_encoder_384_packed_ragged(variant):
+@pytest.mark.parametrize("variant,mlp", [("baseline", 1536), ("wide", 1536), ("baseline", 1024)])
+def test_encoder_384_packed_ragged(variant, mlp):
     """The 384-channel LayerNorm-fused linears on their packed-weight kernel
     (grids past the latency mode: 7 images of 41 x 41 tokens, 11 767 tokens,
     the last 64-token tile 55 rows full): three images of a two-block encoder
-    against the oracle, run on host threads while the GPU works."""
+    against the oracle, run on host threads while the GPU works.  MLP 1536
+    gives fc2 12 K steps (the three-set weight ring), 1024 gives 8 (two
+    sets)."""
     import concurrent.futures as cf
     D, H, B, grid, windows = 384, 6, 7, (41, 41), [(0, 0), (0, 0)]
-    say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}")
+    say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}, MLP {mlp}")
     g = rng(384 + B)
-    blocks = [synth.block_params(g, D, H, 64, 4 * D, variant, ln_iters=10 + 4 * i,
+    blocks = [synth.block_params(g, D, H, 64, mlp, variant, ln_iters=10 + 4 * i,
                                  smax_s_d=(-1 if i == 0 else 5)) for i in range(2)]
     x = g.integers(-127, 128, (B, grid[0] * grid[1], D)).astype(np.int8)
     images = [0, 3, 6]
