@@ -60,6 +60,7 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   __shared__ RqI64 rqc[LN_N];    // linear output requantization per channel
   __shared__ RqI64 lnq[LN_N];    // LayerNorm output requantization per channel
   __shared__ int32_t lnred[LN_NW][LN_TM][2];  // per-wave row sums
+  __shared__ int32_t lnst[LN_TM][2];          // per token: mean, 1 / sigma factor
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -213,46 +214,19 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
       lnred[wave][j * 16 + lane][1] = SS;
     }
   }
-  lds_sync();
-  // statistics of token `lane` (every wave computes all 64: one serial
-  // Newton chain per lane), then each lane fetches those of its tokens
-  int32_t mu_l, F_l;
-  {
-    int32_t s = 0, ss = 0;
-#pragma unroll
-    for (int w = 0; w < LN_NW; ++w) {
-      s += lnred[w][lane][0];
-      ss += lnred[w][lane][1];
-    }
-    mu_l = mean_half_up(s, LN_N);
-    const uint32_t V = (uint32_t)(ss - 2 * mu_l * s + LN_N * mu_l * mu_l);
-    const uint32_t sigma = newton_isqrt_f64(V, a.ln_iters);
-    F_l = sigma ? (int32_t)div_2p31m1(sigma) : 0;
-  }
-  uint32_t yw[LN_FI][LN_FJ];
-#pragma unroll
-  for (int j = 0; j < LN_FJ; ++j) {
-    const int32_t mu = __shfl(mu_l, j * 16 + (lane & 15), 64);
-    const int32_t F = __shfl(F_l, j * 16 + (lane & 15), 64);
-#pragma unroll
-    for (int i = 0; i < LN_FI; ++i) {
-      int32_t o[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int32_t d = (int8_t)(xw[i][j] >> (8 * r)) - mu;
-        o[r] = lnq[nch[i] + r].apply((d * F) >> 1);  // |d| <= sigma: |d * F| < 2^31
-      }
-      yw[i][j] = pack4(o[0], o[1], o[2], o[3]);
-    }
-  }
-  // both outputs through LDS token rows, out as 16-byte row chunks
+  // Both outputs leave through LDS token rows as 16-byte row chunks.  The
+  // residual stream x is staged with the row sums (sbuf is free: the K loop
+  // ends in a barrier); while the other waves copy it out, wave 0 turns the
+  // sums into the 64 tokens' statistics (one serial Newton chain per lane:
+  // computed once, not once per wave) and leaves them in LDS.
   uint32_t* so = (uint32_t*)sbuf;
-  auto stage_out = [&](const uint32_t(&wd)[LN_FI][LN_FJ], int8_t* dst) {
+  auto stage = [&](const uint32_t(&wd)[LN_FI][LN_FJ]) {
 #pragma unroll
     for (int i = 0; i < LN_FI; ++i)
 #pragma unroll
       for (int j = 0; j < LN_FJ; ++j) so[(j * 16 + (lane & 15)) * LN_OSTR + (nch[i] >> 2)] = wd[i][j];
-    lds_sync();
+  };
+  auto copy_out = [&](int8_t* dst) {
     const bool a16 = ((uintptr_t)dst & 15) == 0;
     for (int c = tid; c < LN_TM * (LN_N / 16); c += 64 * LN_NW) {
       const int r = c / (LN_N / 16), q = c - r * (LN_N / 16);
@@ -272,10 +246,42 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
       }
     }
   };
-  // (every wave is past its K-loop reads of sbuf: the loop ends in a barrier)
-  stage_out(xw, a.y);
+  stage(xw);
   lds_sync();
-  stage_out(yw, a.y2);
+  if (wave == 0) {
+    int32_t s = 0, ss = 0;
+#pragma unroll
+    for (int w = 0; w < LN_NW; ++w) {
+      s += lnred[w][lane][0];
+      ss += lnred[w][lane][1];
+    }
+    const int32_t mu = mean_half_up(s, LN_N);
+    const uint32_t V = (uint32_t)(ss - 2 * mu * s + LN_N * mu * mu);
+    const uint32_t sigma = newton_isqrt_f64(V, a.ln_iters);
+    lnst[lane][0] = mu;
+    lnst[lane][1] = sigma ? (int32_t)div_2p31m1(sigma) : 0;
+  }
+  copy_out(a.y);
+  lds_sync();  // statistics written; every read of the staged x done
+  uint32_t yw[LN_FI][LN_FJ];
+#pragma unroll
+  for (int j = 0; j < LN_FJ; ++j) {
+    const int32_t mu = lnst[j * 16 + (lane & 15)][0];
+    const int32_t F = lnst[j * 16 + (lane & 15)][1];
+#pragma unroll
+    for (int i = 0; i < LN_FI; ++i) {
+      int32_t o[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int32_t d = (int8_t)(xw[i][j] >> (8 * r)) - mu;
+        o[r] = lnq[nch[i] + r].apply((d * F) >> 1);  // |d| <= sigma: |d * F| < 2^31
+      }
+      yw[i][j] = pack4(o[0], o[1], o[2], o[3]);
+    }
+  }
+  stage(yw);
+  lds_sync();
+  copy_out(a.y2);
 }
 
 // Weight packing: one 16-byte chunk per thread over a list of matrices.
