@@ -564,7 +564,19 @@ hipError_t launch_lpr(const AttnArgs& a, int32_t clampL, int64_t emax, int64_t w
   // batch 1).
   if (wgs * 4 <= 2048) return launch_fit16<32, 32, 16>(a, clampL, emax, s);
   // (P V split by key blocks over the 4 waves: P read from LDS once)
-  if constexpr (R == 32) return launch_fit16<32, 32, 4, true>(a, clampL, emax, s);
+  if constexpr (R == 32) {
+    // Padded rows of more than 1408 and at most 1600 bytes with 32-bit lane
+    // sums: 16 lanes per row,
+    // 25 words each, so a wave normalizes 4 rows at a time and the per-row
+    // work (sum shuffles, shift calibration, reciprocal) is shared by twice
+    // the scores: 130 VGPRs, global attention of the 384-wide encoder 5%
+    // faster than 32 lanes of 13 words.  (With 64-bit lane sums the
+    // variant needs over 200 VGPRs.)
+    const int32_t words = a.Twp >> 2;
+    if (words > 22 * 16 && words <= 25 * 16 && emax * 4 * 25 < ((int64_t)1 << 32))
+      return launch_rows<32, 16, 4, 25, true>(a, clampL, emax, s);
+    return launch_fit16<32, 32, 4, true>(a, clampL, emax, s);
+  }
   return launch_rows<R, 64, 4>(a, clampL, emax, s);
 }
 

@@ -393,6 +393,8 @@ def test_attention(case, s_d):
     # (B, grid_h, grid_w, heads, head_dim): grids of 32-row blocks large enough
     # for the split-key P V phase (rows past 1024 keys, 4 waves)
     (4, 40, 40, 3, 64),     # 1600 keys, 25 key blocks over 4 waves (7, 6, 6, 6)
+    (4, 30, 50, 3, 64),     # 1500 keys: Shiftmax rows of 16 lanes, padded words
+    (4, 37, 41, 3, 64),     # 1517 keys: the same with a ragged last word
     (5, 45, 45, 2, 64),     # 2025 keys: a ragged last block, 2048 padded
     (6, 26, 40, 3, 64),     # 1040 keys: 17 blocks, just past the threshold
     (4, 40, 40, 3, 32),     # 32-channel heads: two of the four groups unused
