@@ -91,13 +91,16 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   constexpr bool BRANCH_FREE = LN && RSTAGED && TN >= 384;
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
   // KB K bytes per step (one or two MFMA K chunks): CPR 16-byte chunks per
-  // staged row, rows padded by 16 bytes (80 or 144: the 16 rows of a fragment
-  // read then fall on disjoint LDS banks)
-  constexpr int CPR = KB / 16, LROW = KB + 16;
+  // staged row, rows unpadded with their chunks swizzled (lds_chunk)
+  constexpr int CPR = KB / 16, LROW = KB;
   static_assert(KB == TK || KB == 2 * TK, "one or two MFMA K chunks per step");
   static_assert(!XP || KB == TK, "the image gather takes 64-byte steps");
-  __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LROW];
-  __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LROW];
+  // Operand double buffers (W tiles, then X tiles); after the K loop the same
+  // bytes hold the transposed output tile (TM rows of OSTR words).
+  constexpr int SOPS = 2 * (TN + TM) * LROW, SOUT = TM * OSTR * 4;
+  __shared__ __attribute__((aligned(16))) int8_t sbuf[SOPS > SOUT ? SOPS : SOUT];
+  auto sW = [&](int buf) { return sbuf + buf * (TN * LROW); };
+  auto sX = [&](int buf) { return sbuf + (2 * TN + buf * TM) * LROW; };
   __shared__ int8_t glut[EPI == EPI_GELU ? 256 : 1];
   __shared__ RqI64 rqc[TN];                         // output requantization per channel
   __shared__ int64_t qoff[EPI == EPI_QKV ? TM : 1][2];  // QKV: Q/K and V^T offsets per token
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // per-wave row sums of the LayerNorm epilogue: in the first weight tile,
   // free once the K loop's last barrier has passed
   static_assert(2 * WN * TM * 4 <= TN * LROW, "row sums fit one weight tile");
-  int32_t* const lnred = (int32_t*)&sW[0][0];
+  int32_t* const lnred = (int32_t*)sbuf;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -192,13 +195,13 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     for (int i = 0; i < PW; ++i) {
       const int c = tid + i * NT;
       if (CW % NT == 0 || c < CW)
-        *(v4i*)(&sW[buf][(c / CPR) * LROW + (c % CPR) * 16]) = rw[sl][i];
+        *(v4i*)(sW(buf) + lds_chunk<CPR>(c / CPR, c % CPR)) = rw[sl][i];
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
       const int c = tid + i * NT;
       if (CX % NT == 0 || c < CX)
-        *(v4i*)(&sX[buf][(c / CPR) * LROW + (c % CPR) * 16]) = rx[sl][i];
+        *(v4i*)(sX(buf) + lds_chunk<CPR>(c / CPR, c % CPR)) = rx[sl][i];
     }
   };
 
@@ -293,7 +296,11 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   for (int i = 0; i < FI; ++i)
 #pragma unroll
     for (int j = 0; j < FJ; ++j) acc[i][j] = zero;
-  const int frag_off = (lane & 15) * LROW + (lane >> 4) * 16;
+  // fragment rows start at multiples of 16, so a lane's swizzle depends on
+  // lane % 16 only: its chunk offsets for the KB / TK halves of a step
+  int frag_off[KB / TK];
+#pragma unroll
+  for (int h = 0; h < KB / TK; ++h) frag_off[h] = lds_chunk<CPR>(lane & 15, h * 4 + (lane >> 4));
   // compute(buf, kt): the MFMAs of K step kt; with a K tail, 64-byte halves
   // of the last step that lie wholly past K are skipped (their chunks are
   // zero-filled anyway)
@@ -304,10 +311,10 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       v4i fa[FI], fb[FJ];
 #pragma unroll
       for (int i = 0; i < FI; ++i)
-        fa[i] = *(const v4i*)(&sW[buf][(wn * WTN + i * 16) * LROW + h * TK + frag_off]);
+        fa[i] = *(const v4i*)(sW(buf) + (wn * WTN + i * 16) * LROW + frag_off[h]);
 #pragma unroll
       for (int j = 0; j < FJ; ++j)
-        fb[j] = *(const v4i*)(&sX[buf][(wm * WTM + j * 16) * LROW + h * TK + frag_off]);
+        fb[j] = *(const v4i*)(sX(buf) + (wm * WTM + j * 16) * LROW + frag_off[h]);
 #pragma unroll
       for (int i = 0; i < FI; ++i)
 #pragma unroll
@@ -398,7 +405,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
               EPI == EPI_GELU
                   ? pack4(glut[u[0] + 128], glut[u[1] + 128], glut[u[2] + 128], glut[u[3] + 128])
                   : pack4(u[0], u[1], u[2], u[3]);
-          ((uint32_t*)&sW[0][0])[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((n - n0) >> 2)] = word;
+          ((uint32_t*)sbuf)[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((n - n0) >> 2)] = word;
         } else if (EPI == EPI_STORE) {
           *(uint32_t*)(a.y + tok[j] + n) = pack4(u[0], u[1], u[2], u[3]);
         } else if (EPI == EPI_GELU) {
@@ -446,7 +453,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // rows (the weight tiles, free after the K loop; LayerNorm's row sums are
   // past their last read at the first barrier).
   auto stage_words = [&](const uint32_t(&wd)[FI][FJ]) {
-    uint32_t* so = (uint32_t*)&sW[0][0];
+    uint32_t* so = (uint32_t*)sbuf;
     lds_sync();
 #pragma unroll
     for (int i = 0; i < FI; ++i)
@@ -458,7 +465,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // The staged tile out to dst (row stride N) in 16-byte row chunks.
   constexpr int CPT = TN / 16;  // 16-byte chunks per token row
   auto copy_rows = [&](int8_t* dst) {
-    const uint32_t* so = (const uint32_t*)&sW[0][0];
+    const uint32_t* so = (const uint32_t*)sbuf;
     const bool a16 = ((uintptr_t)dst & 15) == 0;
     for (int c = tid; c < TM * CPT; c += NT) {
       const int r = c / CPT, q = c - r * CPT;
@@ -467,8 +474,6 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
       if (m < M && n < N) store16(dst + m * N + n, *(const v4i*)(so + r * OSTR + q * 4), a16);
     }
   };
-  static_assert(!(STAGED || RSTAGED || QSTAGED) || TM * OSTR * 4 <= 2 * TN * LROW,
-                "the output tile fits the weight tiles");
   if constexpr (STAGED) {  // the words went to LDS in the loop above
     lds_sync();
     copy_rows(a.y);
@@ -481,7 +486,7 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
     // Q and K chunks to their window-major rows (16-byte aligned: the rows
     // are 64 bytes, the workspace 16-byte aligned)
     stage_words(xw);
-    const uint32_t* so = (const uint32_t*)&sW[0][0];
+    const uint32_t* so = (const uint32_t*)sbuf;
     const QkvLayout& Lq = a.qkv;
     for (int c = tid; c < TM * CPT; c += NT) {
       const int r = c / CPT, q = c - r * CPT;

@@ -82,6 +82,21 @@ __device__ __forceinline__ int32_t sd_gelu(int32_t x, int32_t I0, int32_t k_inte
   return x * (int32_t)(((uint64_t)f * (z >= 0 ? one : t)) >> (32 - k_out));
 }
 
+// Operand tiles in LDS: rows of CPR 16-byte chunks (64 or 128 bytes), not
+// padded; chunk c of row r sits at chunk position c ^ s(r), s(r) = 2 (r & 4)
+// / 4 for 4 chunks per row and r & 6 for 8.  MFMA fragment reads (lane L:
+// row L % 16, chunk L / 16) then hit every LDS bank once per 16-lane group,
+// and so do the staging stores of whole rows.  Measured on MI355X with
+// ds_read_b128: fragment reads at a padded row stride of 80 or 144 bytes take
+// 8.8 cycles per wave instruction and CU, swizzled 5.4; 16-byte-chunk row
+// stores 16.3 (80-byte stride) against 13.6.
+template <int CPR>
+__device__ __forceinline__ int lds_chunk(int r, int c) {
+  static_assert(CPR == 4 || CPR == 8, "64- or 128-byte rows");
+  const int sw = CPR == 4 ? (r & 4) >> 1 : (r & 6);
+  return r * (CPR * 16) + ((c ^ sw) << 4);
+}
+
 // Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
 // operations (lgkmcnt(0)), then s_barrier.  Unlike __syncthreads() it does
 // not wait for outstanding global loads (vmcnt), so loads issued for later K

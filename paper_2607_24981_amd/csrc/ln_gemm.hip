@@ -36,7 +36,7 @@ namespace ilw {
 namespace {
 
 constexpr int LN_N = 384, LN_TM = 64, LN_FJ = 4;
-constexpr int LN_KB = 128, LN_LROW = LN_KB + 16;  // 144-byte rows: conflict-free fragments
+constexpr int LN_KB = 128, LN_LROW = LN_KB;  // 128-byte rows, chunks swizzled (lds_chunk)
 constexpr int LN_OSTR = LN_N / 4 + 4;  // output staging: 100 words per token row (odd x 4)
 constexpr int LN_XBUF = 3;  // activation tile buffers (the ring's length at most)
 constexpr int LN_SBUF = LN_XBUF * LN_TM * LN_LROW > LN_TM * LN_OSTR * 4
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   // operands: this thread's 16-byte chunk of the activation tile (row tid / 8)
   // and this wave's weight fragments
   const int8_t* xsrc = a.x + min(m0 + tid / 8, M - 1) * K + (tid % 8) * 16;
-  const int xo = (tid / 8) * LN_LROW + (tid % 8) * 16;
+  const int xo = lds_chunk<LN_KB / 16>(tid / 8, tid % 8);
   static_assert(64 * LN_NW >= LN_TM * LN_KB / 16, "one activation chunk per thread at most");
   const bool xown = tid < LN_TM * LN_KB / 16;  // threads that stage an activation chunk
   // this wave's fragments: K chunk k64, fragment i at (k64 LN_FI + i) KB
@@ -109,13 +109,15 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   for (int i = 0; i < LN_FI; ++i)
 #pragma unroll
     for (int j = 0; j < LN_FJ; ++j) acc[i][j] = zero;
-  const int fo = (lane & 15) * LN_LROW + (lane >> 4) * 16;
+  // fragment rows start at multiples of 16: the swizzle depends on lane % 16
+  const int fo[2] = {lds_chunk<LN_KB / 16>(lane & 15, lane >> 4),
+                     lds_chunk<LN_KB / 16>(lane & 15, 4 + (lane >> 4))};
   auto compute = [&](const int8_t* sx, const v4i(&wf)[2][LN_FI]) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       v4i fb[LN_FJ];
 #pragma unroll
-      for (int j = 0; j < LN_FJ; ++j) fb[j] = *(const v4i*)(sx + j * 16 * LN_LROW + fo + h * 64);
+      for (int j = 0; j < LN_FJ; ++j) fb[j] = *(const v4i*)(sx + j * 16 * LN_LROW + fo[h]);
 #pragma unroll
       for (int i = 0; i < LN_FI; ++i)
 #pragma unroll
