@@ -85,10 +85,12 @@ __global__ __launch_bounds__(64 * WN * WM) void gemm_i8_kernel(GemmArgs a, int32
   // QKV: the Q and K words likewise (a 16-channel chunk of a token lies in
   // one head's 64-byte window-major row); V^T keeps its byte scatter
   constexpr bool QSTAGED = !LAT && EPI == EPI_QKV;
-  // The 384-channel LayerNorm tile holds one workgroup per CU: tiles inside
-  // M x N take an epilogue without per-lane validity tests there (elsewhere
-  // the extra registers would cost workgroups per CU).
-  constexpr bool BRANCH_FREE = LN && RSTAGED && TN >= 384;
+  // Tiles inside M x N take an epilogue without per-lane validity tests in
+  // the 384-channel LayerNorm tile (one workgroup per CU) and in the staged
+  // store and GELU tiles (the staged words of rows or channels past the
+  // edges are never copied out; same registers there, fc1 3% faster).
+  // Elsewhere the extra registers would cost workgroups per CU.
+  constexpr bool BRANCH_FREE = (LN && RSTAGED && TN >= 384) || STAGED;
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
   // KB K bytes per step (one or two MFMA K chunks): CPR 16-byte chunks per
   // staged row, rows unpadded with their chunks swizzled (lds_chunk)
