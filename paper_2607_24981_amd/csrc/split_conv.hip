@@ -21,7 +21,7 @@
 namespace ilw {
 namespace {
 
-constexpr int TK = 64, LDS_ROW = 80, NXCD = 8;
+constexpr int TK = 64, LDS_ROW = 64, NXCD = 8;  // 64-byte rows, chunks swizzled (lds_chunk)
 
 // 16 bytes to dst, which the entry points require to be 4-byte aligned: one
 // 16-byte store when the output base is 16-byte aligned (a16), else four
@@ -49,9 +49,12 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
   constexpr int TN = WTN * WN, TM = WTM * WM, NT = 64 * WN * WM;
   // output staging: OSTR words per token row, an odd multiple of 4
   constexpr int OSTR = (TN / 4) % 8 == 0 ? TN / 4 + 4 : TN / 4;
-  static_assert(TM * OSTR * 4 <= 2 * TN * LDS_ROW, "the output tile fits the weight tiles");
-  __shared__ __attribute__((aligned(16))) int8_t sW[2][TN * LDS_ROW];
-  __shared__ __attribute__((aligned(16))) int8_t sX[2][TM * LDS_ROW];
+  // operand double buffers (W tiles, then X tiles); after the K loop the
+  // same bytes hold the transposed output tile
+  constexpr int SOPS = 2 * (TN + TM) * LDS_ROW, SOUT = TM * OSTR * 4;
+  __shared__ __attribute__((aligned(16))) int8_t sbuf[SOPS > SOUT ? SOPS : SOUT];
+  auto sW = [&](int buf) { return sbuf + buf * (TN * LDS_ROW); };
+  auto sX = [&](int buf) { return sbuf + (2 * TN + buf * TM) * LDS_ROW; };
   __shared__ BrChan brc[kMaxBranches][TN];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -125,13 +128,13 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
     for (int i = 0; i < PW; ++i) {
       const int c = tid + i * NT;
       if (CW % NT == 0 || c < CW)
-        *(v4i*)(&sW[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rw[sl][i];
+        *(v4i*)(sW(buf) + lds_chunk<4>(c >> 2, c & 3)) = rw[sl][i];
     }
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
       const int c = tid + i * NT;
       if (CX % NT == 0 || c < CX)
-        *(v4i*)(&sX[buf][(c >> 2) * LDS_ROW + (c & 3) * 16]) = rx[sl][i];
+        *(v4i*)(sX(buf) + lds_chunk<4>(c >> 2, c & 3)) = rx[sl][i];
     }
   };
 
@@ -156,15 +159,15 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
 #pragma unroll
       for (int r = 0; r < 4; ++r) tot[i][j][r] = 0;
     }
-  const int frag_off = (lane & 15) * LDS_ROW + (lane >> 4) * 16;
+  const int frag_off = lds_chunk<4>(lane & 15, lane >> 4);  // rows start at multiples of 16
   auto compute = [&](int buf) {
     v4i fa[FI], fb[FJ];
 #pragma unroll
     for (int i = 0; i < FI; ++i)
-      fa[i] = *(const v4i*)(&sW[buf][(wn * WTN + i * 16) * LDS_ROW + frag_off]);
+      fa[i] = *(const v4i*)(sW(buf) + (wn * WTN + i * 16) * LDS_ROW + frag_off);
 #pragma unroll
     for (int j = 0; j < FJ; ++j)
-      fb[j] = *(const v4i*)(&sX[buf][(wm * WTM + j * 16) * LDS_ROW + frag_off]);
+      fb[j] = *(const v4i*)(sX(buf) + (wm * WTM + j * 16) * LDS_ROW + frag_off);
 #pragma unroll
     for (int i = 0; i < FI; ++i)
 #pragma unroll
@@ -238,7 +241,7 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
         t = t < -(int64_t)cr[r].L ? -(int64_t)cr[r].L : (t > cr[r].L ? cr[r].L : t);
         v[r] = cr[r].apply((int32_t)t);
       }
-      ((uint32_t*)&sW[0][0])[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((n - n0) >> 2)] =
+      ((uint32_t*)sbuf)[(wm * WTM + j * 16 + (lane & 15)) * OSTR + ((n - n0) >> 2)] =
           pack4(v[0], v[1], v[2], v[3]);
     }
   }
@@ -247,7 +250,7 @@ __global__ __launch_bounds__(64 * WN * WM) void split_conv_kernel(SplitArgs a, i
   // 16 rows of 4 bytes each into every store instruction.
   __syncthreads();
   {
-    const uint32_t* so = (const uint32_t*)&sW[0][0];
+    const uint32_t* so = (const uint32_t*)sbuf;
     const bool a16 = ((uintptr_t)a.y & 15) == 0;
     constexpr int CPT = TN / 16;
     for (int c = tid; c < TM * CPT; c += NT) {
