@@ -289,27 +289,28 @@ struct BlockLayout {
 bool ln_fusable(int32_t D);
 
 // Which of the block's residual linears take the packed-weight kernel: the
-// projection (its LayerNorm is LN2) and fc2 when a next block's LN1 follows.
+// projection (its LayerNorm is LN2) and fc2 (with the next block's LN1, or
+// without a LayerNorm after the last block).
 bool packs_proj(const ilw_block_params* p, int64_t M) {
   return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->dim);
 }
-bool packs_fc2(const ilw_block_params* p, bool has_next, int64_t M) {
-  return has_next && ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim);
+bool packs_fc2(const ilw_block_params* p, int64_t M) {
+  return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim);
 }
-size_t packed_bytes(const ilw_block_params* p, bool has_next, int64_t M) {
+size_t packed_bytes(const ilw_block_params* p, int64_t M) {
   return (packs_proj(p, M) ? align256(packed_frag_bytes(p->dim, p->dim)) : 0) +
-         (packs_fc2(p, has_next, M) ? align256(packed_frag_bytes(p->dim, p->mlp_dim)) : 0);
+         (packs_fc2(p, M) ? align256(packed_frag_bytes(p->dim, p->mlp_dim)) : 0);
 }
 // Carves the packed weights of a block from base + off; returns the bytes used.
-size_t packed_layout(const ilw_block_params* p, bool has_next, int64_t M, int8_t* base,
-                     size_t off, BlockLayout* L) {
+size_t packed_layout(const ilw_block_params* p, int64_t M, int8_t* base, size_t off,
+                     BlockLayout* L) {
   size_t used = 0;
   L->wp_proj = L->wp_fc2 = nullptr;
   if (packs_proj(p, M)) {
     L->wp_proj = carve(base, off);
     used += align256(packed_frag_bytes(p->dim, p->dim));
   }
-  if (packs_fc2(p, has_next, M)) {
+  if (packs_fc2(p, M)) {
     L->wp_fc2 = carve(base, off + used);
     used += align256(packed_frag_bytes(p->dim, p->mlp_dim));
   }
@@ -368,7 +369,7 @@ size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
   off += align256(M * p->mlp_dim);
   // a single block has no next block: its fc2 takes the plain residual tile
   L.wp_proj = L.wp_fc2 = nullptr;
-  if (with_packed) off += packed_layout(p, false, (int64_t)M, base, off, &L);
+  if (with_packed) off += packed_layout(p, (int64_t)M, base, off, &L);
   L.total = off;
   if (out) *out = L;
   return off;
@@ -582,7 +583,7 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
   if (he != hipSuccess) return hip_status(he, "block fc1");
   // y = Res(fc2(g), x1);  h = LN1'(y) of the next block
   a = gemm_args(L.g, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
-  a.wp = next && fuse ? L.wp_fc2 : nullptr;
+  a.wp = L.wp_fc2;  // set only where packs_fc2 holds
   a.resid = L.x1;
   a.res_ma = p->res2_mult_a;
   a.res_mb = p->res2_mult_b;
@@ -641,7 +642,7 @@ size_t encoder_workspace(const ilw_block_params* blocks, int32_t n_blocks,
     check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
     const size_t n = block_layout(&blocks[b], batch, g, nullptr, nullptr, q, false);
     need = n > need ? n : need;
-    packed += packed_bytes(&blocks[b], b + 1 < n_blocks, (int64_t)batch * g.T);
+    packed += packed_bytes(&blocks[b], (int64_t)batch * g.T);
   }
   // every block's packed weights after the shared per-block region
   return need + packed;
@@ -1055,8 +1056,7 @@ int ilw_encoder_forward(const ilw_block_params* blocks, int32_t n_blocks,
       Geometry g;
       check_geometry(batch, grid_h, grid_w, windows[2 * b], windows[2 * b + 1], &g);
       block_layout(&blocks[b], batch, g, (int8_t*)workspace, &Ls[b], qres, false);
-      off += packed_layout(&blocks[b], b + 1 < n_blocks, (int64_t)batch * g.T,
-                           (int8_t*)workspace, off, &Ls[b]);
+      off += packed_layout(&blocks[b], (int64_t)batch * g.T, (int8_t*)workspace, off, &Ls[b]);
       ps[b] = &blocks[b];
     }
     const hipError_t he = pack_block_weights(ps.data(), Ls.data(), n_blocks, s);

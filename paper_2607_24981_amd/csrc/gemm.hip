@@ -673,7 +673,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     if (a.N == 384) {
       // weights packed in fragment order: the register-operand kernel
       if (!lat && a.wp && ln384_packed_kernel_applies(a.M, a.N, a.K))
-        return launch_ln384_packed(a, s);
+        return launch_ln384_packed(a, true, s);
       if (lat)  // 384 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 4, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 4, 1, 3>(a, s);
@@ -686,6 +686,10 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     }
     return hipErrorInvalidValue;
   }
+  // The 384-channel residual linear with packed weights (the last block's
+  // fc2): the LayerNorm kernel without its LayerNorm.
+  if (epi == EPI_RESID && a.wp && ln384_packed_kernel_applies(a.M, a.N, a.K))
+    return launch_ln384_packed(a, false, s);
   // Small grids: 64 x 64 workgroup tiles split over 4 waves of 32 x 32, with
   // the latency-mode pipeline.  Otherwise, from a sweep over the encoder
   // shapes on MI355X: 192-channel tiles for the deep-K linears and N = 192,

@@ -395,11 +395,11 @@ struct PackList {
 };
 size_t packed_frag_bytes(int32_t N, int32_t K);
 hipError_t launch_pack_frags(const PackList& L, hipStream_t s);
-// True where launch_gemm(EPI_RESID_LN) takes the packed-weight kernel when
-// GemmArgs::wp is set (N = 384, K a multiple of 128, a grid past the latency
-// mode).
+// True where launch_gemm(EPI_RESID_LN or EPI_RESID) takes the packed-weight
+// kernel when GemmArgs::wp is set (N = 384, K a multiple of 128, a grid past
+// the latency mode).
 bool ln384_packed_kernel_applies(int64_t M, int32_t N, int32_t K);
-hipError_t launch_ln384_packed(const GemmArgs& a, hipStream_t s);
+hipError_t launch_ln384_packed(const GemmArgs& a, bool layernorm, hipStream_t s);
 bool gemm_latency_mode(int64_t M, int32_t N);
 
 // The rest of an encoder block after attention, for one 16-token slab per

@@ -48,8 +48,9 @@ constexpr int kPackGroup = LN_N / 16 / LN_WAVES;  // fragments per wave, packed 
 
 // LN_NW waves of LN_FI 16-channel fragments each (LN_NW * LN_FI = 24); RING
 // weight register sets (2: one K step ahead, any step count; 3: two steps
-// ahead, step count a multiple of 3)
-template <bool WIDE_RES, int LN_NW, int RING>
+// ahead, step count a multiple of 3); DO_LN false: the residual output only
+// (the last block's fc2, which no LayerNorm follows)
+template <bool WIDE_RES, int LN_NW, int RING, bool DO_LN>
 __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_t tiles) {
   constexpr int LN_FI = LN_N / 16 / LN_NW;
   static_assert(LN_FI * LN_NW * 16 == LN_N, "whole fragments per wave");
@@ -98,9 +99,11 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
     RqI64 r;
     r.init(a.mult[a.nq == 1 ? 0 : c], a.shift[a.nq == 1 ? 0 : c], a.bias ? a.bias[c] : 0);
     rqc[c] = r;
-    const int q = a.ln_nq == 1 ? 0 : c;
-    r.init(a.ln_mult[q], a.ln_shift[q], a.ln_beta[c]);
-    lnq[c] = r;
+    if (DO_LN) {
+      const int q = a.ln_nq == 1 ? 0 : c;
+      r.init(a.ln_mult[q], a.ln_shift[q], a.ln_beta[c]);
+      lnq[c] = r;
+    }
   }
 
   v4i acc[LN_FI][LN_FJ];
@@ -200,7 +203,7 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   // row sums: in the lane (byte dot products), across the 4 lanes of a token
   // (shuffles), across the waves (LDS)
 #pragma unroll
-  for (int j = 0; j < LN_FJ; ++j) {
+  for (int j = 0; j < (DO_LN ? LN_FJ : 0); ++j) {
     int32_t S = 0, SS = 0;
 #pragma unroll
     for (int i = 0; i < LN_FI; ++i) {
@@ -250,6 +253,10 @@ __global__ __launch_bounds__(64 * LN_NW) void ln384_wp_kernel(GemmArgs a, int64_
   };
   stage(xw);
   lds_sync();
+  if (!DO_LN) {
+    copy_out(a.y);
+    return;
+  }
   if (wave == 0) {
     int32_t s = 0, ss = 0;
 #pragma unroll
@@ -321,21 +328,25 @@ hipError_t launch_pack_frags(const PackList& L, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int NW, int RING>
+template <int NW, int RING, bool DO_LN>
 hipError_t launch_ln384_nw(const GemmArgs& a, int64_t tiles, hipStream_t s) {
   if (a.res_shift < 9)
-    hipLaunchKernelGGL((ln384_wp_kernel<true, NW, RING>), dim3((unsigned)tiles), dim3(64 * NW), 0,
-                       s, a, tiles);
+    hipLaunchKernelGGL((ln384_wp_kernel<true, NW, RING, DO_LN>), dim3((unsigned)tiles),
+                       dim3(64 * NW), 0, s, a, tiles);
   else
-    hipLaunchKernelGGL((ln384_wp_kernel<false, NW, RING>), dim3((unsigned)tiles), dim3(64 * NW),
-                       0, s, a, tiles);
+    hipLaunchKernelGGL((ln384_wp_kernel<false, NW, RING, DO_LN>), dim3((unsigned)tiles),
+                       dim3(64 * NW), 0, s, a, tiles);
   return hipGetLastError();
 }
 
-hipError_t launch_ln384_packed(const GemmArgs& a, hipStream_t s) {
+hipError_t launch_ln384_packed(const GemmArgs& a, bool layernorm, hipStream_t s) {
   const int64_t tiles = (a.M + LN_TM - 1) / LN_TM;
-  if ((a.K / LN_KB) % 3 == 0) return launch_ln384_nw<LN_WAVES, 3>(a, tiles, s);
-  return launch_ln384_nw<LN_WAVES, 2>(a, tiles, s);
+  const bool ring3 = (a.K / LN_KB) % 3 == 0;
+  if (layernorm)
+    return ring3 ? launch_ln384_nw<LN_WAVES, 3, true>(a, tiles, s)
+                 : launch_ln384_nw<LN_WAVES, 2, true>(a, tiles, s);
+  return ring3 ? launch_ln384_nw<LN_WAVES, 3, false>(a, tiles, s)
+               : launch_ln384_nw<LN_WAVES, 2, false>(a, tiles, s);
 }
 
 }  // namespace ilw
