@@ -282,7 +282,7 @@ struct BlockLayout {
   int8_t *h, *att, *x1, *g;
   // proj and fc2 weights packed in MFMA fragment order for the 384-channel
   // LayerNorm-fused kernel, or null where that kernel does not run
-  int8_t *wp_proj, *wp_fc2;
+  int8_t *wp_proj, *wp_fc2, *wp_fc1;
   size_t total;
 };
 
@@ -297,15 +297,25 @@ bool packs_proj(const ilw_block_params* p, int64_t M) {
 bool packs_fc2(const ilw_block_params* p, int64_t M) {
   return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim);
 }
+// fc1 too where the whole MLP runs as one kernel (ILW_FUSE_MLP=0 turns that
+// off, read once)
+bool packs_fc1(const ilw_block_params* p, int64_t M) {
+  static const bool on = [] {  // thread-safe static initialisation
+    const char* e = getenv("ILW_FUSE_MLP");
+    return !(e && e[0] == '0');
+  }();
+  return on && packs_fc2(p, M) && mlp384_kernel_applies(M, p->dim, p->mlp_dim);
+}
 size_t packed_bytes(const ilw_block_params* p, int64_t M) {
   return (packs_proj(p, M) ? align256(packed_frag_bytes(p->dim, p->dim)) : 0) +
-         (packs_fc2(p, M) ? align256(packed_frag_bytes(p->dim, p->mlp_dim)) : 0);
+         (packs_fc2(p, M) ? align256(packed_frag_bytes(p->dim, p->mlp_dim)) : 0) +
+         (packs_fc1(p, M) ? align256(packed_frag_bytes(p->mlp_dim, p->dim)) : 0);
 }
 // Carves the packed weights of a block from base + off; returns the bytes used.
 size_t packed_layout(const ilw_block_params* p, int64_t M, int8_t* base, size_t off,
                      BlockLayout* L) {
   size_t used = 0;
-  L->wp_proj = L->wp_fc2 = nullptr;
+  L->wp_proj = L->wp_fc2 = L->wp_fc1 = nullptr;
   if (packs_proj(p, M)) {
     L->wp_proj = carve(base, off);
     used += align256(packed_frag_bytes(p->dim, p->dim));
@@ -313,6 +323,10 @@ size_t packed_layout(const ilw_block_params* p, int64_t M, int8_t* base, size_t 
   if (packs_fc2(p, M)) {
     L->wp_fc2 = carve(base, off + used);
     used += align256(packed_frag_bytes(p->dim, p->mlp_dim));
+  }
+  if (packs_fc1(p, M)) {
+    L->wp_fc1 = carve(base, off + used);
+    used += align256(packed_frag_bytes(p->mlp_dim, p->dim));
   }
   return used;
 }
@@ -343,6 +357,8 @@ hipError_t pack_block_weights(const ilw_block_params* const* ps, const BlockLayo
     if (Ls[b].wp_proj) e = add(ps[b]->w_proj, Ls[b].wp_proj, ps[b]->dim, ps[b]->dim);
     if (e == hipSuccess && Ls[b].wp_fc2)
       e = add(ps[b]->w_fc2, Ls[b].wp_fc2, ps[b]->dim, ps[b]->mlp_dim);
+    if (e == hipSuccess && Ls[b].wp_fc1)
+      e = add(ps[b]->w_fc1, Ls[b].wp_fc1, ps[b]->mlp_dim, ps[b]->dim);
     if (e != hipSuccess) return e;
   }
   return flush();
@@ -368,7 +384,7 @@ size_t block_layout(const ilw_block_params* p, int32_t batch, const Geometry& g,
   L.g = carve(base, off);
   off += align256(M * p->mlp_dim);
   // a single block has no next block: its fc2 takes the plain residual tile
-  L.wp_proj = L.wp_fc2 = nullptr;
+  L.wp_proj = L.wp_fc2 = L.wp_fc1 = nullptr;
   if (with_packed) off += packed_layout(p, (int64_t)M, base, off, &L);
   L.total = off;
   if (out) *out = L;
@@ -569,6 +585,32 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
     if (he != hipSuccess) return hip_status(he, "block LN2");
   }
   // g = rq(SD-ShiftGELU(fc1(h)))
+  GemmArgs f1 = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
+  f1.g_I0 = p->gelu_I0;
+  f1.g_kinter = p->gelu_k_inter;
+  f1.g_kout = p->gelu_k_out;
+  f1.g_mult = p->gelu_mult;
+  f1.g_shift = p->gelu_shift;
+  if (L.wp_fc1 && L.wp_fc2) {
+    // the whole MLP in one launch: g stays in LDS
+    f1.wp = L.wp_fc1;
+    GemmArgs f2 = gemm_args(nullptr, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
+    f2.wp = L.wp_fc2;
+    f2.resid = L.x1;
+    f2.res_ma = p->res2_mult_a;
+    f2.res_mb = p->res2_mult_b;
+    f2.res_shift = p->res2_shift;
+    const bool ln = next && fuse;
+    if (ln) f2 = with_ln(f2, next->ln1_beta, next->ln1_out, next->ln_iters, L.h);
+    {
+      StageTimer t(ILW_STAGE_MLP, s);
+      he = launch_mlp384(f1, f2, ln, s);
+      t.done();
+    }
+    if (he != hipSuccess) return hip_status(he, "block MLP");
+    *ready_out = ln ? READY_H : READY_NONE;
+    return ok();
+  }
   a = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
   a.g_I0 = p->gelu_I0;
   a.g_kinter = p->gelu_k_inter;

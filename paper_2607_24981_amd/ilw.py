@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 # ILW_LIBRARY_PATH loads another build of the same sources instead (the
 # sanitizer run of the CPU test-suite uses a host-instrumented one).
 LIB_PATH = os.environ.get("ILW_LIBRARY_PATH") or os.path.join(_HERE, "libilw.so")
-ABI_VERSION = 8
+ABI_VERSION = 9
 
 c_i32, c_i64, c_vp, c_size = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
 
@@ -577,7 +577,7 @@ def ilw_deform_attn_boxes(value, level_hw, level_start, ref, offsets, logits, I0
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
-          "relayout", "deform", "block_tail", "split_conv", "patch_embed", "decoder"]
+          "relayout", "deform", "block_tail", "split_conv", "patch_embed", "decoder", "mlp"]
 
 
 def profile_enable(on: bool = True):

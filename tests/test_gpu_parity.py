@@ -810,14 +810,17 @@ def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
     assert_same(host(enc.forward(dev(x))), ref, "encoder residual shift forms")
 
 
-@pytest.mark.parametrize("variant,mlp", [("baseline", 1536), ("wide", 1536), ("baseline", 1024)])
+@pytest.mark.parametrize("variant,mlp", [("baseline", 1536), ("wide", 1536), ("baseline", 1024),
+                                         ("baseline", 768), ("wide", 1152)])
 def test_encoder_384_packed_ragged(variant, mlp):
     """The 384-channel LayerNorm-fused linears on their packed-weight kernel
     (grids past the latency mode: 7 images of 41 x 41 tokens, 11 767 tokens,
     the last 64-token tile 55 rows full): three images of a two-block encoder
-    against the oracle, run on host threads while the GPU works.  MLP 1536
-    gives fc2 12 K steps (the three-set weight ring), 1024 gives 8 (two
-    sets)."""
+    against the oracle, run on host threads while the GPU works.  MLP 1536,
+    1152 and 768 run the whole MLP as one kernel (4, 3 and 2 chunks of 384
+    fc1 channels; the first block with the next LayerNorm, the second
+    without); MLP 1024 runs fc1 and fc2 apart, fc2 with 8 K steps (the
+    two-set weight ring)."""
     import concurrent.futures as cf
     D, H, B, grid, windows = 384, 6, 7, (41, 41), [(0, 0), (0, 0)]
     say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}, MLP {mlp}")
