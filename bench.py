@@ -59,8 +59,8 @@ def stage_work(wl, B, launches):
         "gemm_proj": ("ops", n("gemm_proj") * proj),
         "gemm_fc1": ("ops", n("gemm_fc1") * mlp),
         "gemm_fc2": ("ops", n("gemm_fc2") * mlp),
-        # fc1 and fc2 in one launch
-        "mlp": ("ops", n("mlp") * 2 * mlp),
+        # projection, fc1 and fc2 in one launch
+        "tail384": ("ops", n("tail384") * (proj + 2 * mlp)),
         # projection, fc1, fc2, and the QKV linear of the next block
         "block_tail": ("ops", n("block_tail") * (proj + 2 * mlp) + (nb - n("gemm_qkv")) * qkv
                        if n("block_tail") else 0),
@@ -76,7 +76,7 @@ KERNEL_OF_STAGE = {
     "gemm_proj": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
     "gemm_fc1": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
     "gemm_fc2": ("gemm_i8_kernel", ["paper_2607_24981_amd/csrc/gemm.hip", _INTERNAL]),
-    "mlp": ("mlp384_kernel", ["paper_2607_24981_amd/csrc/mlp.hip", _INTERNAL]),
+    "tail384": ("tail384_kernel", ["paper_2607_24981_amd/csrc/tail384.hip", _INTERNAL]),
     "block_tail": ("block_tail_kernel", ["paper_2607_24981_amd/csrc/block_tail.hip", _INTERNAL]),
     "layernorm": ("layernorm_rows_kernel", ["paper_2607_24981_amd/csrc/rowops.hip", _INTERNAL]),
     "split_conv": ("split_conv_kernel", ["paper_2607_24981_amd/csrc/split_conv.hip", _INTERNAL]),

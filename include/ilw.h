@@ -438,8 +438,8 @@ typedef enum {
   ILW_STAGE_SPLIT_CONV = 9,  /* scale-preserving split convolution          */
   ILW_STAGE_PATCH_EMBED = 10, /* patch embedding + positional embedding     */
   ILW_STAGE_DECODER = 11,    /* decoder linears, LayerNorms, offset widening */
-  ILW_STAGE_MLP = 12,        /* fc1 + SD-ShiftGELU + fc2 + residual (+ next
-                                LN1) in one launch (dim 384)                */
+  ILW_STAGE_TAIL384 = 12,    /* projection ... fc2 + residual (+ next LN1),
+                                one launch (dim 384)                        */
   ILW_NUM_STAGES = 13
 } ilw_stage;
 

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 SO = os.path.join(HERE, "libilw.so")
-SOURCES = ["api.hip", "gemm.hip", "ln_gemm.hip", "mlp.hip", "attention.hip", "rowops.hip",
+SOURCES = ["api.hip", "gemm.hip", "ln_gemm.hip", "tail384.hip", "attention.hip", "rowops.hip",
            "deform.hip", "block_tail.hip", "split_conv.hip"]
 ARCH = "gfx950"
 

@@ -297,14 +297,15 @@ bool packs_proj(const ilw_block_params* p, int64_t M) {
 bool packs_fc2(const ilw_block_params* p, int64_t M) {
   return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim);
 }
-// fc1 too where the whole MLP runs as one kernel (ILW_FUSE_MLP=0 turns that
-// off, read once)
+// fc1 too where everything after attention runs as one kernel
+// (ILW_FUSE_TAIL=0 turns that off, read once)
 bool packs_fc1(const ilw_block_params* p, int64_t M) {
   static const bool on = [] {  // thread-safe static initialisation
-    const char* e = getenv("ILW_FUSE_MLP");
+    const char* e = getenv("ILW_FUSE_TAIL");
     return !(e && e[0] == '0');
   }();
-  return on && packs_fc2(p, M) && mlp384_kernel_applies(M, p->dim, p->mlp_dim);
+  return on && packs_proj(p, M) && packs_fc2(p, M) &&
+         tail384_kernel_applies(M, p->dim, p->mlp_dim);
 }
 size_t packed_bytes(const ilw_block_params* p, int64_t M) {
   return (packs_proj(p, M) ? align256(packed_frag_bytes(p->dim, p->dim)) : 0) +
@@ -563,6 +564,38 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
     return ok();
   }
 
+  if (L.wp_fc1) {
+    // everything after attention in one launch: x1, h and g stay on chip
+    GemmArgs fp = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
+    fp.wp = L.wp_proj;
+    fp.resid = x;
+    fp.res_ma = p->res1_mult_a;
+    fp.res_mb = p->res1_mult_b;
+    fp.res_shift = p->res1_shift;
+    fp = with_ln(fp, p->ln2_beta, p->ln2_out, p->ln_iters, L.h);
+    GemmArgs f1 = gemm_args(nullptr, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
+    f1.wp = L.wp_fc1;
+    f1.g_I0 = p->gelu_I0;
+    f1.g_kinter = p->gelu_k_inter;
+    f1.g_kout = p->gelu_k_out;
+    f1.g_mult = p->gelu_mult;
+    f1.g_shift = p->gelu_shift;
+    GemmArgs f2 = gemm_args(nullptr, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
+    f2.wp = L.wp_fc2;
+    f2.res_ma = p->res2_mult_a;
+    f2.res_mb = p->res2_mult_b;
+    f2.res_shift = p->res2_shift;
+    const bool ln = next && fuse;
+    if (ln) f2 = with_ln(f2, next->ln1_beta, next->ln1_out, next->ln_iters, L.h);
+    {
+      StageTimer t(ILW_STAGE_TAIL384, s);
+      he = launch_tail384(fp, f1, f2, ln, s);
+      t.done();
+    }
+    if (he != hipSuccess) return hip_status(he, "block tail (dim 384)");
+    *ready_out = ln ? READY_H : READY_NONE;
+    return ok();
+  }
   // x1 = Res(proj(att), x);  h = LN2(x1)
   a = gemm_args(L.att, p->w_proj, p->b_proj, p->proj, L.x1, M, D, D);
   a.wp = fuse ? L.wp_proj : nullptr;
@@ -585,32 +618,6 @@ int run_block(const ilw_block_params* p, const ilw_block_params* next,
     if (he != hipSuccess) return hip_status(he, "block LN2");
   }
   // g = rq(SD-ShiftGELU(fc1(h)))
-  GemmArgs f1 = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
-  f1.g_I0 = p->gelu_I0;
-  f1.g_kinter = p->gelu_k_inter;
-  f1.g_kout = p->gelu_k_out;
-  f1.g_mult = p->gelu_mult;
-  f1.g_shift = p->gelu_shift;
-  if (L.wp_fc1 && L.wp_fc2) {
-    // the whole MLP in one launch: g stays in LDS
-    f1.wp = L.wp_fc1;
-    GemmArgs f2 = gemm_args(nullptr, p->w_fc2, p->b_fc2, p->fc2, y, M, D, Hm);
-    f2.wp = L.wp_fc2;
-    f2.resid = L.x1;
-    f2.res_ma = p->res2_mult_a;
-    f2.res_mb = p->res2_mult_b;
-    f2.res_shift = p->res2_shift;
-    const bool ln = next && fuse;
-    if (ln) f2 = with_ln(f2, next->ln1_beta, next->ln1_out, next->ln_iters, L.h);
-    {
-      StageTimer t(ILW_STAGE_MLP, s);
-      he = launch_mlp384(f1, f2, ln, s);
-      t.done();
-    }
-    if (he != hipSuccess) return hip_status(he, "block MLP");
-    *ready_out = ln ? READY_H : READY_NONE;
-    return ok();
-  }
   a = gemm_args(L.h, p->w_fc1, p->b_fc1, p->fc1, L.g, M, Hm, D);
   a.g_I0 = p->gelu_I0;
   a.g_kinter = p->gelu_k_inter;

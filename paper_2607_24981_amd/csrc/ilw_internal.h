@@ -400,13 +400,16 @@ hipError_t launch_pack_frags(const PackList& L, hipStream_t s);
 // the latency mode).
 bool ln384_packed_kernel_applies(int64_t M, int32_t N, int32_t K);
 hipError_t launch_ln384_packed(const GemmArgs& a, bool layernorm, hipStream_t s);
-// The 384-wide block's MLP in one kernel: f1 describes fc1 + SD-ShiftGELU
-// (x = its input, wp = packed fc1 weights, N = mlp, K = 384, the GELU
-// fields), f2 fc2 + residual (wp = packed fc2 weights, N = 384, K = mlp, y,
-// resid and its dyadic, and with layernorm the next LayerNorm's fields and
-// y2).  Applies for mlp a multiple of 384 up to 1536 past the latency mode.
-bool mlp384_kernel_applies(int64_t M, int32_t D, int32_t mlp);
-hipError_t launch_mlp384(const GemmArgs& f1, const GemmArgs& f2, bool layernorm, hipStream_t s);
+// Everything of a 384-wide block after attention in one kernel: fp is the
+// projection + residual + LN2 (x = the attention output, wp = packed
+// weights, resid = the block input, LN2's fields), f1 fc1 + SD-ShiftGELU
+// (wp, N = mlp, K = 384, the GELU fields), f2 fc2 + residual onto x1 (wp,
+// N = 384, K = mlp, y, its residual dyadic, and with layernorm the next
+// block's LN1 fields and y2).  x1, h and the fc1 output never leave the
+// chip.  Applies for mlp a multiple of 384 up to 1536 past the latency mode.
+bool tail384_kernel_applies(int64_t M, int32_t D, int32_t mlp);
+hipError_t launch_tail384(const GemmArgs& fp, const GemmArgs& f1, const GemmArgs& f2,
+                          bool layernorm, hipStream_t s);
 bool gemm_latency_mode(int64_t M, int32_t N);
 
 // The rest of an encoder block after attention, for one 16-token slab per

@@ -577,7 +577,7 @@ def ilw_deform_attn_boxes(value, level_hw, level_start, ref, offsets, logits, I0
 
 
 STAGES = ["layernorm", "gemm_qkv", "attention", "gemm_proj", "gemm_fc1", "gemm_fc2",
-          "relayout", "deform", "block_tail", "split_conv", "patch_embed", "decoder", "mlp"]
+          "relayout", "deform", "block_tail", "split_conv", "patch_embed", "decoder", "tail384"]
 
 
 def profile_enable(on: bool = True):
