@@ -306,6 +306,14 @@ struct RqI64 {
     const int32_t v = (int32_t)(((int64_t)a * mult + c) >> shift);
     return min(max(v, kQmin), kQmax);
   }
+  // The same without the accumulator clamp, for callers that know
+  // |acc * mult + c| < min(2^63, 2^(shift + 31)): the 64-bit sum is then
+  // exact, its shift lies in int32, and the clamp, which only ever maps
+  // saturating accumulators to saturating ones, changes nothing.
+  __device__ __forceinline__ int32_t apply_unclamped(int32_t acc) const {
+    const int32_t v = (int32_t)(((int64_t)acc * mult + c) >> shift);
+    return min(max(v, kQmin), kQmax);
+  }
 };
 
 template <bool B>

@@ -117,7 +117,10 @@ __global__ __launch_bounds__(64 * T_NW) void tail384_kernel(GemmArgs fp, GemmArg
   __shared__ __attribute__((aligned(16))) int8_t sX[3 * T_BLK];
   __shared__ __attribute__((aligned(16))) int8_t sH[3 * T_MAXCH * T_BLK];
   __shared__ RqI64 rq1[T_MAXCH * T_D];  // fc1 output requantization per channel
-  __shared__ int8_t glut[256];          // SD-ShiftGELU of an int8 value, requantized
+  // SD-ShiftGELU of an int8 value, requantized.  Aligned so that it sits at
+  // LDS address 0: a lookup's +128 then folds into the instruction offset.
+  __shared__ __attribute__((aligned(1024))) int8_t glut[256];
+  __shared__ int32_t fc1_needs_clamp[T_NW];  // per wave: see the fc1 constants below
   static_assert(2 * T_D * sizeof(RqI64) <= sizeof(sX), "fc2 constants fit the h tile");
   constexpr int RED = (T_NW + 1) * T_TM * 2 * 4;  // row sums and statistics
   static_assert(3 * T_BLK + 2 * T_D * sizeof(RqI64) + RED <= sizeof(sH), "projection phase fits");
@@ -197,15 +200,33 @@ __global__ __launch_bounds__(64 * T_NW) void tail384_kernel(GemmArgs fp, GemmArg
     r.init(fp.ln_mult[qn], fp.ln_shift[qn], fp.ln_beta[c]);
     lnq2[c] = r;
   }
+  // fc1's requantization can skip the accumulator clamp when, for every
+  // channel and every |acc| <= 384 * 2^14, |acc * mult + c| stays below
+  // min(2^63, 2^(shift + 31)) (c = bias * mult + 2^(shift - 1)).  The bound
+  // |mult| (|bias| + 384 * 2^14) + 2^(shift - 1) is below 2^62 + 2^61 for any
+  // int32 mult and bias, so only shifts under 32 need the test.
+  bool needs_clamp = false;
   for (int c = tid; c < mlp; c += 64 * T_NW) {
+    const int32_t m = f1.mult[f1.nq == 1 ? 0 : c], sh = f1.shift[f1.nq == 1 ? 0 : c];
+    const int32_t b = f1.bias ? f1.bias[c] : 0;
     RqI64 r;
-    r.init(f1.mult[f1.nq == 1 ? 0 : c], f1.shift[f1.nq == 1 ? 0 : c], f1.bias ? f1.bias[c] : 0);
+    r.init(m, sh, b);
     rq1[c] = r;
+    const uint64_t bound = (uint64_t)(m < 0 ? -(int64_t)m : m) *
+                               ((uint64_t)(b < 0 ? -(int64_t)b : b) + 384u * 16384u) +
+                           ((uint64_t)1 << (sh - 1));
+    needs_clamp |= sh < 32 && bound >= ((uint64_t)1 << (sh + 31));
   }
+  const bool wave_needs = __any(needs_clamp);
+  if (lane == 0) fc1_needs_clamp[wave] = wave_needs;
   if (tid < 256)
     glut[tid] = (int8_t)rq(sd_gelu(tid - 128, f1.g_I0, f1.g_kinter, f1.g_kout), f1.g_mult,
                            f1.g_shift);
   lds_sync();
+  int32_t any_needs = 0;
+#pragma unroll
+  for (int w = 0; w < T_NW; ++w) any_needs |= fc1_needs_clamp[w];
+  const bool fc1_unclamped = __builtin_amdgcn_readfirstlane(any_needs) == 0;
 
   v4i acc[T_FI][T_FJ];
   const v4i zero = {0, 0, 0, 0};
@@ -292,13 +313,24 @@ __global__ __launch_bounds__(64 * T_NW) void tail384_kernel(GemmArgs fp, GemmArg
         RqI64 rf[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) rf[r] = rq1[n + r];
+        if (fc1_unclamped) {
 #pragma unroll
-        for (int j = 0; j < T_FJ; ++j) {
-          int32_t g[4];
+          for (int j = 0; j < T_FJ; ++j) {
+            int32_t g[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) g[r] = glut[rf[r].apply(acc[i][j][r]) + 128];
-          put_word(sH, n, j * 16 + (lane & 15), pack4(g[0], g[1], g[2], g[3]));
-          acc[i][j] = zero;
+            for (int r = 0; r < 4; ++r) g[r] = glut[rf[r].apply_unclamped(acc[i][j][r]) + 128];
+            put_word(sH, n, j * 16 + (lane & 15), pack4(g[0], g[1], g[2], g[3]));
+            acc[i][j] = zero;
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < T_FJ; ++j) {
+            int32_t g[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) g[r] = glut[rf[r].apply(acc[i][j][r]) + 128];
+            put_word(sH, n, j * 16 + (lane & 15), pack4(g[0], g[1], g[2], g[3]));
+            acc[i][j] = zero;
+          }
         }
       }
       if (k0 + 3 == S1) {

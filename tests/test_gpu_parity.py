@@ -811,7 +811,8 @@ def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
 
 
 @pytest.mark.parametrize("variant,mlp", [("baseline", 1536), ("wide", 1536), ("baseline", 1024),
-                                         ("baseline", 768), ("wide", 1152)])
+                                         ("baseline", 768), ("wide", 1152),
+                                         ("wide_big_bias", 1536), ("fc1_clamped", 1536)])
 def test_encoder_384_packed_ragged(variant, mlp):
     """The 384-channel LayerNorm-fused linears on their packed-weight kernel
     (grids past the latency mode: 7 images of 41 x 41 tokens, 11 767 tokens,
@@ -820,13 +821,25 @@ def test_encoder_384_packed_ragged(variant, mlp):
     1152 and 768 run the whole MLP as one kernel (4, 3 and 2 chunks of 384
     fc1 channels; the first block with the next LayerNorm, the second
     without); MLP 1024 runs fc1 and fc2 apart, fc2 with 8 K steps (the
-    two-set weight ring)."""
+    two-set weight ring).  fc1's requantization skips the accumulator clamp
+    unless a channel's shift and |mult| (|bias| + 384 * 2^14) would let the
+    shifted value leave int32: 'wide_big_bias' puts biases near +-2^31 on
+    that path (shifts 39-42), 'fc1_clamped' adds shifts of 20-23 on some of
+    those channels, which sends every tile through the clamp."""
     import concurrent.futures as cf
     D, H, B, grid, windows = 384, 6, 7, (41, 41), [(0, 0), (0, 0)]
     say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}, MLP {mlp}")
     g = rng(384 + B)
-    blocks = [synth.block_params(g, D, H, 64, mlp, variant, ln_iters=10 + 4 * i,
+    base = "baseline" if variant == "baseline" else "wide"
+    blocks = [synth.block_params(g, D, H, 64, mlp, base, ln_iters=10 + 4 * i,
                                  smax_s_d=(-1 if i == 0 else 5)) for i in range(2)]
+    if variant in ("wide_big_bias", "fc1_clamped"):
+        for p in blocks:
+            for j, b in enumerate(BIG_BIAS):
+                n = (j * 131 + 7) % mlp
+                p["b_fc1"][n] = b
+                if variant == "fc1_clamped":
+                    p["fc1_shift"][n] = 20 + j % 4
     x = g.integers(-127, 128, (B, grid[0] * grid[1], D)).astype(np.int8)
     images = [0, 3, 6]
     with cf.ThreadPoolExecutor(max_workers=1) as bg:
