@@ -306,6 +306,28 @@ struct RqI64 {
     const int32_t v = (int32_t)(((int64_t)a * mult + c) >> shift);
     return min(max(v, kQmin), kQmax);
   }
+  // init for accumulators with |acc| <= acc_max.  Where the bound
+  // |mult| (|bias| + acc_max) + 2^(shift - 1) on |acc * mult + c| is below
+  // min(2^63, 2^(shift + 31)), the clamp-free form below is exact: the clamp
+  // bounds are then the whole int32 range and the float work is skipped.
+  // Returns whether that holds.
+  __device__ __forceinline__ bool init_bounded(int32_t m, int32_t s, int32_t b, uint32_t acc_max) {
+    const uint64_t am = (uint64_t)(m < 0 ? -(int64_t)m : (int64_t)m);
+    const uint64_t ab = (uint64_t)(b < 0 ? -(int64_t)b : (int64_t)b);
+    // at most 2^31 (2^31 + 2^32) + 2^61 < 2^64: no wrap
+    const uint64_t bound = am * (ab + acc_max) + ((uint64_t)1 << (s - 1));
+    const uint64_t lim = s >= 32 ? ((uint64_t)1 << 63) : ((uint64_t)1 << (s + 31));
+    if (bound >= lim) {
+      init(m, s, b);
+      return false;
+    }
+    mult = m;
+    shift = s;
+    c = (int64_t)b * m + ((int64_t)1 << (s - 1));
+    lo = INT32_MIN;
+    hi = INT32_MAX;
+    return true;
+  }
   // The same without the accumulator clamp, for callers that know
   // |acc * mult + c| < min(2^63, 2^(shift + 31)): the 64-bit sum is then
   // exact, its shift lies in int32, and the clamp, which only ever maps

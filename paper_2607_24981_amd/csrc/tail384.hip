@@ -33,6 +33,9 @@ constexpr int T_BLK = T_TM * T_KB;           // one 64 x 128 activation block in
 constexpr int T_MAXCH = 4;                   // fc1 chunks of 384 channels at most
 constexpr int T_OSTR = T_D / 4 + 4;          // output staging: words per token row
 constexpr int NXCD_T = 8;
+// accumulator bounds for the requantization constants: a 384-deep int8
+// product; a LayerNorm's (d F) >> 1, with |d| <= sigma and F < 2^31 / sigma
+constexpr uint32_t kAccD = (uint32_t)T_D << 14, kAccLN = 1u << 30;
 static_assert(T_FI * T_NW * 16 == T_D, "whole fragments per wave");
 
 // block kb of an activation tile: rows of 128 bytes with swizzled chunks
@@ -194,28 +197,21 @@ __global__ __launch_bounds__(64 * T_NW) void tail384_kernel(GemmArgs fp, GemmArg
   // constants, while the loads are in flight
   for (int c = tid; c < T_D; c += 64 * T_NW) {
     RqI64 r;
-    r.init(fp.mult[fp.nq == 1 ? 0 : c], fp.shift[fp.nq == 1 ? 0 : c], fp.bias ? fp.bias[c] : 0);
+    r.init_bounded(fp.mult[fp.nq == 1 ? 0 : c], fp.shift[fp.nq == 1 ? 0 : c],
+                   fp.bias ? fp.bias[c] : 0, kAccD);
     rqp[c] = r;
     const int qn = fp.ln_nq == 1 ? 0 : c;
-    r.init(fp.ln_mult[qn], fp.ln_shift[qn], fp.ln_beta[c]);
+    r.init_bounded(fp.ln_mult[qn], fp.ln_shift[qn], fp.ln_beta[c], kAccLN);
     lnq2[c] = r;
   }
-  // fc1's requantization can skip the accumulator clamp when, for every
-  // channel and every |acc| <= 384 * 2^14, |acc * mult + c| stays below
-  // min(2^63, 2^(shift + 31)) (c = bias * mult + 2^(shift - 1)).  The bound
-  // |mult| (|bias| + 384 * 2^14) + 2^(shift - 1) is below 2^62 + 2^61 for any
-  // int32 mult and bias, so only shifts under 32 need the test.
+  // fc1's requantization skips the accumulator clamp when every channel
+  // allows it (RqI64::init_bounded)
   bool needs_clamp = false;
   for (int c = tid; c < mlp; c += 64 * T_NW) {
-    const int32_t m = f1.mult[f1.nq == 1 ? 0 : c], sh = f1.shift[f1.nq == 1 ? 0 : c];
-    const int32_t b = f1.bias ? f1.bias[c] : 0;
     RqI64 r;
-    r.init(m, sh, b);
+    needs_clamp |= !r.init_bounded(f1.mult[f1.nq == 1 ? 0 : c], f1.shift[f1.nq == 1 ? 0 : c],
+                                   f1.bias ? f1.bias[c] : 0, kAccD);
     rq1[c] = r;
-    const uint64_t bound = (uint64_t)(m < 0 ? -(int64_t)m : m) *
-                               ((uint64_t)(b < 0 ? -(int64_t)b : b) + 384u * 16384u) +
-                           ((uint64_t)1 << (sh - 1));
-    needs_clamp |= sh < 32 && bound >= ((uint64_t)1 << (sh + 31));
   }
   const bool wave_needs = __any(needs_clamp);
   if (lane == 0) fc1_needs_clamp[wave] = wave_needs;
@@ -339,12 +335,12 @@ __global__ __launch_bounds__(64 * T_NW) void tail384_kernel(GemmArgs fp, GemmArg
         lds_sync();
         for (int c = tid; c < T_D; c += 64 * T_NW) {
           RqI64 r;
-          r.init(f2.mult[f2.nq == 1 ? 0 : c], f2.shift[f2.nq == 1 ? 0 : c],
-                 f2.bias ? f2.bias[c] : 0);
+          r.init_bounded(f2.mult[f2.nq == 1 ? 0 : c], f2.shift[f2.nq == 1 ? 0 : c],
+                         f2.bias ? f2.bias[c] : 0, (uint32_t)mlp << 14);
           rq2[c] = r;
           if (DO_LN) {
             const int qn = f2.ln_nq == 1 ? 0 : c;
-            r.init(f2.ln_mult[qn], f2.ln_shift[qn], f2.ln_beta[c]);
+            r.init_bounded(f2.ln_mult[qn], f2.ln_shift[qn], f2.ln_beta[c], kAccLN);
             lnq[c] = r;
           }
         }
