@@ -93,9 +93,9 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const int8_t* x, int8_t*
 // Each wave walks several row groups and loads the next group's rows before
 // working on the current one; the first group's loads are issued before the
 // constants are staged, so the kernel pays about one memory round trip.
-// When every |beta| <= 2^30 the output path stays in 32 bits:
-// |n| <= 2^30 so |n + beta| < 2^31, which is clamped to [-L, L] and then
-// requantized with one 64-bit multiply-add.
+// The output requantization of n = (d F) >> 1 (|n| < 2^30) folds beta into
+// the per-channel constant (RqI64 with the bias beta); where every channel's
+// bound allows it, the accumulator clamp is skipped (one uniform branch).
 template <int LPR, int JC>
 __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, int8_t* y,
                                                              int64_t rows, int32_t C,
@@ -103,7 +103,7 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
                                                              const int32_t* mult,
                                                              const int32_t* shift, int32_t nq,
                                                              int32_t iters) {
-  extern __shared__ LnChan prm[];
+  extern __shared__ RqI64 prm[];
   constexpr int RG = 64 / LPR;  // rows per wave and group
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sub = lane / LPR, k = lane % LPR;
@@ -120,23 +120,17 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
   v4i nxt[JC];
   if (g < ngroups) load(g, nxt);
 
-  int wide = 0;
+  int clamp = 0;
   for (int32_t c = threadIdx.x; c < C; c += 256) {
     const int32_t q = nq == 1 ? 0 : c;
-    LnChan p;
-    p.beta = beta[c];
-    p.mult = mult[q];
-    p.shift = shift[q];
-    const float am = fabsf((float)p.mult);
-    const float bound = am == 0.f ? 1.f : 130.f * exp2f((float)p.shift) * __builtin_amdgcn_rcpf(am);
-    p.L = bound >= 2147483520.f ? 0x7fffffff : (int32_t)bound + 1;
+    RqI64 p;
+    clamp |= !p.init_bounded(mult[q], shift[q], beta[c], 1u << 30);
     // chunk-transposed: channel 16 ch + i sits at i * n16 + ch, so the LPR
     // lanes of a row (consecutive chunks ch) read consecutive entries instead
-    // of entries 256 bytes apart, all in one LDS bank
+    // of entries 16 * sizeof(RqI64) bytes apart
     prm[(c & 15) * n16 + (c >> 4)] = p;
-    wide |= (p.beta > (1 << 30) || p.beta < -(1 << 30));
   }
-  wide = __syncthreads_or(wide);
+  clamp = __syncthreads_or(clamp);
 
   for (; g < ngroups; g += gstride) {
     v4i xv[JC];
@@ -166,33 +160,31 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(const int8_t* x, in
     const uint32_t sigma = newton_isqrt_f64(V, iters);
     const int32_t F = sigma ? (int32_t)div_2p31m1(sigma) : 0;
     v4i* yr = (v4i*)(y + (live ? row : rows - 1) * C);
+    auto outputs = [&](auto unclamped) {
 #pragma unroll
-    for (int j = 0; j < JC; ++j) {
-      const int32_t ch = k + j * LPR;
-      if (ch >= n16) break;
-      v4i o;
+      for (int j = 0; j < JC; ++j) {
+        const int32_t ch = k + j * LPR;
+        if (ch >= n16) break;
+        v4i o;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        uint32_t ow = 0;
+        for (int w = 0; w < 4; ++w) {
+          int32_t r[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const LnChan p = prm[(w * 4 + b) * n16 + ch];
-          const int32_t d = (int8_t)(xv[j][w] >> (8 * b)) - mu;
-          const int32_t n = (d * F) >> 1;  // |d| <= sigma: |d * F| < 2^31
-          int32_t r;
-          if (!wide) {
-            const int32_t t = min(max(n + p.beta, -p.L), p.L);
-            r = (int32_t)(((int64_t)t * p.mult + ((int64_t)1 << (p.shift - 1))) >> p.shift);
-            r = min(max(r, kQmin), kQmax);
-          } else {
-            r = ln_out((int64_t)n + p.beta, p.mult, p.shift);
+          for (int b = 0; b < 4; ++b) {
+            const RqI64& p = prm[(w * 4 + b) * n16 + ch];
+            const int32_t d = (int8_t)(xv[j][w] >> (8 * b)) - mu;
+            const int32_t n = (d * F) >> 1;  // |d| <= sigma: |d * F| < 2^31
+            r[b] = decltype(unclamped)::value ? p.apply_unclamped(n) : p.apply(n);
           }
-          ow |= (uint32_t)(r & 0xff) << (8 * b);
+          o[w] = (int32_t)pack4(r[0], r[1], r[2], r[3]);
         }
-        o[w] = (int32_t)ow;
+        if (live) yr[ch] = o;
       }
-      if (live) yr[ch] = o;
-    }
+    };
+    if (clamp)
+      outputs(Flag<false>{});
+    else
+      outputs(Flag<true>{});
   }
 }
 
@@ -504,7 +496,7 @@ hipError_t launch_layernorm(const int8_t* x, int8_t* y, int64_t rows, int32_t C,
   // chunks each.  The 16-byte row loads need 16-byte aligned rows.
   if (C % 16 == 0 && C <= 2048 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 15) == 0) {
     const int32_t n16 = C / 16;
-    const size_t smem = (size_t)C * sizeof(LnChan);
+    const size_t smem = (size_t)C * sizeof(RqI64);
     auto go = [&](auto lpr_c, auto jc_c) {
       constexpr int LPR = decltype(lpr_c)::value, JC = decltype(jc_c)::value;
       const int64_t groups = (rows + (64 / LPR) - 1) / (64 / LPR);
