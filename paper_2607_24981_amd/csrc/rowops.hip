@@ -449,19 +449,37 @@ __global__ __launch_bounds__(256) void gelu_kernel(const int8_t* x, int8_t* y, i
 }
 
 // ---------------------------------------------------------------- residual
+// U 16-byte chunks per thread, all loads issued before any arithmetic (the
+// chunk index clamped: a re-read, never stored); WIDE as in rq2i8.
+template <bool WIDE, int U>
 __global__ __launch_bounds__(256) void residual_kernel(const int8_t* a, const int8_t* b,
                                                        int8_t* y, int64_t n, int32_t ma,
                                                        int32_t mb, int32_t shift) {
   const int64_t nchunk = n >> 4;
   const int64_t stride = (int64_t)gridDim.x * 256;
-  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < nchunk; c += stride) {
-    v4i va = *(const v4i*)(a + c * 16);
-    const v4i vb = *(const v4i*)(b + c * 16);
-    int8_t* pa = (int8_t*)&va;
-    const int8_t* pb = (const int8_t*)&vb;
+  for (int64_t c0 = (int64_t)blockIdx.x * 256 + threadIdx.x; c0 < nchunk; c0 += stride * U) {
+    v4i va[U], vb[U];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) pa[i] = (int8_t)rq2(pa[i], pb[i], ma, mb, shift);
-    *(v4i*)(y + c * 16) = va;
+    for (int u = 0; u < U; ++u) {
+      const int64_t c = min(c0 + u * stride, nchunk - 1);
+      va[u] = *(const v4i*)(a + c * 16);
+      vb[u] = *(const v4i*)(b + c * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      v4i o;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        int32_t r[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          r[k] = rq2i8<WIDE>((int8_t)(va[u][w] >> (8 * k)), (int8_t)(vb[u][w] >> (8 * k)), ma, mb,
+                             shift);
+        o[w] = (int32_t)pack4(r[0], r[1], r[2], r[3]);
+      }
+      const int64_t c = c0 + u * stride;
+      if (c < nchunk) *(v4i*)(y + c * 16) = o;
+    }
   }
   const int64_t t = (nchunk << 4) + (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (blockIdx.x == 0 && t < n) y[t] = (int8_t)rq2(a[t], b[t], ma, mb, shift);
@@ -580,8 +598,15 @@ hipError_t launch_gelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0, int32_
 hipError_t launch_residual(const int8_t* a, const int8_t* b, int8_t* y, int64_t n,
                            int32_t ma, int32_t mb, int32_t shift, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(residual_kernel, dim3(stream_grid(n)), dim3(256), 0, s, a, b, y, n,
-                     ma, mb, shift);
+  constexpr int U = 4;
+  int64_t g = ((n >> 4) + 256 * U - 1) / (256 * U);
+  g = g < 1 ? 1 : (g > 2048 ? 2048 : g);
+  if (shift >= 9)
+    hipLaunchKernelGGL((residual_kernel<false, U>), dim3((unsigned)g), dim3(256), 0, s, a, b, y,
+                       n, ma, mb, shift);
+  else
+    hipLaunchKernelGGL((residual_kernel<true, U>), dim3((unsigned)g), dim3(256), 0, s, a, b, y,
+                       n, ma, mb, shift);
   return hipGetLastError();
 }
 

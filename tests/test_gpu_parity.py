@@ -310,8 +310,10 @@ def test_layernorm_in_place():
 
 
 # ------------------------------------------------------------------ residual
-@pytest.mark.parametrize("n", [1, 15, 16, 1000, 1_000_003])
+@pytest.mark.parametrize("n", [1, 15, 16, 1000, 1_000_003, 40_000_017])
 def test_residual(n):
+    """Element-wise residual add; 40 000 017 elements make each thread of the
+    largest grid walk its chunks more than once, with a ragged tail."""
     say(f"residual n={n}")
     g = rng(n)
     a = g.integers(-128, 128, n).astype(np.int8)
