@@ -59,20 +59,6 @@ __device__ __forceinline__ uint32_t pack_bytes(int32_t a, int32_t b, int32_t c, 
   return lo | (hi << 16);
 }
 
-// Bytes 0 of a, b, c, d clamped to cap and packed (a in the low byte), for
-// a..d < 2^16: the pairs go into 16-bit halves, are clamped two at a time
-// (v_pk_min_u16) and their low bytes gathered: 5 instructions for 4 values.
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t pack_min_bytes(uint32_t a, uint32_t b, uint32_t c, uint32_t d,
-                                                   u16x2 cap) {
-  u16x2 lo = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(b, a, 0x05040100u));
-  u16x2 hi = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(d, c, 0x05040100u));
-  lo = __builtin_elementwise_min(lo, cap);
-  hi = __builtin_elementwise_min(hi, cap);
-  return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo),
-                               0x06040200u);
-}
-
 // NW waves per workgroup (4, 8 or 16): keys are split over all waves for the
 // scores, rows for the Shiftmax (R / NW rows per wave), and (channel group,
 // key range) pairs for P V, whose int32 partial sums are added through LDS.

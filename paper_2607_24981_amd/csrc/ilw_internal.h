@@ -52,6 +52,20 @@ __device__ __forceinline__ int32_t rq2i8(int32_t a, int32_t b, int32_t ma, int32
   return min(max((int32_t)(v >> shift), kQmin), kQmax);
 }
 
+// Bytes 0 of a, b, c, d clamped to cap and packed (a in the low byte), for
+// a..d < 2^16: the pairs go into 16-bit halves, are clamped two at a time
+// (v_pk_min_u16) and their low bytes gathered: 5 instructions for 4 values.
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_min_bytes(uint32_t a, uint32_t b, uint32_t c, uint32_t d,
+                                                   u16x2 cap) {
+  u16x2 lo = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(b, a, 0x05040100u));
+  u16x2 hi = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(d, c, 0x05040100u));
+  lo = __builtin_elementwise_min(lo, cap);
+  hi = __builtin_elementwise_min(hi, cap);
+  return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo),
+                               0x06040200u);
+}
+
 // ---------------------------------------------------------------- ShiftExp
 // I-ViT's integer exponential for I <= 0 at scale 1/I0: exp(I / I0) =
 // 2^(-z / I0) with z = -I log2(e) ~ a + a/2 - a/16 for a = -I, the two

@@ -274,11 +274,13 @@ __global__ __launch_bounds__(256) void shiftmax_kernel(const int8_t* x, int8_t* 
 
 // Rows of 16-byte chunks (cols % 16 == 0, aligned rows): LPR lanes per row
 // hold the row in JC chunks each, so it is read from memory once and written
-// once.  Bytes are biased (x + 128, one XOR per word): max - x is then a
-// byte-wise subtraction without borrows, and ShiftExp of it is one lookup in
-// a 256-entry LDS table (S_sum >> s_d is exactly the quotient-remainder
-// denominator of Alg. 2).  The row maximum uses 16-bit packed maxima of the
-// even and odd bytes.
+// once; each wave loads its next row while working on the current one.
+// Bytes are biased (x + 128, one XOR per word): max - x is then a byte-wise
+// subtraction without borrows, and ShiftExp of it is one lookup in a
+// 256-entry LDS table (S_sum >> s_d is exactly the quotient-remainder
+// denominator of Alg. 2), kept in registers from the sum to the
+// normalization.  The row maximum uses 16-bit packed maxima of the even and
+// odd bytes.
 template <int LPR, int JC>
 __global__ __launch_bounds__(256) void shiftmax_rows_kernel(const int8_t* x, int8_t* y,
                                                             int64_t rows, int32_t cols,
@@ -286,37 +288,46 @@ __global__ __launch_bounds__(256) void shiftmax_rows_kernel(const int8_t* x, int
                                                             int32_t k_out, int32_t m_p,
                                                             int32_t s_d) {
   __shared__ uint32_t elut[256];
-  elut[threadIdx.x] = (uint32_t)shift_exp(-(int32_t)threadIdx.x, I0, k_inter);
-  __syncthreads();
   constexpr int RG = 64 / LPR;
-  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sub = lane / LPR, k = lane % LPR;
   const int32_t n16 = cols >> 4;
   const int64_t ngroups = (rows + RG - 1) / RG;
-  for (int64_t g = (int64_t)blockIdx.x * 4 + wave; g < ngroups; g += (int64_t)gridDim.x * 4) {
-    const int64_t row = g * RG + sub;
-    const bool live = row < rows;
-    const v4i* xr = (const v4i*)(x + (live ? row : rows - 1) * cols);
+  const int64_t gstride = (int64_t)gridDim.x * 4;
+  // chunks past the row repeat the last one: they cannot raise the max
+  auto load = [&](int64_t g, v4i(&v)[JC]) {
+    const int64_t row = min(g * RG + sub, rows - 1);
+    const v4i* xr = (const v4i*)(x + row * cols);
+#pragma unroll
+    for (int j = 0; j < JC; ++j) v[j] = xr[min(k + j * LPR, n16 - 1)];
+  };
+  int64_t g = (int64_t)blockIdx.x * 4 + wave;
+  v4i nxt[JC];
+  if (g < ngroups) load(g, nxt);
+  elut[threadIdx.x] = (uint32_t)shift_exp(-(int32_t)threadIdx.x, I0, k_inter);
+  __syncthreads();
+  const uint32_t cap = (1u << (k_out - 1)) - 1;
+  const u16x2 cap2 = {(unsigned short)cap, (unsigned short)cap};
+  for (; g < ngroups; g += gstride) {
     uint32_t w[JC][4];
     u16x2 mx = {0, 0};
 #pragma unroll
-    for (int j = 0; j < JC; ++j) {
-      const int32_t ch = k + j * LPR;
-      const v4i v = xr[min(ch, n16 - 1)];
+    for (int j = 0; j < JC; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        // chunks past the row repeat the last one: they cannot raise the max
-        w[j][q] = (uint32_t)v[q] ^ 0x80808080u;
+        w[j][q] = (uint32_t)nxt[j][q] ^ 0x80808080u;
         const u16x2 ev = __builtin_bit_cast(u16x2, w[j][q] & 0x00ff00ffu);
         const u16x2 od = __builtin_bit_cast(u16x2, (w[j][q] >> 8) & 0x00ff00ffu);
         mx = __builtin_elementwise_max(mx, __builtin_elementwise_max(ev, od));
       }
-    }
+    if (g + gstride < ngroups) load(g + gstride, nxt);
+    const int64_t row = g * RG + sub;
+    const bool live = row < rows;
     uint32_t m = max((uint32_t)mx[0], (uint32_t)mx[1]);
 #pragma unroll
     for (int o = LPR / 2; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o, 64));
     const uint32_t m4 = m * 0x01010101u;
+    uint32_t e[JC][4][4];
     uint64_t sum = 0;
 #pragma unroll
     for (int j = 0; j < JC; ++j) {
@@ -326,7 +337,10 @@ __global__ __launch_bounds__(256) void shiftmax_rows_kernel(const int8_t* x, int
         const uint32_t d4 = m4 - w[j][q];
         uint32_t ws = 0;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) ws += elut[(d4 >> (8 * b)) & 255];
+        for (int b = 0; b < 4; ++b) {
+          e[j][q][b] = elut[(d4 >> (8 * b)) & 255];
+          ws += e[j][q][b];
+        }
         sum += ws;  // 4 values of at most 2^30 each
       }
     }
@@ -340,26 +354,35 @@ __global__ __launch_bounds__(256) void shiftmax_rows_kernel(const int8_t* x, int
     const uint32_t F = shiftmax_factor(sum, sd);
     // e F < 2^30 2^31: a shift of 61 or more leaves 0, as does 63
     const int32_t sh = min(32 - k_out + sd, 63);
-    const uint32_t cap = (1u << (k_out - 1)) - 1;
     v4i* yr = (v4i*)(y + (live ? row : rows - 1) * cols);
+    // With sh < 32 and F < 2^sh, F 2^(32 - sh) fits 32 bits and
+    // floor(e F / 2^sh) is the high word of e F 2^(32 - sh); either way the
+    // quotient is below 2^k_out <= 2^8, so the 16-bit clamp-and-pack holds
+    // it.  (A uniform branch: every row of the wave must qualify.)
+    auto outputs = [&](auto hi_word) {
+      const uint32_t Fs = F << ((32 - sh) & 31);
 #pragma unroll
-    for (int j = 0; j < JC; ++j) {
-      const int32_t ch = k + j * LPR;
-      if (ch >= n16) break;
-      v4i o;
+      for (int j = 0; j < JC; ++j) {
+        const int32_t ch = k + j * LPR;
+        if (ch >= n16) break;
+        v4i o;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t d4 = m4 - w[j][q];
-        uint32_t ow = 0;
+        for (int q = 0; q < 4; ++q) {
+          uint32_t p[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const uint64_t p = ((uint64_t)elut[(d4 >> (8 * b)) & 255] * F) >> sh;
-          ow |= (uint32_t)(p > cap ? cap : p) << (8 * b);
+          for (int b = 0; b < 4; ++b)
+            p[b] = decltype(hi_word)::value
+                       ? __umulhi(e[j][q][b], Fs)
+                       : (uint32_t)min(((uint64_t)e[j][q][b] * F) >> sh, (uint64_t)cap);
+          o[q] = (int32_t)pack_min_bytes(p[0], p[1], p[2], p[3], cap2);
         }
-        o[q] = (int32_t)ow;
+        if (live) yr[ch] = o;
       }
-      if (live) yr[ch] = o;
-    }
+    };
+    if (__all(sh < 32 && F < (1u << (sh & 31))))
+      outputs(Flag<true>{});
+    else
+      outputs(Flag<false>{});
   }
 }
 

@@ -186,14 +186,16 @@ def test_shiftmax_in_place():
 
 
 @pytest.mark.parametrize("rows,cols", [(5, 16), (9, 32), (17, 256), (33, 272), (6, 1024),
-                                       (3, 2048), (1000, 1600), (4, 2064)])
+                                       (3, 2048), (1000, 1600), (4, 2064), (20001, 1024)])
 @pytest.mark.parametrize("s_d", [-1, 0, 9])
 def test_shiftmax_row_chunks(rows, cols, s_d):
     """Rows of whole 16-byte chunks held in registers (8, 32 or 64 lanes per
     row, partially filled lanes, several rows per wave, a row count that
     leaves the last wave's rows partly past the end), with the full int8
     range (-128 gives the 255-step table entry), static and dynamic s_d;
-    2064 columns take the byte-wise kernel."""
+    2064 columns take the byte-wise kernel; 20 001 rows of 1024 make each
+    wave of the largest grid walk more than one row (the next row's loads in
+    flight)."""
     say(f"shiftmax row chunks rows={rows} cols={cols} s_d={s_d}")
     g = rng(rows * 7 + cols + s_d)
     x = g.integers(-128, 128, (rows, cols)).astype(np.int8)
