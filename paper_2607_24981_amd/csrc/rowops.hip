@@ -449,22 +449,41 @@ __global__ __launch_bounds__(256) void shiftgelu_ivit_kernel(const int8_t* x, in
 }
 
 // ---------------------------------------------------------------- GELU
+// U 16-byte chunks per thread; the first U chunks' loads are issued before
+// the table is built (the chunk index clamped: a re-read, never stored).
+template <int U>
 __global__ __launch_bounds__(256) void gelu_kernel(const int8_t* x, int8_t* y, int64_t n,
                                                    int32_t I0, int32_t k_inter,
                                                    int32_t k_out, int32_t mult,
                                                    int32_t shift) {
   __shared__ int8_t lut[256];
+  const int64_t nchunk = n >> 4;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t c0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  v4i v[U];
+  auto load = [&](int64_t cb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = *(const v4i*)(x + min(cb + u * stride, nchunk - 1) * 16);
+  };
+  if (c0 < nchunk) load(c0);
   lut[threadIdx.x] =
       (int8_t)rq(sd_gelu((int32_t)threadIdx.x - 128, I0, k_inter, k_out), mult, shift);
   __syncthreads();
-  const int64_t nchunk = n >> 4;
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < nchunk; c += stride) {
-    v4i v = *(const v4i*)(x + c * 16);
-    int8_t* b = (int8_t*)&v;
+  for (; c0 < nchunk; c0 += stride * U) {
+    if (c0 != (int64_t)blockIdx.x * 256 + threadIdx.x) load(c0);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) b[i] = lut[(int32_t)b[i] + 128];
-    *(v4i*)(y + c * 16) = v;
+    for (int u = 0; u < U; ++u) {
+      v4i o;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        int32_t r[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) r[b] = lut[(int8_t)(v[u][w] >> (8 * b)) + 128];
+        o[w] = (int32_t)pack4(r[0], r[1], r[2], r[3]);
+      }
+      const int64_t c = c0 + u * stride;
+      if (c < nchunk) *(v4i*)(y + c * 16) = o;
+    }
   }
   // tail (n not a multiple of 16)
   const int64_t t = (nchunk << 4) + (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -508,12 +527,6 @@ __global__ __launch_bounds__(256) void residual_kernel(const int8_t* a, const in
   if (blockIdx.x == 0 && t < n) y[t] = (int8_t)rq2(a[t], b[t], ma, mb, shift);
 }
 
-unsigned stream_grid(int64_t n) {
-  const int64_t chunks = (n >> 4) + 1;
-  int64_t g = (chunks + 255) / 256;
-  if (g > 4096) g = 4096;
-  return (unsigned)g;
-}
 
 }  // namespace
 
@@ -613,8 +626,11 @@ hipError_t launch_shiftgelu_ivit(const int8_t* x, int8_t* y, int64_t rows, int32
 hipError_t launch_gelu(const int8_t* x, int8_t* y, int64_t n, int32_t I0, int32_t k_inter,
                        int32_t k_out, int32_t mult, int32_t shift, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(gelu_kernel, dim3(stream_grid(n)), dim3(256), 0, s, x, y, n, I0,
-                     k_inter, k_out, mult, shift);
+  constexpr int U = 4;
+  int64_t g = ((n >> 4) + 256 * U - 1) / (256 * U);
+  g = g < 1 ? 1 : (g > 4096 ? 4096 : g);
+  hipLaunchKernelGGL((gelu_kernel<U>), dim3((unsigned)g), dim3(256), 0, s, x, y, n, I0, k_inter,
+                     k_out, mult, shift);
   return hipGetLastError();
 }
 

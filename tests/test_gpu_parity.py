@@ -228,9 +228,12 @@ def test_sdshiftgelu_exhaustive(I0):
         assert_same(got, ref, f"gelu k_out={k_out} k_inter={k_inter}")
 
 
-def test_sdshiftgelu_large_in_place():
-    say("sdshiftgelu 3M elements in place")
-    x = synth.int8_tensor(10, (3_000_017,), -128, 127)
+@pytest.mark.parametrize("n", [3_000_017, 70_000_003])
+def test_sdshiftgelu_large_in_place(n):
+    """In place; 70 000 003 elements make each thread of the largest grid
+    walk its chunks more than once."""
+    say(f"sdshiftgelu {n} elements in place")
+    x = synth.int8_tensor(10, (n,), -128, 127)
     ref = oracle.sdshiftgelu_tensor(x, 21, 1 << 30, 36)
     t = dev(x)
     ilw.ilw_sdshiftgelu(t, 21, 1 << 30, 36, y=t)
