@@ -819,7 +819,8 @@ def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
 
 @pytest.mark.parametrize("variant,mlp", [("baseline", 1536), ("wide", 1536), ("baseline", 1024),
                                          ("baseline", 768), ("wide", 1152),
-                                         ("wide_big_bias", 1536), ("fc1_clamped", 1536)])
+                                         ("wide_big_bias", 1536), ("fc1_clamped", 1536),
+                                         ("res_shift_8", 1536), ("res_shift_mixed", 1152)])
 def test_encoder_384_packed_ragged(variant, mlp):
     """The 384-channel LayerNorm-fused linears on their packed-weight kernel
     (grids past the latency mode: 7 images of 41 x 41 tokens, 11 767 tokens,
@@ -832,7 +833,10 @@ def test_encoder_384_packed_ragged(variant, mlp):
     unless a channel's shift and |mult| (|bias| + 384 * 2^14) would let the
     shifted value leave int32: 'wide_big_bias' puts biases near +-2^31 on
     that path (shifts 39-42), 'fc1_clamped' adds shifts of 20-23 on some of
-    those channels, which sends every tile through the clamp."""
+    those channels, which sends every tile through the clamp.  Residual
+    shifts below 9 take the general 64-bit residual saturation:
+    'res_shift_8' in both residual adds, 'res_shift_mixed' in the first
+    only (shift 5 there, 9 in the second)."""
     import concurrent.futures as cf
     D, H, B, grid, windows = 384, 6, 7, (41, 41), [(0, 0), (0, 0)]
     say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}, MLP {mlp}")
@@ -847,6 +851,13 @@ def test_encoder_384_packed_ragged(variant, mlp):
                 p["b_fc1"][n] = b
                 if variant == "fc1_clamped":
                     p["fc1_shift"][n] = 20 + j % 4
+    if variant in ("res_shift_8", "res_shift_mixed"):
+        for p in blocks:
+            for r, sh in (("res1", 8 if variant == "res_shift_8" else 5),
+                          ("res2", 8 if variant == "res_shift_8" else 9)):
+                p[r + "_shift"] = sh
+                for k in ("_mult_a", "_mult_b"):
+                    p[r + k] = int(g.integers(1 << (sh - 1), 3 << (sh - 1)))
     x = g.integers(-127, 128, (B, grid[0] * grid[1], D)).astype(np.int8)
     images = [0, 3, 6]
     with cf.ThreadPoolExecutor(max_workers=1) as bg:
