@@ -820,7 +820,8 @@ def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
 @pytest.mark.parametrize("variant,mlp", [("baseline", 1536), ("wide", 1536), ("baseline", 1024),
                                          ("baseline", 768), ("wide", 1152),
                                          ("wide_big_bias", 1536), ("fc1_clamped", 1536),
-                                         ("res_shift_8", 1536), ("res_shift_mixed", 1152)])
+                                         ("res_shift_8", 1536), ("res_shift_mixed", 1152),
+                                         ("res_shift_8", 1024)])
 def test_encoder_384_packed_ragged(variant, mlp):
     """The 384-channel LayerNorm-fused linears on their packed-weight kernel
     (grids past the latency mode: 7 images of 41 x 41 tokens, 11 767 tokens,
@@ -835,8 +836,9 @@ def test_encoder_384_packed_ragged(variant, mlp):
     that path (shifts 39-42), 'fc1_clamped' adds shifts of 20-23 on some of
     those channels, which sends every tile through the clamp.  Residual
     shifts below 9 take the general 64-bit residual saturation:
-    'res_shift_8' in both residual adds, 'res_shift_mixed' in the first
-    only (shift 5 there, 9 in the second)."""
+    'res_shift_8' in both residual adds (with MLP 1024 on the separate
+    LayerNorm-fused linears), 'res_shift_mixed' in the first only (shift 5
+    there, 9 in the second)."""
     import concurrent.futures as cf
     D, H, B, grid, windows = 384, 6, 7, (41, 41), [(0, 0), (0, 0)]
     say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}, MLP {mlp}")
