@@ -593,6 +593,23 @@ def test_block_shapes(dims, grid, win, B):
     assert_same(got, ref, "block in place")
 
 
+@pytest.mark.parametrize("dims,B,win", [((384, 6, 1536), 9, (20, 20)), ((384, 6, 1536), 9, (0, 0)),
+                                        ((256, 4, 1024), 11, (20, 20))])
+def test_block_large_unpacked(dims, B, win):
+    """One block through the block entry point (weights not packed) on grids
+    past the GEMM latency mode: the throughput QKV, fused-LayerNorm (128-byte
+    K steps at 384 channels) and GELU tiles; two images against the oracle."""
+    D, H, Hm = dims
+    grid = (40, 40)
+    say(f"block large D={D} B={B} win={win}")
+    p = synth.block_params(rng(D + B), D, H, 64, Hm, "baseline", ln_iters=10, smax_s_d=-1)
+    x = rng(8 + B).integers(-127, 128, (B, grid[0] * grid[1], D)).astype(np.int8)
+    got = host(ilw.ilw_block_forward(ilw.DeviceBlock(p), dev(x), *grid, *win))
+    for b in (0, B - 1):
+        ref = oracle.block_forward(p, x[b:b + 1], *grid, *win)
+        assert_same(got[b:b + 1], ref, f"block large image {b}")
+
+
 @pytest.mark.parametrize("dims", [(128, 2, 512), (384, 6, 1536)])
 def test_block_requant_fallback(dims):
     """A block whose QKV, projection, fc1 and fc2 layers each hold a channel
@@ -821,7 +838,7 @@ def test_encoder_residual_shift_forms(D, H, B, grid, win, shift):
                                          ("baseline", 768), ("wide", 1152),
                                          ("wide_big_bias", 1536), ("fc1_clamped", 1536),
                                          ("res_shift_8", 1536), ("res_shift_mixed", 1152),
-                                         ("res_shift_8", 1024)])
+                                         ("res_shift_8", 1024), ("res_shift_mixed2", 768)])
 def test_encoder_384_packed_ragged(variant, mlp):
     """The 384-channel LayerNorm-fused linears on their packed-weight kernel
     (grids past the latency mode: 7 images of 41 x 41 tokens, 11 767 tokens,
@@ -838,7 +855,7 @@ def test_encoder_384_packed_ragged(variant, mlp):
     shifts below 9 take the general 64-bit residual saturation:
     'res_shift_8' in both residual adds (with MLP 1024 on the separate
     LayerNorm-fused linears), 'res_shift_mixed' in the first only (shift 5
-    there, 9 in the second)."""
+    there, 9 in the second), 'res_shift_mixed2' in the second only."""
     import concurrent.futures as cf
     D, H, B, grid, windows = 384, 6, 7, (41, 41), [(0, 0), (0, 0)]
     say(f"encoder D=384 packed weights, {B} images of {grid}, {variant}, MLP {mlp}")
@@ -853,10 +870,11 @@ def test_encoder_384_packed_ragged(variant, mlp):
                 p["b_fc1"][n] = b
                 if variant == "fc1_clamped":
                     p["fc1_shift"][n] = 20 + j % 4
-    if variant in ("res_shift_8", "res_shift_mixed"):
+    if variant.startswith("res_shift"):
+        sh1, sh2 = {"res_shift_8": (8, 8), "res_shift_mixed": (5, 9),
+                    "res_shift_mixed2": (9, 6)}[variant]
         for p in blocks:
-            for r, sh in (("res1", 8 if variant == "res_shift_8" else 5),
-                          ("res2", 8 if variant == "res_shift_8" else 9)):
+            for r, sh in (("res1", sh1), ("res2", sh2)):
                 p[r + "_shift"] = sh
                 for k in ("_mult_a", "_mult_b"):
                     p[r + k] = int(g.integers(1 << (sh - 1), 3 << (sh - 1)))
