@@ -397,6 +397,38 @@ def test_attention(case, s_d):
 
 
 @pytest.mark.parametrize("case", [
+    # (B, grid_h, grid_w, win_h, win_w, heads, I0): one case per branch of the
+    # kernel choice (row block, lanes and words per row, waves, 32- or 64-bit
+    # lane sums, masking) not taken by the cases above; I0 = 3000 makes the
+    # lane sums 64-bit
+    (4, 32, 48, 0, 0, 3, 40),       # 1536 keys: 16-lane rows of 25 words, whole last step
+    (4, 40, 40, 0, 0, 3, 3000),     # 1600 keys, 64-bit sums: 32 lanes x 13 words, split P V
+    (1, 40, 40, 20, 20, 3, 3000),   # 400-key windows in 16-row blocks, 64-bit sums
+    (4, 40, 40, 20, 20, 3, 3000),   # the same in 32-row blocks (8 lanes x 14 words)
+    (1, 30, 30, 0, 0, 2, 40),       # 900 keys in 16-row blocks: 32 lanes x 8 words
+    (2, 40, 40, 0, 0, 3, 40),       # 1600 keys in 16-row blocks: 64 lanes x 8 words
+    (1, 34, 34, 0, 0, 2, 40),       # 1156 keys, 16 waves: 10 words
+    (1, 42, 42, 0, 0, 2, 3000),     # 1764 keys, 16 waves: 14 words, 64-bit sums
+])
+def test_attention_dispatch(case):
+    """Attention against the oracle on shapes that select kernel variants the
+    other attention tests leave out."""
+    B, gh, gw, wh, ww, H, I0 = case
+    say(f"attention variants B={B} grid={gh}x{gw} win={wh}x{ww} heads={H} I0={I0}")
+    g = rng(gh * 7 + gw + wh + H + I0)
+    T, D = gh * gw, 64 * H
+    qkv = g.integers(-127, 128, (B, T, 3 * D)).astype(np.int8)
+    p = {"score_mult": int(g.integers(2 ** 29, 2 ** 30)), "score_shift": 39,
+         "smax_I0": I0, "smax_s_d": -1,
+         "pv_mult": int(g.integers(2 ** 29, 2 ** 30)), "pv_shift": 36}
+    ref = np.stack([oracle.attention(qkv[b], gh, gw, wh, ww, H, 64, p["score_mult"],
+                                     p["score_shift"], p["smax_I0"], p["pv_mult"],
+                                     p["pv_shift"], s_d=-1) for b in range(B)])
+    got = host(ilw.ilw_attention(dev(qkv), gh, gw, wh, ww, H, p))
+    assert_same(got, ref, "attention variants")
+
+
+@pytest.mark.parametrize("case", [
     # (B, grid_h, grid_w, heads, head_dim): grids of 32-row blocks large enough
     # for the split-key P V phase (rows past 1024 keys, 4 waves)
     (4, 40, 40, 3, 64),     # 1600 keys, 25 key blocks over 4 waves (7, 6, 6, 6)
