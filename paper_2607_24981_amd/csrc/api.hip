@@ -288,24 +288,27 @@ struct BlockLayout {
 
 bool ln_fusable(int32_t D);
 
-// Which of the block's residual linears take the packed-weight kernel: the
-// projection (its LayerNorm is LN2) and fc2 (with the next block's LN1, or
-// without a LayerNorm after the last block).
-bool packs_proj(const ilw_block_params* p, int64_t M) {
-  return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->dim);
-}
-bool packs_fc2(const ilw_block_params* p, int64_t M) {
-  return ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim);
-}
-// fc1 too where everything after attention runs as one kernel
-// (ILW_FUSE_TAIL=0 turns that off, read once)
+// Where everything after attention runs as one packed-weight kernel (dim
+// 384; ILW_FUSE_TAIL=0 turns it off, read once) the projection, fc1 and fc2
+// weights are packed.
 bool packs_fc1(const ilw_block_params* p, int64_t M) {
   static const bool on = [] {  // thread-safe static initialisation
     const char* e = getenv("ILW_FUSE_TAIL");
     return !(e && e[0] == '0');
   }();
-  return on && packs_proj(p, M) && packs_fc2(p, M) &&
-         tail384_kernel_applies(M, p->dim, p->mlp_dim);
+  return on && ln_fusable(p->dim) && tail384_kernel_applies(M, p->dim, p->mlp_dim);
+}
+// Otherwise the 384-channel residual linears past the GEMM latency mode take
+// the packed-weight LayerNorm kernel: the projection (its LayerNorm is LN2)
+// and fc2 (with the next block's LN1, or without a LayerNorm after the last
+// block).
+bool packs_proj(const ilw_block_params* p, int64_t M) {
+  return packs_fc1(p, M) ||
+         (ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->dim));
+}
+bool packs_fc2(const ilw_block_params* p, int64_t M) {
+  return packs_fc1(p, M) ||
+         (ln_fusable(p->dim) && ln384_packed_kernel_applies(M, p->dim, p->mlp_dim));
 }
 size_t packed_bytes(const ilw_block_params* p, int64_t M) {
   return (packs_proj(p, M) ? align256(packed_frag_bytes(p->dim, p->dim)) : 0) +
