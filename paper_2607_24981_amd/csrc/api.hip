@@ -459,7 +459,7 @@ GemmArgs with_ln(GemmArgs a, const int32_t* beta, const ilw_dyadic& out, int32_t
 
 // The block tail kernel (projection ... next block's QKV in one launch) covers
 // dim 192 / MLP 768.  It pays off where launches dominate: by default for up
-// to 16384 tokens per call; ILW_TAIL=0 / 1 turns it off / on wherever it
+// to 8192 tokens per call; ILW_TAIL=0 / 1 turns it off / on wherever it
 // applies (same results), read once.
 bool use_tail(const ilw_block_params* p, const ilw_block_params* next, int64_t M) {
   static const int mode = [] {  // read once (thread-safe static initialisation)
@@ -468,7 +468,9 @@ bool use_tail(const ilw_block_params* p, const ilw_block_params* next, int64_t M
   }();
   if (mode == 0 || p->dim != 192 || p->mlp_dim != 768) return false;
   if (next && next->dim != 192) return false;
-  return mode == 1 || M <= 16384;
+  // measured on the 1600-token encoder: the block tail wins up to batch 5,
+  // the separate linears from batch 6
+  return mode == 1 || M <= 8192;
 }
 
 // What the previous block already left for this one in the workspace.

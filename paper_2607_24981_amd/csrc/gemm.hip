@@ -655,7 +655,11 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
     // stay on chip.  These tiles fill few workgroups per CU (one at N = 384),
     // so the deep-K linears (fc2) keep two K steps of loads in flight: 4-7%
     // faster there, slower at K <= 384.
-    const bool lat = latency_mode(mt64 * (a.N / 64));
+    // (at 192 channels the count is the throughput tile's own waves, 12 per
+    // 128 tokens: on the 1600-token encoder its tiles win from batch 7,
+    // 11 200 tokens, against a tie at batch 6)
+    const bool lat = a.N == 192 ? latency_mode(((a.M + 127) / 128) * 12)
+                                : latency_mode(mt64 * (a.N / 64));
     if (a.N == 192) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
