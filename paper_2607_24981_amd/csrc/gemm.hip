@@ -702,14 +702,15 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
   if (latency_mode(mt64 * ((a.N + 63) / 64)))
     return a.K >= 6 * TK ? launch_tile<2, 2, 2, 2, 6>(epi, a, s)
                          : launch_tile<2, 2, 2, 2, 3>(epi, a, s);
+  // Wide QKV linears on 256-channel x 128-token tiles of 8 waves of 64 x 64
+  // (12% faster than 128 x 128 on the 1152-channel QKV of the 384-wide
+  // encoder at batch 8, slower for fc1; at batch 3 and 4, or half of batch 8
+  // on each of two streams, 15-20% faster than the one-wave tiles below)
+  if (epi == EPI_QKV && a.N >= 1024) return launch_tile<4, 2, 4, 4, 1>(epi, a, s);
   const int64_t big_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
   if (big_tiles < 512) return launch_tile<1, 1, 4, 4, 1>(epi, a, s);
   if (a.N % 192 == 0 && a.K >= 768) return launch_tile<3, 2, 4, 4, 1>(epi, a, s);
   if (a.N == 192) return launch_tile<3, 1, 4, 4, 1>(epi, a, s);
-  // Wide QKV linears on 256-channel x 128-token tiles of 8 waves of 64 x 64
-  // (12% faster than 128 x 128 on the 1152-channel QKV of the 384-wide
-  // encoder at batch 8; slower for fc1)
-  if (epi == EPI_QKV && a.N >= 1024) return launch_tile<4, 2, 4, 4, 1>(epi, a, s);
   return launch_tile<2, 4, 4, 2, 1>(epi, a, s);
 }
 
