@@ -664,8 +664,10 @@ hipError_t launch_gemm(int epi, const GemmArgs& a_in, hipStream_t s) {
       if (lat)  // 192 x 16 tokens
         return a.K >= 6 * TK ? launch_ln_tile<6, 1, 2, 1, 6>(a, s)
                              : launch_ln_tile<6, 1, 2, 1, 3>(a, s);
-      // 192 x 128 tokens, 12 waves of 64 x 32
-      return a.K >= 12 * TK ? launch_ln_tile<3, 4, 4, 2, 2>(a, s)
+      // 192 x 128 tokens, 12 waves of 64 x 32; the deep-K fc2 with two K
+      // steps of loads in flight but the throughput epilogue (outputs staged
+      // through LDS): 3% faster than with the latency-mode epilogue
+      return a.K >= 12 * TK ? launch_ln_tile<3, 4, 4, 2, 2, TK, false>(a, s)
                             : launch_ln_tile<3, 4, 4, 2, 1>(a, s);
     }
     if (a.N == 256) {
