@@ -800,6 +800,9 @@ def _encoder_case(D, H, Hm, depth, seed, variant="wide"):
     (128, 2, 512, (6, 8), [(3, 4), (0, 0)], 2),
     # one block: no next block to fuse LN1 into
     (192, 3, 384, (8, 8), [(4, 4)], 1),
+    # 384 channels, 15 tokens: the one-kernel block tail on a single,
+    # mostly empty 64-token tile; MLP 768 (two fc1 chunks)
+    (384, 6, 768, (3, 5), [(0, 0), (3, 5)], 1),
 ])
 def test_encoder_shapes(D, H, Hm, grid, windows, B):
     """ilw_encoder_forward on ragged token counts against the oracle block
