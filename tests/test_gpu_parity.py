@@ -67,7 +67,11 @@ def rng(seed):
 # ------------------------------------------------------------------ linear
 @pytest.mark.parametrize("M,N,K", [(1, 16, 16), (37, 48, 64), (300, 576, 192),
                                    (129, 768, 192), (257, 192, 768), (1000, 144, 208),
-                                   (4099, 1152, 384)])
+                                   (4099, 1152, 384),
+                                   # K not a multiple of 64 on the other tiles: the
+                                   # latency tile with 6 steps in flight, the one-wave
+                                   # 64 x 64 tile and the 128 x 128 tile
+                                   (500, 64, 400), (20000, 256, 208), (40000, 512, 208)])
 @pytest.mark.parametrize("per_tensor", [False, True])
 def test_linear(M, N, K, per_tensor):
     say(f"linear M={M} N={N} K={K} per_tensor={per_tensor}")
