@@ -752,6 +752,30 @@ def _encoder_full_batch(name, seed, variant, images=None):
     return wl, blocks, x, full
 
 
+@pytest.mark.parametrize("name,batch", [("encoder_t1600_d192_b32", 6), ("encoder_t1600_d192_b32", 8),
+                                        ("encoder_t1600_d192_b32", 12),
+                                        ("encoder_t1600_d384_b8", 3)])
+def test_encoder_mid_batches(name, batch):
+    """The encoders at batch sizes between the block-tail and throughput
+    regimes: the tiny encoder on its separate linears from batch 6 (batch 6
+    on the latency-mode LayerNorm tiles, 8 and 12 on the throughput ones, the
+    QKV on one-wave 64 x 64 tiles at batch 8), the medium encoder at batch 3
+    (the one-kernel block tail on 75 tiles, the QKV on its wide tiles).  The
+    first and last images against the oracle."""
+    import concurrent.futures as cf
+    wl = synth.WORKLOADS[name]
+    blocks, x = synth.encoder_inputs(wl, 40 + batch, "baseline", batch=batch)
+    images = [0, batch - 1]
+    say(f"{wl.name} at batch {batch}: oracle on {len(images)} images")
+    with cf.ThreadPoolExecutor(max_workers=1) as bg:
+        refs = bg.submit(_oracle_images, blocks, wl.windows, x, wl.grid_h, wl.grid_w, images)
+        enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
+        full = host(enc.forward(dev(x)))
+        refs = refs.result()
+    for b in images:
+        assert_same(full[b:b + 1], refs[b], f"{wl.name} batch {batch} image {b}")
+
+
 def test_encoder_c4_full():
     """The tiny encoder at batch 32 (51 200 tokens per layer) with the
     specified parameter distributions: all 32 images against the oracle."""
