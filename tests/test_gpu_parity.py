@@ -1420,12 +1420,16 @@ def test_deform_shiftmax_params(smax, dh, boxes, mode):
     assert_same(got, ref, "deform shiftmax params")
 
 
-@pytest.mark.parametrize("parts,B", [(2, 4), (2, 3), (3, 5)])
-def test_encoder_batch_split_streams(parts, B):
+@pytest.mark.parametrize("name,parts,B", [("encoder_t1600_d192_b1", 2, 4),
+                                          ("encoder_t1600_d192_b1", 2, 3),
+                                          ("encoder_t1600_d192_b1", 3, 5),
+                                          ("encoder_t1600_d384_b8", 2, 8)])
+def test_encoder_batch_split_streams(name, parts, B):
     """The batch split over streams (forked from and joined back into the
     capturing stream), captured into a HIP graph: every replay equals the
-    one-stream eager forward, uneven splits included."""
-    wl = synth.WORKLOADS["encoder_t1600_d192_b1"]
+    one-stream eager forward, uneven splits included; the medium encoder at
+    batch 8 in two halves is the benchmark's default."""
+    wl = synth.WORKLOADS[name]
     say(f"encoder batch split over {parts} streams, B={B}")
     blocks, x = synth.encoder_inputs(wl, 8, "wide", batch=B)
     enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
