@@ -518,8 +518,8 @@ hipError_t launch_rows(const AttnArgs& a, int32_t clampL, int64_t emax, hipStrea
 }
 
 // The 16-word variants with the smallest word count the window needs: 13
-// words cover 1600-token rows over 32 lanes, 14 the 448-byte padded
-// 400-token rows over 8 lanes, 10 the 320-byte padded 300-query rows.
+// words cover 1600-token rows over 32 lanes, 14 rows of up to 1792 bytes
+// over 32 lanes, 10 the 320-byte padded 300-query rows.
 template <int R, int LPR, int NW, bool P3K = false>
 hipError_t launch_fit16(const AttnArgs& a, int32_t clampL, int64_t emax, hipStream_t s) {
   const int32_t jw = ((a.Twp >> 2) + LPR - 1) / LPR;
