@@ -132,8 +132,8 @@ def main():
                          "per step is shorter than a replay's host-side submission)")
     ap.add_argument("--streams", type=int, default=None,
                     help="encoder workloads: split the batch over this many streams "
-                         "(default: 2 for the 192-wide encoder at batch >= 32 and the "
-                         "384-wide one at batch >= 8, where it measured faster, else 1)")
+                         "(default: 2 for the 192-wide encoder at batch >= 14 and the "
+                         "384-wide one at batch >= 5, where it measured faster, else 1)")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--from-image", action="store_true",
@@ -188,9 +188,11 @@ def main():
         f"{len(wl.windows)} blocks")
     if args.streams is None:
         # two half-batches on two streams where measured faster: the tiny
-        # encoder from batch 32, the 384-wide one from batch 8 (each half's
-        # block tails and attention then share the CUs)
-        args.streams = 2 if (B >= 32 or (wl.dim == 384 and B >= 8)) else 1
+        # encoder from batch 14, the 384-wide one from batch 5 (each half's
+        # block tails and attention then share the CUs); below those one
+        # stream wins (batch 12: 0.53 against 0.64 ms, batch 4: 0.68
+        # against 0.70 ms)
+        args.streams = 2 if (B >= 14 or (wl.dim == 384 and B >= 5)) else 1
     blocks, x = synth.encoder_inputs(wl, args.seed, "baseline", batch=B)
     enc = ilw.Encoder(blocks, wl.windows, wl.grid_h, wl.grid_w)
     xd = ilw.to_device(x)

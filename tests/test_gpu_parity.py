@@ -1423,7 +1423,8 @@ def test_deform_shiftmax_params(smax, dh, boxes, mode):
 @pytest.mark.parametrize("name,parts,B", [("encoder_t1600_d192_b1", 2, 4),
                                           ("encoder_t1600_d192_b1", 2, 3),
                                           ("encoder_t1600_d192_b1", 3, 5),
-                                          ("encoder_t1600_d384_b8", 2, 8)])
+                                          ("encoder_t1600_d384_b8", 2, 8),
+                                          ("encoder_t1600_d384_b8", 2, 5)])
 def test_encoder_batch_split_streams(name, parts, B):
     """The batch split over streams (forked from and joined back into the
     capturing stream), captured into a HIP graph: every replay equals the
